@@ -1,0 +1,290 @@
+/*
+ * rl_decode.h -- C ABI of the MI355X (gfx950) RL-rollout decode library.
+ *
+ * The library runs the generation step of an RL iteration: a policy decoder
+ * extends a batch of sampled responses by one token per call and returns,
+ * with every token, its log-probability (RLinf, arXiv 2509.15965, Sec. 2.1:
+ * GRPO generates several responses per query and the RL loss consumes their
+ * per-token log-probabilities; Sec. 5.1.2: one forward pass yields both the
+ * action token and its log-probability).  Generation is the bandwidth-bound
+ * phase of the iteration (Sec. 2.1, characteristics of RL workflows) and its
+ * speed is set by how much KV cache the engine can keep (Sec. 5.1.1).
+ *
+ * The decoder is a pre-norm transformer: RMSNorm, fused q|k|v projection,
+ * rotate-half RoPE, grouped-query attention over a per-sequence KV cache,
+ * output projection, RMSNorm, SwiGLU MLP, final RMSNorm, untied LM head,
+ * then temperature-scaled log-softmax with Gumbel-max sampling keyed by a
+ * counter-based generator (Philox4x32-10, Salmon et al., SC'11).
+ *
+ * Conventions for every entry point:
+ *  - All device memory (weights, KV pool, workspace, token and output
+ *    buffers) is owned by the caller and borrowed by the library; it must
+ *    outlive the context.  The library never frees it.
+ *  - "host" arguments are read before the call returns; "device" arguments
+ *    are read or written asynchronously on the context's stream.
+ *  - Every call returns an rl_status.  Arguments are validated on the host
+ *    before anything is enqueued: a call that returns an error has enqueued
+ *    no work and changed no state.  RL_ERR_HIP reports a failed HIP runtime
+ *    call (including a device fault surfaced by the runtime).
+ *  - Work is asynchronous: outputs are valid once the caller synchronises
+ *    the stream.  No entry point synchronises the stream, except
+ *    rl_decode_create, rl_decode_kernel_stats and rl_decode_destroy.
+ *  - A context is used by one host thread at a time.
+ */
+#ifndef RL_DECODE_H
+#define RL_DECODE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rl_status {
+    RL_OK = 0,
+    RL_ERR_INVALID_ARG = 1,   /* null pointer, bad value, duplicate slot ...      */
+    RL_ERR_UNSUPPORTED = 2,   /* shape the kernels do not handle                  */
+    RL_ERR_CAPACITY = 3,      /* too many rows / positions, buffer too small      */
+    RL_ERR_HIP = 4,           /* HIP runtime error                                */
+    RL_ERR_STATE = 5          /* destroyed or corrupted context                   */
+} rl_status;
+
+typedef enum rl_dtype {
+    RL_DTYPE_FP32 = 0,        /* weights, activations and KV in fp32              */
+    RL_DTYPE_BF16 = 1         /* weights, GEMM inputs and KV in bf16              */
+} rl_dtype;
+
+/* Decoder shape and capacity.
+ * Supported: head_dim in {64, 128}; n_q_heads a multiple of n_kv_heads with
+ * n_q_heads / n_kv_heads <= 16; hidden, ffn and vocab multiples of 8.
+ * rms_eps > 0, rope_theta > 1.  Capacity: max_seqs KV slots (also the most
+ * rows one rl_decode_step takes), max_ctx positions per slot, and
+ * max_prefill_tokens packed prompt tokens per rl_prefill call. */
+typedef struct rl_model_config {
+    int32_t n_layers;
+    int32_t hidden;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn;
+    int32_t vocab;
+    int32_t dtype;                /* rl_dtype */
+    double  rms_eps;
+    double  rope_theta;
+    int32_t max_seqs;
+    int32_t max_ctx;
+    int32_t max_prefill_tokens;
+    int32_t reserved;             /* must be 0 */
+} rl_model_config;
+
+/* Device pointers to the weights, all in the model dtype, row-major
+ * [out][in]; layer tensors are stacked over layers (layer-major).
+ * With Hq = n_q_heads, Hkv = n_kv_heads, d = head_dim, H = hidden, F = ffn:
+ *   embed      [vocab][H]
+ *   attn_norm  [L][H]
+ *   w_qkv      [L][(Hq + 2*Hkv)*d][H]   q rows (head-major), then k, then v
+ *   w_o        [L][H][Hq*d]
+ *   mlp_norm   [L][H]
+ *   w_gate_up  [L][2*F][H]              gate rows first, then up rows
+ *   w_down     [L][H][F]
+ *   final_norm [H]
+ *   lm_head    [vocab][H]
+ * q-head j attends with kv-head j / (Hq / Hkv).  Every row must be 16-byte
+ * aligned (guaranteed by the multiple-of-8 shape rules for bf16 and fp32). */
+typedef struct rl_weights {
+    const void* embed;
+    const void* attn_norm;
+    const void* w_qkv;
+    const void* w_o;
+    const void* mlp_norm;
+    const void* w_gate_up;
+    const void* w_down;
+    const void* final_norm;
+    const void* lm_head;
+} rl_weights;
+
+/* Sampling: seed keys the generator; temperature T >= 0 divides the logits
+ * both for sampling and for the reported log-probability.  T == 0 selects
+ * the arg-max token (lowest index on ties) and reports its T = 1
+ * log-probability. */
+typedef struct rl_sample_params {
+    uint64_t seed;
+    float    temperature;
+    int32_t  reserved;            /* must be 0 */
+} rl_sample_params;
+
+typedef struct rl_decode_ctx rl_decode_ctx;
+
+/* ---------------------------------------------------------------------
+ * Sizes.
+ *
+ * KV pool layout (model dtype), with S = max_seqs, cap = max_ctx rounded
+ * up to a multiple of 32, and E = element size:
+ *   K slab at byte offset 0:
+ *     K[l][s][h][t][i]  at element  (((l*S + s)*Hkv + h)*cap + t)*d + i
+ *   V slab at byte offset rl_decode_kv_bytes(cfg) / 2, in 8-position blocks:
+ *     V[l][s][h][t][i]  at element  ((((l*S + s)*Hkv + h)*(cap/8) + t/8)*d + i)*8 + t%8
+ * Position t of a slot holds the token at position t of that sequence.
+ * Returns 0 when cfg is invalid or unsupported.
+ * ------------------------------------------------------------------- */
+size_t rl_decode_kv_bytes(const rl_model_config* cfg);
+
+/* Workspace bytes: activations for max(max_seqs, max_prefill_tokens) rows,
+ * split-K and split-KV partial sums, fp32 logits for max_seqs rows, the
+ * RoPE table and per-call index metadata.  0 when cfg is invalid. */
+size_t rl_decode_workspace_bytes(const rl_model_config* cfg);
+
+/* ---------------------------------------------------------------------
+ * Life cycle.
+ * ------------------------------------------------------------------- */
+
+/* Create a context on the current HIP device.
+ *  cfg        host; copied.
+ *  w          host struct of device pointers; copied (the memory is borrowed).
+ *  kv_pool    device, kv_bytes >= rl_decode_kv_bytes(cfg), 256-byte aligned.
+ *  workspace  device, ws_bytes >= rl_decode_workspace_bytes(cfg), 256-byte aligned.
+ *  stream     hipStream_t to run on (NULL = the null stream); borrowed.
+ *  out        receives the context; set to NULL on error.
+ * Every slot starts empty (length 0).  Uploads the RoPE table and
+ * synchronises the stream once.  The context owns host memory only
+ * (metadata and a small pinned staging ring). */
+rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w,
+                           void* kv_pool, size_t kv_bytes,
+                           void* workspace, size_t ws_bytes,
+                           void* stream, rl_decode_ctx** out);
+
+/* Free the context's host state.  NULL is accepted (no-op).  Waits for the
+ * context's outstanding work first.  The context must not be used again. */
+rl_status rl_decode_destroy(rl_decode_ctx* ctx);
+
+/* ---------------------------------------------------------------------
+ * Prefill (generation start, Sec. 2.1: G responses per query).
+ *
+ * Runs the causal forward over n_prompts packed prompts, each computed once,
+ * writes each prompt's K/V into all `group` slots of its group, and samples
+ * the first response token of every slot.
+ *  n_prompts, group   >= 1, n_prompts*group <= max_seqs.
+ *  slots          host [n_prompts*group]; slots of prompt p are
+ *                 slots[p*group .. p*group+group-1]; distinct, < max_seqs.
+ *  seq_uids       host [n_prompts*group]; per-sequence sampling identity.
+ *  prompt_offsets host [n_prompts+1], CSR offsets into tokens; offsets[0] = 0,
+ *                 every prompt length in [1, max_ctx - 1], total
+ *                 <= max_prefill_tokens.
+ *  tokens         device int32 [offsets[n_prompts]]; an id v >= 0 selects
+ *                 embedding row v (< vocab); an id v < 0 selects row -v-1 of
+ *                 `embeds` (< n_embed_rows).  Out-of-range ids embed as zeros.
+ *  embeds         device [n_embed_rows][hidden] model dtype, or NULL.
+ *  forced_first   device int32 [n_prompts*group] or NULL: when given, the
+ *                 log-probability reported is that of this token.
+ *  sp             host.
+ *  out_tok        device int32 [n_prompts*group]: the sampled first tokens.
+ *  out_logp       device float [n_prompts*group].
+ *  out_logits     device float [n_prompts][vocab] (logits of each prompt's
+ *                 last position) or NULL.
+ * Afterwards each slot's length is its prompt length; the sampled token
+ * takes position `length` and is fed back through rl_decode_step. */
+rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group,
+                     const int32_t* slots, const uint64_t* seq_uids,
+                     const int32_t* prompt_offsets, const int32_t* tokens,
+                     const void* embeds, int32_t n_embed_rows,
+                     const int32_t* forced_first, const rl_sample_params* sp,
+                     int32_t* out_tok, float* out_logp, float* out_logits);
+
+/* ---------------------------------------------------------------------
+ * One decode step (the rollout's hot loop).
+ *
+ * For each row i < n: appends in_tok[i] to slot slots[i] at position
+ * p = length(slot), attends over positions 0..p, and samples the token of
+ * position p + 1 with noise keyed by (sp->seed, seq_uids[i], p + 1, vocab
+ * index) -- independent of the slot and of the other rows.
+ *  n          0 <= n <= max_seqs (0 is a no-op).
+ *  slots      host int32 [n], distinct, each with length < max_ctx.
+ *  seq_uids   host uint64 [n].
+ *  in_tok     device int32 [n]; out-of-range ids embed as zeros.
+ *  forced_tok device int32 [n] or NULL (teacher forcing: report the
+ *             log-probability of this token instead of the sampled one).
+ *  out_tok    device int32 [n]  sampled token.
+ *  out_logp   device float [n]  log-probability (forced or sampled token).
+ *  out_logits device float [n][vocab] or NULL.
+ * Every slot's length grows by one.  Nothing synchronises the stream. */
+rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots,
+                         const uint64_t* seq_uids, const int32_t* in_tok,
+                         const int32_t* forced_tok, const rl_sample_params* sp,
+                         int32_t* out_tok, float* out_logp, float* out_logits);
+
+/* Sample from caller-provided fp32 logits with the same rule as the step.
+ *  logits   device float [n][vocab];  n <= max_seqs.
+ *  seq_uids host uint64 [n]; pos_new host int32 [n] (position the sampled
+ *           token takes, >= 0).
+ *  forced   device int32 [n] or NULL.  out_tok/out_logp device [n]. */
+rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits,
+                           const uint64_t* seq_uids, const int32_t* pos_new,
+                           const int32_t* forced, const rl_sample_params* sp,
+                           int32_t* out_tok, float* out_logp);
+
+/* ---------------------------------------------------------------------
+ * Slot bookkeeping (host only; nothing is enqueued).
+ * ------------------------------------------------------------------- */
+
+/* Mark slots empty (length 0) so they can take new sequences. */
+rl_status rl_release_slots(rl_decode_ctx* ctx, int32_t n, const int32_t* slots);
+
+/* Declare lengths of slots whose K/V the caller wrote into the pool itself
+ * (layout above).  lengths[i] in [0, max_ctx]. */
+rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slots,
+                              const int32_t* lengths);
+
+/* Length of a slot, or -1 for an invalid context or slot. */
+int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot);
+
+/* ---------------------------------------------------------------------
+ * Options and measurement.
+ * ------------------------------------------------------------------- */
+
+typedef enum rl_option {
+    RL_OPT_ATTN_CHUNK = 1,   /* positions per split-KV chunk: 0 = automatic,
+                                else a multiple of 32 in [32, 65536]          */
+    RL_OPT_PROFILE = 2       /* 1 = time every kernel class with HIP events on
+                                the context's stream, 0 = off (default)       */
+} rl_option;
+
+rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value);
+
+typedef enum rl_kernel_class {
+    RL_K_EMBED = 0, RL_K_RMSNORM, RL_K_GEMM_QKV, RL_K_ROPE_APPEND, RL_K_ATTENTION,
+    RL_K_ATTN_COMBINE, RL_K_GEMM_O, RL_K_GEMM_GATE_UP, RL_K_GEMM_DOWN, RL_K_GEMM_LM_HEAD,
+    RL_K_SPLITK_REDUCE, RL_K_SAMPLE, RL_K_COUNT
+} rl_kernel_class;
+
+/* Accumulated per-class figures since the last reset, collected while
+ * RL_OPT_PROFILE is on.  alg_bytes / alg_flops are the algorithmic HBM bytes
+ * and FLOPs of the launches (what the operation must move or compute, not
+ * what the kernel happens to move).  Synchronises the stream. */
+typedef struct rl_kernel_stats {
+    int64_t launches;
+    double  total_ms;
+    double  alg_bytes;
+    double  alg_flops;
+    char    name[48];
+} rl_kernel_stats;
+
+rl_status rl_decode_kernel_stats(rl_decode_ctx* ctx, int32_t kclass, rl_kernel_stats* out);
+rl_status rl_decode_reset_stats(rl_decode_ctx* ctx);
+
+/* Plain device-to-device copy kernel (16-byte vector loads and stores) of
+ * `bytes` bytes (a multiple of 16; both pointers 16-byte aligned) on
+ * `stream`.  Used to calibrate hardware byte counters against a known size. */
+rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream);
+
+/* Static description of a status code. */
+const char* rl_status_string(rl_status s);
+
+/* Message describing the last error seen by this context ("" if none). */
+const char* rl_decode_last_error(const rl_decode_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RL_DECODE_H */
