@@ -63,6 +63,8 @@ def load():
     lib.orc_seq_create.restype = C.c_void_p
     lib.orc_seq_create.argtypes = [C.POINTER(_Model), C.c_int32]
     lib.orc_seq_destroy.argtypes = [C.c_void_p]
+    lib.orc_seq_clone.restype = C.c_void_p
+    lib.orc_seq_clone.argtypes = [C.POINTER(_Model), C.c_void_p]
     lib.orc_seq_len.restype = C.c_int32
     lib.orc_seq_len.argtypes = [C.c_void_p]
     lib.orc_seq_set_len.argtypes = [C.c_void_p, C.c_int32]
@@ -226,13 +228,19 @@ class OracleModel:
 class OracleSeq:
     """One sequence's KV cache ([L][max_ctx][Hkv][D] doubles) and length."""
 
-    def __init__(self, model: OracleModel, max_ctx: int):
+    def __init__(self, model: OracleModel, max_ctx: int, _handle=None):
         self.model = model
         self.lib = model.lib
-        self.h = self.lib.orc_seq_create(C.byref(model.m), int(max_ctx))
+        self.h = _handle if _handle else self.lib.orc_seq_create(C.byref(model.m), int(max_ctx))
         if not self.h:
             raise MemoryError("oracle sequence allocation failed")
         self.max_ctx = max_ctx
+
+    def clone(self) -> "OracleSeq":
+        h = self.lib.orc_seq_clone(C.byref(self.model.m), self.h)
+        if not h:
+            raise MemoryError("oracle sequence allocation failed")
+        return OracleSeq(self.model, self.max_ctx, _handle=h)
 
     def __del__(self):
         h = getattr(self, "h", None)

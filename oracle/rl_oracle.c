@@ -337,6 +337,18 @@ void orc_seq_destroy(orc_seq* s)
     free(s->K); free(s->Vc); free(s);
 }
 
+/* Duplicate a sequence's cache and length (same max_ctx and model). */
+orc_seq* orc_seq_clone(const orc_model* m, const orc_seq* src)
+{
+    orc_seq* d = orc_seq_create(m, src->max_ctx);
+    if (!d) return NULL;
+    size_t n = (size_t)m->L * (size_t)src->max_ctx * (size_t)m->Hkv * (size_t)m->D;
+    memcpy(d->K, src->K, n * sizeof(double));
+    memcpy(d->Vc, src->Vc, n * sizeof(double));
+    d->len = src->len;
+    return d;
+}
+
 int32_t orc_seq_len(const orc_seq* s) { return s->len; }
 void orc_seq_set_len(orc_seq* s, int32_t len) { s->len = len; }
 

@@ -1,0 +1,933 @@
+// engine.cpp -- host side of the rollout decode library: argument validation,
+// workspace layout, per-call index metadata, split-KV planning and kernel
+// sequencing on the caller's stream.  Implements include/rl_decode.h.
+#include "rl_decode.h"
+#include "rl_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace rl;
+
+namespace {
+
+constexpr uint32_t kMagic = 0x524C4443u;   // "RLDC"
+constexpr uint32_t kDead = 0xDEADDEADu;
+constexpr int kStages = 3;                  // pinned metadata staging ring
+constexpr int kPartItems = 8192;            // split-KV partial slots per call
+constexpr int kAttnWaveTarget = 4096;       // split-KV parallelism target (waves)
+constexpr int kPrefillChunk = 1024;         // default keys per prefill work item
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+struct Layout {
+    int es = 0, cap = 0, R = 0, nqkv = 0, items_cap = 0;
+    size_t kv_bytes = 0, ws_bytes = 0;
+    size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
+    size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
+    size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
+};
+
+bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
+    auto bad = [&](rl_status s, const char* m) { *code = s; *why = m; return false; };
+    if (!c) return bad(RL_ERR_INVALID_ARG, "config is NULL");
+    if (c->reserved != 0) return bad(RL_ERR_INVALID_ARG, "config.reserved must be 0");
+    if (c->n_layers < 1 || c->n_layers > 4096) return bad(RL_ERR_INVALID_ARG, "n_layers out of range");
+    if (c->hidden < 8 || c->hidden > (1 << 16)) return bad(RL_ERR_INVALID_ARG, "hidden out of range");
+    if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads > 1024) return bad(RL_ERR_INVALID_ARG, "head counts out of range");
+    if (c->ffn < 8 || c->ffn > (1 << 20)) return bad(RL_ERR_INVALID_ARG, "ffn out of range");
+    if (c->vocab < 8 || c->vocab > (1 << 24)) return bad(RL_ERR_INVALID_ARG, "vocab out of range");
+    if (c->dtype != RL_DTYPE_FP32 && c->dtype != RL_DTYPE_BF16) return bad(RL_ERR_INVALID_ARG, "unknown dtype");
+    if (!(c->rms_eps > 0.0) || !std::isfinite(c->rms_eps)) return bad(RL_ERR_INVALID_ARG, "rms_eps must be > 0");
+    if (!(c->rope_theta > 1.0) || !std::isfinite(c->rope_theta)) return bad(RL_ERR_INVALID_ARG, "rope_theta must be > 1");
+    if (c->max_seqs < 1 || c->max_seqs > (1 << 16)) return bad(RL_ERR_INVALID_ARG, "max_seqs out of range");
+    if (c->max_ctx < 2 || c->max_ctx > (1 << 20)) return bad(RL_ERR_INVALID_ARG, "max_ctx out of range");
+    if (c->max_prefill_tokens < 1 || c->max_prefill_tokens > (1 << 22)) return bad(RL_ERR_INVALID_ARG, "max_prefill_tokens out of range");
+    if (c->head_dim != 64 && c->head_dim != 128) return bad(RL_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->n_q_heads % c->n_kv_heads != 0) return bad(RL_ERR_UNSUPPORTED, "n_q_heads must be a multiple of n_kv_heads");
+    if (c->n_q_heads / c->n_kv_heads > 16) return bad(RL_ERR_UNSUPPORTED, "more than 16 q-heads per kv-head");
+    if (c->hidden % 8 || c->ffn % 8 || c->vocab % 8) return bad(RL_ERR_UNSUPPORTED, "hidden, ffn and vocab must be multiples of 8");
+    return true;
+}
+
+Layout make_layout(const rl_model_config& c) {
+    Layout L;
+    L.es = c.dtype == RL_DTYPE_BF16 ? 2 : 4;
+    L.cap = static_cast<int>(align_up(static_cast<size_t>(c.max_ctx), 32));
+    L.R = std::max(c.max_seqs, c.max_prefill_tokens);
+    L.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+    L.items_cap = std::max(kPartItems, L.R + c.max_seqs);
+    const size_t es = L.es, R = L.R, H = c.hidden, F = c.ffn, V = c.vocab;
+    const size_t HqD = static_cast<size_t>(c.n_q_heads) * c.head_dim;
+    L.kv_bytes = 2ull * c.n_layers * c.max_seqs * c.n_kv_heads * static_cast<size_t>(L.cap) * c.head_dim * es;
+    L.part_floats = kPartCapFloats;
+    if (c.dtype == RL_DTYPE_FP32) L.part_floats = std::max(L.part_floats, R * std::max(H, 2 * F));
+    L.apart_floats = static_cast<size_t>(kPartItems) * c.n_kv_heads * 16 * (c.head_dim + 2);
+    L.meta_bytes = 4 * (3 * R + 4 * static_cast<size_t>(c.max_seqs)) + 8 * static_cast<size_t>(c.max_seqs) +
+                   sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + sizeof(RowCombine) * R + 4096;
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
+    L.off_x = take(R * H * 4);
+    L.off_h = take(R * H * es);
+    L.off_qkv = take(R * L.nqkv * 4);
+    L.off_q = take(R * HqD * es);
+    L.off_attn = take(R * HqD * es);
+    L.off_mlp = take(R * F * es);
+    L.off_part = take(L.part_floats * 4);
+    L.off_apart = take(L.apart_floats * 4);
+    L.off_logits = take(static_cast<size_t>(c.max_seqs) * V * 4);
+    L.off_rope = take(static_cast<size_t>(L.cap) * (c.head_dim / 2) * 2 * 4);
+    L.off_meta = take(L.meta_bytes);
+    L.ws_bytes = o;
+    return L;
+}
+
+}  // namespace
+
+struct rl_decode_ctx {
+    uint32_t magic = kMagic;
+    rl_model_config cfg{};
+    rl_weights w{};
+    Layout lay;
+    uint8_t* kv = nullptr;
+    uint8_t* ws = nullptr;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::vector<int32_t> len;
+    uint8_t* staging[kStages] = {nullptr, nullptr, nullptr};
+    hipEvent_t stage_ev[kStages] = {nullptr, nullptr, nullptr};
+    bool stage_used[kStages] = {false, false, false};
+    int stage_next = 0;
+    int64_t opt_chunk = 0;
+    bool profile = false;
+    struct Pending { int kc; hipEvent_t a, b; };
+    std::vector<Pending> pending;
+    std::vector<hipEvent_t> ev_pool;
+    rl_kernel_stats stats[RL_K_COUNT]{};
+    std::string err;
+
+    template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+    uint8_t* kslab() const { return kv; }
+    uint8_t* vslab() const { return kv + lay.kv_bytes / 2; }
+    bool bf16() const { return cfg.dtype == RL_DTYPE_BF16; }
+};
+
+namespace {
+
+const char* kClassNames[RL_K_COUNT] = {
+    "embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "attn_combine", "gemm_o",
+    "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample"};
+
+rl_status fail(rl_decode_ctx* c, rl_status s, const std::string& m) {
+    if (c) c->err = m;
+    return s;
+}
+
+rl_status hip_fail(rl_decode_ctx* c, hipError_t e, const char* where) {
+    std::string m = std::string(where) + ": " + hipGetErrorString(e);
+    return fail(c, RL_ERR_HIP, m);
+}
+
+bool ctx_ok(const rl_decode_ctx* c) { return c && c->magic == kMagic; }
+
+// ---- profiling -----------------------------------------------------------
+hipEvent_t get_event(rl_decode_ctx* c) {
+    if (!c->ev_pool.empty()) { hipEvent_t e = c->ev_pool.back(); c->ev_pool.pop_back(); return e; }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+hipError_t harvest(rl_decode_ctx* c) {
+    if (c->pending.empty()) return hipSuccess;
+    hipError_t e = hipEventSynchronize(c->pending.back().b);
+    if (e != hipSuccess) return e;
+    for (auto& p : c->pending) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) c->stats[p.kc].total_ms += ms;
+        c->ev_pool.push_back(p.a);
+        c->ev_pool.push_back(p.b);
+    }
+    c->pending.clear();
+    return hipSuccess;
+}
+
+struct Prof {
+    rl_decode_ctx* c; int kc; hipEvent_t a = nullptr;
+    Prof(rl_decode_ctx* c_, int kc_) : c(c_), kc(kc_) {
+        if (c->profile && (a = get_event(c))) (void)hipEventRecord(a, c->stream);
+    }
+    void done(double bytes, double flops) {
+        c->stats[kc].launches += 1;
+        c->stats[kc].alg_bytes += bytes;
+        c->stats[kc].alg_flops += flops;
+        if (!a) return;
+        hipEvent_t b = get_event(c);
+        if (!b) { c->ev_pool.push_back(a); return; }
+        (void)hipEventRecord(b, c->stream);
+        c->pending.push_back({kc, a, b});
+        if (c->pending.size() >= 4096) (void)harvest(c);
+    }
+};
+
+// ---- metadata staging ------------------------------------------------------
+struct Meta {
+    uint8_t* host; uint8_t* dev; size_t cap; size_t used = 0; bool overflow = false;
+    template <typename T> T* take(size_t n, T** dptr) {
+        used = align_up(used, 16);
+        size_t bytes = n * sizeof(T);
+        if (used + bytes > cap) { overflow = true; *dptr = nullptr; return nullptr; }
+        T* h = reinterpret_cast<T*>(host + used);
+        *dptr = reinterpret_cast<T*>(dev + used);
+        used += bytes;
+        return h;
+    }
+};
+
+rl_status begin_meta(rl_decode_ctx* c, Meta* m, int* stage) {
+    int s = c->stage_next;
+    if (c->stage_used[s]) {
+        hipError_t e = hipEventSynchronize(c->stage_ev[s]);
+        if (e != hipSuccess) return hip_fail(c, e, "staging wait");
+    }
+    *stage = s;
+    m->host = c->staging[s];
+    m->dev = c->ws + c->lay.off_meta;
+    m->cap = c->lay.meta_bytes;
+    m->used = 0;
+    return RL_OK;
+}
+
+rl_status upload_meta(rl_decode_ctx* c, Meta* m, int stage) {
+    if (m->overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    hipError_t e = hipMemcpyAsync(m->dev, m->host, m->used, hipMemcpyHostToDevice, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "metadata upload");
+    e = hipEventRecord(c->stage_ev[stage], c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "metadata event");
+    c->stage_used[stage] = true;
+    c->stage_next = (stage + 1) % kStages;
+    return RL_OK;
+}
+
+// ---- forward pass description ----------------------------------------------
+struct Fwd {
+    int rows = 0;
+    const int32_t* tok = nullptr;
+    const void* embeds = nullptr;
+    int n_embed_rows = 0;
+    const int32_t* row_pos = nullptr;
+    const int32_t* row_dst = nullptr;
+    int n_dst = 1;
+    const int32_t* dst_slots = nullptr;
+    const int32_t* row_slot = nullptr;      // fp32 attention: slot each row reads
+    const AttnItem* items = nullptr;
+    int n_items = 0;
+    const RowCombine* rowc = nullptr;
+    bool any_combine = false;
+    int n_partial_items = 0;
+    double attn_kv_positions = 0;           // algorithmic KV positions read per kv-head
+    double attn_score_positions = 0;        // sum over rows of keys attended
+    const int32_t* final_sel = nullptr;     // rows fed to the LM head (nullptr: all)
+    int n_final = 0;
+    float* logits = nullptr;
+    int n_out = 0;
+    const int32_t* logit_row = nullptr;
+    const uint64_t* uid = nullptr;
+    const int32_t* pos_new = nullptr;
+    const int32_t* forced = nullptr;
+    uint64_t seed = 0;
+    float T = 1.0f;
+    int32_t* out_tok = nullptr;
+    float* out_logp = nullptr;
+};
+
+rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void* W, int M, int Nw,
+                   int K, int epi, float* out_f32, int ldo, float* resid, int ldr, void* act,
+                   int ld_act) {
+    const rl_model_config& cf = c->cfg;
+    GemmArgs a{};
+    a.A = A; a.lda = lda; a.W = W; a.ldw = K; a.M = M; a.Nw = Nw; a.K = K; a.epi = epi;
+    a.out_f32 = out_f32; a.ldo = ldo; a.resid = resid; a.ldr = ldr; a.act = act; a.ld_act = ld_act;
+    a.F = cf.ffn;
+    a.partial = c->wsp<float>(c->lay.off_part);
+    const double es = c->lay.es;
+    const int n_out = epi == EPI_SWIGLU ? cf.ffn : Nw;
+    double out_bytes = epi == EPI_F32 ? 4.0 * M * n_out : epi == EPI_RESID ? 8.0 * M * n_out : es * M * n_out;
+    double bytes = es * Nw * K + es * M * K + out_bytes;
+    double flops = 2.0 * M * Nw * K;
+    hipError_t e;
+    if (c->bf16()) {
+        GemmPlan p = plan_gemm_bf16(M, Nw, K, epi, cf.ffn);
+        {
+            Prof pr(c, kc);
+            e = launch_gemm_bf16(a, p, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "gemm launch");
+            pr.done(bytes, flops);
+        }
+        if (p.splits > 1) {
+            Prof pr(c, RL_K_SPLITK_REDUCE);
+            e = launch_splitk_reduce(DT_BF16, a, p.splits, a.partial, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "split-K reduce launch");
+            pr.done(4.0 * p.splits * M * Nw + out_bytes, 0.0);
+        }
+        return RL_OK;
+    }
+    // fp32 model: plain GEMM into the output (F32) or into the partial buffer
+    GemmArgs g = a;
+    if (epi != EPI_F32) { g.out_f32 = a.partial; g.ldo = Nw; }
+    {
+        Prof pr(c, kc);
+        e = launch_gemm_f32(g, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "gemm launch");
+        pr.done(bytes, flops);
+    }
+    if (epi != EPI_F32) {
+        Prof pr(c, RL_K_SPLITK_REDUCE);
+        e = launch_splitk_reduce(DT_F32, a, 1, a.partial, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "epilogue launch");
+        pr.done(4.0 * M * Nw + out_bytes, 0.0);
+    }
+    return RL_OK;
+}
+
+rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
+    const rl_model_config& cf = c->cfg;
+    const Layout& L = c->lay;
+    const int dt = c->bf16() ? DT_BF16 : DT_F32;
+    const int H = cf.hidden, Hq = cf.n_q_heads, Hkv = cf.n_kv_heads, D = cf.head_dim, F = cf.ffn;
+    const int HqD = Hq * D;
+    const double es = L.es;
+    float* x = c->wsp<float>(L.off_x);
+    void* h = c->ws + L.off_h;
+    float* qkv = c->wsp<float>(L.off_qkv);
+    void* q = c->ws + L.off_q;
+    void* attn = c->ws + L.off_attn;
+    void* mlp = c->ws + L.off_mlp;
+    float* apart = c->wsp<float>(L.off_apart);
+    const float* cs = c->wsp<float>(L.off_rope);
+    const int cs_stride = L.cap * (D / 2);
+    hipError_t e;
+    const int n = f.rows;
+
+    {
+        Prof pr(c, RL_K_EMBED);
+        e = launch_embed(dt, f.tok, n, c->w.embed, cf.vocab,
+                         f.embeds, f.n_embed_rows, H, x, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "embed launch");
+        pr.done(n * H * (es + 4.0), 0.0);
+    }
+    for (int l = 0; l < cf.n_layers; ++l) {
+        const uint8_t* an = static_cast<const uint8_t*>(c->w.attn_norm) + static_cast<size_t>(l) * H * L.es;
+        const uint8_t* wqkv = static_cast<const uint8_t*>(c->w.w_qkv) + static_cast<size_t>(l) * L.nqkv * H * L.es;
+        const uint8_t* wo = static_cast<const uint8_t*>(c->w.w_o) + static_cast<size_t>(l) * H * HqD * L.es;
+        const uint8_t* mn = static_cast<const uint8_t*>(c->w.mlp_norm) + static_cast<size_t>(l) * H * L.es;
+        const uint8_t* wgu = static_cast<const uint8_t*>(c->w.w_gate_up) + static_cast<size_t>(l) * 2 * F * H * L.es;
+        const uint8_t* wd = static_cast<const uint8_t*>(c->w.w_down) + static_cast<size_t>(l) * H * F * L.es;
+
+        {
+            Prof pr(c, RL_K_RMSNORM);
+            e = launch_rmsnorm(dt, x, nullptr, n, H, an, static_cast<float>(cf.rms_eps), h, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+            pr.done(n * H * (4.0 + es) + H * es, 0.0);
+        }
+        rl_status st = run_gemm(c, RL_K_GEMM_QKV, h, H, wqkv, n, L.nqkv, H, EPI_F32, qkv, L.nqkv,
+                                nullptr, 0, nullptr, 0);
+        if (st != RL_OK) return st;
+        {
+            Prof pr(c, RL_K_ROPE_APPEND);
+            e = launch_rope_append(dt, qkv, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride,
+                                   Hq, Hkv, D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "rope/append launch");
+            pr.done(n * (L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
+        }
+        {
+            Prof pr(c, RL_K_ATTENTION);
+            if (c->bf16())
+                e = launch_attention_bf16(f.items, f.n_items, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv,
+                                          D, L.cap, l, attn, apart, c->stream);
+            else
+                e = launch_attention_f32(n, f.row_slot, f.row_pos, static_cast<const float*>(q),
+                                         reinterpret_cast<const float*>(c->kslab()),
+                                         reinterpret_cast<const float*>(c->vslab()), cf.max_seqs, Hq, Hkv, D,
+                                         L.cap, l, static_cast<float*>(attn), c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "attention launch");
+            pr.done(f.attn_kv_positions * Hkv * 2.0 * D * es + 2.0 * n * HqD * es,
+                    4.0 * Hq * D * f.attn_score_positions);
+        }
+        if (f.any_combine) {
+            Prof pr(c, RL_K_ATTN_COMBINE);
+            e = launch_attn_combine(dt, f.rowc, n, f.items, apart, Hq, Hkv, D, attn, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "combine launch");
+            pr.done(f.n_partial_items * 16.0 * Hkv * (D + 2) * 4.0, 0.0);
+        }
+        st = run_gemm(c, RL_K_GEMM_O, attn, HqD, wo, n, H, HqD, EPI_RESID, nullptr, 0, x, H, nullptr, 0);
+        if (st != RL_OK) return st;
+        {
+            Prof pr(c, RL_K_RMSNORM);
+            e = launch_rmsnorm(dt, x, nullptr, n, H, mn, static_cast<float>(cf.rms_eps), h, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+            pr.done(n * H * (4.0 + es) + H * es, 0.0);
+        }
+        st = run_gemm(c, RL_K_GEMM_GATE_UP, h, H, wgu, n, 2 * F, H, EPI_SWIGLU, nullptr, 0, nullptr, 0, mlp, F);
+        if (st != RL_OK) return st;
+        st = run_gemm(c, RL_K_GEMM_DOWN, mlp, F, wd, n, H, F, EPI_RESID, nullptr, 0, x, H, nullptr, 0);
+        if (st != RL_OK) return st;
+    }
+    const int nf = f.final_sel ? f.n_final : n;
+    {
+        Prof pr(c, RL_K_RMSNORM);
+        e = launch_rmsnorm(dt, x, f.final_sel, nf, H, c->w.final_norm, static_cast<float>(cf.rms_eps), h,
+                           c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "final rmsnorm launch");
+        pr.done(nf * H * (4.0 + es) + H * es, 0.0);
+    }
+    rl_status st = run_gemm(c, RL_K_GEMM_LM_HEAD, h, H, c->w.lm_head, nf, cf.vocab, H, EPI_F32, f.logits,
+                            cf.vocab, nullptr, 0, nullptr, 0);
+    if (st != RL_OK) return st;
+    {
+        Prof pr(c, RL_K_SAMPLE);
+        e = launch_sample(f.logits, cf.vocab, f.n_out, cf.vocab, f.logit_row, f.uid, f.pos_new, f.forced,
+                          f.seed, f.T, f.out_tok, f.out_logp, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "sample launch");
+        pr.done(f.n_out * (cf.vocab * 4.0 + 8.0), 0.0);
+    }
+    return RL_OK;
+}
+
+// Split-KV work items for a set of query blocks.  Each block: nq tokens at
+// positions pos0 .. pos0+nq-1 of a slot, keys [0, pos0 + nq).
+struct Block { int qrow, nq, slot, pos0; };
+
+int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int default_min,
+                 int items_cap, bool decode) {
+    auto count = [&](int C, long* items, long* multi) {
+        *items = 0; *multi = 0;
+        for (const Block& b : blocks) {
+            long k = ceil_div(b.pos0 + b.nq, C);
+            *items += k;
+            if (k > 1) *multi += k;
+        }
+    };
+    long items, multi;
+    int C;
+    if (forced > 0) {
+        C = static_cast<int>(forced);
+    } else if (decode) {
+        C = 64;
+        while (C < (1 << 16)) {
+            count(2 * C, &items, &multi);
+            if (items * Hkv < kAttnWaveTarget) break;
+            C *= 2;
+        }
+    } else {
+        C = default_min;
+    }
+    for (;;) {
+        count(C, &items, &multi);
+        if ((items <= items_cap && multi <= kPartItems) || C >= (1 << 20)) break;
+        C *= 2;
+    }
+    return C;
+}
+
+rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& blocks, int C,
+                      Fwd* f, int n_rows) {
+    long total = 0;
+    for (const Block& b : blocks) total += ceil_div(b.pos0 + b.nq, C);
+    if (total > c->lay.items_cap) return fail(c, RL_ERR_CAPACITY, "too many attention work items");
+    AttnItem* dItems = nullptr;
+    AttnItem* items = m->take<AttnItem>(static_cast<size_t>(total), &dItems);
+    RowCombine* dRowc = nullptr;
+    RowCombine* rowc = m->take<RowCombine>(static_cast<size_t>(n_rows), &dRowc);
+    if (!items || !rowc) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    int k = 0, part = 0;
+    double kvpos = 0, scorepos = 0;
+    bool any = false;
+    for (const Block& b : blocks) {
+        const int hi_all = b.pos0 + b.nq;
+        const int nch = ceil_div(hi_all, C);
+        const int begin = k;
+        for (int ch = 0; ch < nch; ++ch) {
+            AttnItem& it = items[k++];
+            it.qrow = b.qrow; it.nq = b.nq; it.slot = b.slot; it.pos0 = b.pos0;
+            it.kv_lo = ch * C;
+            it.kv_hi = std::min(hi_all, (ch + 1) * C);
+            it.part = nch > 1 ? part++ : -1;
+            it.pad = 0;
+        }
+        for (int t = 0; t < b.nq; ++t) {
+            RowCombine& rc = rowc[b.qrow + t];
+            rc.item_begin = begin;
+            rc.item_count = nch;
+            rc.col0 = t * (c->cfg.n_q_heads / c->cfg.n_kv_heads);
+            rc.pad = 0;
+            scorepos += b.pos0 + t + 1;
+        }
+        if (nch > 1) any = true;
+    }
+    (void)kvpos;
+    f->items = dItems;
+    f->n_items = k;
+    f->rowc = dRowc;
+    f->any_combine = any;
+    f->n_partial_items = part;
+    f->attn_score_positions = scorepos;
+    return RL_OK;
+}
+
+void fill_rope_table(const rl_model_config& c, int cap, std::vector<float>* out) {
+    const int half = c.head_dim / 2;
+    out->assign(static_cast<size_t>(cap) * half * 2, 0.0f);
+    for (int i = 0; i < half; ++i) {
+        const double w = std::pow(c.rope_theta, -2.0 * i / static_cast<double>(c.head_dim));
+        for (int p = 0; p < cap; ++p) {
+            const double a = static_cast<double>(p) * w;
+            (*out)[static_cast<size_t>(p) * half + i] = static_cast<float>(std::cos(a));
+            (*out)[static_cast<size_t>(cap) * half + static_cast<size_t>(p) * half + i] = static_cast<float>(std::sin(a));
+        }
+    }
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+rl_status check_sp(rl_decode_ctx* c, const rl_sample_params* sp) {
+    if (!sp) return fail(c, RL_ERR_INVALID_ARG, "sample params are NULL");
+    if (sp->reserved != 0) return fail(c, RL_ERR_INVALID_ARG, "sample_params.reserved must be 0");
+    if (!(sp->temperature >= 0.0f) || !std::isfinite(sp->temperature))
+        return fail(c, RL_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+    return RL_OK;
+}
+
+rl_status check_slots(rl_decode_ctx* c, int n, const int32_t* slots, std::vector<char>* seen) {
+    seen->assign(static_cast<size_t>(c->cfg.max_seqs), 0);
+    for (int i = 0; i < n; ++i) {
+        const int s = slots[i];
+        if (s < 0 || s >= c->cfg.max_seqs) return fail(c, RL_ERR_INVALID_ARG, "slot out of range");
+        if ((*seen)[s]) return fail(c, RL_ERR_INVALID_ARG, "duplicate slot");
+        (*seen)[s] = 1;
+    }
+    return RL_OK;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) (void)hipSetDevice(dev);
+        else prev = -1;
+    }
+    ~DeviceGuard() { if (prev >= 0) (void)hipSetDevice(prev); }
+};
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* rl_status_string(rl_status s) {
+    switch (s) {
+        case RL_OK: return "ok";
+        case RL_ERR_INVALID_ARG: return "invalid argument";
+        case RL_ERR_UNSUPPORTED: return "unsupported shape";
+        case RL_ERR_CAPACITY: return "capacity exceeded";
+        case RL_ERR_HIP: return "HIP runtime error";
+        case RL_ERR_STATE: return "invalid or destroyed context";
+    }
+    return "unknown status";
+}
+
+const char* rl_decode_last_error(const rl_decode_ctx* ctx) {
+    if (!ctx_ok(ctx)) return "invalid or destroyed context";
+    return ctx->err.c_str();
+}
+
+size_t rl_decode_kv_bytes(const rl_model_config* cfg) {
+    rl_status s; std::string why;
+    if (!cfg_check(cfg, &s, &why)) return 0;
+    return make_layout(*cfg).kv_bytes;
+}
+
+size_t rl_decode_workspace_bytes(const rl_model_config* cfg) {
+    rl_status s; std::string why;
+    if (!cfg_check(cfg, &s, &why)) return 0;
+    return make_layout(*cfg).ws_bytes;
+}
+
+rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void* kv_pool,
+                           size_t kv_bytes, void* workspace, size_t ws_bytes, void* stream,
+                           rl_decode_ctx** out) {
+    if (!out) return RL_ERR_INVALID_ARG;
+    *out = nullptr;
+    rl_status code; std::string why;
+    if (!cfg_check(cfg, &code, &why)) return code;
+    if (!w || !w->embed || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up ||
+        !w->w_down || !w->final_norm || !w->lm_head)
+        return RL_ERR_INVALID_ARG;
+    const void* wp[9] = {w->embed, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm, w->w_gate_up, w->w_down,
+                         w->final_norm, w->lm_head};
+    for (const void* p : wp)
+        if (!aligned(p, 16)) return RL_ERR_INVALID_ARG;
+    if (!kv_pool || !workspace || !aligned(kv_pool, 256) || !aligned(workspace, 256)) return RL_ERR_INVALID_ARG;
+    Layout L = make_layout(*cfg);
+    if (kv_bytes < L.kv_bytes || ws_bytes < L.ws_bytes) return RL_ERR_CAPACITY;
+
+    rl_decode_ctx* c = new (std::nothrow) rl_decode_ctx();
+    if (!c) return RL_ERR_CAPACITY;
+    c->cfg = *cfg;
+    c->w = *w;
+    c->lay = L;
+    c->kv = static_cast<uint8_t*>(kv_pool);
+    c->ws = static_cast<uint8_t*>(workspace);
+    c->stream = static_cast<hipStream_t>(stream);
+    c->len.assign(static_cast<size_t>(cfg->max_seqs), 0);
+    auto cleanup = [&](rl_status s) {
+        for (int i = 0; i < kStages; ++i) {
+            if (c->staging[i]) (void)hipHostFree(c->staging[i]);
+            if (c->stage_ev[i]) (void)hipEventDestroy(c->stage_ev[i]);
+        }
+        delete c;
+        return s;
+    };
+    if (hipGetDevice(&c->device) != hipSuccess) return cleanup(RL_ERR_HIP);
+    for (int i = 0; i < kStages; ++i) {
+        if (hipHostMalloc(reinterpret_cast<void**>(&c->staging[i]), L.meta_bytes, hipHostMallocDefault) != hipSuccess)
+            return cleanup(RL_ERR_HIP);
+        if (hipEventCreateWithFlags(&c->stage_ev[i], hipEventDisableTiming) != hipSuccess)
+            return cleanup(RL_ERR_HIP);
+    }
+    std::vector<float> table;
+    fill_rope_table(*cfg, L.cap, &table);
+    if (hipMemcpyAsync(c->ws + L.off_rope, table.data(), table.size() * sizeof(float), hipMemcpyHostToDevice,
+                       c->stream) != hipSuccess)
+        return cleanup(RL_ERR_HIP);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return cleanup(RL_ERR_HIP);
+    for (int i = 0; i < RL_K_COUNT; ++i)
+        std::snprintf(c->stats[i].name, sizeof(c->stats[i].name), "%s", kClassNames[i]);
+    *out = c;
+    return RL_OK;
+}
+
+rl_status rl_decode_destroy(rl_decode_ctx* ctx) {
+    if (!ctx) return RL_OK;
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    DeviceGuard g(ctx->device);
+    (void)hipStreamSynchronize(ctx->stream);
+    for (auto& p : ctx->pending) { (void)hipEventDestroy(p.a); (void)hipEventDestroy(p.b); }
+    for (hipEvent_t e : ctx->ev_pool) (void)hipEventDestroy(e);
+    for (int i = 0; i < kStages; ++i) {
+        if (ctx->staging[i]) (void)hipHostFree(ctx->staging[i]);
+        if (ctx->stage_ev[i]) (void)hipEventDestroy(ctx->stage_ev[i]);
+    }
+    ctx->magic = kDead;
+    delete ctx;
+    return RL_OK;
+}
+
+rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const int32_t* slots,
+                     const uint64_t* seq_uids, const int32_t* prompt_offsets, const int32_t* tokens,
+                     const void* embeds, int32_t n_embed_rows, const int32_t* forced_first,
+                     const rl_sample_params* sp, int32_t* out_tok, float* out_logp, float* out_logits) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    const rl_model_config& cf = c->cfg;
+    if (n_prompts < 1 || group < 1) return fail(c, RL_ERR_INVALID_ARG, "n_prompts and group must be >= 1");
+    if (static_cast<int64_t>(n_prompts) * group > cf.max_seqs)
+        return fail(c, RL_ERR_CAPACITY, "n_prompts * group exceeds max_seqs");
+    if (!slots || !seq_uids || !prompt_offsets || !tokens || !out_tok || !out_logp)
+        return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    if (n_embed_rows < 0 || (n_embed_rows > 0 && !embeds)) return fail(c, RL_ERR_INVALID_ARG, "bad embedding rows");
+    if (embeds && !aligned(embeds, 16)) return fail(c, RL_ERR_INVALID_ARG, "embeds must be 16-byte aligned");
+    if (out_logits && !aligned(out_logits, 16)) return fail(c, RL_ERR_INVALID_ARG, "out_logits must be 16-byte aligned");
+    rl_status st = check_sp(c, sp);
+    if (st != RL_OK) return st;
+    const int n_out = n_prompts * group;
+    std::vector<char> seen;
+    st = check_slots(c, n_out, slots, &seen);
+    if (st != RL_OK) return st;
+    if (prompt_offsets[0] != 0) return fail(c, RL_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
+    int64_t total = 0;
+    for (int p = 0; p < n_prompts; ++p) {
+        const int64_t len = static_cast<int64_t>(prompt_offsets[p + 1]) - prompt_offsets[p];
+        if (len < 1) return fail(c, RL_ERR_INVALID_ARG, "empty prompt");
+        if (len > cf.max_ctx - 1) return fail(c, RL_ERR_CAPACITY, "prompt longer than max_ctx - 1");
+        total += len;
+    }
+    if (total > cf.max_prefill_tokens) return fail(c, RL_ERR_CAPACITY, "prompts exceed max_prefill_tokens");
+    const int R = static_cast<int>(total);
+    DeviceGuard g(c->device);
+
+    Meta m{};
+    int stage = 0;
+    st = begin_meta(c, &m, &stage);
+    if (st != RL_OK) return st;
+    int32_t *d_row_pos, *d_row_dst, *d_row_slot, *d_dst, *d_lrow, *d_posn, *d_last;
+    uint64_t* d_uid;
+    int32_t* row_pos = m.take<int32_t>(R, &d_row_pos);
+    int32_t* row_dst = m.take<int32_t>(R, &d_row_dst);
+    int32_t* row_slot = m.take<int32_t>(R, &d_row_slot);
+    int32_t* dst = m.take<int32_t>(n_out, &d_dst);
+    int32_t* lrow = m.take<int32_t>(n_out, &d_lrow);
+    int32_t* posn = m.take<int32_t>(n_out, &d_posn);
+    int32_t* last = m.take<int32_t>(n_prompts, &d_last);
+    uint64_t* uid = m.take<uint64_t>(n_out, &d_uid);
+    if (m.overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    std::vector<Block> blocks;
+    const int G = cf.n_q_heads / cf.n_kv_heads;
+    const int tq = std::max(1, 16 / G);
+    double kvpos = 0;
+    for (int p = 0; p < n_prompts; ++p) {
+        const int b = prompt_offsets[p], len = prompt_offsets[p + 1] - b;
+        for (int t = 0; t < len; ++t) {
+            row_pos[b + t] = t;
+            row_dst[b + t] = p * group;
+            row_slot[b + t] = slots[p * group];
+        }
+        last[p] = b + len - 1;
+        for (int k = 0; k < group; ++k) {
+            const int o = p * group + k;
+            dst[o] = slots[o];
+            lrow[o] = p;
+            posn[o] = len;
+            uid[o] = seq_uids[o];
+        }
+        for (int t = 0; t < len; t += tq) blocks.push_back(Block{b + t, std::min(tq, len - t), slots[p * group], t});
+        kvpos += len;
+    }
+    Fwd f;
+    f.rows = R;
+    f.tok = tokens;
+    f.embeds = embeds;
+    f.n_embed_rows = n_embed_rows;
+    f.row_pos = d_row_pos;
+    f.row_dst = d_row_dst;
+    f.n_dst = group;
+    f.dst_slots = d_dst;
+    f.row_slot = d_row_slot;
+    f.attn_kv_positions = kvpos;
+    if (c->bf16()) {
+        const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, kPrefillChunk, c->lay.items_cap, false);
+        st = build_items(c, &m, blocks, C, &f, R);
+        if (st != RL_OK) return st;
+    } else {
+        double sp_ = 0;
+        for (int p = 0; p < n_prompts; ++p) {
+            const double len = prompt_offsets[p + 1] - prompt_offsets[p];
+            sp_ += len * (len + 1) / 2;
+        }
+        f.attn_score_positions = sp_;
+    }
+    f.final_sel = d_last;
+    f.n_final = n_prompts;
+    f.logits = out_logits ? out_logits : c->wsp<float>(c->lay.off_logits);
+    f.n_out = n_out;
+    f.logit_row = d_lrow;
+    f.uid = d_uid;
+    f.pos_new = d_posn;
+    f.forced = forced_first;
+    f.seed = sp->seed;
+    f.T = sp->temperature;
+    f.out_tok = out_tok;
+    f.out_logp = out_logp;
+    st = upload_meta(c, &m, stage);
+    if (st != RL_OK) return st;
+    st = run_forward(c, f);
+    if (st != RL_OK) return st;
+    for (int p = 0; p < n_prompts; ++p)
+        for (int k = 0; k < group; ++k) c->len[slots[p * group + k]] = prompt_offsets[p + 1] - prompt_offsets[p];
+    return RL_OK;
+}
+
+rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, const uint64_t* seq_uids,
+                         const int32_t* in_tok, const int32_t* forced_tok, const rl_sample_params* sp,
+                         int32_t* out_tok, float* out_logp, float* out_logits) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    const rl_model_config& cf = c->cfg;
+    if (n < 0) return fail(c, RL_ERR_INVALID_ARG, "n must be >= 0");
+    if (n > cf.max_seqs) return fail(c, RL_ERR_CAPACITY, "n exceeds max_seqs");
+    rl_status st = check_sp(c, sp);
+    if (st != RL_OK) return st;
+    if (n == 0) return RL_OK;
+    if (!slots || !seq_uids || !in_tok || !out_tok || !out_logp)
+        return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    if (out_logits && !aligned(out_logits, 16)) return fail(c, RL_ERR_INVALID_ARG, "out_logits must be 16-byte aligned");
+    std::vector<char> seen;
+    st = check_slots(c, n, slots, &seen);
+    if (st != RL_OK) return st;
+    for (int i = 0; i < n; ++i)
+        if (c->len[slots[i]] >= cf.max_ctx) return fail(c, RL_ERR_CAPACITY, "slot is full (length == max_ctx)");
+    DeviceGuard g(c->device);
+
+    Meta m{};
+    int stage = 0;
+    st = begin_meta(c, &m, &stage);
+    if (st != RL_OK) return st;
+    int32_t *d_pos, *d_dst, *d_slot, *d_posn;
+    uint64_t* d_uid;
+    int32_t* pos = m.take<int32_t>(n, &d_pos);
+    int32_t* dstr = m.take<int32_t>(n, &d_dst);
+    int32_t* slot = m.take<int32_t>(n, &d_slot);
+    int32_t* posn = m.take<int32_t>(n, &d_posn);
+    uint64_t* uid = m.take<uint64_t>(n, &d_uid);
+    if (m.overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    std::vector<Block> blocks(static_cast<size_t>(n));
+    double kvpos = 0;
+    for (int i = 0; i < n; ++i) {
+        const int p = c->len[slots[i]];
+        pos[i] = p;
+        dstr[i] = i;
+        slot[i] = slots[i];
+        posn[i] = p + 1;
+        uid[i] = seq_uids[i];
+        blocks[i] = Block{i, 1, slots[i], p};
+        kvpos += p + 1;
+    }
+    Fwd f;
+    f.rows = n;
+    f.tok = in_tok;
+    f.row_pos = d_pos;
+    f.row_dst = d_dst;
+    f.n_dst = 1;
+    f.dst_slots = d_slot;
+    f.row_slot = d_slot;
+    f.attn_kv_positions = kvpos;
+    f.attn_score_positions = kvpos;
+    if (c->bf16()) {
+        const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, 0, c->lay.items_cap, true);
+        st = build_items(c, &m, blocks, C, &f, n);
+        if (st != RL_OK) return st;
+    }
+    f.logits = out_logits ? out_logits : c->wsp<float>(c->lay.off_logits);
+    f.n_out = n;
+    f.uid = d_uid;
+    f.pos_new = d_posn;
+    f.forced = forced_tok;
+    f.seed = sp->seed;
+    f.T = sp->temperature;
+    f.out_tok = out_tok;
+    f.out_logp = out_logp;
+    st = upload_meta(c, &m, stage);
+    if (st != RL_OK) return st;
+    st = run_forward(c, f);
+    if (st != RL_OK) return st;
+    for (int i = 0; i < n; ++i) c->len[slots[i]] += 1;
+    return RL_OK;
+}
+
+rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits, const uint64_t* seq_uids,
+                           const int32_t* pos_new, const int32_t* forced, const rl_sample_params* sp,
+                           int32_t* out_tok, float* out_logp) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    if (n < 0) return fail(c, RL_ERR_INVALID_ARG, "n must be >= 0");
+    if (n > c->cfg.max_seqs) return fail(c, RL_ERR_CAPACITY, "n exceeds max_seqs");
+    rl_status st = check_sp(c, sp);
+    if (st != RL_OK) return st;
+    if (n == 0) return RL_OK;
+    if (!logits || !seq_uids || !pos_new || !out_tok || !out_logp)
+        return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    if (!aligned(logits, 16)) return fail(c, RL_ERR_INVALID_ARG, "logits must be 16-byte aligned");
+    for (int i = 0; i < n; ++i)
+        if (pos_new[i] < 0) return fail(c, RL_ERR_INVALID_ARG, "pos_new must be >= 0");
+    DeviceGuard g(c->device);
+    Meta m{};
+    int stage = 0;
+    st = begin_meta(c, &m, &stage);
+    if (st != RL_OK) return st;
+    int32_t* d_posn;
+    uint64_t* d_uid;
+    int32_t* posn = m.take<int32_t>(n, &d_posn);
+    uint64_t* uid = m.take<uint64_t>(n, &d_uid);
+    if (m.overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    for (int i = 0; i < n; ++i) { posn[i] = pos_new[i]; uid[i] = seq_uids[i]; }
+    st = upload_meta(c, &m, stage);
+    if (st != RL_OK) return st;
+    Prof pr(c, RL_K_SAMPLE);
+    hipError_t e = launch_sample(logits, c->cfg.vocab, n, c->cfg.vocab, nullptr, d_uid, d_posn, forced, sp->seed,
+                                 sp->temperature, out_tok, out_logp, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "sample launch");
+    pr.done(n * (c->cfg.vocab * 4.0 + 8.0), 0.0);
+    return RL_OK;
+}
+
+rl_status rl_release_slots(rl_decode_ctx* ctx, int32_t n, const int32_t* slots) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    if (n < 0 || (n > 0 && !slots)) return fail(ctx, RL_ERR_INVALID_ARG, "bad slot list");
+    for (int i = 0; i < n; ++i)
+        if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return fail(ctx, RL_ERR_INVALID_ARG, "slot out of range");
+    for (int i = 0; i < n; ++i) ctx->len[slots[i]] = 0;
+    return RL_OK;
+}
+
+rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* lengths) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    if (n < 0 || (n > 0 && (!slots || !lengths))) return fail(ctx, RL_ERR_INVALID_ARG, "bad slot list");
+    for (int i = 0; i < n; ++i) {
+        if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return fail(ctx, RL_ERR_INVALID_ARG, "slot out of range");
+        if (lengths[i] < 0 || lengths[i] > ctx->cfg.max_ctx) return fail(ctx, RL_ERR_INVALID_ARG, "length out of range");
+    }
+    for (int i = 0; i < n; ++i) ctx->len[slots[i]] = lengths[i];
+    return RL_OK;
+}
+
+int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot) {
+    if (!ctx_ok(ctx) || slot < 0 || slot >= ctx->cfg.max_seqs) return -1;
+    return ctx->len[slot];
+}
+
+rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    switch (option) {
+        case RL_OPT_ATTN_CHUNK:
+            if (value != 0 && (value < 32 || value > 65536 || value % 32 != 0))
+                return fail(ctx, RL_ERR_INVALID_ARG, "attention chunk must be 0 or a multiple of 32 in [32, 65536]");
+            ctx->opt_chunk = value;
+            return RL_OK;
+        case RL_OPT_PROFILE:
+            if (value != 0 && value != 1) return fail(ctx, RL_ERR_INVALID_ARG, "profile must be 0 or 1");
+            ctx->profile = value == 1;
+            return RL_OK;
+        default:
+            return fail(ctx, RL_ERR_INVALID_ARG, "unknown option");
+    }
+}
+
+rl_status rl_decode_kernel_stats(rl_decode_ctx* ctx, int32_t kclass, rl_kernel_stats* out) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    if (kclass < 0 || kclass >= RL_K_COUNT || !out) return fail(ctx, RL_ERR_INVALID_ARG, "bad kernel class");
+    DeviceGuard g(ctx->device);
+    hipError_t e = harvest(ctx);
+    if (e != hipSuccess) return hip_fail(ctx, e, "profile harvest");
+    *out = ctx->stats[kclass];
+    return RL_OK;
+}
+
+rl_status rl_decode_reset_stats(rl_decode_ctx* ctx) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    DeviceGuard g(ctx->device);
+    hipError_t e = harvest(ctx);
+    if (e != hipSuccess) return hip_fail(ctx, e, "profile harvest");
+    for (int i = 0; i < RL_K_COUNT; ++i) {
+        ctx->stats[i].launches = 0;
+        ctx->stats[i].total_ms = 0;
+        ctx->stats[i].alg_bytes = 0;
+        ctx->stats[i].alg_flops = 0;
+    }
+    return RL_OK;
+}
+
+rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream) {
+    if (!dst || !src || bytes % 16 || !aligned(dst, 16) || !aligned(src, 16)) return RL_ERR_INVALID_ARG;
+    hipError_t e = launch_copy16(dst, src, bytes / 16, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? RL_OK : RL_ERR_HIP;
+}
+
+}  // extern "C"

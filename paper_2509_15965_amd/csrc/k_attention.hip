@@ -1,0 +1,292 @@
+// k_attention.hip -- grouped-query attention over the per-sequence KV cache.
+//
+// bf16 path (split-KV, MFMA).  One wave owns one work item: up to 16 query
+// columns (query tokens x the q-heads of one kv-head) against one chunk of
+// key positions of one KV slot.  Every K and V byte of the chunk is read
+// once for all q-heads of the group.
+//   scores   S^T[t][c] = K[t] . Q[c]     (A = 16 key rows, B = 16 columns)
+//   output   O^T[d][c] += V^T[d][t] P^T[t][c]
+// Key rows of the two 16-row score tiles of a 32-position step are permuted
+// so that the lane holding column c and k-group q owns the scores of
+// positions t0 + 8q .. t0 + 8q + 7; those eight probabilities are exactly
+// the lane's B operand of the P.V product, and the matching A operand is one
+// 16-byte load from the V cache's 8-position blocks.  No LDS, no transposes.
+// Online softmax in the exp2 domain, fp32 state.  A work item that covers
+// all keys of its tokens writes the normalised output; otherwise it writes
+// (max, sum, unnormalised output) partials that attn_combine merges.
+//
+// fp32 path: one workgroup per (row, q-head), plain VALU (tiny model only).
+#include "rl_device.h"
+#include "rl_internal.h"
+
+namespace rl {
+
+// Zero the bf16 elements e >= nvalid of an 8-element vector (0 <= nvalid <= 8).
+__device__ __forceinline__ u32x4 mask_tail8(u32x4 v, int nvalid) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const int e0 = 2 * w;
+        uint32_t keep = (e0 < nvalid ? 0x0000FFFFu : 0u) | (e0 + 1 < nvalid ? 0xFFFF0000u : 0u);
+        v[w] &= keep;
+    }
+    return v;
+}
+
+template <int D>
+__global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restrict__ items,
+        int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+        const uint16_t* __restrict__ vc, int S, int Hq, int Hkv, int cap, int layer,
+        float scale_log2, uint16_t* __restrict__ out, float* __restrict__ part) {
+    constexpr int KG = D / 32;   // 32-wide k groups of a head
+    constexpr int DT = D / 16;   // 16-wide d tiles of the output
+    const int lane = threadIdx.x & 63;
+    const int item_id = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (item_id >= n_items) return;
+    const int kvh = blockIdx.y;
+    const int G = Hq / Hkv;
+    const AttnItem it = items[item_id];
+
+    const int col = lane & 15, kq = lane >> 4;
+    const int ncols = it.nq * G;
+    const bool cvalid = col < ncols;
+    const int tau = cvalid ? col / G : 0;
+    const int head = kvh * G + (cvalid ? col - tau * G : 0);
+    const int qrow = it.qrow + tau;
+    const int limit = cvalid ? it.pos0 + tau : -1;   // last key this column sees
+
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 qf[KG];
+    {
+        const uint16_t* qp = q + (static_cast<size_t>(qrow) * Hq + head) * D + 8 * kq;
+#pragma unroll
+        for (int j = 0; j < KG; ++j) qf[j] = cvalid ? ld16(qp + 32 * j) : zero;
+    }
+
+    const size_t base = ((static_cast<size_t>(layer) * S + it.slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
+    const uint16_t* kb = kc + base;
+    const uint16_t* vb = vc + base;
+
+    float m = -INFINITY, l = 0.0f;
+    f32x4 o[DT];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int hi = it.kv_hi;
+    // key row r of score tile 0 is position t0 + 8(r/4) + r%4; tile 1 adds 4
+    const int krow = 8 * (col >> 2) + (col & 3);
+    for (int t0 = it.kv_lo; t0 < hi; t0 += 32) {
+        u32x4 k0[KG], k1[KG];
+        const uint16_t* kp0 = kb + static_cast<size_t>(t0 + krow) * D + 8 * kq;
+        const uint16_t* kp1 = kp0 + 4 * D;
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+            k0[j] = ld16(kp0 + 32 * j);
+            k1[j] = ld16(kp1 + 32 * j);
+        }
+        // V blocks of this lane's eight positions, one per d tile
+        const int pb = t0 + 8 * kq;
+        const uint16_t* vp = vb + (static_cast<size_t>(pb >> 3) * D + col) * 8;
+        u32x4 vf[DT];
+#pragma unroll
+        for (int i = 0; i < DT; ++i) vf[i] = ld16(vp + 16 * 8 * i);
+
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+            s0 = mfma16x16x32(as_bf16x8(k0[j]), as_bf16x8(qf[j]), s0);
+            s1 = mfma16x16x32(as_bf16x8(k1[j]), as_bf16x8(qf[j]), s1);
+        }
+        // this lane now holds the scores of column col at positions pb + 0..7
+        const int lim = min(hi - 1, limit);
+        float sv[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sv[e] = (pb + e <= lim) ? s0[e] * scale_log2 : -INFINITY;
+            sv[4 + e] = (pb + 4 + e <= lim) ? s1[e] * scale_log2 : -INFINITY;
+        }
+        float mx = sv[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m, mx);
+        const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+        const float alpha = exp2f(m - m_use);
+        float psum = 0.0f;
+        uint32_t pw[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float p0 = exp2f(sv[2 * w] - m_use);
+            const float p1 = exp2f(sv[2 * w + 1] - m_use);
+            psum += p0 + p1;
+            pw[w] = static_cast<uint32_t>(f32_to_bf16(p0)) | (static_cast<uint32_t>(f32_to_bf16(p1)) << 16);
+        }
+        l = l * alpha + psum;
+        m = m_new;
+        const u32x4 pf = {pw[0], pw[1], pw[2], pw[3]};
+        const int nvalid = hi - pb;   // keys past the chunk end carry no data
+#pragma unroll
+        for (int i = 0; i < DT; ++i) {
+            u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
+            o[i] = o[i] * alpha;
+            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pf), o[i]);
+        }
+    }
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+
+    // lane holds O^T[d = 16 i + 4 kq + e][col]
+    if (!cvalid) return;
+    if (it.part < 0) {
+        const float inv = 1.0f / l;
+        uint16_t* op = out + (static_cast<size_t>(qrow) * Hq + head) * D + 4 * kq;
+#pragma unroll
+        for (int i = 0; i < DT; ++i) {
+            const uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(o[i][0] * inv)) |
+                                (static_cast<uint32_t>(f32_to_bf16(o[i][1] * inv)) << 16);
+            const uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(o[i][2] * inv)) |
+                                (static_cast<uint32_t>(f32_to_bf16(o[i][3] * inv)) << 16);
+            *reinterpret_cast<uint2*>(op + 16 * i) = make_uint2(w0, w1);
+        }
+    } else {
+        float* pp = part + ((static_cast<size_t>(it.part) * Hkv + kvh) * 16 + col) * (D + 2);
+#pragma unroll
+        for (int i = 0; i < DT; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) pp[16 * i + 4 * kq + e] = o[i][e];
+        if (kq == 0) {
+            pp[D] = m;
+            pp[D + 1] = l;
+        }
+    }
+}
+
+hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
+                                 const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
+                                 int D, int cap, int layer, void* out, float* part,
+                                 hipStream_t s) {
+    if (n_items <= 0) return hipSuccess;
+    const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
+    dim3 grid((n_items + 3) / 4, Hkv), block(256);
+    if (D == 128)
+        hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, items, n_items,
+                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
+                           static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer,
+                           scale_log2, static_cast<uint16_t*>(out), part);
+    else
+        hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, items, n_items,
+                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
+                           static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer,
+                           scale_log2, static_cast<uint16_t*>(out), part);
+    return hipGetLastError();
+}
+
+// Merge the split-KV partials of one (row, q-head): weights 2^(m_c - M).
+template <typename T>
+__global__ void __launch_bounds__(128) attn_combine_kernel(const RowCombine* __restrict__ rows,
+        const AttnItem* __restrict__ items, const float* __restrict__ part, int Hq, int Hkv, int D,
+        T* __restrict__ out) {
+    const int r = blockIdx.x, h = blockIdx.y;
+    const RowCombine rc = rows[r];
+    if (rc.item_count <= 1) return;
+    const int G = Hq / Hkv;
+    const int kvh = h / G;
+    const int col = rc.col0 + (h - kvh * G);
+    float M = -INFINITY;
+    for (int c = 0; c < rc.item_count; ++c) {
+        const float* pp = part + ((static_cast<size_t>(items[rc.item_begin + c].part) * Hkv + kvh) * 16 + col) * (D + 2);
+        M = fmaxf(M, pp[D]);
+    }
+    float L = 0.0f;
+    for (int d = threadIdx.x; d < D; d += blockDim.x) {
+        float acc = 0.0f;
+        L = 0.0f;
+        for (int c = 0; c < rc.item_count; ++c) {
+            const float* pp = part + ((static_cast<size_t>(items[rc.item_begin + c].part) * Hkv + kvh) * 16 + col) * (D + 2);
+            const float w = exp2f(pp[D] - M);
+            acc += w * pp[d];
+            L += w * pp[D + 1];
+        }
+        Elem<T>::store(out, (static_cast<size_t>(r) * Hq + h) * D + d, acc / L);
+    }
+}
+
+hipError_t launch_attn_combine(int dt, const RowCombine* rows, int n_rows, const AttnItem* items,
+                               const float* part, int Hq, int Hkv, int D, void* out,
+                               hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    dim3 grid(n_rows, Hq), block(128);
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, block, 0, s, rows, items, part, Hq,
+                           Hkv, D, static_cast<uint16_t*>(out));
+    else
+        hipLaunchKernelGGL(attn_combine_kernel<float>, grid, block, 0, s, rows, items, part, Hq,
+                           Hkv, D, static_cast<float*>(out));
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// fp32: one 64-lane workgroup per (row, q-head); keys 0..pos of the row's slot.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict__ row_slot,
+        const int32_t* __restrict__ row_pos, const float* __restrict__ q,
+        const float* __restrict__ kc, const float* __restrict__ vc, int S, int Hq, int Hkv, int D,
+        int cap, int layer, float* __restrict__ out) {
+    __shared__ float qs[128];
+    __shared__ float ps[64];
+    const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int G = Hq / Hkv, kvh = h / G;
+    const int pos = row_pos[r], slot = row_slot[r];
+    const float* qr = q + (static_cast<size_t>(r) * Hq + h) * D;
+    for (int i = lane; i < D; i += 64) qs[i] = qr[i];
+    __syncthreads();
+    const size_t base = ((static_cast<size_t>(layer) * S + slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
+    const float* kb = kc + base;
+    const float* vb = vc + base;
+    const float scale = 1.0f / sqrtf(static_cast<float>(D));
+    float m = -INFINITY, l = 0.0f;
+    float acc0 = 0.0f, acc1 = 0.0f;   // d = lane, lane + 64
+    for (int t0 = 0; t0 <= pos; t0 += 64) {
+        const int t = t0 + lane;
+        float s = -INFINITY;
+        if (t <= pos) {
+            const float* kr = kb + static_cast<size_t>(t) * D;
+            float d = 0.0f;
+            for (int i = 0; i < D; ++i) d = fmaf(qs[i], kr[i], d);
+            s = d * scale;
+        }
+        const float mx = wave_max(s);
+        const float m_new = fmaxf(m, mx);
+        const float alpha = expf(m - m_new);
+        const float p = t <= pos ? expf(s - m_new) : 0.0f;
+        l = l * alpha + wave_sum(p);
+        m = m_new;
+        ps[lane] = p;
+        __syncthreads();
+        acc0 *= alpha;
+        acc1 *= alpha;
+        const int nt = min(64, pos + 1 - t0);
+        for (int tt = 0; tt < nt; ++tt) {
+            const int tp = t0 + tt;
+            const float* vblk = vb + static_cast<size_t>(tp >> 3) * D * 8 + (tp & 7);
+            if (lane < D) acc0 = fmaf(ps[tt], vblk[static_cast<size_t>(lane) * 8], acc0);
+            if (lane + 64 < D) acc1 = fmaf(ps[tt], vblk[static_cast<size_t>(lane + 64) * 8], acc1);
+        }
+        __syncthreads();
+    }
+    float* orow = out + (static_cast<size_t>(r) * Hq + h) * D;
+    if (lane < D) orow[lane] = acc0 / l;
+    if (lane + 64 < D) orow[lane + 64] = acc1 / l;
+}
+
+hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
+                                const float* q, const float* kc, const float* vc, int max_seqs,
+                                int Hq, int Hkv, int D, int cap, int layer, float* out,
+                                hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(attn_f32_kernel, dim3(n_rows, Hq), dim3(64), 0, s, row_slot, row_pos, q, kc,
+                       vc, max_seqs, Hq, Hkv, D, cap, layer, out);
+    return hipGetLastError();
+}
+
+}  // namespace rl

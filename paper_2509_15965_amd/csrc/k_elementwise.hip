@@ -1,0 +1,166 @@
+// k_elementwise.hip -- embedding gather, RMSNorm, RoPE + KV append, copy probe.
+#include "rl_device.h"
+#include "rl_internal.h"
+
+namespace rl {
+
+// x[r][:] = fp32(row of the embedding table or of the caller's rows).
+// tok >= 0 selects table row tok (< V); tok < 0 selects rows[-tok-1]
+// (< n_rows); anything else embeds as zeros.
+template <typename T>
+__global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ tok,
+        const T* __restrict__ table, int V, const T* __restrict__ rows, int n_rows, int H,
+        float* __restrict__ x) {
+    const int r = blockIdx.x;
+    const int t = tok[r];
+    const T* src = nullptr;
+    if (t >= 0 && t < V) src = table + static_cast<size_t>(t) * H;
+    else if (t < 0 && rows != nullptr && -(t + 1) < n_rows) src = rows + static_cast<size_t>(-(t + 1)) * H;
+    float* dst = x + static_cast<size_t>(r) * H;
+    for (int i = threadIdx.x; i < H; i += blockDim.x)
+        dst[i] = src ? Elem<T>::load(src, i) : 0.0f;
+}
+
+hipError_t launch_embed(int dt, const int32_t* tok, int n, const void* table, int V,
+                        const void* rows, int n_rows, int H, float* x, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(n), dim3(256), 0, s, tok,
+                           static_cast<const uint16_t*>(table), V,
+                           static_cast<const uint16_t*>(rows), n_rows, H, x);
+    else
+        hipLaunchKernelGGL(embed_kernel<float>, dim3(n), dim3(256), 0, s, tok,
+                           static_cast<const float*>(table), V, static_cast<const float*>(rows),
+                           n_rows, H, x);
+    return hipGetLastError();
+}
+
+// out[o][:] = storage( x[row] / sqrt(mean(x[row]^2) + eps) * g ), row = sel ? sel[o] : o.
+// fp32 statistics; one workgroup per row.
+template <typename T>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x,
+        const int32_t* __restrict__ sel, int H, const T* __restrict__ g, float eps,
+        T* __restrict__ out) {
+    __shared__ float red[4];
+    const int o = blockIdx.x;
+    const int row = sel ? sel[o] : o;
+    const float* xr = x + static_cast<size_t>(row) * H;
+    float ss = 0.0f;
+    for (int i = threadIdx.x; i < H; i += 256) {
+        float v = xr[i];
+        ss = fmaf(v, v, ss);
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    ss = red[0] + red[1] + red[2] + red[3];
+    const float r = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+    T* orow = out + static_cast<size_t>(o) * H;
+    for (int i = threadIdx.x; i < H; i += 256)
+        Elem<T>::store(orow, i, xr[i] * r * Elem<T>::load(g, i));
+}
+
+hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int H,
+                          const void* g, float eps, void* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(n), dim3(256), 0, s, x, sel, H,
+                           static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(out));
+    else
+        hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n), dim3(256), 0, s, x, sel, H,
+                           static_cast<const float*>(g), eps, static_cast<float*>(out));
+    return hipGetLastError();
+}
+
+// Rotate-half RoPE on q and k of one row (pairs i, i + D/2 rotated by the
+// angle of position pos at frequency i), storage rounding, and the KV append.
+// cs: cos table [cap][D/2] followed by the sin table [cap][D/2].
+// K cache element (l, s, h, t, i): (((l*S + s)*Hkv + h)*cap + t)*D + i.
+// V cache element: ((((l*S + s)*Hkv + h)*(cap/8) + t/8)*D + i)*8 + t%8.
+template <typename T>
+__global__ void __launch_bounds__(256) rope_append_kernel(const float* __restrict__ qkv,
+        const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_dst, int n_dst,
+        const int32_t* __restrict__ dst_slots, const float* __restrict__ cs, int cs_stride,
+        int Hq, int Hkv, int D, int S, int cap, int layer, T* __restrict__ q_out,
+        T* __restrict__ kc, T* __restrict__ vc) {
+    const int r = blockIdx.x;
+    const int pos = row_pos[r];
+    const int half = D / 2;
+    const int nqkv = (Hq + 2 * Hkv) * D;
+    const float* src = qkv + static_cast<size_t>(r) * nqkv;
+    const float* cosr = cs + static_cast<size_t>(pos) * half;
+    const float* sinr = cs + static_cast<size_t>(cs_stride) + static_cast<size_t>(pos) * half;
+    const int d0 = row_dst[r];
+
+    // q heads
+    for (int idx = threadIdx.x; idx < Hq * half; idx += blockDim.x) {
+        const int h = idx / half, i = idx - h * half;
+        const float a = src[h * D + i], b = src[h * D + i + half];
+        const float c = cosr[i], s = sinr[i];
+        T* qo = q_out + (static_cast<size_t>(r) * Hq + h) * D;
+        Elem<T>::store(qo, i, a * c - b * s);
+        Elem<T>::store(qo, i + half, b * c + a * s);
+    }
+    // k heads -> cache
+    for (int idx = threadIdx.x; idx < Hkv * half; idx += blockDim.x) {
+        const int h = idx / half, i = idx - h * half;
+        const float a = src[(Hq + h) * D + i], b = src[(Hq + h) * D + i + half];
+        const float c = cosr[i], s = sinr[i];
+        const float k0 = a * c - b * s, k1 = b * c + a * s;
+        for (int g = 0; g < n_dst; ++g) {
+            const int slot = dst_slots[d0 + g];
+            T* kr = kc + ((static_cast<size_t>(layer) * S + slot) * Hkv + h) * static_cast<size_t>(cap) * D
+                    + static_cast<size_t>(pos) * D;
+            Elem<T>::store(kr, i, k0);
+            Elem<T>::store(kr, i + half, k1);
+        }
+    }
+    // v heads -> cache (8-position blocks)
+    for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
+        const int h = idx / D, i = idx - h * D;
+        const float v = src[(Hq + Hkv + h) * D + i];
+        for (int g = 0; g < n_dst; ++g) {
+            const int slot = dst_slots[d0 + g];
+            T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + h) * static_cast<size_t>(cap) * D;
+            Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i) * 8 + (pos & 7), v);
+        }
+    }
+}
+
+hipError_t launch_rope_append(int dt, const float* qkv, int n_rows, const int32_t* row_pos,
+                              const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
+                              const float* cs, int cs_stride, int Hq, int Hkv, int D,
+                              int max_seqs, int cap, int layer,
+                              void* q_out, void* kc, void* vc, hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(rope_append_kernel<uint16_t>, dim3(n_rows), dim3(256), 0, s, qkv,
+                           row_pos, row_dst, n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D,
+                           max_seqs, cap, layer, static_cast<uint16_t*>(q_out),
+                           static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc));
+    else
+        hipLaunchKernelGGL(rope_append_kernel<float>, dim3(n_rows), dim3(256), 0, s, qkv,
+                           row_pos, row_dst, n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D,
+                           max_seqs, cap, layer, static_cast<float*>(q_out),
+                           static_cast<float*>(kc), static_cast<float*>(vc));
+    return hipGetLastError();
+}
+
+// Plain streaming copy: 16 bytes per lane per iteration, grid-stride.
+__global__ void __launch_bounds__(256) copy16_kernel(u32x4* __restrict__ dst,
+        const u32x4* __restrict__ src, size_t n16) {
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride)
+        dst[i] = src[i];
+}
+
+hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s) {
+    if (n16 == 0) return hipSuccess;
+    size_t blocks = (n16 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(copy16_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                       static_cast<u32x4*>(dst), static_cast<const u32x4*>(src), n16);
+    return hipGetLastError();
+}
+
+}  // namespace rl

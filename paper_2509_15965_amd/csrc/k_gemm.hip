@@ -1,0 +1,314 @@
+// k_gemm.hip -- Y = X . W^T for the projections, MLP and LM head.
+//
+// bf16: MFMA 16x16x32 tiles fed straight from global memory.  A lane loads
+// 16 contiguous bytes of one row (8 k values) per 32-wide k group, so 16
+// lanes sharing a k group read 16 rows and the 4 k groups of a wave read 64
+// contiguous bytes of every row: weight rows stream from HBM in full 128-byte
+// lines across the two MFMAs of a 64-wide k step, each weight byte read once
+// per workgroup row.  Small batches (M <= 64) use one 16/32/64-row M tile per
+// workgroup and split K across workgroups when the weight alone cannot fill
+// the 256 CUs; fp32 partials are then summed in a fixed order by
+// splitk_reduce (deterministic).
+//
+// fp32: a plain LDS-tiled VALU kernel (the tiny fp32 decoder only).
+#include "rl_device.h"
+#include "rl_internal.h"
+
+namespace rl {
+
+const GemmShape kGemmShapes[kNumGemmShapes] = {
+    {1, 4, 1, 4},   // M <= 16 : 16 x 256 weight rows per workgroup
+    {2, 4, 1, 4},   // M <= 32 : 32 x 256
+    {4, 4, 1, 4},   // M <= 64 : 64 x 256
+    {4, 4, 2, 2},   // M >  64 : 128 x 128
+};
+
+static int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
+    GemmPlan p{};
+    p.variant = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : 3;
+    const GemmShape& s = kGemmShapes[p.variant];
+    const int BM = 16 * s.MT * s.WR;
+    const int BNw = 16 * s.NT * s.WC;
+    const int n_out = epi == EPI_SWIGLU ? F : Nw;
+    const int BNo = epi == EPI_SWIGLU ? BNw / 2 : BNw;
+    p.grid_x = ceil_div(n_out, BNo);
+    p.grid_y = ceil_div(M, BM);
+    int S = 1;
+    const long tiles = static_cast<long>(p.grid_x) * p.grid_y;
+    while (tiles * S * 2 <= 1024 && ceil_div(K, 2 * S) >= 256 &&
+           static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
+        S *= 2;
+    int ks = ceil_div(ceil_div(K, S), 64) * 64;
+    p.ksplit = ks;
+    p.splits = ceil_div(K, ks);
+    return p;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA kernel
+// ---------------------------------------------------------------------------
+template <int MT, int NT, int WR, int WC, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmArgs p, int ksplit) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wr = wave / WC, wc = wave % WC;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const int M = p.M, Nw = p.Nw, K = p.K;
+
+    const int m_base = (blockIdx.y * WR + wr) * 16 * MT;
+    // weight row of tile t (the SwiGLU wave takes matching gate and up tiles)
+    int wrow[NT];
+    if (EPI == EPI_SWIGLU) {
+        const int c0 = (blockIdx.x * WC + wc) * 16 * (NT / 2);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            wrow[t] = t < NT / 2 ? c0 + 16 * t : p.F + c0 + 16 * (t - NT / 2);
+    } else {
+        const int n0 = (blockIdx.x * WC + wc) * 16 * NT;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) wrow[t] = n0 + 16 * t;
+    }
+
+    const int kb = blockIdx.z * ksplit;
+    const int ke = min(K, kb + ksplit);
+
+    const uint16_t* A = static_cast<const uint16_t*>(p.A);
+    const uint16_t* W = static_cast<const uint16_t*>(p.W);
+    const uint16_t* ap[MT];
+    bool aok[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+        const int m = m_base + 16 * i + r16;
+        aok[i] = m < M;
+        ap[i] = A + static_cast<size_t>(aok[i] ? m : 0) * p.lda + 8 * kq;
+    }
+    const uint16_t* wp[NT];
+    bool wok[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int n = wrow[t] + r16;
+        bool ok = n < Nw;
+        if (EPI == EPI_SWIGLU) {
+            const int c = t < NT / 2 ? n : n - p.F;
+            ok = c < p.F;
+        }
+        wok[t] = ok;
+        wp[t] = W + static_cast<size_t>(ok ? n : 0) * p.ldw + 8 * kq;
+    }
+
+    f32x4 acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 a_cur[MT][2], b_cur[NT][2];
+    auto load = [&](u32x4 (&a)[MT][2], u32x4 (&b)[NT][2], int k0) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int kk = k0 + 32 * j + 8 * kq;
+            const bool kok = kk < ke;
+#pragma unroll
+            for (int i = 0; i < MT; ++i) a[i][j] = (aok[i] && kok) ? ld16(ap[i] + k0 + 32 * j) : zero;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) b[t][j] = (wok[t] && kok) ? ld16(wp[t] + k0 + 32 * j) : zero;
+        }
+    };
+
+    if (kb < ke) load(a_cur, b_cur, kb);
+    for (int k0 = kb; k0 < ke; k0 += 64) {
+        u32x4 a_nxt[MT][2], b_nxt[NT][2];
+        const bool more = k0 + 64 < ke;
+        if (more) load(a_nxt, b_nxt, k0 + 64);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    acc[i][t] = mfma16x16x32(as_bf16x8(a_cur[i][j]), as_bf16x8(b_cur[t][j]), acc[i][t]);
+        if (more) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+#pragma unroll
+                for (int i = 0; i < MT; ++i) a_cur[i][j] = a_nxt[i][j];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) b_cur[t][j] = b_nxt[t][j];
+            }
+        }
+    }
+
+    // epilogue: lane holds rows m_base + 16 i + 4 kq + e, weight row wrow[t] + r16
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int m = m_base + 16 * i + 4 * kq + e;
+            if (m >= M) continue;
+            if (SPLIT) {
+                float* dst = p.partial + (static_cast<size_t>(blockIdx.z) * M + m) * Nw;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int n = wrow[t] + r16;
+                    if (wok[t]) dst[n] = acc[i][t][e];
+                }
+            } else if (EPI == EPI_F32) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int n = wrow[t] + r16;
+                    if (wok[t]) p.out_f32[static_cast<size_t>(m) * p.ldo + n] = acc[i][t][e];
+                }
+            } else if (EPI == EPI_RESID) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int n = wrow[t] + r16;
+                    if (wok[t]) p.resid[static_cast<size_t>(m) * p.ldr + n] += acc[i][t][e];
+                }
+            } else {  // EPI_SWIGLU
+                uint16_t* act = static_cast<uint16_t*>(p.act);
+#pragma unroll
+                for (int t = 0; t < NT / 2; ++t) {
+                    const int c = wrow[t] + r16;
+                    if (!wok[t]) continue;
+                    const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
+                    const float silu = g / (1.0f + expf(-g));
+                    act[static_cast<size_t>(m) * p.ld_act + c] = f32_to_bf16(silu * u);
+                }
+            }
+        }
+    }
+}
+
+template <int MT, int NT, int WR, int WC>
+static hipError_t launch_shape(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    dim3 grid(p.grid_x, p.grid_y, p.splits), block(256);
+    if (p.splits > 1) {
+        if (a.epi == EPI_SWIGLU)
+            hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, WR, WC, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit);
+        else
+            hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, WR, WC, EPI_F32, true>), grid, block, 0, s, a, p.ksplit);
+    } else if (a.epi == EPI_F32) {
+        hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, WR, WC, EPI_F32, false>), grid, block, 0, s, a, p.ksplit);
+    } else if (a.epi == EPI_RESID) {
+        hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, WR, WC, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit);
+    } else {
+        hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, WR, WC, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    if (a.M <= 0) return hipSuccess;
+    switch (p.variant) {
+        case 0: return launch_shape<1, 4, 1, 4>(a, p, s);
+        case 1: return launch_shape<2, 4, 1, 4>(a, p, s);
+        case 2: return launch_shape<4, 4, 1, 4>(a, p, s);
+        default: return launch_shape<4, 4, 2, 2>(a, p, s);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// split-K reduction (fixed summation order) + epilogue
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs p, int splits,
+        const float* __restrict__ part) {
+    const int n_out = p.epi == EPI_SWIGLU ? p.F : p.Nw;
+    const size_t total = static_cast<size_t>(p.M) * n_out;
+    const size_t slice = static_cast<size_t>(p.M) * p.Nw;
+    for (size_t idx = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+         idx += static_cast<size_t>(gridDim.x) * blockDim.x) {
+        const int m = static_cast<int>(idx / n_out);
+        const int c = static_cast<int>(idx - static_cast<size_t>(m) * n_out);
+        const float* src = part + static_cast<size_t>(m) * p.Nw + c;
+        float v = 0.0f;
+        for (int z = 0; z < splits; ++z) v += src[z * slice];
+        if (p.epi == EPI_F32) {
+            p.out_f32[static_cast<size_t>(m) * p.ldo + c] = v;
+        } else if (p.epi == EPI_RESID) {
+            p.resid[static_cast<size_t>(m) * p.ldr + c] += v;
+        } else {
+            float u = 0.0f;
+            for (int z = 0; z < splits; ++z) u += src[z * slice + p.F];
+            const float silu = v / (1.0f + expf(-v));
+            Elem<T>::store(static_cast<T*>(p.act), static_cast<size_t>(m) * p.ld_act + c, silu * u);
+        }
+    }
+}
+
+hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const float* partial,
+                                hipStream_t s) {
+    const int n_out = a.epi == EPI_SWIGLU ? a.F : a.Nw;
+    const size_t total = static_cast<size_t>(a.M) * n_out;
+    if (total == 0) return hipSuccess;
+    size_t blocks = (total + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(splitk_reduce_kernel<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                           a, splits, partial);
+    else
+        hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                           a, splits, partial);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// fp32 VALU kernel: out_f32[m][n] = sum_k A[m][k] W[n][k]
+// 32 x 64 output tile, 2 x 4 per thread, k tiles of 32 through LDS.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A, int lda,
+        const float* __restrict__ W, int ldw, int M, int N, int K, float* __restrict__ out, int ldo) {
+    __shared__ float As[32][33];
+    __shared__ float Ws[32][65];
+    const int tid = threadIdx.x;
+    const int tx = tid & 15, ty = tid >> 4;
+    const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 64;
+    float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    for (int k0 = 0; k0 < K; k0 += 32) {
+        for (int e = tid; e < 32 * 32; e += 256) {
+            const int r = e >> 5, k = e & 31;
+            const int m = m0 + r, kk = k0 + k;
+            As[k][r] = (m < M && kk < K) ? A[static_cast<size_t>(m) * lda + kk] : 0.0f;
+        }
+        for (int e = tid; e < 64 * 32; e += 256) {
+            const int r = e >> 5, k = e & 31;
+            const int n = n0 + r, kk = k0 + k;
+            Ws[k][r] = (n < N && kk < K) ? W[static_cast<size_t>(n) * ldw + kk] : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int k = 0; k < 32; ++k) {
+            const float a0 = As[k][ty * 2], a1 = As[k][ty * 2 + 1];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float w = Ws[k][tx * 4 + j];
+                acc[0][j] = fmaf(a0, w, acc[0][j]);
+                acc[1][j] = fmaf(a1, w, acc[1][j]);
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int m = m0 + ty * 2 + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + tx * 4 + j;
+            if (n < N) out[static_cast<size_t>(m) * ldo + n] = acc[i][j];
+        }
+    }
+}
+
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
+    if (a.M <= 0) return hipSuccess;
+    dim3 grid(ceil_div(a.Nw, 64), ceil_div(a.M, 32));
+    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(a.A), a.lda,
+                       static_cast<const float*>(a.W), a.ldw, a.M, a.Nw, a.K, a.out_f32, a.ldo);
+    return hipGetLastError();
+}
+
+}  // namespace rl

@@ -1,0 +1,120 @@
+// k_sample.hip -- temperature log-softmax, Gumbel-max sampling and the
+// per-token log-probability, one workgroup per output row.
+//
+// Noise: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit seed with
+// counter (v / 4, position of the new token, uid lo, uid hi); word v % 4 of
+// the block is the noise word x_v of vocabulary entry v.  u = (x + 1/2) 2^-32,
+// g = fl32(-log(-log u)) evaluated in fp64.  The sample is the arg-max of
+// fl32(z_v / T + g_v) with ties to the lowest index; the log-probability is
+// z_y / T - LSE(z / T).  T == 0: arg-max of z, log-probability at T = 1.
+#include "rl_device.h"
+#include "rl_internal.h"
+
+namespace rl {
+
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+    constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    constexpr uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) { k0 += W0; k1 += W1; }
+        const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
+        const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+        const uint32_t n0 = hi1 ^ c[1] ^ k0;
+        const uint32_t n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+    }
+}
+
+__device__ __forceinline__ float gumbel_of_word(uint32_t x) {
+    const double u = (static_cast<double>(x) + 0.5) * 2.3283064365386963e-10;
+    return static_cast<float>(-log(-log(u)));
+}
+
+struct Best { float s; int v; };
+__device__ __forceinline__ Best better(Best a, Best b) {
+    if (b.s > a.s || (b.s == a.s && b.v < a.v)) return b;
+    return a;
+}
+struct Lse { float m, s; };
+__device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
+    if (a.m == -INFINITY) return b;
+    if (b.m == -INFINITY) return a;
+    const float m = fmaxf(a.m, b.m);
+    return Lse{m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
+}
+
+__global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ logits, int ld,
+        int V, const int32_t* __restrict__ logit_row, const uint64_t* __restrict__ uid,
+        const int32_t* __restrict__ pos_new, const int32_t* __restrict__ forced, uint32_t seed_lo,
+        uint32_t seed_hi, float T, int32_t* __restrict__ out_tok, float* __restrict__ out_logp) {
+    __shared__ Best sb[4];
+    __shared__ Lse sl[4];
+    const int o = blockIdx.x;
+    const int row = logit_row ? logit_row[o] : o;
+    const float* z = logits + static_cast<size_t>(row) * ld;
+    const uint64_t u64 = uid[o];
+    const uint32_t pos = static_cast<uint32_t>(pos_new[o]);
+    const bool greedy = T == 0.0f;
+
+    Best best{-INFINITY, 0x7FFFFFFF};
+    Lse acc{-INFINITY, 0.0f};
+    for (int v4 = threadIdx.x; 4 * v4 < V; v4 += blockDim.x) {
+        const float4 zz = *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4));
+        const float zv[4] = {zz.x, zz.y, zz.z, zz.w};
+        uint32_t c[4] = {static_cast<uint32_t>(v4), pos, static_cast<uint32_t>(u64),
+                         static_cast<uint32_t>(u64 >> 32)};
+        if (!greedy) philox4x32_10(c, seed_lo, seed_hi);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const int v = 4 * v4 + w;
+            if (v >= V) break;
+            const float zt = greedy ? zv[w] : zv[w] / T;
+            const float s = greedy ? zt : zt + gumbel_of_word(c[w]);
+            best = better(best, Best{s, v});
+            if (zt > acc.m) {
+                acc.s = acc.s * expf(acc.m - zt) + 1.0f;
+                acc.m = zt;
+            } else {
+                acc.s += expf(zt - acc.m);
+            }
+        }
+    }
+    // wave reduction, then across the 4 waves
+    for (int off = 32; off > 0; off >>= 1) {
+        Best ob{__shfl_xor(best.s, off, 64), __shfl_xor(best.v, off, 64)};
+        best = better(best, ob);
+        Lse ol{__shfl_xor(acc.m, off, 64), __shfl_xor(acc.s, off, 64)};
+        acc = lse_merge(acc, ol);
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) { sb[wave] = best; sl[wave] = acc; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        Best b = sb[0];
+        Lse a = sl[0];
+        for (int w = 1; w < 4; ++w) { b = better(b, sb[w]); a = lse_merge(a, sl[w]); }
+        const float lse = a.m + logf(a.s);
+        int r = b.v;
+        if (forced) {
+            const int f = forced[o];
+            r = (f >= 0 && f < V) ? f : b.v;
+        }
+        const float zr = greedy ? z[r] : z[r] / T;
+        out_tok[o] = b.v;
+        out_logp[o] = zr - lse;
+    }
+}
+
+hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
+                         const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
+                         uint64_t seed, float T, int32_t* out_tok, float* out_logp,
+                         hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sample_kernel, dim3(n), dim3(256), 0, s, logits, ld, V, logit_row, uid,
+                       pos_new, forced, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                       T, out_tok, out_logp);
+    return hipGetLastError();
+}
+
+}  // namespace rl

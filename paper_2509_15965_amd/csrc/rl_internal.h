@@ -1,0 +1,117 @@
+// rl_internal.h -- declarations shared by the HIP kernels and the host engine
+// of the rollout decode library (not part of the public C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rl {
+
+// Element encodings of the model dtype.
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// GEMM epilogues: Y = X . W^T followed by
+enum Epi {
+    EPI_F32 = 0,      // store fp32 Y
+    EPI_RESID = 1,    // fp32 residual += Y
+    EPI_SWIGLU = 2    // act[m][c] = storage(silu(Y[m][c]) * Y[m][F + c]), c < F
+};
+
+// One split-KV attention work item: a block of nq consecutive query tokens
+// of one sequence (nq * group <= 16 columns) against key positions
+// [kv_lo, kv_hi) of one KV slot.  kv_lo is a multiple of 32.
+struct AttnItem {
+    int32_t qrow;   // workspace row of the first query token
+    int32_t nq;     // query tokens in the block
+    int32_t slot;   // KV slot read
+    int32_t pos0;   // position of the first query token
+    int32_t kv_lo;
+    int32_t kv_hi;
+    int32_t part;   // partial-sum index, or -1 when this item covers every key
+                    // its tokens see (it then writes the final output)
+    int32_t pad;
+};
+
+// Per query row: the items whose partial sums the combine step merges.
+struct RowCombine {
+    int32_t item_begin;
+    int32_t item_count;   // <= 1: nothing to combine
+    int32_t col0;         // column of this row's first head inside its items
+    int32_t pad;
+};
+
+struct GemmArgs {
+    const void* A;   int lda;     // [M][K] model dtype
+    const void* W;   int ldw;     // [Nw][K] model dtype (Nw = 2F for SwiGLU)
+    int M, Nw, K;
+    int epi;
+    float* out_f32;  int ldo;     // EPI_F32
+    float* resid;    int ldr;     // EPI_RESID
+    void* act;       int ld_act;  // EPI_SWIGLU output, model dtype
+    int F;                        // EPI_SWIGLU
+    float* partial;               // [splits][M][Nw] when splits > 1
+};
+
+struct GemmPlan {
+    int variant;   // index into the tile-shape table
+    int splits;
+    int ksplit;    // K elements per split (multiple of 64)
+    int grid_x, grid_y;
+};
+
+// Tile shapes of the bf16 MFMA GEMM: wave tile (16*MT) x (16*NT) weight rows,
+// 4 waves per workgroup arranged WR x WC.
+struct GemmShape { int MT, NT, WR, WC; };
+constexpr int kNumGemmShapes = 4;
+extern const GemmShape kGemmShapes[kNumGemmShapes];
+
+constexpr int kMaxSplits = 32;
+constexpr size_t kPartCapFloats = size_t(16) << 20;   // split-K partials budget
+
+GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F);
+
+// ---- launchers (enqueue only; return hipGetLastError()) -----------------
+hipError_t launch_embed(int dt, const int32_t* tok, int n, const void* table, int V,
+                        const void* rows, int n_rows, int H, float* x, hipStream_t s);
+
+hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int H,
+                          const void* g, float eps, void* out, hipStream_t s);
+
+hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);   // writes a.out_f32 [M][Nw]
+hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const float* partial,
+                                hipStream_t s);
+
+// RoPE on q and k, q stored to q_out [rows][Hq][d]; k and v appended to the
+// cache of every destination slot of the row (dst_slots[row_dst[r] + g],
+// g < n_dst) at position row_pos[r].
+hipError_t launch_rope_append(int dt, const float* qkv, int n_rows, const int32_t* row_pos,
+                              const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
+                              const float* cs, int cs_stride, int Hq, int Hkv, int D,
+                              int max_seqs, int cap, int layer,
+                              void* q_out, void* kc, void* vc, hipStream_t s);
+
+hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
+                                 const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
+                                 int D, int cap, int layer, void* out, float* part,
+                                 hipStream_t s);
+
+hipError_t launch_attn_combine(int dt, const RowCombine* rows, int n_rows, const AttnItem* items,
+                               const float* part, int Hq, int Hkv, int D, void* out,
+                               hipStream_t s);
+
+// fp32 model dtype: one workgroup per (row, q-head), keys 0..row_pos[r].
+hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
+                                const float* q, const float* kc, const float* vc, int max_seqs,
+                                int Hq, int Hkv, int D, int cap, int layer, float* out,
+                                hipStream_t s);
+
+hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
+                         const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
+                         uint64_t seed, float T, int32_t* out_tok, float* out_logp,
+                         hipStream_t s);
+
+hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
+
+}  // namespace rl

@@ -1,0 +1,259 @@
+"""Python binding of the C ABI in include/rl_decode.h (argument marshalling only).
+
+PyTorch supplies device memory (weights, KV pool, workspace, token and output
+buffers) and the stream; every step of the decoder runs in the library's HIP
+kernels.  There is no fallback: if librl_decode.so is missing or a call
+fails, an exception is raised.
+"""
+import ctypes as C
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+from .configs import ModelShape
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "librl_decode.so")
+
+RL_OK, RL_ERR_INVALID_ARG, RL_ERR_UNSUPPORTED, RL_ERR_CAPACITY, RL_ERR_HIP, RL_ERR_STATE = range(6)
+RL_DTYPE_FP32, RL_DTYPE_BF16 = 0, 1
+RL_OPT_ATTN_CHUNK, RL_OPT_PROFILE = 1, 2
+KERNEL_CLASSES = ("embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "attn_combine",
+                  "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample")
+
+EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create", "rl_decode_destroy",
+           "rl_prefill", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
+           "rl_set_slot_lengths", "rl_slot_length", "rl_decode_set_option", "rl_decode_kernel_stats",
+           "rl_decode_reset_stats", "rl_probe_copy", "rl_status_string", "rl_decode_last_error")
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("hidden", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn", C.c_int32),
+                ("vocab", C.c_int32), ("dtype", C.c_int32), ("rms_eps", C.c_double),
+                ("rope_theta", C.c_double), ("max_seqs", C.c_int32), ("max_ctx", C.c_int32),
+                ("max_prefill_tokens", C.c_int32), ("reserved", C.c_int32)]
+
+
+class Weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("embed", "attn_norm", "w_qkv", "w_o", "mlp_norm",
+                                          "w_gate_up", "w_down", "final_norm", "lm_head")]
+
+
+class SampleParams(C.Structure):
+    _fields_ = [("seed", C.c_uint64), ("temperature", C.c_float), ("reserved", C.c_int32)]
+
+
+class KernelStats(C.Structure):
+    _fields_ = [("launches", C.c_int64), ("total_ms", C.c_double), ("alg_bytes", C.c_double),
+                ("alg_flops", C.c_double), ("name", C.c_char * 48)]
+
+
+_lib = None
+
+
+def lib():
+    """Load librl_decode.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2509_15965_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, u64, sz = C.c_void_p, C.c_int32, C.c_uint64, C.c_size_t
+    cfgp = C.POINTER(ModelConfig)
+    L.rl_decode_kv_bytes.restype = sz
+    L.rl_decode_kv_bytes.argtypes = [cfgp]
+    L.rl_decode_workspace_bytes.restype = sz
+    L.rl_decode_workspace_bytes.argtypes = [cfgp]
+    L.rl_decode_create.restype = C.c_int
+    L.rl_decode_create.argtypes = [cfgp, C.POINTER(Weights), vp, sz, vp, sz, vp, C.POINTER(vp)]
+    L.rl_decode_destroy.restype = C.c_int
+    L.rl_decode_destroy.argtypes = [vp]
+    L.rl_prefill.restype = C.c_int
+    L.rl_prefill.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, C.POINTER(SampleParams), vp, vp, vp]
+    L.rl_decode_step.restype = C.c_int
+    L.rl_decode_step.argtypes = [vp, i32, vp, vp, vp, vp, C.POINTER(SampleParams), vp, vp, vp]
+    L.rl_sample_logits.restype = C.c_int
+    L.rl_sample_logits.argtypes = [vp, i32, vp, vp, vp, vp, C.POINTER(SampleParams), vp, vp]
+    L.rl_release_slots.restype = C.c_int
+    L.rl_release_slots.argtypes = [vp, i32, vp]
+    L.rl_set_slot_lengths.restype = C.c_int
+    L.rl_set_slot_lengths.argtypes = [vp, i32, vp, vp]
+    L.rl_slot_length.restype = i32
+    L.rl_slot_length.argtypes = [vp, i32]
+    L.rl_decode_set_option.restype = C.c_int
+    L.rl_decode_set_option.argtypes = [vp, i32, C.c_int64]
+    L.rl_decode_kernel_stats.restype = C.c_int
+    L.rl_decode_kernel_stats.argtypes = [vp, i32, C.POINTER(KernelStats)]
+    L.rl_decode_reset_stats.restype = C.c_int
+    L.rl_decode_reset_stats.argtypes = [vp]
+    L.rl_probe_copy.restype = C.c_int
+    L.rl_probe_copy.argtypes = [vp, vp, sz, vp]
+    L.rl_status_string.restype = C.c_char_p
+    L.rl_status_string.argtypes = [C.c_int]
+    L.rl_decode_last_error.restype = C.c_char_p
+    L.rl_decode_last_error.argtypes = [vp]
+    _lib = L
+    return L
+
+
+class RLError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{lib().rl_status_string(status).decode()} ({status}): {msg}")
+        self.status = status
+
+
+def make_config(shape: ModelShape, max_seqs: int, max_ctx: int, max_prefill_tokens: int) -> ModelConfig:
+    c = ModelConfig()
+    c.n_layers, c.hidden, c.n_q_heads = shape.n_layers, shape.hidden, shape.n_q_heads
+    c.n_kv_heads, c.head_dim, c.ffn, c.vocab = shape.n_kv_heads, shape.head_dim, shape.ffn, shape.vocab
+    c.dtype = RL_DTYPE_BF16 if shape.dtype == "bf16" else RL_DTYPE_FP32
+    c.rms_eps, c.rope_theta = float(shape.rms_eps), float(shape.rope_theta)
+    c.max_seqs, c.max_ctx, c.max_prefill_tokens, c.reserved = max_seqs, max_ctx, max_prefill_tokens, 0
+    return c
+
+
+def kv_bytes(cfg: ModelConfig) -> int:
+    return int(lib().rl_decode_kv_bytes(C.byref(cfg)))
+
+
+def workspace_bytes(cfg: ModelConfig) -> int:
+    return int(lib().rl_decode_workspace_bytes(C.byref(cfg)))
+
+
+def _p(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _host_u64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.uint64))
+
+
+class Engine:
+    """One decode context: borrowed weights, a KV pool and a workspace
+    allocated here with torch, and the current torch stream."""
+
+    def __init__(self, shape: ModelShape, weights: Dict[str, torch.Tensor], max_seqs: int,
+                 max_ctx: int, max_prefill_tokens: int, device="cuda", stream=None):
+        L = lib()
+        self.shape = shape
+        self.cfg = make_config(shape, max_seqs, max_ctx, max_prefill_tokens)
+        self.kv_nbytes = kv_bytes(self.cfg)
+        self.ws_nbytes = workspace_bytes(self.cfg)
+        if self.kv_nbytes == 0 or self.ws_nbytes == 0:
+            raise RLError(RL_ERR_INVALID_ARG, "configuration rejected")
+        self.device = torch.device(device)
+        self.kv = torch.empty(self.kv_nbytes, dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(self.ws_nbytes, dtype=torch.uint8, device=self.device)
+        self.weights = weights
+        w = Weights()
+        for name, _ in Weights._fields_:
+            setattr(w, name, weights[name].data_ptr())
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        h = C.c_void_p()
+        st = L.rl_decode_create(C.byref(self.cfg), C.byref(w), self.kv.data_ptr(), self.kv_nbytes,
+                                self.ws.data_ptr(), self.ws_nbytes, self.stream.cuda_stream, C.byref(h))
+        if st != RL_OK:
+            raise RLError(st, "rl_decode_create failed")
+        self.h = h
+
+    # -- helpers ----------------------------------------------------------
+    def _check(self, st: int, what: str):
+        if st != RL_OK:
+            raise RLError(st, f"{what}: {lib().rl_decode_last_error(self.h).decode()}")
+
+    def close(self):
+        if getattr(self, "h", None):
+            lib().rl_decode_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- entry points -----------------------------------------------------
+    def prefill(self, slots: Sequence[int], uids: Sequence[int], prompt_offsets: Sequence[int],
+                tokens: torch.Tensor, out_tok: torch.Tensor, out_logp: torch.Tensor, *, group: int = 1,
+                embeds: Optional[torch.Tensor] = None, forced: Optional[torch.Tensor] = None,
+                seed: int = 0, temperature: float = 1.0, out_logits: Optional[torch.Tensor] = None):
+        slots, uids, offs = _host_i32(slots), _host_u64(uids), _host_i32(prompt_offsets)
+        n_prompts = len(offs) - 1
+        sp = SampleParams(seed, temperature, 0)
+        n_rows = 0 if embeds is None else int(embeds.shape[0])
+        st = lib().rl_prefill(self.h, n_prompts, group, slots.ctypes.data, uids.ctypes.data,
+                              offs.ctypes.data, _p(tokens), _p(embeds), n_rows, _p(forced), C.byref(sp),
+                              _p(out_tok), _p(out_logp), _p(out_logits))
+        self._check(st, "rl_prefill")
+
+    def step(self, slots: Sequence[int], uids: Sequence[int], in_tok: torch.Tensor, out_tok: torch.Tensor,
+             out_logp: torch.Tensor, *, forced: Optional[torch.Tensor] = None, seed: int = 0,
+             temperature: float = 1.0, out_logits: Optional[torch.Tensor] = None):
+        slots, uids = _host_i32(slots), _host_u64(uids)
+        sp = SampleParams(seed, temperature, 0)
+        st = lib().rl_decode_step(self.h, len(slots), slots.ctypes.data, uids.ctypes.data, _p(in_tok),
+                                  _p(forced), C.byref(sp), _p(out_tok), _p(out_logp), _p(out_logits))
+        self._check(st, "rl_decode_step")
+
+    def sample_logits(self, logits: torch.Tensor, uids: Sequence[int], pos_new: Sequence[int],
+                      out_tok: torch.Tensor, out_logp: torch.Tensor, *, forced=None, seed: int = 0,
+                      temperature: float = 1.0):
+        uids, pos = _host_u64(uids), _host_i32(pos_new)
+        sp = SampleParams(seed, temperature, 0)
+        st = lib().rl_sample_logits(self.h, len(uids), _p(logits), uids.ctypes.data, pos.ctypes.data,
+                                    _p(forced), C.byref(sp), _p(out_tok), _p(out_logp))
+        self._check(st, "rl_sample_logits")
+
+    def release(self, slots: Sequence[int]):
+        s = _host_i32(slots)
+        self._check(lib().rl_release_slots(self.h, len(s), s.ctypes.data), "rl_release_slots")
+
+    def set_lengths(self, slots: Sequence[int], lengths: Sequence[int]):
+        s, l = _host_i32(slots), _host_i32(lengths)
+        self._check(lib().rl_set_slot_lengths(self.h, len(s), s.ctypes.data, l.ctypes.data),
+                    "rl_set_slot_lengths")
+
+    def slot_length(self, slot: int) -> int:
+        return int(lib().rl_slot_length(self.h, slot))
+
+    def set_option(self, option: int, value: int):
+        self._check(lib().rl_decode_set_option(self.h, option, value), "rl_decode_set_option")
+
+    def kernel_stats(self) -> Dict[str, dict]:
+        out = {}
+        for k, name in enumerate(KERNEL_CLASSES):
+            s = KernelStats()
+            self._check(lib().rl_decode_kernel_stats(self.h, k, C.byref(s)), "rl_decode_kernel_stats")
+            out[name] = {"launches": s.launches, "total_ms": s.total_ms, "alg_bytes": s.alg_bytes,
+                         "alg_flops": s.alg_flops}
+        return out
+
+    def reset_stats(self):
+        self._check(lib().rl_decode_reset_stats(self.h), "rl_decode_reset_stats")
+
+    # -- KV pool views (layout of include/rl_decode.h) --------------------
+    def kv_views(self):
+        """(K, V) torch views of the pool: K [L][S][Hkv][cap][d],
+        V [L][S][Hkv][cap/8][d][8] (8-position blocks), model dtype."""
+        s = self.shape
+        cap = (self.cfg.max_ctx + 31) // 32 * 32
+        dt = torch.float32 if s.dtype == "fp32" else torch.bfloat16
+        half = self.kv_nbytes // 2
+        K = self.kv[:half].view(dt).view(s.n_layers, self.cfg.max_seqs, s.n_kv_heads, cap, s.head_dim)
+        V = self.kv[half:].view(dt).view(s.n_layers, self.cfg.max_seqs, s.n_kv_heads, cap // 8, s.head_dim, 8)
+        return K, V
+
+
+def probe_copy(dst: torch.Tensor, src: torch.Tensor, nbytes: int, stream=None):
+    stream = stream if stream is not None else torch.cuda.current_stream(dst.device)
+    st = lib().rl_probe_copy(dst.data_ptr(), src.data_ptr(), nbytes, stream.cuda_stream)
+    if st != RL_OK:
+        raise RLError(st, "rl_probe_copy")

@@ -1,0 +1,117 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host-side sizing and validation behave as documented.  No call here
+reaches the GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2509_15965_amd import rl_decode as R
+from paper_2509_15965_amd.configs import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rl_decode.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rl_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported():
+    lib = R.lib()
+    names = declared_functions()
+    assert len(names) >= 16
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(R.EXPORTS) == names
+
+
+def cfg_for(name, max_seqs=8, max_ctx=64, max_prefill=64):
+    return R.make_config(WORKLOADS[name].model, max_seqs, max_ctx, max_prefill)
+
+
+def test_kv_bytes_follow_documented_layout():
+    for name in WORKLOADS:
+        m = WORKLOADS[name].model
+        c = cfg_for(name, max_seqs=3, max_ctx=50)
+        cap = 64                                   # 50 rounded up to a multiple of 32
+        es = 4 if m.dtype == "fp32" else 2
+        assert R.kv_bytes(c) == 2 * m.n_layers * 3 * m.n_kv_heads * cap * m.head_dim * es
+
+
+def test_workspace_grows_with_capacity():
+    a = R.workspace_bytes(cfg_for("qwen7b", 8, 64, 64))
+    b = R.workspace_bytes(cfg_for("qwen7b", 512, 5120, 32768))
+    assert 0 < a < b
+    assert b % 256 == 0
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, R.RL_ERR_UNSUPPORTED),
+    ("n_kv_heads", 3, R.RL_ERR_UNSUPPORTED),
+    ("vocab", 1001, R.RL_ERR_UNSUPPORTED),
+    ("dtype", 7, R.RL_ERR_INVALID_ARG),
+    ("max_ctx", 1, R.RL_ERR_INVALID_ARG),
+    ("rms_eps", 0.0, R.RL_ERR_INVALID_ARG),
+    ("rope_theta", 1.0, R.RL_ERR_INVALID_ARG),
+    ("reserved", 1, R.RL_ERR_INVALID_ARG),
+    ("max_seqs", 0, R.RL_ERR_INVALID_ARG),
+])
+def test_invalid_configs_rejected_before_any_device_call(field, value, status):
+    c = cfg_for("tiny")
+    setattr(c, field, value)
+    assert R.kv_bytes(c) == 0
+    assert R.workspace_bytes(c) == 0
+    w = R.Weights(*([256] * 9))
+    h = C.c_void_p(123)
+    st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
+    assert st == status
+    assert not h.value
+
+
+def test_create_validates_pointers_and_sizes_first():
+    lib = R.lib()
+    c = cfg_for("tiny")
+    h = C.c_void_p(1)
+    w = R.Weights(*([256] * 9))
+    assert lib.rl_decode_create(C.byref(c), None, 256, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG
+    w_bad = R.Weights(*([256] * 8 + [0]))
+    assert lib.rl_decode_create(C.byref(c), C.byref(w_bad), 256, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG
+    w_mis = R.Weights(*([256] * 8 + [258]))
+    assert lib.rl_decode_create(C.byref(c), C.byref(w_mis), 256, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG
+    assert lib.rl_decode_create(C.byref(c), C.byref(w), 128, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG
+    small = R.kv_bytes(c) - 1
+    assert lib.rl_decode_create(C.byref(c), C.byref(w), 256, small, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_CAPACITY
+    assert lib.rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, None) == R.RL_ERR_INVALID_ARG
+    assert not h.value
+
+
+def test_null_and_foreign_contexts():
+    lib = R.lib()
+    assert lib.rl_decode_destroy(None) == R.RL_OK
+    assert lib.rl_slot_length(None, 0) == -1
+    sp = R.SampleParams(1, 1.0, 0)
+    assert lib.rl_decode_step(None, 1, None, None, None, None, C.byref(sp), None, None, None) == R.RL_ERR_STATE
+    assert lib.rl_prefill(None, 1, 1, None, None, None, None, None, 0, None, C.byref(sp), None, None, None) == R.RL_ERR_STATE
+    junk = (C.c_uint32 * 64)()
+    assert lib.rl_decode_step(C.addressof(junk), 1, None, None, None, None, C.byref(sp), None, None, None) == R.RL_ERR_STATE
+    assert lib.rl_release_slots(None, 0, None) == R.RL_ERR_STATE
+    assert lib.rl_decode_set_option(None, 1, 0) == R.RL_ERR_STATE
+    assert lib.rl_decode_last_error(None) == b"invalid or destroyed context"
+
+
+def test_status_strings():
+    lib = R.lib()
+    for s in range(6):
+        assert lib.rl_status_string(s)
+    assert lib.rl_status_string(99) == b"unknown status"
+
+
+def test_probe_copy_argument_checks():
+    lib = R.lib()
+    assert lib.rl_probe_copy(None, None, 16, None) == R.RL_ERR_INVALID_ARG
+    assert lib.rl_probe_copy(256, 512, 15, None) == R.RL_ERR_INVALID_ARG
+    assert lib.rl_probe_copy(258, 512, 16, None) == R.RL_ERR_INVALID_ARG

@@ -1,0 +1,293 @@
+"""GPU path vs the CPU oracle, through the C ABI (needs an MI355X).
+
+Sizes here are small enough for the oracle to finish in seconds while
+spanning several GEMM and attention tiles with ragged tails.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL, LOGIT_REL_TOL, LOGP_ABS_TOL, OracleRollout,
+                     build_models, check_token, inject_random_kv, row_rel_err)
+from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
+from paper_2509_15965_amd.inputs import rollout_plan, uniform_tokens
+from paper_2509_15965_amd.rl_decode import RL_OPT_ATTN_CHUNK, Engine
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _i32(a):
+    return torch.as_tensor(np.asarray(a, dtype=np.int32), device=DEV)
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def teacher_forced_run(shape, seed, prompts, group, n_steps, T=1.0, sample_seed=5, max_ctx=None,
+                       embed_rows=None):
+    """Prefill `prompts` (group slots each), then n_steps decode steps that feed
+    seeded forced tokens.  Returns per-step (gpu logits, oracle logits, gpu
+    logp, oracle logp, gpu tokens, oracle sampled tokens)."""
+    w_dev, w_host, om = build_models(shape, seed)
+    n_seq = len(prompts) * group
+    plens = [len(p) for p in prompts]
+    max_ctx = max_ctx or (max(plens) + n_steps + 2)
+    eng = Engine(shape, w_dev, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=sum(plens))
+    slots = list(range(n_seq))
+    uids = [1000 + i for i in range(n_seq)]
+    offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
+    toks = _i32(np.concatenate(prompts))
+    forced = [uniform_tokens(n_seq, shape.vocab, seed + 100 + s) for s in range(n_steps + 1)]
+    out_tok = torch.empty(n_seq, dtype=torch.int32, device=DEV)
+    out_lp = torch.empty(n_seq, dtype=torch.float32, device=DEV)
+    logits_p = torch.empty((len(prompts), shape.vocab), dtype=torch.float32, device=DEV)
+    emb = None if embed_rows is None else embed_rows.to(DEV)
+    eng.prefill(slots, uids, offs, toks, out_tok, out_lp, group=group, forced=_i32(forced[0]),
+                seed=sample_seed, temperature=T, out_logits=logits_p, embeds=emb)
+    torch.cuda.synchronize()
+    emb_host = None
+    if embed_rows is not None:
+        from paper_2509_15965_amd.inputs import to_host_numpy
+        emb_host = to_host_numpy(embed_rows)
+    orc = OracleRollout(om, max_ctx)
+    zo_p = []
+    for p in range(len(prompts)):
+        zo_p.append(orc.prefill(p * group, prompts[p], emb_host))
+        for k in range(1, group):
+            orc.seqs[p * group + k] = orc.seqs[p * group].clone()
+    zg = logits_p.cpu().numpy()
+    zo = np.stack(zo_p)
+    lo = np.array([oracle.sample(zo[i // group].astype(np.float32), T, sample_seed, uids[i], plens[i // group],
+                                 forced=int(forced[0][i]))[1] for i in range(n_seq)])
+    so = [oracle.sample(zo[i // group].astype(np.float32), T, sample_seed, uids[i], plens[i // group])[0]
+          for i in range(n_seq)]
+    res = [(zg, zo, out_lp.cpu().numpy(), lo, out_tok.cpu().numpy(), np.array(so))]
+    logits = torch.empty((n_seq, shape.vocab), dtype=torch.float32, device=DEV)
+    for s in range(1, n_steps + 1):
+        in_tok = _i32(forced[s - 1])
+        eng.step(slots, uids, in_tok, out_tok, out_lp, forced=_i32(forced[s]), seed=sample_seed,
+                 temperature=T, out_logits=logits)
+        torch.cuda.synchronize()
+        zg = logits.cpu().numpy()
+        zo = np.stack([orc.step(i, forced[s - 1][i]) for i in range(n_seq)])
+        pos_new = [orc.length(i) for i in range(n_seq)]
+        lo = np.array([oracle.sample(zo[i].astype(np.float32), T, sample_seed, uids[i], pos_new[i],
+                                     forced=int(forced[s][i]))[1] for i in range(n_seq)])
+        so = [oracle.sample(zo[i].astype(np.float32), T, sample_seed, uids[i], pos_new[i])[0] for i in range(n_seq)]
+        res.append((zg, zo, out_lp.cpu().numpy(), lo, out_tok.cpu().numpy(), np.array(so)))
+    for i in range(n_seq):
+        assert eng.slot_length(i) == plens[i // group] + n_steps
+    eng.close()
+    return res
+
+
+def test_sampler_matches_oracle_on_given_logits():
+    shape = WORKLOADS["tiny"].model
+    w_dev, _, _ = build_models(shape, 3)
+    n, V = 37, shape.vocab
+    eng = Engine(shape, w_dev, max_seqs=64, max_ctx=16, max_prefill_tokens=16)
+    rng = np.random.default_rng(0)
+    z = rng.normal(0, 2.5, size=(n, V)).astype(np.float32)
+    z[5, 100] = z[5, 7] = 30.0                                # exact tie for greedy
+    zt = torch.from_numpy(z).to(DEV)
+    uids = [int(u) for u in rng.integers(0, 2 ** 63, size=n, dtype=np.int64)]
+    pos = [int(p) for p in rng.integers(0, 5000, size=n)]
+    forced = rng.integers(0, V, size=n).astype(np.int32)
+    out_tok = torch.empty(n, dtype=torch.int32, device=DEV)
+    out_lp = torch.empty(n, dtype=torch.float32, device=DEV)
+    for T in (1.0, 0.6, 0.0):
+        for use_forced in (False, True):
+            eng.sample_logits(zt, uids, pos, out_tok, out_lp, seed=0xABCDEF0123, temperature=T,
+                              forced=_i32(forced) if use_forced else None)
+            torch.cuda.synchronize()
+            gt, gl = out_tok.cpu().numpy(), out_lp.cpu().numpy()
+            for i in range(n):
+                ot, ol = oracle.sample(z[i], T, 0xABCDEF0123, uids[i], pos[i],
+                                       forced=int(forced[i]) if use_forced else -1)
+                assert gt[i] == ot, (T, i)
+                assert abs(gl[i] - ol) < 1e-5, (T, i, gl[i], ol)
+    assert out_tok.cpu().numpy()[5] in (7, 100)
+    eng.close()
+
+
+def test_tiny_fp32_rollout_bit_exact_tokens():
+    """The tiny fp32 workload end to end: 2 prompts x 4 samples, 32 prompt
+    tokens, 32 generated tokens, seeded Gumbel noise at T = 1.  Every GPU token
+    equals the oracle's (near ties excused and counted); the oracle follows
+    the GPU's tokens so one excused tie does not end the comparison."""
+    wl = WORKLOADS["tiny"]
+    shape = wl.model
+    plan = rollout_plan(wl)
+    w_dev, _, om = build_models(shape, wl.seed)
+    G, P = wl.group, wl.n_prompts
+    n = P * G
+    max_ctx = 64
+    eng = Engine(shape, w_dev, max_seqs=n, max_ctx=max_ctx, max_prefill_tokens=64)
+    prompts = plan["prompts"]
+    offs = np.concatenate([[0], np.cumsum([len(p) for p in prompts])]).astype(np.int32)
+    uids = [int(u) for u in plan["uids"]]
+    slots = list(range(n))
+    seed, T = 777, wl.temperature
+    out_tok = torch.empty(n, dtype=torch.int32, device=DEV)
+    out_lp = torch.empty(n, dtype=torch.float32, device=DEV)
+    lg_p = torch.empty((P, shape.vocab), dtype=torch.float32, device=DEV)
+    lg = torch.empty((n, shape.vocab), dtype=torch.float32, device=DEV)
+    eng.prefill(slots, uids, offs, _i32(np.concatenate(prompts)), out_tok, out_lp, group=G, seed=seed,
+                temperature=T, out_logits=lg_p)
+    torch.cuda.synchronize()
+    orc = {}
+    excused = []
+    toks = out_tok.cpu().numpy().copy()
+    lps = out_lp.cpu().numpy().copy()
+    zg = lg_p.cpu().numpy()
+    for i in range(n):
+        s = om.new_seq(max_ctx)
+        for t in prompts[i // G]:
+            z = s.forward(int(t))
+        orc[i] = s
+        assert row_rel_err(zg[i // G], z) < F32_LOGIT_REL_TOL
+        assert check_token(int(toks[i]), z, T, seed, uids[i], len(prompts[i // G]), excused), (i, 0)
+        _, ol = oracle.sample(z.astype(np.float32), T, seed, uids[i], len(prompts[i // G]), forced=int(toks[i]))
+        assert abs(lps[i] - ol) < F32_LOGP_ABS_TOL
+    all_tokens = [toks.copy()]
+    for step in range(1, wl.response_cap):
+        eng.step(slots, uids, out_tok.clone(), out_tok, out_lp, seed=seed, temperature=T, out_logits=lg)
+        torch.cuda.synchronize()
+        new = out_tok.cpu().numpy().copy()
+        lps = out_lp.cpu().numpy()
+        zg = lg.cpu().numpy()
+        for i in range(n):
+            z = orc[i].forward(int(toks[i]))
+            assert row_rel_err(zg[i], z) < F32_LOGIT_REL_TOL, (i, step)
+            assert check_token(int(new[i]), z, T, seed, uids[i], orc[i].length, excused), (i, step)
+            _, ol = oracle.sample(z.astype(np.float32), T, seed, uids[i], orc[i].length, forced=int(new[i]))
+            assert abs(lps[i] - ol) < F32_LOGP_ABS_TOL
+        toks = new
+        all_tokens.append(new)
+    assert len(excused) <= 2, excused
+    # samples of one prompt differ (uid-keyed noise) though their prefill logits are equal
+    first = all_tokens[0]
+    assert len(set(first[:G].tolist())) > 1 or len(set(first[G:].tolist())) > 1
+    eng.close()
+
+
+@pytest.mark.parametrize("shape", [
+    # GQA group 4, head_dim 128, ragged hidden/ffn/vocab tiles
+    ModelShape(2, 320, 8, 2, 128, 712, 1000, 1e-6, 1e6, "bf16"),
+    # MHA, head_dim 64
+    ModelShape(2, 256, 4, 4, 64, 520, 776, 1e-5, 1e4, "bf16"),
+    # group 7 (the 7B shape's ratio), head_dim 128
+    ModelShape(1, 448, 7, 1, 128, 384, 512, 1e-6, 1e6, "bf16"),
+])
+def test_bf16_prefill_and_decode_teacher_forced(shape):
+    rng = np.random.default_rng(11)
+    lens = [1, 7, 33, 70]
+    prompts = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in lens]
+    res = teacher_forced_run(shape, 21, prompts, group=2, n_steps=6, T=1.0)
+    agree = total = 0
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+        agree += int((tg == to).sum())
+        total += len(tg)
+    assert agree >= 0.8 * total          # sampled tokens mostly agree despite bf16 round-off
+
+
+def test_bf16_prefill_with_embedding_rows_and_temperature():
+    shape = ModelShape(2, 256, 4, 2, 64, 512, 640, 1e-5, 1e4, "bf16")
+    from paper_2509_15965_amd.inputs import patch_rows
+    rows = patch_rows(12, shape.hidden, 3)
+    rng = np.random.default_rng(4)
+    p0 = np.concatenate([-(np.arange(12) + 1), rng.integers(0, shape.vocab, size=5)]).astype(np.int32)
+    p1 = rng.integers(0, shape.vocab, size=9).astype(np.int32)
+    res = teacher_forced_run(shape, 8, [p0, p1], group=3, n_steps=3, T=0.6, embed_rows=rows)
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+
+
+def test_split_kv_long_context_matches_oracle_and_any_chunk():
+    """Injected caches up to 3000 positions: the split-KV decode step matches
+    the oracle, and every chunk size gives the same result up to bf16
+    probability rounding."""
+    shape = ModelShape(2, 256, 8, 2, 128, 512, 1024, 1e-6, 1e6, "bf16")
+    w_dev, _, om = build_models(shape, 31)
+    lengths = [3000, 1, 31, 32, 33, 777]
+    n = len(lengths)
+    eng = Engine(shape, w_dev, max_seqs=n, max_ctx=3008, max_prefill_tokens=8)
+    slots = list(range(n))
+    uids = list(range(n))
+    tok = uniform_tokens(n, shape.vocab, 2)
+    results = {}
+    for chunk in (0, 32, 64, 256, 4096):
+        seqs = inject_random_kv(eng, om, slots, lengths, seed=99)
+        eng.set_option(RL_OPT_ATTN_CHUNK, chunk)
+        logits = torch.empty((n, shape.vocab), dtype=torch.float32, device=DEV)
+        ot = torch.empty(n, dtype=torch.int32, device=DEV)
+        ol = torch.empty(n, dtype=torch.float32, device=DEV)
+        eng.step(slots, uids, _i32(tok), ot, ol, seed=1, out_logits=logits)
+        torch.cuda.synchronize()
+        results[chunk] = logits.cpu().numpy()
+        if chunk == 0:
+            zo = np.stack([seqs[s].forward(int(tok[s])) for s in slots])
+            assert row_rel_err(results[0], zo) < LOGIT_REL_TOL
+    for chunk, z in results.items():
+        assert row_rel_err(z, results[4096]) < 1e-2, chunk
+    eng.close()
+
+
+def test_decode_is_deterministic():
+    shape = ModelShape(2, 256, 4, 2, 64, 512, 512, 1e-6, 1e6, "bf16")
+    w_dev, _, _ = build_models(shape, 5)
+    outs = []
+    for _ in range(2):
+        eng = Engine(shape, w_dev, max_seqs=4, max_ctx=64, max_prefill_tokens=64)
+        toks = _i32(uniform_tokens(40, shape.vocab, 1))
+        ot = torch.empty(4, dtype=torch.int32, device=DEV)
+        ol = torch.empty(4, dtype=torch.float32, device=DEV)
+        lg = torch.empty((4, shape.vocab), dtype=torch.float32, device=DEV)
+        eng.prefill([0, 1, 2, 3], [9, 8, 7, 6], [0, 10, 40], toks, ot, ol, group=2, seed=3)
+        run = []
+        for _ in range(5):
+            eng.step([0, 1, 2, 3], [9, 8, 7, 6], ot.clone(), ot, ol, seed=3, out_logits=lg)
+            run.append((ot.cpu().numpy().copy(), ol.cpu().numpy().copy(), lg.cpu().numpy().copy()))
+        outs.append(run)
+        eng.close()
+    for a, b in zip(*outs):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+def test_step_rejects_bad_arguments_without_side_effects():
+    shape = ModelShape(1, 64, 2, 1, 64, 64, 64, 1e-6, 1e4, "bf16")
+    w_dev, _, _ = build_models(shape, 1)
+    eng = Engine(shape, w_dev, max_seqs=4, max_ctx=8, max_prefill_tokens=8)
+    ot = torch.empty(4, dtype=torch.int32, device=DEV)
+    ol = torch.empty(4, dtype=torch.float32, device=DEV)
+    t = _i32([1, 2, 3, 4])
+    from paper_2509_15965_amd.rl_decode import RLError
+    with pytest.raises(RLError) as e:
+        eng.step([0, 0], [1, 2], t, ot, ol)                    # duplicate slot
+    assert e.value.status == 1
+    with pytest.raises(RLError) as e:
+        eng.step([0, 9], [1, 2], t, ot, ol)                    # slot out of range
+    assert e.value.status == 1
+    with pytest.raises(RLError) as e:
+        eng.step([0], [1], t, ot, ol, temperature=-1.0)
+    assert e.value.status == 1
+    eng.set_lengths([1], [8])
+    with pytest.raises(RLError) as e:
+        eng.step([1], [1], t, ot, ol)                          # full slot
+    assert e.value.status == 3
+    assert eng.slot_length(0) == 0 and eng.slot_length(1) == 8
+    with pytest.raises(RLError) as e:
+        eng.prefill([0], [1], [0, 8], t, ot, ol)               # prompt of max_ctx tokens
+    assert e.value.status == 3
+    eng.close()
