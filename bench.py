@@ -1,0 +1,249 @@
+"""Rollout benchmark: batched generation on one MI355X at the Qwen2.5-7B shape.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+A step is one decode step of the whole hot path (embedding, 28 layers of
+RMSNorm / q|k|v projection + RoPE + KV append / split-KV attention /
+o-projection / SwiGLU MLP, final norm, LM head, log-softmax + Gumbel-max
+sampling + log-probability) over the sequences still generating.  The
+workload is the GRPO rollout of 32 prompts x 16 samples (uniform prompt
+lengths in [256, 1024], lognormal response lengths around 1500 capped at
+4096) on a randomly initialised bf16 decoder; by default every decode step of
+the rollout is timed (K = longest response - 1), after W warm-up steps of a
+separate warm-up rollout.  Inputs and weights are resident in HBM before
+timing starts; the prefill that opens the rollout is timed and reported
+separately.
+
+Prints one JSON line: generated tokens/s over the timed steps, the roofline
+of the dominant kernel measured with HIP events on the library's stream, and
+the CPU oracle timed on a bounded sample on this host.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0, help="decode steps to time (0 = the whole rollout)")
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="qwen7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true",
+                    help="time every kernel class (adds event overhead; diagnostics only)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def cpu_baseline(shape, weights, seconds: float):
+    """Oracle decode tokens/s on this host's cores: one new token per sequence
+    at the rollout's mean starting context, until `seconds` have elapsed."""
+    import oracle
+    from paper_2509_15965_amd.inputs import weights_to_host
+    cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(cores)
+    host = weights_to_host(weights)
+    om = oracle.OracleModel(shape.as_dict(), host, oracle.MODE_BF16)
+    ctx = 640
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        s = om.new_seq(ctx + 1)
+        s.set_length(ctx)            # cache rows are zeros: the arithmetic per token is the same
+        s.forward(1 + n)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 256:
+            break
+    del om, host
+    return {"value": n / el, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n} decode tokens of the 7B-shape decoder at context {ctx + 1} "
+                      f"(one token per sequence, fp64 accumulation), {el:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights, rollout_plan
+    from paper_2509_15965_amd.rl_decode import KERNEL_CLASSES, RL_OPT_PROFILE, Engine
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    plan = rollout_plan(wl)
+    P, G = wl.n_prompts, wl.group
+    n_seq = P * G
+    plens = plan["prompt_lens"]
+    resp = plan["response_lens"]
+    weights = make_weights(shape, wl.seed, device=dev)
+    max_ctx = int(plens.max() + resp.max())
+    eng = Engine(shape, weights, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=int(plens.sum()),
+                 device=dev)
+    stream = eng.stream
+
+    # sequences ordered by response length (longest first): the active set of
+    # decode step t is always a prefix of this order
+    seq_prompt = np.repeat(np.arange(P), G)
+    order = np.argsort(-resp, kind="stable")
+    slot_of = np.empty(n_seq, dtype=np.int64)
+    slot_of[order] = np.arange(n_seq)
+    uids_sorted = plan["uids"][order].astype(np.uint64)
+    resp_sorted = resp[order]
+    # prefill wants slots grouped by prompt: slots[p*G + k] = slot of sample k of prompt p
+    pre_slots = slot_of.astype(np.int32)
+    pre_uids = plan["uids"].astype(np.uint64)
+    offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
+    prompt_tok = torch.as_tensor(np.concatenate(plan["prompts"]), dtype=torch.int32, device=dev)
+    max_steps = int(resp.max()) - 1
+    active = np.array([(resp_sorted > t + 1).sum() for t in range(max_steps)], dtype=np.int64)
+    steps = max_steps if args.steps <= 0 else min(args.steps, max_steps)
+    seed, T = 20250919, wl.temperature
+
+    toks = torch.zeros((max_steps + 1, n_seq), dtype=torch.int32, device=dev)
+    logps = torch.zeros((max_steps + 1, n_seq), dtype=torch.float32, device=dev)
+    first_tok = torch.empty(n_seq, dtype=torch.int32, device=dev)
+    first_lp = torch.empty(n_seq, dtype=torch.float32, device=dev)
+    slots_sorted = np.arange(n_seq, dtype=np.int32)
+
+    def prefill():
+        eng.release(slots_sorted)
+        eng.prefill(pre_slots, pre_uids, offs, prompt_tok, first_tok, first_lp, group=G, seed=seed,
+                    temperature=T)
+        # row 0 of the token table in slot order
+        toks[0].index_copy_(0, torch.as_tensor(pre_slots.astype(np.int64), device=dev), first_tok)
+        logps[0].index_copy_(0, torch.as_tensor(pre_slots.astype(np.int64), device=dev), first_lp)
+
+    def decode(t):
+        n = int(active[t])
+        eng.step(slots_sorted[:n], uids_sorted[:n], toks[t, :n], toks[t + 1, :n], logps[t + 1, :n],
+                 seed=seed, temperature=T)
+        return n
+
+    # ---- warm-up rollout (untimed) ----
+    prefill()
+    for t in range(min(args.warmup, max_steps)):
+        decode(t)
+    torch.cuda.synchronize()
+
+    # ---- optional per-class breakdown on a few sampled steps (untimed) ----
+    breakdown = None
+    if args.breakdown:
+        eng.reset_stats()
+        eng.set_option(RL_OPT_PROFILE, -1)
+        prefill()
+        for t in range(min(64, max_steps)):
+            decode(t)
+        st = eng.kernel_stats()
+        eng.set_option(RL_OPT_PROFILE, 0)
+        breakdown = {k: {"ms": round(v["total_ms"], 3), "launches": v["launches"],
+                         "GB/s": round(v["alg_bytes"] / (v["total_ms"] * 1e6), 1) if v["total_ms"] > 0 else None}
+                     for k, v in st.items() if v["launches"]}
+        print(json.dumps({"breakdown_first_64_steps": breakdown}), file=sys.stderr, flush=True)
+
+    # ---- timed rollout ----
+    prof_classes = ("attention", "gemm_gate_up", "gemm_down", "gemm_lm_head", "gemm_qkv", "gemm_o")
+    mask = 0
+    for c in prof_classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    t_pf0 = time.perf_counter()
+    prefill()
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t_pf0
+    eng.reset_stats()
+    eng.set_option(RL_OPT_PROFILE, mask)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    gen = 0
+    last_print = t0
+    for t in range(steps):
+        gen += decode(t)
+        now = time.perf_counter()
+        if now - last_print > 20.0:
+            print(f"[bench] step {t + 1}/{steps}", file=sys.stderr, flush=True)
+            last_print = now
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    stats = eng.kernel_stats()
+    eng.set_option(RL_OPT_PROFILE, 0)
+
+    # dominant kernel (largest measured time among the timed classes)
+    dom = max(prof_classes, key=lambda c: stats[c]["total_ms"])
+    d = stats[dom]
+    avg_ms = d["total_ms"] / max(1, d["launches"])
+    gbs = d["alg_bytes"] / (d["total_ms"] * 1e-3) / 1e9
+    tflops = d["alg_flops"] / (d["total_ms"] * 1e-3) / 1e12
+    intensity = d["alg_flops"] / max(1.0, d["alg_bytes"])
+    if intensity > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    roof.update({"kernel": dom, "launches": d["launches"], "avg_launch_ms": round(avg_ms, 5),
+                 "alg_bytes_per_launch": round(d["alg_bytes"] / max(1, d["launches"]))})
+
+    all_bytes = sum(v["alg_bytes"] for k, v in stats.items() if k not in ("splitk_reduce", "attn_combine"))
+    prompt_tokens = int(plens.sum())
+    gen_total = gen
+    value = gen_total / wall
+    out = {
+        "metric": "rollout tokens/sec (1 GPU) at 7B shape; decode-step HBM GB/s vs peak",
+        "value": round(value, 1),
+        "unit": "generated tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / max(1, steps), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights and uniform prompt tokens)",
+        "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped decoder (28 layers, hidden 3584, 28 q / 4 kv heads, "
+                               f"ffn 18944, vocab 152064); {P} prompts x {G} samples, prompts U[{wl.prompt_len[0]},"
+                               f"{wl.prompt_len[1]}], lognormal responses (median {wl.response_median}, sigma "
+                               f"{wl.response_sigma}, cap {wl.response_cap})",
+                   "n_seqs": n_seq, "prompt_tokens": prompt_tokens,
+                   "generated_tokens_timed": gen_total, "decode_steps_in_rollout": max_steps},
+        "gpu_ms_timed": round(gpu_ms, 2),
+        "decode_step_alg_GBps": round(all_bytes / (gpu_ms * 1e-3) / 1e9, 1) if steps == max_steps else None,
+        "prefill_s": round(prefill_s, 4),
+        "paper_style_tokens_per_s": round((prompt_tokens + gen_total + n_seq) / (wall + prefill_s), 1)
+        if steps == max_steps else None,
+        "roofline": roof,
+    }
+    if breakdown:
+        out["breakdown_first_64_steps"] = breakdown
+    eng.close()
+    del eng
+    torch.cuda.synchronize()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, weights, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -106,7 +106,7 @@ struct rl_decode_ctx {
     bool stage_used[kStages] = {false, false, false};
     int stage_next = 0;
     int64_t opt_chunk = 0;
-    bool profile = false;
+    uint32_t profile = 0;             // bit mask over kernel classes
     struct Pending { int kc; hipEvent_t a, b; };
     std::vector<Pending> pending;
     std::vector<hipEvent_t> ev_pool;
@@ -162,7 +162,9 @@ hipError_t harvest(rl_decode_ctx* c) {
 struct Prof {
     rl_decode_ctx* c; int kc; hipEvent_t a = nullptr;
     Prof(rl_decode_ctx* c_, int kc_) : c(c_), kc(kc_) {
-        if (c->profile && (a = get_event(c))) (void)hipEventRecord(a, c->stream);
+        if ((c->profile >> kc) & 1u) {
+            if ((a = get_event(c))) (void)hipEventRecord(a, c->stream);
+        }
     }
     void done(double bytes, double flops) {
         c->stats[kc].launches += 1;
@@ -892,8 +894,9 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
             ctx->opt_chunk = value;
             return RL_OK;
         case RL_OPT_PROFILE:
-            if (value != 0 && value != 1) return fail(ctx, RL_ERR_INVALID_ARG, "profile must be 0 or 1");
-            ctx->profile = value == 1;
+            if (value < -1 || value >= (int64_t(1) << RL_K_COUNT))
+                return fail(ctx, RL_ERR_INVALID_ARG, "profile must be a class bit mask or -1");
+            ctx->profile = value == -1 ? ((1u << RL_K_COUNT) - 1u) : static_cast<uint32_t>(value);
             return RL_OK;
         default:
             return fail(ctx, RL_ERR_INVALID_ARG, "unknown option");

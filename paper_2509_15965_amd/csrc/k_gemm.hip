@@ -8,7 +8,8 @@
 // per workgroup row.  Small batches (M <= 64) use one 16/32/64-row M tile per
 // workgroup and split K across workgroups when the weight alone cannot fill
 // the 256 CUs; fp32 partials are then summed in a fixed order by
-// splitk_reduce (deterministic).
+// splitk_reduce (deterministic).  Larger batches go to the LDS-tiled kernel
+// (k_gemm_lds.hip).
 //
 // fp32: a plain LDS-tiled VALU kernel (the tiny fp32 decoder only).
 #include "rl_device.h"
@@ -20,27 +21,49 @@ const GemmShape kGemmShapes[kNumGemmShapes] = {
     {1, 4, 1, 4},   // M <= 16 : 16 x 256 weight rows per workgroup
     {2, 4, 1, 4},   // M <= 32 : 32 x 256
     {4, 4, 1, 4},   // M <= 64 : 64 x 256
-    {4, 4, 2, 2},   // M >  64 : 128 x 128
 };
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     GemmPlan p{};
-    p.variant = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : 3;
-    const GemmShape& s = kGemmShapes[p.variant];
-    const int BM = 16 * s.MT * s.WR;
-    const int BNw = 16 * s.NT * s.WC;
     const int n_out = epi == EPI_SWIGLU ? F : Nw;
-    const int BNo = epi == EPI_SWIGLU ? BNw / 2 : BNw;
-    p.grid_x = ceil_div(n_out, BNo);
-    p.grid_y = ceil_div(M, BM);
+    long tiles;
+    long target;
+    if (M > 64) {
+        // LDS-tiled kernels; split K only when the tiles cannot fill the CUs
+        int BM, BN;
+        if (M > 128 && K % 32 == 0) {
+            p.variant = kLdsVariant256x256; BM = 256; BN = 256;
+        } else if (K % 32 == 0) {
+            p.variant = kDmaVariant128; BM = 128; BN = 256;
+        } else {
+            p.variant = M > 128 ? kLdsVariant256 : kLdsVariant128; BM = M > 128 ? 256 : 128; BN = 128;
+        }
+        const int bno = epi == EPI_SWIGLU ? BN / 2 : BN;
+        p.grid_x = ceil_div(n_out, bno);
+        p.grid_y = ceil_div(M, BM);
+        tiles = static_cast<long>(p.grid_x) * p.grid_y;
+        target = 240;
+    } else {
+        p.variant = M <= 16 ? 0 : M <= 32 ? 1 : 2;
+        const GemmShape& s = kGemmShapes[p.variant];
+        const int BM = 16 * s.MT * s.WR;
+        const int BNw = 16 * s.NT * s.WC;
+        const int BNo = epi == EPI_SWIGLU ? BNw / 2 : BNw;
+        p.grid_x = ceil_div(n_out, BNo);
+        p.grid_y = ceil_div(M, BM);
+        tiles = static_cast<long>(p.grid_x) * p.grid_y;
+        target = 1024;
+    }
     int S = 1;
-    const long tiles = static_cast<long>(p.grid_x) * p.grid_y;
-    while (tiles * S * 2 <= 1024 && ceil_div(K, 2 * S) >= 256 &&
+    while (tiles * S * 2 <= target && ceil_div(K, 2 * S) >= 256 &&
            static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
         S *= 2;
-    int ks = ceil_div(ceil_div(K, S), 64) * 64;
+    if (M > 64 && tiles * S < target && ceil_div(K, 2 * S) >= 256 &&
+        static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
+        S *= 2;
+    const int ks = ceil_div(ceil_div(K, S), 64) * 64;   // multiple of 64 (and so of 32)
     p.ksplit = ks;
     p.splits = ceil_div(K, ks);
     return p;
@@ -206,7 +229,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s)
         case 0: return launch_shape<1, 4, 1, 4>(a, p, s);
         case 1: return launch_shape<2, 4, 1, 4>(a, p, s);
         case 2: return launch_shape<4, 4, 1, 4>(a, p, s);
-        default: return launch_shape<4, 4, 2, 2>(a, p, s);
+        default: return launch_gemm_bf16_lds(a, p, s);
     }
 }
 

@@ -63,11 +63,15 @@ struct GemmPlan {
 // Tile shapes of the bf16 MFMA GEMM: wave tile (16*MT) x (16*NT) weight rows,
 // 4 waves per workgroup arranged WR x WC.
 struct GemmShape { int MT, NT, WR, WC; };
-constexpr int kNumGemmShapes = 4;
+constexpr int kNumGemmShapes = 3;           // direct-load shapes for M <= 64
 extern const GemmShape kGemmShapes[kNumGemmShapes];
+constexpr int kLdsVariant128 = 3;           // LDS-tiled 128 x 128 (64 < M <= 128)
+constexpr int kLdsVariant256 = 4;           // LDS-tiled 256 x 128 (M > 128)
+constexpr int kLdsVariant256x256 = 5;       // direct-to-LDS 256 x 256 (M > 128, K % 64 == 0)
+constexpr int kDmaVariant128 = 6;           // direct-to-LDS 128 x 128 (64 < M <= 128, K % 64 == 0)
 
 constexpr int kMaxSplits = 32;
-constexpr size_t kPartCapFloats = size_t(16) << 20;   // split-K partials budget
+constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget
 
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F);
 
@@ -79,6 +83,7 @@ hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int
                           const void* g, float eps, void* out, hipStream_t s);
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);   // writes a.out_f32 [M][Nw]
 hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const float* partial,
                                 hipStream_t s);

@@ -291,3 +291,16 @@ def test_step_rejects_bad_arguments_without_side_effects():
         eng.prefill([0], [1], [0, 8], t, ot, ol)               # prompt of max_ctx tokens
     assert e.value.status == 3
     eng.close()
+
+
+@pytest.mark.parametrize("n_prompts,plen", [(100, 3), (140, 4), (9, 70)])
+def test_large_batch_gemm_tiles_match_oracle(n_prompts, plen):
+    """Batches above 64 rows take the LDS-tiled GEMM (128- and 256-row tiles,
+    split K for the narrow matrices) in both prefill and decode."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1096, 1032, 1e-6, 1e6, "bf16")
+    rng = np.random.default_rng(n_prompts)
+    prompts = [rng.integers(0, shape.vocab, size=plen).astype(np.int32) for _ in range(n_prompts)]
+    res = teacher_forced_run(shape, 40 + n_prompts, prompts, group=1, n_steps=2, T=1.0)
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
