@@ -11,7 +11,8 @@
 // positions t0 + 8q .. t0 + 8q + 7; those eight probabilities are exactly
 // the lane's B operand of the P.V product, and the matching A operand is one
 // 16-byte load from the V cache's 8-position blocks.  No LDS, no transposes.
-// Online softmax in the exp2 domain, fp32 state.  A work item that covers
+// Online softmax in the exp2 domain, fp32 state; the probabilities enter the
+// P.V MFMA as a bf16 hi/lo pair, so they are not rounded to bf16.  A work item that covers
 // all keys of its tokens writes the normalised output; otherwise it writes
 // (max, sum, unnormalised output) partials that attn_combine merges.
 //
@@ -112,24 +113,32 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restri
         const float m_new = fmaxf(m, mx);
         const float m_use = m_new == -INFINITY ? 0.0f : m_new;
         const float alpha = exp2f(m - m_use);
+        // probabilities as a bf16 pair hi + lo (hi = rne(p), lo = rne(p - hi)):
+        // the P.V product then carries ~16 significant bits of p, so the
+        // only storage rounding left is the one of the attention output
         float psum = 0.0f;
-        uint32_t pw[4];
+        uint32_t ph[4], pl[4];
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const float p0 = exp2f(sv[2 * w] - m_use);
             const float p1 = exp2f(sv[2 * w + 1] - m_use);
             psum += p0 + p1;
-            pw[w] = static_cast<uint32_t>(f32_to_bf16(p0)) | (static_cast<uint32_t>(f32_to_bf16(p1)) << 16);
+            const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+            const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
+            ph[w] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+            pl[w] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
         }
         l = l * alpha + psum;
         m = m_new;
-        const u32x4 pf = {pw[0], pw[1], pw[2], pw[3]};
+        const u32x4 pfh = {ph[0], ph[1], ph[2], ph[3]};
+        const u32x4 pfl = {pl[0], pl[1], pl[2], pl[3]};
         const int nvalid = hi - pb;   // keys past the chunk end carry no data
 #pragma unroll
         for (int i = 0; i < DT; ++i) {
             u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
             o[i] = o[i] * alpha;
-            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pf), o[i]);
+            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
+            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
         }
     }
     l += __shfl_xor(l, 16, 64);

@@ -41,9 +41,11 @@ def weight_shapes(m: ModelShape) -> Dict[str, tuple]:
     }
 
 
-def make_weights(m: ModelShape, seed: int, device="cpu") -> Dict[str, torch.Tensor]:
+def make_weights(m: ModelShape, seed: int, device="cpu", resid_scaled: bool = False) -> Dict[str, torch.Tensor]:
     """Random-init decoder weights on `device`, drawn one layer slice at a time
-    (bounded temporary memory) from a single seeded generator."""
+    (bounded temporary memory) from a single seeded generator.  With
+    resid_scaled, the two residual-branch output projections (w_o, w_down)
+    use std 0.02 / sqrt(2 * n_layers) instead of 0.02."""
     dt = torch_dtype(m)
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
@@ -53,9 +55,12 @@ def make_weights(m: ModelShape, seed: int, device="cpu") -> Dict[str, torch.Tens
         if name.endswith("norm"):
             t.fill_(1.0)
         elif len(shp) == 3:
+            std = INIT_STD
+            if resid_scaled and name in ("w_o", "w_down"):
+                std = INIT_STD / math.sqrt(2.0 * m.n_layers)
             for l in range(shp[0]):
                 r = torch.randn(shp[1:], generator=gen, device=device, dtype=torch.float32)
-                t[l].copy_(r.mul_(INIT_STD))
+                t[l].copy_(r.mul_(std))
                 del r
         else:
             rows = shp[0]
