@@ -244,7 +244,9 @@ int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot);
 
 typedef enum rl_option {
     RL_OPT_ATTN_CHUNK = 1,   /* positions per split-KV chunk: 0 = automatic,
-                                else a multiple of 32 in [32, 65536]          */
+                                else a multiple of 32 in [32, 65536]; doubled
+                                as needed so no sequence has more than 64
+                                chunks                                         */
     RL_OPT_PROFILE = 2       /* bit mask over rl_kernel_class: launches of the
                                 selected classes are timed with HIP events on
                                 the context's stream; 0 = off (default),

@@ -32,6 +32,7 @@ struct Layout {
     size_t kv_bytes = 0, ws_bytes = 0;
     size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
     size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
+    size_t off_cnt = 0, cnt_bytes = 0, off_spart = 0;
     size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
 };
 
@@ -71,7 +72,7 @@ Layout make_layout(const rl_model_config& c) {
     if (c.dtype == RL_DTYPE_FP32) L.part_floats = std::max(L.part_floats, R * std::max(H, 2 * F));
     L.apart_floats = static_cast<size_t>(kPartItems) * c.n_kv_heads * 16 * (c.head_dim + 2);
     L.meta_bytes = 4 * (3 * R + 4 * static_cast<size_t>(c.max_seqs)) + 8 * static_cast<size_t>(c.max_seqs) +
-                   sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + sizeof(RowCombine) * R + 4096;
+                   sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + 4 * R + 4096;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     L.off_x = take(R * H * 4);
@@ -85,6 +86,10 @@ Layout make_layout(const rl_model_config& c) {
     L.off_logits = take(static_cast<size_t>(c.max_seqs) * V * 4);
     L.off_rope = take(static_cast<size_t>(L.cap) * (c.head_dim / 2) * 2 * 4);
     L.off_meta = take(L.meta_bytes);
+    // sampler completion counters (one per row): zero between launches
+    L.cnt_bytes = 4 * static_cast<size_t>(c.max_seqs);
+    L.off_cnt = take(L.cnt_bytes);
+    L.off_spart = take(sizeof(SamplePart) * static_cast<size_t>(c.max_seqs) * kSampleMaxChunks);
     L.ws_bytes = o;
     return L;
 }
@@ -116,6 +121,8 @@ struct rl_decode_ctx {
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
     uint8_t* kslab() const { return kv; }
     uint8_t* vslab() const { return kv + lay.kv_bytes / 2; }
+    int* sample_counters() const { return reinterpret_cast<int*>(ws + lay.off_cnt); }
+    SamplePart* sample_parts() const { return reinterpret_cast<SamplePart*>(ws + lay.off_spart); }
     bool bf16() const { return cfg.dtype == RL_DTYPE_BF16; }
 };
 
@@ -231,9 +238,9 @@ struct Fwd {
     const int32_t* row_slot = nullptr;      // fp32 attention: slot each row reads
     const AttnItem* items = nullptr;
     int n_items = 0;
-    const RowCombine* rowc = nullptr;
-    bool any_combine = false;
     int n_partial_items = 0;
+    const int32_t* split_blocks = nullptr;   // first item of every split block
+    int n_split_blocks = 0;
     double attn_kv_positions = 0;           // algorithmic KV positions read per kv-head
     double attn_score_positions = 0;        // sum over rows of keys attended
     const int32_t* final_sel = nullptr;     // rows fed to the LM head (nullptr: all)
@@ -250,9 +257,14 @@ struct Fwd {
     float* out_logp = nullptr;
 };
 
+// Y = A . W^T with the given epilogue.  When the plan splits K, fp32 partials
+// land in the split-K buffer: SwiGLU and plain fp32 outputs are reduced here;
+// with `defer` set (q|k|v and residual projections) *splits reports the slice
+// count and the caller reduces.  A residual GEMM with one split adds into x
+// directly (bf16); the fp32 model always goes through the partial buffer.
 rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void* W, int M, int Nw,
                    int K, int epi, float* out_f32, int ldo, float* resid, int ldr, void* act,
-                   int ld_act) {
+                   int ld_act, bool defer, int* splits) {
     const rl_model_config& cf = c->cfg;
     GemmArgs a{};
     a.A = A; a.lda = lda; a.W = W; a.ldw = K; a.M = M; a.Nw = Nw; a.K = K; a.epi = epi;
@@ -265,6 +277,7 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
     double bytes = es * Nw * K + es * M * K + out_bytes;
     double flops = 2.0 * M * Nw * K;
     hipError_t e;
+    *splits = 0;
     if (c->bf16()) {
         GemmPlan p = plan_gemm_bf16(M, Nw, K, epi, cf.ffn);
         {
@@ -274,6 +287,10 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
             pr.done(bytes, flops);
         }
         if (p.splits > 1) {
+            if (defer) {
+                *splits = p.splits;
+                return RL_OK;
+            }
             Prof pr(c, RL_K_SPLITK_REDUCE);
             e = launch_splitk_reduce(DT_BF16, a, p.splits, a.partial, c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "split-K reduce launch");
@@ -281,7 +298,6 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
         }
         return RL_OK;
     }
-    // fp32 model: plain GEMM into the output (F32) or into the partial buffer
     GemmArgs g = a;
     if (epi != EPI_F32) { g.out_f32 = a.partial; g.ldo = Nw; }
     {
@@ -289,6 +305,10 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
         e = launch_gemm_f32(g, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "gemm launch");
         pr.done(bytes, flops);
+    }
+    if (epi == EPI_RESID && defer) {
+        *splits = 1;
+        return RL_OK;
     }
     if (epi != EPI_F32) {
         Prof pr(c, RL_K_SPLITK_REDUCE);
@@ -299,6 +319,19 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
     return RL_OK;
 }
 
+// Sum `splits` fp32 slices of the split-K buffer (fixed order) into out (F32)
+// or into the residual x (RESID), spread over many workgroups.
+rl_status reduce_splits(rl_decode_ctx* c, int epi, int M, int N, int splits, float* out, int ldo, float* resid) {
+    GemmArgs a{};
+    a.M = M; a.Nw = N; a.epi = epi; a.out_f32 = out; a.ldo = ldo; a.resid = resid; a.ldr = N; a.F = c->cfg.ffn;
+    Prof pr(c, RL_K_SPLITK_REDUCE);
+    hipError_t e = launch_splitk_reduce(c->bf16() ? DT_BF16 : DT_F32, a, splits, c->wsp<float>(c->lay.off_part),
+                                        c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "split-K reduce launch");
+    pr.done(4.0 * splits * M * N + (epi == EPI_RESID ? 8.0 : 4.0) * M * N, 0.0);
+    return RL_OK;
+}
+
 rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
     const rl_model_config& cf = c->cfg;
     const Layout& L = c->lay;
@@ -306,6 +339,7 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
     const int H = cf.hidden, Hq = cf.n_q_heads, Hkv = cf.n_kv_heads, D = cf.head_dim, F = cf.ffn;
     const int HqD = Hq * D;
     const double es = L.es;
+    const float eps = static_cast<float>(cf.rms_eps);
     float* x = c->wsp<float>(L.off_x);
     void* h = c->ws + L.off_h;
     float* qkv = c->wsp<float>(L.off_qkv);
@@ -317,35 +351,43 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
     const int cs_stride = L.cap * (D / 2);
     hipError_t e;
     const int n = f.rows;
+    const size_t esz = static_cast<size_t>(L.es);
+    auto lw = [&](const void* base, int l, size_t per_layer) {
+        return static_cast<const uint8_t*>(base) + static_cast<size_t>(l) * per_layer * esz;
+    };
 
-    {
+
+    {   // embedding, fused with the first layer's attention norm
         Prof pr(c, RL_K_EMBED);
-        e = launch_embed(dt, f.tok, n, c->w.embed, cf.vocab,
-                         f.embeds, f.n_embed_rows, H, x, c->stream);
+        e = launch_embed(dt, f.tok, n, c->w.embed, cf.vocab, f.embeds, f.n_embed_rows, H, x,
+                         c->w.attn_norm, eps, h, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "embed launch");
-        pr.done(n * H * (es + 4.0), 0.0);
+        pr.done(n * H * (2.0 * es + 4.0), 0.0);
     }
     for (int l = 0; l < cf.n_layers; ++l) {
-        const uint8_t* an = static_cast<const uint8_t*>(c->w.attn_norm) + static_cast<size_t>(l) * H * L.es;
-        const uint8_t* wqkv = static_cast<const uint8_t*>(c->w.w_qkv) + static_cast<size_t>(l) * L.nqkv * H * L.es;
-        const uint8_t* wo = static_cast<const uint8_t*>(c->w.w_o) + static_cast<size_t>(l) * H * HqD * L.es;
-        const uint8_t* mn = static_cast<const uint8_t*>(c->w.mlp_norm) + static_cast<size_t>(l) * H * L.es;
-        const uint8_t* wgu = static_cast<const uint8_t*>(c->w.w_gate_up) + static_cast<size_t>(l) * 2 * F * H * L.es;
-        const uint8_t* wd = static_cast<const uint8_t*>(c->w.w_down) + static_cast<size_t>(l) * H * F * L.es;
+        const uint8_t* wqkv = lw(c->w.w_qkv, l, static_cast<size_t>(L.nqkv) * H);
+        const uint8_t* wo = lw(c->w.w_o, l, static_cast<size_t>(H) * HqD);
+        const uint8_t* mn = lw(c->w.mlp_norm, l, H);
+        const uint8_t* wgu = lw(c->w.w_gate_up, l, static_cast<size_t>(2) * F * H);
+        const uint8_t* wd = lw(c->w.w_down, l, static_cast<size_t>(H) * F);
+        const bool last_layer = l + 1 == cf.n_layers;
+        // norm applied after this layer's down projection: the next layer's
+        // attention norm, or the final norm (all rows; prefill selects rows later)
+        const void* next_norm = last_layer ? c->w.final_norm : static_cast<const void*>(lw(c->w.attn_norm, l + 1, H));
+        const bool norm_after_down = !last_layer || f.final_sel == nullptr;
 
-        {
-            Prof pr(c, RL_K_RMSNORM);
-            e = launch_rmsnorm(dt, x, nullptr, n, H, an, static_cast<float>(cf.rms_eps), h, c->stream);
-            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
-            pr.done(n * H * (4.0 + es) + H * es, 0.0);
-        }
+        int splits = 0;
         rl_status st = run_gemm(c, RL_K_GEMM_QKV, h, H, wqkv, n, L.nqkv, H, EPI_F32, qkv, L.nqkv,
-                                nullptr, 0, nullptr, 0);
+                                nullptr, 0, nullptr, 0, true, &splits);
         if (st != RL_OK) return st;
+        if (splits > 1) {   // wide split-K reduction into q|k|v
+            st = reduce_splits(c, EPI_F32, n, L.nqkv, splits, qkv, L.nqkv, nullptr);
+            if (st != RL_OK) return st;
+        }
         {
             Prof pr(c, RL_K_ROPE_APPEND);
-            e = launch_rope_append(dt, qkv, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride,
-                                   Hq, Hkv, D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
+            e = launch_rope_append(dt, qkv, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride, Hq, Hkv,
+                                   D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "rope/append launch");
             pr.done(n * (L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
         }
@@ -363,40 +405,58 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
             pr.done(f.attn_kv_positions * Hkv * 2.0 * D * es + 2.0 * n * HqD * es,
                     4.0 * Hq * D * f.attn_score_positions);
         }
-        if (f.any_combine) {
+        if (f.n_split_blocks > 0) {
             Prof pr(c, RL_K_ATTN_COMBINE);
-            e = launch_attn_combine(dt, f.rowc, n, f.items, apart, Hq, Hkv, D, attn, c->stream);
+            e = launch_attn_combine(f.split_blocks, f.n_split_blocks, f.items, apart, Hq, Hkv, D, attn, c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "combine launch");
             pr.done(f.n_partial_items * 16.0 * Hkv * (D + 2) * 4.0, 0.0);
         }
-        st = run_gemm(c, RL_K_GEMM_O, attn, HqD, wo, n, H, HqD, EPI_RESID, nullptr, 0, x, H, nullptr, 0);
+        st = run_gemm(c, RL_K_GEMM_O, attn, HqD, wo, n, H, HqD, EPI_RESID, nullptr, 0, x, H, nullptr, 0,
+                      true, &splits);
         if (st != RL_OK) return st;
-        {
+        if (splits > 0) {   // wide split-K reduction into the residual
+            st = reduce_splits(c, EPI_RESID, n, H, splits, nullptr, 0, x);
+            if (st != RL_OK) return st;
+        }
+        {   // MLP norm
             Prof pr(c, RL_K_RMSNORM);
-            e = launch_rmsnorm(dt, x, nullptr, n, H, mn, static_cast<float>(cf.rms_eps), h, c->stream);
+            e = launch_rmsnorm(dt, x, nullptr, n, H, mn, eps, h, c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
             pr.done(n * H * (4.0 + es) + H * es, 0.0);
         }
-        st = run_gemm(c, RL_K_GEMM_GATE_UP, h, H, wgu, n, 2 * F, H, EPI_SWIGLU, nullptr, 0, nullptr, 0, mlp, F);
+        st = run_gemm(c, RL_K_GEMM_GATE_UP, h, H, wgu, n, 2 * F, H, EPI_SWIGLU, nullptr, 0, nullptr, 0, mlp, F,
+                      false, &splits);
         if (st != RL_OK) return st;
-        st = run_gemm(c, RL_K_GEMM_DOWN, mlp, F, wd, n, H, F, EPI_RESID, nullptr, 0, x, H, nullptr, 0);
+        st = run_gemm(c, RL_K_GEMM_DOWN, mlp, F, wd, n, H, F, EPI_RESID, nullptr, 0, x, H, nullptr, 0, true,
+                      &splits);
         if (st != RL_OK) return st;
+        if (splits > 0) {
+            st = reduce_splits(c, EPI_RESID, n, H, splits, nullptr, 0, x);
+            if (st != RL_OK) return st;
+        }
+        if (norm_after_down) {   // next layer's attention norm, or the final norm (decode)
+            Prof pr(c, RL_K_RMSNORM);
+            e = launch_rmsnorm(dt, x, nullptr, n, H, next_norm, eps, h, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+            pr.done(n * H * (4.0 + es) + H * es, 0.0);
+        }
     }
     const int nf = f.final_sel ? f.n_final : n;
-    {
+    if (f.final_sel) {   // prefill: final norm of each prompt's last row only
         Prof pr(c, RL_K_RMSNORM);
-        e = launch_rmsnorm(dt, x, f.final_sel, nf, H, c->w.final_norm, static_cast<float>(cf.rms_eps), h,
-                           c->stream);
+        e = launch_rmsnorm(dt, x, f.final_sel, nf, H, c->w.final_norm, eps, h, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "final rmsnorm launch");
         pr.done(nf * H * (4.0 + es) + H * es, 0.0);
     }
+    int splits = 0;
     rl_status st = run_gemm(c, RL_K_GEMM_LM_HEAD, h, H, c->w.lm_head, nf, cf.vocab, H, EPI_F32, f.logits,
-                            cf.vocab, nullptr, 0, nullptr, 0);
+                            cf.vocab, nullptr, 0, nullptr, 0, false, &splits);
     if (st != RL_OK) return st;
     {
         Prof pr(c, RL_K_SAMPLE);
         e = launch_sample(f.logits, cf.vocab, f.n_out, cf.vocab, f.logit_row, f.uid, f.pos_new, f.forced,
-                          f.seed, f.T, f.out_tok, f.out_logp, c->stream);
+                          f.seed, f.T, c->sample_parts(), c->sample_counters(), f.out_tok, f.out_logp,
+                          c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "sample launch");
         pr.done(f.n_out * (cf.vocab * 4.0 + 8.0), 0.0);
     }
@@ -431,55 +491,52 @@ int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int 
     } else {
         C = default_min;
     }
+    int longest = 0;
+    for (const Block& b : blocks) longest = std::max(longest, b.pos0 + b.nq);
     for (;;) {
         count(C, &items, &multi);
-        if ((items <= items_cap && multi <= kPartItems) || C >= (1 << 20)) break;
+        const bool fits = items <= items_cap && multi <= kPartItems && ceil_div(longest, C) <= kMaxCombine;
+        if (fits || C >= (1 << 20)) break;
         C *= 2;
     }
     return C;
 }
 
-rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& blocks, int C,
-                      Fwd* f, int n_rows) {
+rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& blocks, int C, Fwd* f) {
     long total = 0;
     for (const Block& b : blocks) total += ceil_div(b.pos0 + b.nq, C);
     if (total > c->lay.items_cap) return fail(c, RL_ERR_CAPACITY, "too many attention work items");
     AttnItem* dItems = nullptr;
     AttnItem* items = m->take<AttnItem>(static_cast<size_t>(total), &dItems);
-    RowCombine* dRowc = nullptr;
-    RowCombine* rowc = m->take<RowCombine>(static_cast<size_t>(n_rows), &dRowc);
-    if (!items || !rowc) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
-    int k = 0, part = 0;
-    double kvpos = 0, scorepos = 0;
-    bool any = false;
+    int32_t* dSplit = nullptr;
+    int32_t* split = m->take<int32_t>(blocks.size(), &dSplit);
+    if (!items || !split) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    int k = 0, part = 0, nsplit = 0;
+    double scorepos = 0;
     for (const Block& b : blocks) {
         const int hi_all = b.pos0 + b.nq;
         const int nch = ceil_div(hi_all, C);
-        const int begin = k;
+        const int part0 = nch > 1 ? part : -1;
+        if (nch > kMaxCombine) return fail(c, RL_ERR_CAPACITY, "too many split-KV chunks in one block");
+        if (nch > 1) split[nsplit++] = k;
         for (int ch = 0; ch < nch; ++ch) {
             AttnItem& it = items[k++];
+            std::memset(&it, 0, sizeof(it));
             it.qrow = b.qrow; it.nq = b.nq; it.slot = b.slot; it.pos0 = b.pos0;
             it.kv_lo = ch * C;
             it.kv_hi = std::min(hi_all, (ch + 1) * C);
             it.part = nch > 1 ? part++ : -1;
-            it.pad = 0;
+            it.part0 = part0;
+            it.nparts = nch;
         }
-        for (int t = 0; t < b.nq; ++t) {
-            RowCombine& rc = rowc[b.qrow + t];
-            rc.item_begin = begin;
-            rc.item_count = nch;
-            rc.col0 = t * (c->cfg.n_q_heads / c->cfg.n_kv_heads);
-            rc.pad = 0;
-            scorepos += b.pos0 + t + 1;
-        }
-        if (nch > 1) any = true;
+        for (int t = 0; t < b.nq; ++t) scorepos += b.pos0 + t + 1;
     }
-    (void)kvpos;
+    if (part > kPartItems) return fail(c, RL_ERR_CAPACITY, "too many split-KV partials");
     f->items = dItems;
     f->n_items = k;
-    f->rowc = dRowc;
-    f->any_combine = any;
     f->n_partial_items = part;
+    f->split_blocks = dSplit;
+    f->n_split_blocks = nsplit;
     f->attn_score_positions = scorepos;
     return RL_OK;
 }
@@ -610,6 +667,7 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
     if (hipMemcpyAsync(c->ws + L.off_rope, table.data(), table.size() * sizeof(float), hipMemcpyHostToDevice,
                        c->stream) != hipSuccess)
         return cleanup(RL_ERR_HIP);
+    if (hipMemsetAsync(c->ws + L.off_cnt, 0, L.cnt_bytes, c->stream) != hipSuccess) return cleanup(RL_ERR_HIP);
     if (hipStreamSynchronize(c->stream) != hipSuccess) return cleanup(RL_ERR_HIP);
     for (int i = 0; i < RL_K_COUNT; ++i)
         std::snprintf(c->stats[i].name, sizeof(c->stats[i].name), "%s", kClassNames[i]);
@@ -716,7 +774,7 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     f.attn_kv_positions = kvpos;
     if (c->bf16()) {
         const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, kPrefillChunk, c->lay.items_cap, false);
-        st = build_items(c, &m, blocks, C, &f, R);
+        st = build_items(c, &m, blocks, C, &f);
         if (st != RL_OK) return st;
     } else {
         double sp_ = 0;
@@ -804,7 +862,7 @@ rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, co
     f.attn_score_positions = kvpos;
     if (c->bf16()) {
         const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, 0, c->lay.items_cap, true);
-        st = build_items(c, &m, blocks, C, &f, n);
+        st = build_items(c, &m, blocks, C, &f);
         if (st != RL_OK) return st;
     }
     f.logits = out_logits ? out_logits : c->wsp<float>(c->lay.off_logits);
@@ -854,7 +912,8 @@ rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits, c
     if (st != RL_OK) return st;
     Prof pr(c, RL_K_SAMPLE);
     hipError_t e = launch_sample(logits, c->cfg.vocab, n, c->cfg.vocab, nullptr, d_uid, d_posn, forced, sp->seed,
-                                 sp->temperature, out_tok, out_logp, c->stream);
+                                 sp->temperature, c->sample_parts(), c->sample_counters(), out_tok, out_logp,
+                                 c->stream);
     if (e != hipSuccess) return hip_fail(c, e, "sample launch");
     pr.done(n * (c->cfg.vocab * 4.0 + 8.0), 0.0);
     return RL_OK;

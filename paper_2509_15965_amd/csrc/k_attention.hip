@@ -12,9 +12,12 @@
 // the lane's B operand of the P.V product, and the matching A operand is one
 // 16-byte load from the V cache's 8-position blocks.  No LDS, no transposes.
 // Online softmax in the exp2 domain, fp32 state; the probabilities enter the
-// P.V MFMA as a bf16 hi/lo pair, so they are not rounded to bf16.  A work item that covers
-// all keys of its tokens writes the normalised output; otherwise it writes
-// (max, sum, unnormalised output) partials that attn_combine merges.
+// P.V MFMA as a bf16 hi/lo pair, so they are not rounded to bf16.  A work
+// item that covers all keys of its tokens writes the normalised output;
+// otherwise it writes (max, sum, unnormalised output) partials that
+// attn_combine merges in item order.  (Merging in the last-arriving wave
+// would need device-scope fences, which on this multi-XCD part write back and
+// invalidate the whole L2 and slow every co-running wave.)
 //
 // fp32 path: one workgroup per (row, q-head), plain VALU (tiny model only).
 #include "rl_device.h"
@@ -33,7 +36,7 @@ __device__ __forceinline__ u32x4 mask_tail8(u32x4 v, int nvalid) {
     return v;
 }
 
-template <int D>
+template <int D, bool PF>
 __global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restrict__ items,
         int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
         const uint16_t* __restrict__ vc, int S, int Hq, int Hkv, int cap, int layer,
@@ -75,22 +78,28 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restri
     const int hi = it.kv_hi;
     // key row r of score tile 0 is position t0 + 8(r/4) + r%4; tile 1 adds 4
     const int krow = 8 * (col >> 2) + (col & 3);
-    for (int t0 = it.kv_lo; t0 < hi; t0 += 32) {
-        u32x4 k0[KG], k1[KG];
+    // K rows and V blocks of one 32-position step; the next step's loads are
+    // issued before the current step's math
+    u32x4 k0[KG], k1[KG], vf[DT];
+    auto load_step = [&](int t0, u32x4 (&a0)[KG], u32x4 (&a1)[KG], u32x4 (&vv)[DT]) {
         const uint16_t* kp0 = kb + static_cast<size_t>(t0 + krow) * D + 8 * kq;
         const uint16_t* kp1 = kp0 + 4 * D;
 #pragma unroll
         for (int j = 0; j < KG; ++j) {
-            k0[j] = ld16(kp0 + 32 * j);
-            k1[j] = ld16(kp1 + 32 * j);
+            a0[j] = ld16(kp0 + 32 * j);
+            a1[j] = ld16(kp1 + 32 * j);
         }
-        // V blocks of this lane's eight positions, one per d tile
-        const int pb = t0 + 8 * kq;
-        const uint16_t* vp = vb + (static_cast<size_t>(pb >> 3) * D + col) * 8;
-        u32x4 vf[DT];
+        const uint16_t* vp = vb + (static_cast<size_t>((t0 + 8 * kq) >> 3) * D + col) * 8;
 #pragma unroll
-        for (int i = 0; i < DT; ++i) vf[i] = ld16(vp + 16 * 8 * i);
-
+        for (int i = 0; i < DT; ++i) vv[i] = ld16(vp + 16 * 8 * i);
+    };
+    if (it.kv_lo < hi) load_step(it.kv_lo, k0, k1, vf);
+    for (int t0 = it.kv_lo; t0 < hi; t0 += 32) {
+        u32x4 nk0[KG], nk1[KG], nvf[DT];
+        const bool more = PF && t0 + 32 < hi;
+        if (more) load_step(t0 + 32, nk0, nk1, nvf);
+        if (!PF && t0 != it.kv_lo) load_step(t0, k0, k1, vf);
+        const int pb = t0 + 8 * kq;
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < KG; ++j) {
@@ -140,13 +149,19 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restri
             o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
             o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
         }
+        if (more) {
+#pragma unroll
+            for (int j = 0; j < KG; ++j) { k0[j] = nk0[j]; k1[j] = nk1[j]; }
+#pragma unroll
+            for (int i = 0; i < DT; ++i) vf[i] = nvf[i];
+        }
     }
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
 
     // lane holds O^T[d = 16 i + 4 kq + e][col]
-    if (!cvalid) return;
     if (it.part < 0) {
+        if (!cvalid) return;
         const float inv = 1.0f / l;
         uint16_t* op = out + (static_cast<size_t>(qrow) * Hq + head) * D + 4 * kq;
 #pragma unroll
@@ -157,16 +172,18 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restri
                                 (static_cast<uint32_t>(f32_to_bf16(o[i][3] * inv)) << 16);
             *reinterpret_cast<uint2*>(op + 16 * i) = make_uint2(w0, w1);
         }
-    } else {
-        float* pp = part + ((static_cast<size_t>(it.part) * Hkv + kvh) * 16 + col) * (D + 2);
+        return;
+    }
+    // split block: (m, l, unnormalised o) partials, merged by attn_combine
+    if (!cvalid) return;
+    float* pp = part + ((static_cast<size_t>(it.part) * Hkv + kvh) * 16 + col) * (D + 2);
 #pragma unroll
-        for (int i = 0; i < DT; ++i)
+    for (int i = 0; i < DT; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) pp[16 * i + 4 * kq + e] = o[i][e];
-        if (kq == 0) {
-            pp[D] = m;
-            pp[D + 1] = l;
-        }
+        for (int e = 0; e < 4; ++e) pp[16 * i + 4 * kq + e] = o[i][e];
+    if (kq == 0) {
+        pp[D] = m;
+        pp[D + 1] = l;
     }
 }
 
@@ -177,60 +194,88 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
     if (n_items <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     dim3 grid((n_items + 3) / 4, Hkv), block(256);
-    if (D == 128)
-        hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, items, n_items,
-                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
-                           static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer,
-                           scale_log2, static_cast<uint16_t*>(out), part);
-    else
-        hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, items, n_items,
-                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
-                           static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer,
-                           scale_log2, static_cast<uint16_t*>(out), part);
+    // Prefetching the next step doubles the K/V registers (one wave per SIMD
+    // at head_dim 128): worth it only when there are enough waves to fill the chip.
+    const bool pf = static_cast<long>(n_items) * Hkv >= 4096;
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
+                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
+                           cap, layer, scale_log2, static_cast<uint16_t*>(out), part);
+    };
+    if (D == 128) {
+        if (pf) go(attn_bf16_kernel<128, true>); else go(attn_bf16_kernel<128, false>);
+    } else {
+        if (pf) go(attn_bf16_kernel<64, true>); else go(attn_bf16_kernel<64, false>);
+    }
     return hipGetLastError();
 }
 
-// Merge the split-KV partials of one (row, q-head): weights 2^(m_c - M).
-template <typename T>
-__global__ void __launch_bounds__(128) attn_combine_kernel(const RowCombine* __restrict__ rows,
-        const AttnItem* __restrict__ items, const float* __restrict__ part, int Hq, int Hkv, int D,
-        T* __restrict__ out) {
-    const int r = blockIdx.x, h = blockIdx.y;
-    const RowCombine rc = rows[r];
-    if (rc.item_count <= 1) return;
+
+// Merge the split partials of one query block and q-head: one workgroup per
+// (split block, q-head), one thread per (token, d).  The block's per-item
+// (m, l) go through LDS; the weighted sums issue their loads 8 at a time.
+template <int D>
+__global__ void __launch_bounds__(256) attn_combine_kernel(const int32_t* __restrict__ blocks,
+        const AttnItem* __restrict__ items, const float* __restrict__ part, int Hq, int Hkv,
+        uint16_t* __restrict__ out) {
+    __shared__ float wsh[16][kMaxCombine];
+    __shared__ float lsh[16][kMaxCombine];
+    __shared__ float lsum[16];
+    const AttnItem it = items[blocks[blockIdx.x]];
+    const int h = blockIdx.y;
     const int G = Hq / Hkv;
-    const int kvh = h / G;
-    const int col = rc.col0 + (h - kvh * G);
-    float M = -INFINITY;
-    for (int c = 0; c < rc.item_count; ++c) {
-        const float* pp = part + ((static_cast<size_t>(items[rc.item_begin + c].part) * Hkv + kvh) * 16 + col) * (D + 2);
-        M = fmaxf(M, pp[D]);
+    const int kvh = h / G, g = h - kvh * G;
+    const int np = it.nparts;
+    const size_t pstride = static_cast<size_t>(Hkv) * 16 * (D + 2);
+    const float* pb0 = part + (static_cast<size_t>(it.part0) * Hkv + kvh) * 16 * (D + 2);
+    // every item's (m, l) for every token, loaded in parallel
+    for (int p = threadIdx.x; p < it.nq * np; p += blockDim.x) {
+        const int t = p / np, j = p - t * np;
+        const float* pc = pb0 + j * pstride + static_cast<size_t>(t * G + g) * (D + 2);
+        wsh[t][j] = pc[D];
+        lsh[t][j] = pc[D + 1];
     }
-    float L = 0.0f;
-    for (int d = threadIdx.x; d < D; d += blockDim.x) {
-        float acc = 0.0f;
-        L = 0.0f;
-        for (int c = 0; c < rc.item_count; ++c) {
-            const float* pp = part + ((static_cast<size_t>(items[rc.item_begin + c].part) * Hkv + kvh) * 16 + col) * (D + 2);
-            const float w = exp2f(pp[D] - M);
-            acc += w * pp[d];
-            L += w * pp[D + 1];
+    __syncthreads();
+    // weights 2^(m_j - M) (M: the token's max) and the total sum
+    for (int t = threadIdx.x; t < it.nq; t += blockDim.x) {
+        float M = -INFINITY;
+        for (int j = 0; j < np; ++j) M = fmaxf(M, wsh[t][j]);
+        float L = 0.0f;
+        for (int j = 0; j < np; ++j) {
+            const float w = exp2f(wsh[t][j] - M);
+            wsh[t][j] = w;
+            L += w * lsh[t][j];
         }
-        Elem<T>::store(out, (static_cast<size_t>(r) * Hq + h) * D + d, acc / L);
+        lsum[t] = L;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < it.nq * D; idx += blockDim.x) {
+        const int t = idx / D, d = idx - t * D;
+        const float* pc = pb0 + static_cast<size_t>(t * G + g) * (D + 2) + d;
+        float acc = 0.0f;
+        int j = 0;
+        for (; j + 8 <= np; j += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = pc[(j + u) * pstride];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += wsh[t][j + u] * v[u];
+        }
+        for (; j < np; ++j) acc += wsh[t][j] * pc[j * pstride];
+        out[(static_cast<size_t>(it.qrow + t) * Hq + h) * D + d] = f32_to_bf16(acc / lsum[t]);
     }
 }
 
-hipError_t launch_attn_combine(int dt, const RowCombine* rows, int n_rows, const AttnItem* items,
-                               const float* part, int Hq, int Hkv, int D, void* out,
-                               hipStream_t s) {
-    if (n_rows <= 0) return hipSuccess;
-    dim3 grid(n_rows, Hq), block(128);
-    if (dt == DT_BF16)
-        hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, block, 0, s, rows, items, part, Hq,
-                           Hkv, D, static_cast<uint16_t*>(out));
+hipError_t launch_attn_combine(const int32_t* blocks, int n_blocks, const AttnItem* items, const float* part,
+                               int Hq, int Hkv, int D, void* out, hipStream_t s) {
+    if (n_blocks <= 0) return hipSuccess;
+    dim3 grid(n_blocks, Hq), block(128);
+    if (D == 128)
+        hipLaunchKernelGGL(attn_combine_kernel<128>, grid, block, 0, s, blocks, items, part, Hq, Hkv,
+                           static_cast<uint16_t*>(out));
     else
-        hipLaunchKernelGGL(attn_combine_kernel<float>, grid, block, 0, s, rows, items, part, Hq,
-                           Hkv, D, static_cast<float*>(out));
+        hipLaunchKernelGGL(attn_combine_kernel<64>, grid, block, 0, s, blocks, items, part, Hq, Hkv,
+                           static_cast<uint16_t*>(out));
     return hipGetLastError();
 }
 

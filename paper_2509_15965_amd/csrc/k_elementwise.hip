@@ -4,34 +4,50 @@
 
 namespace rl {
 
-// x[r][:] = fp32(row of the embedding table or of the caller's rows).
-// tok >= 0 selects table row tok (< V); tok < 0 selects rows[-tok-1]
-// (< n_rows); anything else embeds as zeros.
+// x[r][:] = fp32(row of the embedding table or of the caller's rows), and
+// optionally h[r][:] = storage(x / sqrt(mean(x^2) + eps) * g) (the first
+// layer's attention norm).  tok >= 0 selects table row tok (< V); tok < 0
+// selects rows[-tok-1] (< n_rows); anything else embeds as zeros.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ tok,
         const T* __restrict__ table, int V, const T* __restrict__ rows, int n_rows, int H,
-        float* __restrict__ x) {
+        float* __restrict__ x, const T* __restrict__ g, float eps, T* __restrict__ h) {
+    __shared__ float red[4];
     const int r = blockIdx.x;
     const int t = tok[r];
     const T* src = nullptr;
     if (t >= 0 && t < V) src = table + static_cast<size_t>(t) * H;
     else if (t < 0 && rows != nullptr && -(t + 1) < n_rows) src = rows + static_cast<size_t>(-(t + 1)) * H;
     float* dst = x + static_cast<size_t>(r) * H;
-    for (int i = threadIdx.x; i < H; i += blockDim.x)
-        dst[i] = src ? Elem<T>::load(src, i) : 0.0f;
+    float ss = 0.0f;
+    for (int i = threadIdx.x; i < H; i += blockDim.x) {
+        const float v = src ? Elem<T>::load(src, i) : 0.0f;
+        dst[i] = v;
+        ss = fmaf(v, v, ss);
+    }
+    if (h == nullptr) return;
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    ss = red[0] + red[1] + red[2] + red[3];
+    const float rs = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+    T* hr = h + static_cast<size_t>(r) * H;
+    for (int i = threadIdx.x; i < H; i += blockDim.x) Elem<T>::store(hr, i, dst[i] * rs * Elem<T>::load(g, i));
 }
 
 hipError_t launch_embed(int dt, const int32_t* tok, int n, const void* table, int V,
-                        const void* rows, int n_rows, int H, float* x, hipStream_t s) {
+                        const void* rows, int n_rows, int H, float* x, const void* g, float eps, void* h,
+                        hipStream_t s) {
     if (n <= 0) return hipSuccess;
     if (dt == DT_BF16)
         hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(n), dim3(256), 0, s, tok,
                            static_cast<const uint16_t*>(table), V,
-                           static_cast<const uint16_t*>(rows), n_rows, H, x);
+                           static_cast<const uint16_t*>(rows), n_rows, H, x,
+                           static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(h));
     else
         hipLaunchKernelGGL(embed_kernel<float>, dim3(n), dim3(256), 0, s, tok,
                            static_cast<const float*>(table), V, static_cast<const float*>(rows),
-                           n_rows, H, x);
+                           n_rows, H, x, static_cast<const float*>(g), eps, static_cast<float*>(h));
     return hipGetLastError();
 }
 
@@ -88,6 +104,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
     const int half = D / 2;
     const int nqkv = (Hq + 2 * Hkv) * D;
     const float* src = qkv + static_cast<size_t>(r) * nqkv;
+    auto val = [&](int c) { return src[c]; };
     const float* cosr = cs + static_cast<size_t>(pos) * half;
     const float* sinr = cs + static_cast<size_t>(cs_stride) + static_cast<size_t>(pos) * half;
     const int d0 = row_dst[r];
@@ -95,7 +112,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
     // q heads
     for (int idx = threadIdx.x; idx < Hq * half; idx += blockDim.x) {
         const int h = idx / half, i = idx - h * half;
-        const float a = src[h * D + i], b = src[h * D + i + half];
+        const float a = val(h * D + i), b = val(h * D + i + half);
         const float c = cosr[i], s = sinr[i];
         T* qo = q_out + (static_cast<size_t>(r) * Hq + h) * D;
         Elem<T>::store(qo, i, a * c - b * s);
@@ -104,7 +121,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
     // k heads -> cache
     for (int idx = threadIdx.x; idx < Hkv * half; idx += blockDim.x) {
         const int h = idx / half, i = idx - h * half;
-        const float a = src[(Hq + h) * D + i], b = src[(Hq + h) * D + i + half];
+        const float a = val((Hq + h) * D + i), b = val((Hq + h) * D + i + half);
         const float c = cosr[i], s = sinr[i];
         const float k0 = a * c - b * s, k1 = b * c + a * s;
         for (int g = 0; g < n_dst; ++g) {
@@ -118,7 +135,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
     // v heads -> cache (8-position blocks)
     for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
         const int h = idx / D, i = idx - h * D;
-        const float v = src[(Hq + Hkv + h) * D + i];
+        const float v = val((Hq + Hkv + h) * D + i);
         for (int g = 0; g < n_dst; ++g) {
             const int slot = dst_slots[d0 + g];
             T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + h) * static_cast<size_t>(cap) * D;

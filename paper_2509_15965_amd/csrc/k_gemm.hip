@@ -56,11 +56,14 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
         tiles = static_cast<long>(p.grid_x) * p.grid_y;
         target = 1024;
     }
+    // smallest K slice per split: partial sums cost 4*M bytes per output for
+    // every 2*slice bytes of weight read, so tiny batches can split finely
+    const int min_ks = M > 64 ? 256 : M <= 16 ? 128 : M <= 32 ? 256 : 512;
     int S = 1;
-    while (tiles * S * 2 <= target && ceil_div(K, 2 * S) >= 256 &&
+    while (tiles * S * 2 <= target && ceil_div(K, 2 * S) >= min_ks &&
            static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
         S *= 2;
-    if (M > 64 && tiles * S < target && ceil_div(K, 2 * S) >= 256 &&
+    if (M > 64 && tiles * S < target && ceil_div(K, 2 * S) >= min_ks &&
         static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
         S *= 2;
     const int ks = ceil_div(ceil_div(K, S), 64) * 64;   // multiple of 64 (and so of 32)

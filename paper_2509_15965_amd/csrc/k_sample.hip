@@ -7,6 +7,8 @@
 // g = fl32(-log(-log u)) evaluated in fp64.  The sample is the arg-max of
 // fl32(z_v / T + g_v) with ties to the lowest index; the log-probability is
 // z_y / T - LSE(z / T).  T == 0: arg-max of z, log-probability at T = 1.
+// The arg-max (ties to the lowest index) and the merge order are fixed, so
+// the result does not depend on how the vocabulary is split.
 #include "rl_device.h"
 #include "rl_internal.h"
 
@@ -44,34 +46,39 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
     return Lse{m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
 }
 
+// One workgroup per (row, vocabulary chunk).  With several chunks per row,
+// each writes its (best score, index, max, sum-exp) and the last chunk of the
+// row to finish (device-scope counter) merges them in chunk order.
 __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ logits, int ld,
         int V, const int32_t* __restrict__ logit_row, const uint64_t* __restrict__ uid,
         const int32_t* __restrict__ pos_new, const int32_t* __restrict__ forced, uint32_t seed_lo,
-        uint32_t seed_hi, float T, int32_t* __restrict__ out_tok, float* __restrict__ out_logp) {
+        uint32_t seed_hi, float T, int chunk, SamplePart* __restrict__ parts, int* __restrict__ counters,
+        int32_t* __restrict__ out_tok, float* __restrict__ out_logp) {
     __shared__ Best sb[4];
     __shared__ Lse sl[4];
-    const int o = blockIdx.x;
+    const int o = blockIdx.x, c = blockIdx.y, nchunks = gridDim.y;
     const int row = logit_row ? logit_row[o] : o;
     const float* z = logits + static_cast<size_t>(row) * ld;
     const uint64_t u64 = uid[o];
     const uint32_t pos = static_cast<uint32_t>(pos_new[o]);
     const bool greedy = T == 0.0f;
+    const int vbeg = c * chunk, vend = min(V, vbeg + chunk);
 
     Best best{-INFINITY, 0x7FFFFFFF};
     Lse acc{-INFINITY, 0.0f};
-    for (int v4 = threadIdx.x; 4 * v4 < V; v4 += blockDim.x) {
+    for (int v4 = vbeg / 4 + threadIdx.x; 4 * v4 < vend; v4 += blockDim.x) {
         const float4 zz = *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4));
         const float zv[4] = {zz.x, zz.y, zz.z, zz.w};
-        uint32_t c[4] = {static_cast<uint32_t>(v4), pos, static_cast<uint32_t>(u64),
-                         static_cast<uint32_t>(u64 >> 32)};
-        if (!greedy) philox4x32_10(c, seed_lo, seed_hi);
+        uint32_t cw[4] = {static_cast<uint32_t>(v4), pos, static_cast<uint32_t>(u64),
+                          static_cast<uint32_t>(u64 >> 32)};
+        if (!greedy) philox4x32_10(cw, seed_lo, seed_hi);
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const int v = 4 * v4 + w;
-            if (v >= V) break;
+            if (v >= vend) break;
             const float zt = greedy ? zv[w] : zv[w] / T;
-            const float s = greedy ? zt : zt + gumbel_of_word(c[w]);
-            best = better(best, Best{s, v});
+            const float sc = greedy ? zt : zt + gumbel_of_word(cw[w]);
+            best = better(best, Best{sc, v});
             if (zt > acc.m) {
                 acc.s = acc.s * expf(acc.m - zt) + 1.0f;
                 acc.m = zt;
@@ -80,7 +87,6 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
             }
         }
     }
-    // wave reduction, then across the 4 waves
     for (int off = 32; off > 0; off >>= 1) {
         Best ob{__shfl_xor(best.s, off, 64), __shfl_xor(best.v, off, 64)};
         best = better(best, ob);
@@ -90,30 +96,48 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
     const int wave = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) { sb[wave] = best; sl[wave] = acc; }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        Best b = sb[0];
-        Lse a = sl[0];
-        for (int w = 1; w < 4; ++w) { b = better(b, sb[w]); a = lse_merge(a, sl[w]); }
-        const float lse = a.m + logf(a.s);
-        int r = b.v;
-        if (forced) {
-            const int f = forced[o];
-            r = (f >= 0 && f < V) ? f : b.v;
+    if (threadIdx.x != 0) return;
+    Best b = sb[0];
+    Lse a = sl[0];
+    for (int w = 1; w < 4; ++w) { b = better(b, sb[w]); a = lse_merge(a, sl[w]); }
+    if (nchunks > 1) {
+        parts[static_cast<size_t>(o) * nchunks + c] = SamplePart{b.s, b.v, a.m, a.s};
+        __threadfence();
+        if (atomicAdd(&counters[o], 1) != nchunks - 1) return;
+        __threadfence();
+        const SamplePart* pr = parts + static_cast<size_t>(o) * nchunks;
+        b = Best{pr[0].best_s, pr[0].best_v};
+        a = Lse{pr[0].m, pr[0].s};
+        for (int k = 1; k < nchunks; ++k) {
+            b = better(b, Best{pr[k].best_s, pr[k].best_v});
+            a = lse_merge(a, Lse{pr[k].m, pr[k].s});
         }
-        const float zr = greedy ? z[r] : z[r] / T;
-        out_tok[o] = b.v;
-        out_logp[o] = zr - lse;
+        counters[o] = 0;
     }
+    const float lse = a.m + logf(a.s);
+    int r = b.v;
+    if (forced) {
+        const int f = forced[o];
+        r = (f >= 0 && f < V) ? f : b.v;
+    }
+    const float zr = greedy ? z[r] : z[r] / T;
+    out_tok[o] = b.v;
+    out_logp[o] = zr - lse;
 }
 
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
-                         uint64_t seed, float T, int32_t* out_tok, float* out_logp,
-                         hipStream_t s) {
+                         uint64_t seed, float T, SamplePart* parts, int* counters,
+                         int32_t* out_tok, float* out_logp, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(sample_kernel, dim3(n), dim3(256), 0, s, logits, ld, V, logit_row, uid,
+    int nchunks = (2048 + n - 1) / n;
+    nchunks = nchunks < 1 ? 1 : nchunks > kSampleMaxChunks ? kSampleMaxChunks : nchunks;
+    int chunk = (V + nchunks - 1) / nchunks;
+    chunk = (chunk + 1023) / 1024 * 1024;
+    nchunks = (V + chunk - 1) / chunk;
+    hipLaunchKernelGGL(sample_kernel, dim3(n, nchunks), dim3(256), 0, s, logits, ld, V, logit_row, uid,
                        pos_new, forced, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
-                       T, out_tok, out_logp);
+                       T, chunk, parts, counters, out_tok, out_logp);
     return hipGetLastError();
 }
 

@@ -30,15 +30,9 @@ struct AttnItem {
     int32_t kv_hi;
     int32_t part;   // partial-sum index, or -1 when this item covers every key
                     // its tokens see (it then writes the final output)
-    int32_t pad;
-};
-
-// Per query row: the items whose partial sums the combine step merges.
-struct RowCombine {
-    int32_t item_begin;
-    int32_t item_count;   // <= 1: nothing to combine
-    int32_t col0;         // column of this row's first head inside its items
-    int32_t pad;
+    int32_t part0;  // first partial index of the block's items (they are consecutive)
+    int32_t nparts; // items of the block (>= 2 when part >= 0)
+    int32_t pad[3];
 };
 
 struct GemmArgs {
@@ -76,8 +70,10 @@ constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F);
 
 // ---- launchers (enqueue only; return hipGetLastError()) -----------------
+// x = embedding rows; h = first-layer attention norm of x when h != nullptr
 hipError_t launch_embed(int dt, const int32_t* tok, int n, const void* table, int V,
-                        const void* rows, int n_rows, int H, float* x, hipStream_t s);
+                        const void* rows, int n_rows, int H, float* x, const void* g, float eps, void* h,
+                        hipStream_t s);
 
 hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int H,
                           const void* g, float eps, void* out, hipStream_t s);
@@ -88,9 +84,9 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);   // writes a.out_
 hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const float* partial,
                                 hipStream_t s);
 
-// RoPE on q and k, q stored to q_out [rows][Hq][d]; k and v appended to the
-// cache of every destination slot of the row (dst_slots[row_dst[r] + g],
-// g < n_dst) at position row_pos[r].
+// RoPE on q and k of fp32 q|k|v rows, q stored to q_out [rows][Hq][d]; k and
+// v appended to the cache of every destination slot of the row
+// (dst_slots[row_dst[r] + g], g < n_dst) at position row_pos[r].
 hipError_t launch_rope_append(int dt, const float* qkv, int n_rows, const int32_t* row_pos,
                               const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
                               const float* cs, int cs_stride, int Hq, int Hkv, int D,
@@ -102,9 +98,12 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
                                  int D, int cap, int layer, void* out, float* part,
                                  hipStream_t s);
 
-hipError_t launch_attn_combine(int dt, const RowCombine* rows, int n_rows, const AttnItem* items,
-                               const float* part, int Hq, int Hkv, int D, void* out,
-                               hipStream_t s);
+// Most items one split block may have (bounds the combine's LDS).
+constexpr int kMaxCombine = 64;
+
+// blocks[b] = index of the first item of split block b.
+hipError_t launch_attn_combine(const int32_t* blocks, int n_blocks, const AttnItem* items, const float* part,
+                               int Hq, int Hkv, int D, void* out, hipStream_t s);
 
 // fp32 model dtype: one workgroup per (row, q-head), keys 0..row_pos[r].
 hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
@@ -112,10 +111,15 @@ hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32
                                 int Hq, int Hkv, int D, int cap, int layer, float* out,
                                 hipStream_t s);
 
+// Per-chunk partial of the sampler (merged by the row's last chunk).
+struct SamplePart { float best_s; int best_v; float m; float s; };
+constexpr int kSampleMaxChunks = 64;
+
+// parts: [n][kSampleMaxChunks]; counters: [n] ints, zero between launches.
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
-                         uint64_t seed, float T, int32_t* out_tok, float* out_logp,
-                         hipStream_t s);
+                         uint64_t seed, float T, SamplePart* parts, int* counters,
+                         int32_t* out_tok, float* out_logp, hipStream_t s);
 
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
 
