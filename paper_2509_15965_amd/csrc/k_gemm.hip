@@ -25,18 +25,93 @@ const GemmShape kGemmShapes[kNumGemmShapes] = {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+namespace {
+
+// Tile kernels of the batched (M > 64) path for the planner's cost model:
+// tile shape, workgroups resident per CU, and the measured time of one
+// round (every CU busy) per 1024 k, in microseconds.  A lone 128 x 128
+// workgroup on a CU runs faster than a co-resident pair (t_alone).
+struct TileKernel { int variant, BM, BN, per_cu; double t_round, t_alone; };
+constexpr TileKernel kLineTiles[] = {
+    {kLineVariant256x256, 256, 256, 1, 29.0, 29.0},
+    {kLineVariant128x256, 128, 256, 1, 18.2, 18.2},
+    {kLineVariant128x128, 128, 128, 2, 19.0, 12.0},
+};
+constexpr int kCUs = 256;
+
+struct Cost { double us; };
+
+double rounds_us(const TileKernel& t, long tiles, double kfrac) {
+    const long per_cu = (tiles + kCUs - 1) / kCUs;
+    if (t.per_cu == 1) return per_cu * t.t_round * kfrac;
+    return (per_cu / 2) * t.t_round * kfrac + (per_cu % 2) * t.t_alone * kfrac;
+}
+
+long tiles_of(const TileKernel& t, int M, int n_cols, int epi) {
+    const int bno = epi == EPI_SWIGLU ? t.BN / 2 : t.BN;
+    return static_cast<long>(ceil_div(M, t.BM)) * ceil_div(n_cols, bno);
+}
+
+}  // namespace
+
+// Plan of one bf16 GEMM.  M <= 64: direct-load kernel, split K until the
+// weight stream fills the CUs.  M > 64 (K % 64 == 0): the cheapest of
+// (a) one tile kernel with split-K s (partials summed by splitk_reduce),
+// (b) 256 x 256 tiles for whole rounds plus a smaller tile kernel for the
+//     remaining output columns, under a cost model of rounds x round time
+//     + partial-sum traffic + output traffic.
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     GemmPlan p{};
     const int n_out = epi == EPI_SWIGLU ? F : Nw;
+    p.n_split = 0;
+    if (M > 64 && K % 64 == 0) {
+        const double kf = K / 1024.0;
+        const double out_us = (epi == EPI_F32 ? 4.0 : epi == EPI_RESID ? 8.0 : 2.0) * M * n_out / 4.0e6;
+        double best = 1e30;
+        for (const TileKernel& t : kLineTiles) {
+            const long tiles = tiles_of(t, M, n_out, epi);
+            for (int s = 1; s <= kMaxSplits; s *= 2) {
+                const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+                const int splits = ceil_div(K, ks);
+                if (splits != s && s > 1) break;
+                if (s > 1 && (ks < 256 || static_cast<size_t>(s) * M * Nw > kPartCapFloats)) break;
+                double us = rounds_us(t, tiles * s, ks / 1024.0) + out_us;
+                if (s > 1) us += 8.0 * s * M * static_cast<double>(Nw) / 3.0e6 + 4.0;
+                if (us < best * 0.98) {
+                    best = us;
+                    p.variant = t.variant; p.splits = s; p.ksplit = ks; p.n_split = 0;
+                }
+            }
+        }
+        // whole rounds of 256 x 256 tiles, then the rest of the columns
+        const TileKernel& big = kLineTiles[0];
+        const long big_tiles = tiles_of(big, M, n_out, epi);
+        const int m_tiles = ceil_div(M, big.BM);
+        const int bno = epi == EPI_SWIGLU ? big.BN / 2 : big.BN;
+        const long full_cols = (big_tiles / kCUs) * kCUs / m_tiles;   // n tiles of whole rounds
+        if (full_cols > 0 && full_cols * bno < n_out) {
+            const int n_split = static_cast<int>(full_cols * bno);
+            for (int v = 1; v < 3; ++v) {
+                const TileKernel& t = kLineTiles[v];
+                const double us = rounds_us(big, full_cols * m_tiles, kf) +
+                                  rounds_us(t, tiles_of(t, M, n_out - n_split, epi), kf) + out_us + 4.0;
+                if (us < best * 0.98) {
+                    best = us;
+                    p.variant = big.variant; p.splits = 1; p.ksplit = K;
+                    p.n_split = n_split; p.variant2 = t.variant;
+                }
+            }
+        }
+        p.grid_x = p.grid_y = 0;
+        return p;
+    }
     long tiles;
     long target;
     if (M > 64) {
-        // LDS-tiled kernels; split K only when the tiles cannot fill the CUs
+        // register-staged / 64-byte-row kernels (K % 64 != 0)
         int BM, BN;
-        if (M > 128 && K % 32 == 0) {
-            p.variant = kLdsVariant256x256; BM = 256; BN = 256;
-        } else if (K % 32 == 0) {
-            p.variant = kDmaVariant128; BM = 128; BN = 256;
+        if (K % 32 == 0) {
+            p.variant = M > 128 ? kDmaVariant256x256 : kDmaVariant128x256; BM = M > 128 ? 256 : 128; BN = 256;
         } else {
             p.variant = M > 128 ? kLdsVariant256 : kLdsVariant128; BM = M > 128 ? 256 : 128; BN = 128;
         }

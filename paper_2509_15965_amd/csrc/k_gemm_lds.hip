@@ -178,14 +178,16 @@ __global__ void __launch_bounds__(256) gemm_lds_kernel(GemmArgs p, int ksplit, i
 // Direct-to-LDS ring variant (K a multiple of 32).  global_load_lds_dwordx4
 // moves each 16-byte chunk from global memory straight into LDS, so no
 // staging registers are needed and a ring of S k-stages (32 wide) keeps
-// S - 2 stages of HBM traffic in flight while the MFMAs consume another; the
-// ring fills most of the 160 KB LDS.  LDS rows are 32 elements (64 bytes);
-// the four 16-byte chunks of row r sit at chunk ^ ((r / 2) % 4), so one DMA
-// instruction fills 16 whole rows (1 KB, lane i -> bytes 16i) and the
-// fragment reads of 8 consecutive rows hit 8 distinct bank groups.  Each
-// stage is guarded by one barrier; the next stage's fragments are read under
-// the current stage's MFMAs.  Rows past M or past the weight are loaded from a
-// clamped valid row and their outputs are never stored.
+// S - 2 to S - 1 stages of HBM traffic in flight while the MFMAs consume
+// another; the ring fills the 160 KB LDS.  LDS rows are 32 elements (64 bytes);
+// the four 16-byte chunks of row r sit at chunk ^ ((r / 4) % 4), so one DMA
+// instruction fills 16 whole rows (1 KB, lane i -> bytes 16i) and the 32x32
+// fragment reads (32 rows x 2 chunks per instruction) are free of bank
+// conflicts.  Each stage is guarded by one barrier; the next stage's
+// fragments are read under the current stage's MFMAs, into the other half of
+// a statically alternating register pair (the k loop is unrolled by two).
+// Rows past M or past the weight are loaded from a clamped valid row and
+// their outputs are never stored.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -200,30 +202,33 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// wait until at most `outstanding` (0..4) later stages of Q DMA ops each are pending
-template <int Q>
+// wait until at most `outstanding` (0..MAXS) later stages of Q DMA ops each are pending
+template <int Q, int MAXS>
 __device__ __forceinline__ void wait_stages(int outstanding) {
+    static_assert(MAXS <= 5 && Q * MAXS < 64, "vmcnt range");
     switch (outstanding) {
         case 0: wait_vm<0>(); break;
         case 1: wait_vm<Q>(); break;
-        case 2: wait_vm<2 * Q>(); break;
-        case 3: wait_vm<3 * Q>(); break;
-        default: wait_vm<4 * Q>(); break;
+        case 2: wait_vm<(2 <= MAXS ? 2 : MAXS) * Q>(); break;
+        case 3: wait_vm<(3 <= MAXS ? 3 : MAXS) * Q>(); break;
+        case 4: wait_vm<(4 <= MAXS ? 4 : MAXS) * Q>(); break;
+        default: wait_vm<MAXS * Q>(); break;
     }
 }
 
-template <int BM, int BN, int WM, int S, int EPI, bool SPLIT>
-__global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs p, int ksplit, int m_tiles, int n_tiles,
-                                                       int gm) {
+template <int BM, int BN, int WM, int NW, int S, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(64 * NW) gemm_dma_kernel(GemmArgs p, int ksplit, int m_tiles, int n_tiles, int n0,
+                                                           int gm) {
     constexpr int BK = 32, ROWB = 64;
-    constexpr int WN = 4 / WM;
+    constexpr int WN = NW / WM;
     constexpr int TM = BM / WM, TN = BN / WN;
-    constexpr int MT = TM / 16, NT = TN / 16;
+    constexpr int MT = TM / 32, NT = TN / 32;
     constexpr int STAGE = (BM + BN) * ROWB;
-    constexpr int AQ = BM / 64, BQ = BN / 64;   // DMA instructions (16 rows each) per wave per stage
+    constexpr int AQ = BM / (16 * NW), BQ = BN / (16 * NW);   // DMA instructions (16 rows each) per wave per stage
     constexpr int Q = AQ + BQ;
-    static_assert(BM % 64 == 0 && BN % 64 == 0, "tile rows must fill whole DMA instructions");
-    static_assert(S >= 3 && S - 2 <= 4 && Q * 4 < 64, "vmcnt range");
+    static_assert(BM % (16 * NW) == 0 && BN % (16 * NW) == 0, "tile rows must fill whole DMA instructions");
+    static_assert(TM % 32 == 0 && TN % 64 == 0, "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
+    static_assert(S >= 3 && S - 1 <= 5, "ring depth");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[S * STAGE];
 
     const int w = blockIdx.x;
@@ -237,19 +242,19 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs p, int ksplit, i
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
-    const int r16 = lane & 15, kq = lane >> 4;
+    const int r32 = lane & 31, kh = lane >> 5;
     const int M = p.M, Nw = p.Nw, K = p.K;
     const int m0 = m_tile * BM;
 
     auto wrow = [&](int b, bool* ok) -> int {
         if (EPI == EPI_SWIGLU) {
             const int wv = b / TN, u = b - wv * TN;
-            const int c0 = n_tile * (BN / 2) + wv * (TN / 2);
+            const int c0 = n0 + n_tile * (BN / 2) + wv * (TN / 2);
             const int c = u < TN / 2 ? c0 + u : c0 + u - TN / 2;
             *ok = c < p.F;
             return u < TN / 2 ? c : p.F + c;
         } else {
-            const int n = n_tile * BN + b;
+            const int n = n0 + n_tile * BN + b;
             *ok = n < Nw;
             return n;
         }
@@ -261,8 +266,8 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs p, int ksplit, i
 
     const uint16_t* A = static_cast<const uint16_t*>(p.A);
     const uint16_t* W = static_cast<const uint16_t*>(p.W);
-    // this lane's DMA source: row 16g + lane/4, original chunk (lane%4) ^ ((lane/8)%4)
-    const int lrow = lane >> 2, lch = (lane & 3) ^ ((lane >> 3) & 3);
+    // this lane's DMA source: row 16g + lane/4, original chunk (lane%4) ^ ((row/4)%4)
+    const int lrow = lane >> 2, lch = (lane & 3) ^ ((lane >> 4) & 3);
     uint32_t aoff[AQ], boff[BQ];
 #pragma unroll
     for (int q = 0; q < AQ; ++q) {
@@ -286,74 +291,82 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs p, int ksplit, i
         for (int q = 0; q < BQ; ++q) dma16(W + boff[q] + k0, bbase + (wave * BQ + q) * 1024);
     };
 
-    f32x4 acc[MT][NT];
+    f32x16 acc[MT][NT];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][t][e] = 0.f;
 
-    const int sw = (kq ^ ((r16 >> 1) & 3)) * 16;
-    const int arow = (wm * TM + r16) * ROWB + sw;
-    const int brow = BM * ROWB + (wn * TN + r16) * ROWB + sw;
-    auto frag_a = [&](int stage, int i) {
-        return *reinterpret_cast<const u32x4*>(smem + (stage % S) * STAGE + arow + 16 * i * ROWB);
+    // lane (r32, kh) reads k chunk 2 ks + kh (16 bytes) of its row in sub-step ks;
+    // every fragment row is r32 plus a multiple of 32, so the swizzle depends on r32 only
+    const int sw0 = ((0 + kh) ^ ((r32 >> 2) & 3)) * 16;
+    const int sw1 = ((2 + kh) ^ ((r32 >> 2) & 3)) * 16;
+    // per-lane byte offsets inside a stage; tile i / t adds an immediate 32 rows
+    const uint32_t la0 = (wm * TM + r32) * ROWB + sw0, la1 = (wm * TM + r32) * ROWB + sw1;
+    const uint32_t lb0 = (BM + wn * TN + r32) * ROWB + sw0, lb1 = (BM + wn * TN + r32) * ROWB + sw1;
+    auto frag = [&](uint32_t lane_stage, int imm) {
+        return *reinterpret_cast<const u32x4*>(smem + lane_stage + imm);
     };
-    auto frag_b = [&](int stage, int t) {
-        return *reinterpret_cast<const u32x4*>(smem + (stage % S) * STAGE + brow + 16 * t * ROWB);
+    // fragments of one k sub-step (16 wide) of a stage
+    auto load_half = [&](int stage, int ks, u32x4 (&fa)[MT], u32x4 (&fb)[NT]) {
+        const uint32_t so = static_cast<uint32_t>(stage % S) * STAGE;
+        const uint32_t a = so + (ks ? la1 : la0), b = so + (ks ? lb1 : lb0);
+#pragma unroll
+        for (int i = 0; i < MT; ++i) fa[i] = frag(a, 32 * i * ROWB);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) fb[t] = frag(b, 32 * t * ROWB);
     };
-
-    // prologue: stages 0 .. S-2 in flight, then stage 0 resident
-#pragma unroll
-    for (int st = 0; st < S - 1; ++st)
-        if (st < nk) issue(st, kb + st * BK);
-    wait_stages<Q>(min(S - 2, nk - 1));
-    __syncthreads();
-    u32x4 fa[MT], fb[NT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) fa[i] = frag_a(0, i);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) fb[t] = frag_b(0, t);
-
-    for (int kt = 0; kt < nk; ++kt) {
-        const bool has_next = kt + 1 < nk;
-        if (has_next) {
-            wait_stages<Q>(min(S - 3, nk - 2 - kt));   // stage kt+1 resident
-            __syncthreads();                               // and every wave is done with stage kt-1
-            if (kt + S - 1 < nk) issue(kt + S - 1, kb + (kt + S - 1) * BK);
-        }
-        const int nxt = has_next ? kt + 1 : kt;
-        u32x4 ga[MT], gb[NT];
-#pragma unroll
-        for (int i = 0; i < MT; ++i) ga[i] = frag_a(nxt, i);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) gb[t] = frag_b(nxt, t);
+    auto mma_half = [&](const u32x4 (&fa)[MT], const u32x4 (&fb)[NT]) {
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
             for (int t = 0; t < NT; ++t)
-                acc[i][t] = mfma16x16x32(as_bf16x8(fa[i]), as_bf16x8(fb[t]), acc[i][t]);
-        constexpr int NRD = MT + NT;
-        constexpr int R = (MT * NT) / NRD > 0 ? (MT * NT) / NRD : 1;
+                acc[i][t] = mfma32x32x16(as_bf16x8(fa[i]), as_bf16x8(fb[t]), acc[i][t]);
+        constexpr int NRD = MT + NT, NMF = MT * NT;
+        constexpr int R = NMF / NRD > 0 ? NMF / NRD : 1;
 #pragma unroll
         for (int g = 0; g < NRD; ++g) {
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, R, 0);
         }
+    };
+
+    // prologue: stages 0 .. S-1 in flight, then stage 0 resident
 #pragma unroll
-        for (int i = 0; i < MT; ++i) fa[i] = ga[i];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) fb[t] = gb[t];
+    for (int st = 0; st < S; ++st)
+        if (st < nk) issue(st, kb + st * BK);
+    wait_stages<Q, S - 1>(min(S - 1, nk - 1));
+    __syncthreads();
+    u32x4 f0a[MT], f0b[NT], f1a[MT], f1b[NT];
+    load_half(0, 0, f0a, f0b);
+
+    // stage kt: [read sub-step 1 | MFMAs of sub-step 0], then stage kt+1
+    // resident + barrier (every wave has read all of stage kt, so its slot
+    // takes stage kt+S), then [read sub-step 0 of kt+1 | MFMAs of sub-step 1].
+    // The last stage re-reads itself (unused).
+    for (int kt = 0; kt < nk; ++kt) {
+        load_half(kt, 1, f1a, f1b);
+        mma_half(f0a, f0b);
+        const int left = nk - 2 - kt;
+        wait_stages<Q, S - 1>(left < 0 ? 0 : left < S - 2 ? left : S - 2);   // stage kt+1 resident
+        __syncthreads();
+        if (kt + S < nk) issue(kt + S, kb + (kt + S) * BK);
+        load_half(kt + 1 < nk ? kt + 1 : kt, 0, f0a, f0b);
+        mma_half(f1a, f1b);
     }
 
+    // epilogue: acc[i][t][e] is row m0 + wm*TM + 32i + 8(e/4) + 4kh + e%4, LDS B row wn*TN + 32t + r32
     int nrow[NT];
     bool nok[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) nrow[t] = wrow(wn * TN + 16 * t + r16, &nok[t]);
+    for (int t = 0; t < NT; ++t) nrow[t] = wrow(wn * TN + 32 * t + r32, &nok[t]);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int m = m0 + wm * TM + 16 * i + 4 * kq + e;
+        for (int e = 0; e < 16; ++e) {
+            const int m = m0 + wm * TM + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
             if (m >= M) continue;
             if (SPLIT) {
                 float* dst = p.partial + (static_cast<size_t>(blockIdx.y) * M + m) * Nw;
@@ -382,27 +395,239 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(GemmArgs p, int ksplit, i
     }
 }
 
-template <int BM, int BN, int WM, int S>
-hipError_t launch_dma(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+// ---------------------------------------------------------------------------
+// Full-line variant (K a multiple of 64): LDS rows of 64 elements (128 bytes),
+// so each DMA instruction moves 8 whole 128-byte lines (the memory system
+// serves full lines markedly faster than the half lines of the 64-byte-row
+// ring).  Chunk c of row r sits at c ^ ((r / 2) % 8), which keeps the 32x32
+// fragment reads free of bank conflicts.  A stage is 64 k (four 16-wide
+// sub-steps); the ring has S stages and the slot of stage kt takes stage
+// kt + S as soon as every wave has read all of stage kt.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int NW, int S, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ksplit, int m_tiles, int n_tiles, int n0,
+                                                              int gm) {
+    constexpr int BK = 64, ROWB = 128;
+    constexpr int WN = NW / WM;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int MT = TM / 32, NT = TN / 32;
+    constexpr int STAGE = (BM + BN) * ROWB;
+    constexpr int AQ = BM / (8 * NW), BQ = BN / (8 * NW);   // DMA instructions (8 rows each) per wave per stage
+    constexpr int Q = AQ + BQ;
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows must fill whole DMA instructions");
+    static_assert(TM % 32 == 0 && TN % 64 == 0, "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
+    static_assert(S >= 2 && S - 1 <= 5, "ring depth");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[S * STAGE];
+
+    const int w = blockIdx.x;
+    const int xcd = w & 7, j = w >> 3;
+    const int ntx = (n_tiles + 7) >> 3;
+    const int grp = j / (gm * ntx);
+    const int rem = j - grp * gm * ntx;
+    const int m_tile = grp * gm + rem % gm;
+    const int n_tile = (rem / gm) * 8 + xcd;
+    if (m_tile >= m_tiles || n_tile >= n_tiles) return;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int r32 = lane & 31, kh = lane >> 5;
+    const int M = p.M, Nw = p.Nw, K = p.K;
+    const int m0 = m_tile * BM;
+
+    auto wrow = [&](int b, bool* ok) -> int {
+        if (EPI == EPI_SWIGLU) {
+            const int wv = b / TN, u = b - wv * TN;
+            const int c0 = n0 + n_tile * (BN / 2) + wv * (TN / 2);
+            const int c = u < TN / 2 ? c0 + u : c0 + u - TN / 2;
+            *ok = c < p.F;
+            return u < TN / 2 ? c : p.F + c;
+        } else {
+            const int n = n0 + n_tile * BN + b;
+            *ok = n < Nw;
+            return n;
+        }
+    };
+
+    const int kb = blockIdx.y * ksplit;
+    const int ke = min(K, kb + ksplit);
+    const int nk = (ke - kb) / BK;
+
+    const uint16_t* A = static_cast<const uint16_t*>(p.A);
+    const uint16_t* W = static_cast<const uint16_t*>(p.W);
+    // DMA lane l of block g: row 8g + l/8, LDS chunk l%8 <- source chunk (l%8) ^ ((row/2)%8)
+    const int lrow = lane >> 3;
+    uint32_t aoff[AQ], boff[BQ];
+#pragma unroll
+    for (int q = 0; q < AQ; ++q) {
+        const int g = wave * AQ + q;
+        int m = m0 + 8 * g + lrow;
+        m = m < M ? m : M - 1;
+        const int ch = (lane & 7) ^ (((8 * g + lrow) >> 1) & 7);
+        aoff[q] = static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda) + 8u * ch;
+    }
+#pragma unroll
+    for (int q = 0; q < BQ; ++q) {
+        const int g = wave * BQ + q;
+        bool ok;
+        int n = wrow(8 * g + lrow, &ok);
+        n = ok ? n : 0;
+        const int ch = (lane & 7) ^ (((8 * g + lrow) >> 1) & 7);
+        boff[q] = static_cast<uint32_t>(n) * static_cast<uint32_t>(p.ldw) + 8u * ch;
+    }
+    auto issue = [&](int stage, int k0) {
+        uint8_t* abase = smem + (stage % S) * STAGE;
+        uint8_t* bbase = abase + BM * ROWB;
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) dma16(A + aoff[q] + k0, abase + (wave * AQ + q) * 1024);
+#pragma unroll
+        for (int q = 0; q < BQ; ++q) dma16(W + boff[q] + k0, bbase + (wave * BQ + q) * 1024);
+    };
+
+    f32x16 acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][t][e] = 0.f;
+
+    // every fragment row is r32 plus a multiple of 32, so the swizzle depends on r32 only
+    const int swz = (r32 >> 1) & 7;
+    const uint32_t la = (wm * TM + r32) * ROWB, lb = (BM + wn * TN + r32) * ROWB;
+    auto load_sub = [&](int stage, int ks, u32x4 (&fa)[MT], u32x4 (&fb)[NT]) {
+        const uint32_t so = static_cast<uint32_t>(stage % S) * STAGE + (((2 * ks + kh) ^ swz) << 4);
+        const uint8_t* pa = smem + so + la;
+        const uint8_t* pb = smem + so + lb;
+#pragma unroll
+        for (int i = 0; i < MT; ++i) fa[i] = *reinterpret_cast<const u32x4*>(pa + 32 * i * ROWB);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) fb[t] = *reinterpret_cast<const u32x4*>(pb + 32 * t * ROWB);
+    };
+    auto mma_sub = [&](const u32x4 (&fa)[MT], const u32x4 (&fb)[NT]) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                acc[i][t] = mfma32x32x16(as_bf16x8(fa[i]), as_bf16x8(fb[t]), acc[i][t]);
+        constexpr int NRD = MT + NT, NMF = MT * NT;
+        constexpr int R = NMF / NRD > 0 ? NMF / NRD : 1;
+#pragma unroll
+        for (int g = 0; g < NRD; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, R, 0);
+        }
+    };
+
+#pragma unroll
+    for (int st = 0; st < S; ++st)
+        if (st < nk) issue(st, kb + st * BK);
+    wait_stages<Q, S - 1>(min(S - 1, nk - 1));
+    __syncthreads();
+    u32x4 f0a[MT], f0b[NT], f1a[MT], f1b[NT];
+    load_sub(0, 0, f0a, f0b);
+
+    // sub-steps 0..3 of stage kt alternate register sets; before the read of
+    // stage kt+1 (under the MFMAs of sub-step 3) stage kt+1 must be resident
+    // and every wave done with stage kt, whose slot then takes stage kt+S.
+    for (int kt = 0; kt < nk; ++kt) {
+        load_sub(kt, 1, f1a, f1b);
+        mma_sub(f0a, f0b);
+        load_sub(kt, 2, f0a, f0b);
+        mma_sub(f1a, f1b);
+        load_sub(kt, 3, f1a, f1b);
+        mma_sub(f0a, f0b);
+        const int left = nk - 2 - kt;
+        wait_stages<Q, S - 1>(left < 0 ? 0 : left < S - 2 ? left : S - 2);   // stage kt+1 resident
+        __syncthreads();
+        if (kt + S < nk) issue(kt + S, kb + (kt + S) * BK);
+        load_sub(kt + 1 < nk ? kt + 1 : kt, 0, f0a, f0b);
+        mma_sub(f1a, f1b);
+    }
+
+    // epilogue: acc[i][t][e] is row m0 + wm*TM + 32i + 8(e/4) + 4kh + e%4, LDS B row wn*TN + 32t + r32
+    int nrow[NT];
+    bool nok[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) nrow[t] = wrow(wn * TN + 32 * t + r32, &nok[t]);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int m = m0 + wm * TM + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
+            if (m >= M) continue;
+            if (SPLIT) {
+                float* dst = p.partial + (static_cast<size_t>(blockIdx.y) * M + m) * Nw;
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (nok[t]) dst[nrow[t]] = acc[i][t][e];
+            } else if (EPI == EPI_F32) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (nok[t]) p.out_f32[static_cast<size_t>(m) * p.ldo + nrow[t]] = acc[i][t][e];
+            } else if (EPI == EPI_RESID) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (nok[t]) p.resid[static_cast<size_t>(m) * p.ldr + nrow[t]] += acc[i][t][e];
+            } else {
+                uint16_t* act = static_cast<uint16_t*>(p.act);
+#pragma unroll
+                for (int t = 0; t < NT / 2; ++t) {
+                    if (!nok[t]) continue;
+                    const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
+                    const float silu = g / (1.0f + expf(-g));
+                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(silu * u);
+                }
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int NW, int S>
+hipError_t launch_dma128(const GemmArgs& a, const GemmPlan& p, int n0, int n1, hipStream_t s) {
     const int m_tiles = (a.M + BM - 1) / BM;
-    const int n_out = a.epi == EPI_SWIGLU ? a.F : a.Nw;
+    const int n_out = n1 - n0;
     const int bno = a.epi == EPI_SWIGLU ? BN / 2 : BN;
     const int n_tiles = (n_out + bno - 1) / bno;
     const int gm = m_tiles < 8 ? m_tiles : 8;
     const int ntx = (n_tiles + 7) / 8;
     const int groups = (m_tiles + gm - 1) / gm;
-    dim3 grid(8 * ntx * groups * gm, p.splits), block(256);
+    dim3 grid(8 * ntx * groups * gm, p.splits), block(64 * NW);
     if (p.splits > 1) {
         if (a.epi == EPI_SWIGLU)
-            hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, S, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
         else
-            hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, S, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_F32) {
-        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, S, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_RESID) {
-        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, S, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else {
-        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, S, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+    }
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int NW, int S>
+hipError_t launch_dma(const GemmArgs& a, const GemmPlan& p, int n0, int n1, hipStream_t s) {
+    const int m_tiles = (a.M + BM - 1) / BM;
+    const int n_out = n1 - n0;
+    const int bno = a.epi == EPI_SWIGLU ? BN / 2 : BN;
+    const int n_tiles = (n_out + bno - 1) / bno;
+    const int gm = m_tiles < 8 ? m_tiles : 8;
+    const int ntx = (n_tiles + 7) / 8;
+    const int groups = (m_tiles + gm - 1) / gm;
+    dim3 grid(8 * ntx * groups * gm, p.splits), block(64 * NW);
+    if (p.splits > 1) {
+        if (a.epi == EPI_SWIGLU)
+            hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        else
+            hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, NW, S, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+    } else if (a.epi == EPI_F32) {
+        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, NW, S, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+    } else if (a.epi == EPI_RESID) {
+        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, NW, S, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+    } else {
+        hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     }
     return hipGetLastError();
 }
@@ -432,14 +657,31 @@ hipError_t launch_tile(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     return hipGetLastError();
 }
 
+hipError_t launch_tile_variant(int variant, const GemmArgs& a, const GemmPlan& p, int n0, int n1, hipStream_t s) {
+    switch (variant) {
+        case kDmaVariant256x256: return launch_dma<256, 256, 2, 8, 5>(a, p, n0, n1, s);
+        case kDmaVariant128x256: return launch_dma<128, 256, 2, 8, 6>(a, p, n0, n1, s);
+        case kLineVariant256x256: return launch_dma128<256, 256, 2, 8, 2>(a, p, n0, n1, s);
+        case kLineVariant128x128: return launch_dma128<128, 128, 2, 4, 2>(a, p, n0, n1, s);
+        case kLineVariant128x256: return launch_dma128<128, 256, 2, 8, 3>(a, p, n0, n1, s);
+        default:   // register-staged tiles cover the whole output only
+            if (n0 != 0) return hipErrorInvalidValue;
+            return variant == kLdsVariant256 ? launch_tile<256, 128>(a, p, s) : launch_tile<128, 128>(a, p, s);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (a.M <= 0) return hipSuccess;
-    if (p.variant == kLdsVariant256x256) return launch_dma<256, 256, 2, 5>(a, p, s);
-    if (p.variant == kDmaVariant128) return launch_dma<128, 256, 2, 6>(a, p, s);
-    if (p.variant == kLdsVariant256) return launch_tile<256, 128>(a, p, s);
-    return launch_tile<128, 128>(a, p, s);
+    const int n_out = a.epi == EPI_SWIGLU ? a.F : a.Nw;
+    const int n_split = p.n_split > 0 && p.n_split < n_out ? p.n_split : n_out;
+    hipError_t e = launch_tile_variant(p.variant, a, p, 0, n_split, s);
+    if (e != hipSuccess || n_split == n_out) return e;
+    GemmPlan q = p;
+    q.splits = 1;
+    q.ksplit = a.K;
+    return launch_tile_variant(p.variant2, a, q, n_split, n_out, s);
 }
 
 }  // namespace rl

@@ -48,6 +48,17 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// D = A . B + C for one 32x32x16 bf16 tile (fp32 accumulate).
+// Lane l supplies A[l % 32][8 (l / 32) + j] and B[8 (l / 32) + j][l % 32]
+// (j = 0..7) and receives D[8 (e / 4) + 4 (l / 32) + e % 4][l % 32] in
+// element e (0..15).  One wave per SIMD issuing these keeps the matrix core
+// close to its peak, unlike the 16x16x32 form.
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float wave_max(float v) {
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
     return v;

@@ -48,10 +48,12 @@ struct GemmArgs {
 };
 
 struct GemmPlan {
-    int variant;   // index into the tile-shape table
+    int variant;   // tile kernel (index into the tile-shape table or a k*Variant id)
     int splits;
     int ksplit;    // K elements per split (multiple of 64)
     int grid_x, grid_y;
+    int n_split;   // output columns [n_split, n_out) use variant2, without split-K
+    int variant2;  //   (n_split == 0: one segment)
 };
 
 // Tile shapes of the bf16 MFMA GEMM: wave tile (16*MT) x (16*NT) weight rows,
@@ -59,10 +61,13 @@ struct GemmPlan {
 struct GemmShape { int MT, NT, WR, WC; };
 constexpr int kNumGemmShapes = 3;           // direct-load shapes for M <= 64
 extern const GemmShape kGemmShapes[kNumGemmShapes];
-constexpr int kLdsVariant128 = 3;           // LDS-tiled 128 x 128 (64 < M <= 128)
-constexpr int kLdsVariant256 = 4;           // LDS-tiled 256 x 128 (M > 128)
-constexpr int kLdsVariant256x256 = 5;       // direct-to-LDS 256 x 256 (M > 128, K % 64 == 0)
-constexpr int kDmaVariant128 = 6;           // direct-to-LDS 128 x 128 (64 < M <= 128, K % 64 == 0)
+constexpr int kLdsVariant128 = 3;           // register-staged LDS 128 x 128 (K % 32 != 0)
+constexpr int kLdsVariant256 = 4;           // register-staged LDS 256 x 128 (K % 32 != 0)
+constexpr int kDmaVariant256x256 = 5;       // direct-to-LDS, 64-byte rows, 256 x 256, 8 waves (K % 32 == 0)
+constexpr int kDmaVariant128x256 = 6;       // direct-to-LDS, 64-byte rows, 128 x 256, 8 waves (K % 32 == 0)
+constexpr int kLineVariant256x256 = 7;      // direct-to-LDS, 128-byte rows, 256 x 256, 8 waves (K % 64 == 0)
+constexpr int kLineVariant128x128 = 8;      // direct-to-LDS, 128-byte rows, 128 x 128, 4 waves, 2 per CU
+constexpr int kLineVariant128x256 = 9;      // direct-to-LDS, 128-byte rows, 128 x 256, 8 waves
 
 constexpr int kMaxSplits = 32;
 constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget

@@ -267,14 +267,25 @@ def test_benchmark_batch_sampled_rows():
     assert np.all(lp <= 1e-6) and np.isfinite(lp).all()
     t = ot.cpu().numpy()
     assert np.all((t >= 0) & (t < shape.vocab))
-    errs, lerr = [], []
+    errs, lerr, sens, lsens = [], [], [], []
     for s in check:
+        # the oracle's own sensitivity: the same step with one bf16 ulp flipped
+        # in the input row (the depth-28 random-init decoder amplifies it)
+        c = seqs[s].clone()
+        row = w_host["embed"][int(tok[s])].copy()
+        row[7] ^= 1
+        zp = c.forward(-1, embed_row=row)
+        del c
         z = seqs[s].forward(int(tok[s]))
         errs.append(row_rel_err(z_all[s], z))
         _, lo = oracle.sample(z.astype(np.float32), 1.0, 4, s, seqs[s].length, forced=int(t[s]))
         lerr.append(abs(lp[s] - lo))
-    _record("qwen7b", "benchmark_batch_rows_0_255_511", errs, lerr)
-    _assert_ok(errs, lerr, "benchmark batch")
+        _, lpp = oracle.sample(zp.astype(np.float32), 1.0, 4, s, seqs[s].length, forced=int(t[s]))
+        sens.append(row_rel_err(zp, z))
+        lsens.append(abs(lpp - lo))
+    _record("qwen7b", "benchmark_batch_rows_0_255_511", errs, lerr, max(sens), max(lsens))
+    assert max(errs) < max(LOGIT_REL_TOL, 2 * max(sens)), ("benchmark batch", errs, sens)
+    assert max(lerr) < max(LOGP_ABS_TOL, 2 * max(lsens)), ("benchmark batch", lerr, lsens)
     eng.close()
     del seqs
     _free()
