@@ -32,10 +32,10 @@ namespace {
 // round (every CU busy) per 1024 k, in microseconds.  A lone 128 x 128
 // workgroup on a CU runs faster than a co-resident pair (t_alone).
 struct TileKernel { int variant, BM, BN, per_cu; double t_round, t_alone; };
-constexpr TileKernel kLineTiles[] = {
+constexpr TileKernel kLineTiles[] = {   // ties go to the earlier entry
     {kLineVariant256x256, 256, 256, 1, 29.0, 29.0},
-    {kLineVariant128x256, 128, 256, 1, 18.2, 18.2},
     {kLineVariant128x128, 128, 128, 2, 19.0, 12.0},
+    {kLineVariant128x256, 128, 256, 1, 18.2, 18.2},
 };
 constexpr int kCUs = 256;
 
@@ -54,61 +54,57 @@ long tiles_of(const TileKernel& t, int M, int n_cols, int epi) {
 
 }  // namespace
 
-// Plan of one bf16 GEMM.  M <= 64: direct-load kernel, split K until the
-// weight stream fills the CUs.  M > 64 (K % 64 == 0): the cheapest of
-// (a) one tile kernel with split-K s (partials summed by splitk_reduce),
-// (b) 256 x 256 tiles for whole rounds plus a smaller tile kernel for the
-//     remaining output columns, under a cost model of rounds x round time
-//     + partial-sum traffic + output traffic.
-GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
+// Direct-load kernel plan for M <= 64 (its own split-K heuristic: split until
+// about 1024 workgroups stream the weight).
+GemmPlan plan_direct(int M, int Nw, int K, int epi, int F) {
     GemmPlan p{};
     const int n_out = epi == EPI_SWIGLU ? F : Nw;
-    p.n_split = 0;
-    if (M > 64 && K % 64 == 0) {
-        const double kf = K / 1024.0;
-        const double out_us = (epi == EPI_F32 ? 4.0 : epi == EPI_RESID ? 8.0 : 2.0) * M * n_out / 4.0e6;
-        double best = 1e30;
-        for (const TileKernel& t : kLineTiles) {
-            const long tiles = tiles_of(t, M, n_out, epi);
-            for (int s = 1; s <= kMaxSplits; s *= 2) {
-                const int ks = ceil_div(ceil_div(K, s), 64) * 64;
-                const int splits = ceil_div(K, ks);
-                if (splits != s && s > 1) break;
-                if (s > 1 && (ks < 256 || static_cast<size_t>(s) * M * Nw > kPartCapFloats)) break;
-                double us = rounds_us(t, tiles * s, ks / 1024.0) + out_us;
-                if (s > 1) us += 8.0 * s * M * static_cast<double>(Nw) / 3.0e6 + 4.0;
-                if (us < best * 0.98) {
-                    best = us;
-                    p.variant = t.variant; p.splits = s; p.ksplit = ks; p.n_split = 0;
-                }
-            }
-        }
-        // whole rounds of 256 x 256 tiles, then the rest of the columns
-        const TileKernel& big = kLineTiles[0];
-        const long big_tiles = tiles_of(big, M, n_out, epi);
-        const int m_tiles = ceil_div(M, big.BM);
-        const int bno = epi == EPI_SWIGLU ? big.BN / 2 : big.BN;
-        const long full_cols = (big_tiles / kCUs) * kCUs / m_tiles;   // n tiles of whole rounds
-        if (full_cols > 0 && full_cols * bno < n_out) {
-            const int n_split = static_cast<int>(full_cols * bno);
-            for (int v = 1; v < 3; ++v) {
-                const TileKernel& t = kLineTiles[v];
-                const double us = rounds_us(big, full_cols * m_tiles, kf) +
-                                  rounds_us(t, tiles_of(t, M, n_out - n_split, epi), kf) + out_us + 4.0;
-                if (us < best * 0.98) {
-                    best = us;
-                    p.variant = big.variant; p.splits = 1; p.ksplit = K;
-                    p.n_split = n_split; p.variant2 = t.variant;
-                }
-            }
-        }
-        p.grid_x = p.grid_y = 0;
-        return p;
+    p.variant = M <= 16 ? 0 : M <= 32 ? 1 : 2;
+    const GemmShape& s = kGemmShapes[p.variant];
+    const int BM = 16 * s.MT * s.WR;
+    const int BNw = 16 * s.NT * s.WC;
+    const int BNo = epi == EPI_SWIGLU ? BNw / 2 : BNw;
+    p.grid_x = ceil_div(n_out, BNo);
+    p.grid_y = ceil_div(M, BM);
+    const long tiles = static_cast<long>(p.grid_x) * p.grid_y;
+    // smallest K slice per split: partial sums cost 4*M bytes per output for
+    // every 2*slice bytes of weight read, so tiny batches can split finely
+    const int min_ks = M <= 16 ? 128 : M <= 32 ? 256 : 512;
+    int S = 1;
+    while (tiles * S * 2 <= 1024 && ceil_div(K, 2 * S) >= min_ks &&
+           static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
+        S *= 2;
+    const int ks = ceil_div(ceil_div(K, S), 64) * 64;
+    p.ksplit = ks;
+    p.splits = ceil_div(K, ks);
+    return p;
+}
+
+// Plan of one bf16 GEMM: the cheapest of
+//  (a) the direct-load kernel (M <= 16, or M <= 64 when K % 64 != 0),
+//  (b) one LDS tile kernel with split-K s (partials summed by splitk_reduce),
+//  (c) 256 x 256 tiles for whole rounds plus a smaller tile kernel for the
+//      remaining output columns,
+// under a cost model (microseconds): rounds x measured round time, partial-sum
+// and output traffic, a fixed pipeline cost for tile kernels on small batches,
+// and a floor at the HBM rate for the weight stream.  K % 64 != 0 (not used by
+// the decoder shapes) falls back to the 64-byte-row / register-staged tiles.
+GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
+    const int n_out = epi == EPI_SWIGLU ? F : Nw;
+    const double wbytes = 2.0 * Nw * K;
+    const double floor_us = wbytes / 5.2e6;
+    const double out_us = (epi == EPI_F32 ? 4.0 : epi == EPI_RESID ? 8.0 : 2.0) * M * n_out / 4.0e6;
+    auto reduce_us = [&](int s) { return s > 1 ? 8.0 * s * M * static_cast<double>(Nw) / 3.0e6 + 4.0 : 0.0; };
+
+    GemmPlan best_p{};
+    double best = 1e30;
+    if (M <= 16 || (M <= 64 && K % 64 != 0)) {
+        best_p = plan_direct(M, Nw, K, epi, F);
+        best = wbytes / 4.6e6 * (1.0 + M / 60.0) + reduce_us(best_p.splits) + 2.0;
     }
-    long tiles;
-    long target;
-    if (M > 64) {
-        // register-staged / 64-byte-row kernels (K % 64 != 0)
+    if (K % 64 != 0) {
+        if (M <= 64) return best_p;
+        GemmPlan p{};
         int BM, BN;
         if (K % 32 == 0) {
             p.variant = M > 128 ? kDmaVariant256x256 : kDmaVariant128x256; BM = M > 128 ? 256 : 128; BN = 256;
@@ -118,33 +114,55 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
         const int bno = epi == EPI_SWIGLU ? BN / 2 : BN;
         p.grid_x = ceil_div(n_out, bno);
         p.grid_y = ceil_div(M, BM);
-        tiles = static_cast<long>(p.grid_x) * p.grid_y;
-        target = 240;
-    } else {
-        p.variant = M <= 16 ? 0 : M <= 32 ? 1 : 2;
-        const GemmShape& s = kGemmShapes[p.variant];
-        const int BM = 16 * s.MT * s.WR;
-        const int BNw = 16 * s.NT * s.WC;
-        const int BNo = epi == EPI_SWIGLU ? BNw / 2 : BNw;
-        p.grid_x = ceil_div(n_out, BNo);
-        p.grid_y = ceil_div(M, BM);
-        tiles = static_cast<long>(p.grid_x) * p.grid_y;
-        target = 1024;
+        const long tiles = static_cast<long>(p.grid_x) * p.grid_y;
+        int S = 1;
+        while (tiles * S * 2 <= 240 && ceil_div(K, 2 * S) >= 256 &&
+               static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
+            S *= 2;
+        const int ks = ceil_div(ceil_div(K, S), 64) * 64;
+        p.ksplit = ks;
+        p.splits = ceil_div(K, ks);
+        return p;
     }
-    // smallest K slice per split: partial sums cost 4*M bytes per output for
-    // every 2*slice bytes of weight read, so tiny batches can split finely
-    const int min_ks = M > 64 ? 256 : M <= 16 ? 128 : M <= 32 ? 256 : 512;
-    int S = 1;
-    while (tiles * S * 2 <= target && ceil_div(K, 2 * S) >= min_ks &&
-           static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
-        S *= 2;
-    if (M > 64 && tiles * S < target && ceil_div(K, 2 * S) >= min_ks &&
-        static_cast<size_t>(2 * S) * M * Nw <= kPartCapFloats && 2 * S <= kMaxSplits)
-        S *= 2;
-    const int ks = ceil_div(ceil_div(K, S), 64) * 64;   // multiple of 64 (and so of 32)
-    p.ksplit = ks;
-    p.splits = ceil_div(K, ks);
-    return p;
+    const double fixed = M <= 64 ? 5.0 : 0.0;
+    for (const TileKernel& t : kLineTiles) {
+        const long tiles = tiles_of(t, M, n_out, epi);
+        for (int s = 1; s <= kMaxSplits; s *= 2) {
+            const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+            if (s > 1 && (ceil_div(K, ks) != s || ks < 256 || static_cast<size_t>(s) * M * Nw > kPartCapFloats))
+                break;
+            double us = rounds_us(t, tiles * s, ks / 1024.0);
+            us = (us > floor_us ? us : floor_us) + out_us + reduce_us(s) + fixed;
+            if (us < best * 0.98) {
+                best = us;
+                best_p = GemmPlan{};
+                best_p.variant = t.variant; best_p.splits = s; best_p.ksplit = ks;
+            }
+        }
+    }
+    // whole rounds of 256 x 256 tiles, then the rest of the columns
+    const TileKernel& big = kLineTiles[0];
+    const long big_tiles = tiles_of(big, M, n_out, epi);
+    const int m_tiles = ceil_div(M, big.BM);
+    const int bno = epi == EPI_SWIGLU ? big.BN / 2 : big.BN;
+    const long full_cols = (big_tiles / kCUs) * kCUs / m_tiles;   // n tiles of whole rounds
+    if (full_cols > 0 && full_cols * bno < n_out) {
+        const int n_split = static_cast<int>(full_cols * bno);
+        const double kf = K / 1024.0;
+        for (int v = 1; v < 3; ++v) {
+            const TileKernel& t = kLineTiles[v];
+            double us = rounds_us(big, full_cols * m_tiles, kf) +
+                        rounds_us(t, tiles_of(t, M, n_out - n_split, epi), kf);
+            us = (us > floor_us ? us : floor_us) + out_us + 4.0 + fixed;
+            if (us < best * 0.98) {
+                best = us;
+                best_p = GemmPlan{};
+                best_p.variant = big.variant; best_p.splits = 1; best_p.ksplit = K;
+                best_p.n_split = n_split; best_p.variant2 = t.variant;
+            }
+        }
+    }
+    return best_p;
 }
 
 // ---------------------------------------------------------------------------
