@@ -33,6 +33,16 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
+# HBM traffic of the attention kernel per algorithmic byte, from two
+# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over the first 48 decode
+# steps of this workload, each counter scaled by what it reads for the
+# library's plain copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x
+# 1.0): 716.0 MB fetched + 23.3 MB written per launch against 700.9 MB
+# algorithmic.  Valid for the attention kernel as of that measurement; set to
+# None when the kernel changes until the counters are taken again.
+ATTN_TRAFFIC_PER_ALG_BYTE = 1.0548
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -43,7 +53,25 @@ def parse():
     ap.add_argument("--breakdown", action="store_true",
                     help="time every kernel class (adds event overhead; diagnostics only)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run the library's plain copy kernel over this many MiB, 4 times "
+                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters against a known size)")
     return ap.parse_args()
+
+
+def copy_probe(mib: int):
+    import torch
+
+    from paper_2509_15965_amd.rl_decode import probe_copy
+    n = mib << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        probe_copy(dst, src, n)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 4}), flush=True)
 
 
 def cpu_baseline(shape, weights, seconds: float):
@@ -74,6 +102,9 @@ def cpu_baseline(shape, weights, seconds: float):
 
 def main():
     args = parse()
+    if args.copy_probe_mib > 0:
+        copy_probe(args.copy_probe_mib)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -202,9 +233,15 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    if dom == "attention" and ATTN_TRAFFIC_PER_ALG_BYTE is not None:
+        roof["traffic"] = round(ATTN_TRAFFIC_PER_ALG_BYTE * d["alg_bytes"] / max(1, d["launches"]))
     roof.update({"kernel": dom, "launches": d["launches"], "avg_launch_ms": round(avg_ms, 5),
                  "alg_bytes_per_launch": round(d["alg_bytes"] / max(1, d["launches"]))})
 
+    classes = {c: {"launches": stats[c]["launches"],
+                   "avg_launch_ms": round(stats[c]["total_ms"] / max(1, stats[c]["launches"]), 5),
+                   "alg_bytes_per_launch": round(stats[c]["alg_bytes"] / max(1, stats[c]["launches"]))}
+               for c in prof_classes}
     all_bytes = sum(v["alg_bytes"] for k, v in stats.items() if k not in ("splitk_reduce", "attn_combine"))
     prompt_tokens = int(plens.sum())
     gen_total = gen
@@ -234,6 +271,7 @@ def main():
         "paper_style_tokens_per_s": round((prompt_tokens + gen_total + n_seq) / (wall + prefill_s), 1)
         if steps == max_steps else None,
         "roofline": roof,
+        "timed_classes": classes,
     }
     if breakdown:
         out["breakdown_first_64_steps"] = breakdown
