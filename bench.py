@@ -40,7 +40,7 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 # 1.0): 716.0 MB fetched + 23.3 MB written per launch against 700.9 MB
 # algorithmic.  Valid for the attention kernel as of that measurement; set to
 # None when the kernel changes until the counters are taken again.
-ATTN_TRAFFIC_PER_ALG_BYTE = 1.0548
+ATTN_TRAFFIC_PER_ALG_BYTE = None
 
 
 def parse():

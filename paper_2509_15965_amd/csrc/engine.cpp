@@ -21,7 +21,7 @@ constexpr uint32_t kMagic = 0x524C4443u;   // "RLDC"
 constexpr uint32_t kDead = 0xDEADDEADu;
 constexpr int kStages = 3;                  // pinned metadata staging ring
 constexpr int kPartItems = 8192;            // split-KV partial slots per call
-constexpr int kAttnWaveTarget = 4096;       // split-KV parallelism target (waves)
+constexpr int kAttnWaveTarget = 1024;       // split-KV: keep about one wave per SIMD, each as long as possible
 constexpr int kPrefillChunk = 1024;         // default keys per prefill work item
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }

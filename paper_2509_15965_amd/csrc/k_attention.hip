@@ -37,7 +37,7 @@ __device__ __forceinline__ u32x4 mask_tail8(u32x4 v, int nvalid) {
 }
 
 template <int D, bool PF>
-__global__ void __launch_bounds__(256) attn_bf16_kernel(const AttnItem* __restrict__ items,
+__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __restrict__ items,
         int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
         const uint16_t* __restrict__ vc, int S, int Hq, int Hkv, int cap, int layer,
         float scale_log2, uint16_t* __restrict__ out, float* __restrict__ part) {
@@ -194,9 +194,10 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
     if (n_items <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     dim3 grid((n_items + 3) / 4, Hkv), block(256);
-    // Prefetching the next step doubles the K/V registers (one wave per SIMD
-    // at head_dim 128): worth it only when there are enough waves to fill the chip.
-    const bool pf = static_cast<long>(n_items) * Hkv >= 4096;
+    // Each wave keeps the next 32-position step's K/V loads in flight while it
+    // computes the current one; at two waves per SIMD (<= 256 registers) that
+    // is the most bytes in flight the register file allows.
+    const bool pf = true;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
                            static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
