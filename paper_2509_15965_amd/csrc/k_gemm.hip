@@ -32,10 +32,11 @@ namespace {
 // round (every CU busy) per 1024 k, in microseconds.  A lone 128 x 128
 // workgroup on a CU runs faster than a co-resident pair (t_alone).
 struct TileKernel { int variant, BM, BN, per_cu; double t_round, t_alone; };
-constexpr TileKernel kLineTiles[] = {   // ties go to the earlier entry
-    {kLineVariant256x256, 256, 256, 1, 29.0, 29.0},
-    {kLineVariant128x128, 128, 128, 2, 19.0, 12.0},
-    {kLineVariant128x256, 128, 256, 1, 18.2, 18.2},
+constexpr TileKernel kLineTiles[] = {   // ties go to the earlier entry (weights not cache resident)
+    {kLineVariant256x256, 256, 256, 1, 31.0, 31.0},
+    {kLineVariant128x128, 128, 128, 2, 20.3, 15.0},
+    {kLineVariant128x256, 128, 256, 1, 19.5, 19.5},
+    {kLineVariant128x128Deep, 128, 128, 1, 12.0, 12.0},
 };
 constexpr int kCUs = 256;
 
@@ -81,7 +82,8 @@ GemmPlan plan_direct(int M, int Nw, int K, int epi, int F) {
 }
 
 // Plan of one bf16 GEMM: the cheapest of
-//  (a) the direct-load kernel (M <= 16, or M <= 64 when K % 64 != 0),
+//  (a) the direct-load kernel (M <= 16, or M <= 64 when K % 64 != 0) or the
+//      GEMV-shaped kernel (M <= 32, no split-K),
 //  (b) one LDS tile kernel with split-K s (partials summed by splitk_reduce),
 //  (c) 256 x 256 tiles for whole rounds plus a smaller tile kernel for the
 //      remaining output columns,
@@ -100,7 +102,21 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     double best = 1e30;
     if (M <= 16 || (M <= 64 && K % 64 != 0)) {
         best_p = plan_direct(M, Nw, K, epi, F);
-        best = wbytes / 4.6e6 * (1.0 + M / 60.0) + reduce_us(best_p.splits) + 2.0;
+        best = wbytes / 3.6e6 * (1.0 + M / 60.0) + reduce_us(best_p.splits) + 2.0;
+    }
+    if (M <= 32 && K % 64 == 0) {
+        // GEMV-shaped kernel: a CU streams ~24 GB/s of its workgroups' 16
+        // weight rows; each workgroup also reads the M activation rows from L2
+        // (measured to cost ~0.65 of the same bytes of weight)
+        const double wg_bytes = 16.0 * K * 2.0 * (1.0 + 0.65 * M / 16.0);
+        const long wgs = epi == EPI_SWIGLU ? ceil_div(F, 8) : ceil_div(Nw, 16);
+        const long per_cu = (wgs + kCUs - 1) / kCUs;
+        const double us = per_cu * wg_bytes / 24.0e3 + 3.0 + out_us;
+        if (us < best * 0.98) {
+            best = us;
+            best_p = GemmPlan{};
+            best_p.variant = kGemvVariant; best_p.splits = 1; best_p.ksplit = K;
+        }
     }
     if (K % 64 != 0) {
         if (M <= 64) return best_p;
@@ -149,7 +165,7 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     if (full_cols > 0 && full_cols * bno < n_out) {
         const int n_split = static_cast<int>(full_cols * bno);
         const double kf = K / 1024.0;
-        for (int v = 1; v < 3; ++v) {
+        for (int v = 1; v < 4; ++v) {
             const TileKernel& t = kLineTiles[v];
             double us = rounds_us(big, full_cols * m_tiles, kf) +
                         rounds_us(t, tiles_of(t, M, n_out - n_split, epi), kf);
@@ -319,14 +335,122 @@ static hipError_t launch_shape(const GemmArgs& a, const GemmPlan& p, hipStream_t
     return hipGetLastError();
 }
 
+hipError_t launch_gemv(const GemmArgs& a, hipStream_t s);
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (a.M <= 0) return hipSuccess;
     switch (p.variant) {
         case 0: return launch_shape<1, 4, 1, 4>(a, p, s);
         case 1: return launch_shape<2, 4, 1, 4>(a, p, s);
         case 2: return launch_shape<4, 4, 1, 4>(a, p, s);
+        case kGemvVariant: return launch_gemv(a, s);
         default: return launch_gemm_bf16_lds(a, p, s);
     }
+}
+
+// ---------------------------------------------------------------------------
+// GEMV-shaped kernel for M <= 32: one workgroup (8 waves) owns 16 weight rows
+// (SwiGLU: 8 gate rows and the matching 8 up rows) and the whole K.  Wave w
+// takes the w-th eighth of K, streams its weight and activation fragments
+// straight from global memory (16-byte loads, four 64-wide k blocks in flight
+// per wave) into 16x16x32 MFMAs, and the eight partial 16x16 tiles are summed
+// through LDS in wave order (deterministic) before the epilogue.  No split-K
+// partials and no reduction kernel.
+// ---------------------------------------------------------------------------
+template <int MR, int EPI>
+__global__ void __launch_bounds__(512) gemv_kernel(GemmArgs p, int kw) {
+    constexpr int U = 4;   // 64-wide k blocks per batch of loads
+    __shared__ f32x4 red[8][MR][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const int M = p.M, K = p.K;
+
+    int n;
+    bool ok;
+    if (EPI == EPI_SWIGLU) {
+        const int c = blockIdx.x * 8 + (r16 & 7);
+        ok = c < p.F;
+        n = r16 < 8 ? c : p.F + c;
+    } else {
+        n = blockIdx.x * 16 + r16;
+        ok = n < p.Nw;
+    }
+    const uint16_t* wp = static_cast<const uint16_t*>(p.W) + static_cast<size_t>(ok ? n : 0) * p.ldw + 8 * kq;
+    const uint16_t* ap[MR];
+    bool aok[MR];
+#pragma unroll
+    for (int i = 0; i < MR; ++i) {
+        const int m = 16 * i + r16;
+        aok[i] = m < M;
+        ap[i] = static_cast<const uint16_t*>(p.A) + static_cast<size_t>(aok[i] ? m : 0) * p.lda + 8 * kq;
+    }
+    const int kb = wave * kw;
+    const int ke = min(K, kb + kw);
+
+    f32x4 acc[MR];
+#pragma unroll
+    for (int i = 0; i < MR; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int k0 = kb; k0 < ke; k0 += 64 * U) {
+        u32x4 wf[U][2], af[U][2][MR];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int kk = k0 + 64 * u + 32 * j;
+                const bool kok = kk + 8 * kq < ke;
+                wf[u][j] = (ok && kok) ? ld16(wp + kk) : zero;
+#pragma unroll
+                for (int i = 0; i < MR; ++i) af[u][j][i] = (aok[i] && kok) ? ld16(ap[i] + kk) : zero;
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int i = 0; i < MR; ++i)
+                    acc[i] = mfma16x16x32(as_bf16x8(af[u][j][i]), as_bf16x8(wf[u][j]), acc[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < MR; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    if (wave >= MR) return;
+    // wave i sums A tile i over the 8 waves in order; lane holds D[4 kq + e][r16]
+    f32x4 v = red[0][wave][lane];
+#pragma unroll
+    for (int w = 1; w < 8; ++w) v += red[w][wave][lane];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int m = 16 * wave + 4 * kq + e;
+        const float val = v[e];
+        if (EPI == EPI_SWIGLU) {
+            const float up = __shfl(val, (lane & ~15) | ((r16 + 8) & 15), 64);
+            if (r16 < 8 && ok && m < M) {
+                const float silu = val / (1.0f + expf(-val));
+                static_cast<uint16_t*>(p.act)[static_cast<size_t>(m) * p.ld_act + n] = f32_to_bf16(silu * up);
+            }
+        } else if (ok && m < M) {
+            if (EPI == EPI_F32) p.out_f32[static_cast<size_t>(m) * p.ldo + n] = val;
+            else p.resid[static_cast<size_t>(m) * p.ldr + n] += val;
+        }
+    }
+}
+
+hipError_t launch_gemv(const GemmArgs& a, hipStream_t s) {
+    const int kw = ceil_div(ceil_div(a.K, 8), 64) * 64;
+    const int blocks = a.epi == EPI_SWIGLU ? ceil_div(a.F, 8) : ceil_div(a.Nw, 16);
+    dim3 grid(blocks), block(512);
+#define RL_GV(MR)                                                                                        \
+    do {                                                                                                 \
+        if (a.epi == EPI_F32) hipLaunchKernelGGL((gemv_kernel<MR, EPI_F32>), grid, block, 0, s, a, kw);   \
+        else if (a.epi == EPI_RESID) hipLaunchKernelGGL((gemv_kernel<MR, EPI_RESID>), grid, block, 0, s, a, kw); \
+        else hipLaunchKernelGGL((gemv_kernel<MR, EPI_SWIGLU>), grid, block, 0, s, a, kw);                 \
+    } while (0)
+    if (a.M <= 16) RL_GV(1);
+    else if (a.M <= 32) RL_GV(2);
+    else return hipErrorInvalidValue;
+#undef RL_GV
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -664,6 +664,7 @@ hipError_t launch_tile_variant(int variant, const GemmArgs& a, const GemmPlan& p
         case kLineVariant256x256: return launch_dma128<256, 256, 2, 8, 2>(a, p, n0, n1, s);
         case kLineVariant128x128: return launch_dma128<128, 128, 2, 4, 2>(a, p, n0, n1, s);
         case kLineVariant128x256: return launch_dma128<128, 256, 2, 8, 3>(a, p, n0, n1, s);
+        case kLineVariant128x128Deep: return launch_dma128<128, 128, 2, 4, 4>(a, p, n0, n1, s);
         default:   // register-staged tiles cover the whole output only
             if (n0 != 0) return hipErrorInvalidValue;
             return variant == kLdsVariant256 ? launch_tile<256, 128>(a, p, s) : launch_tile<128, 128>(a, p, s);

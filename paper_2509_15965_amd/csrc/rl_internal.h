@@ -68,6 +68,8 @@ constexpr int kDmaVariant128x256 = 6;       // direct-to-LDS, 64-byte rows, 128 
 constexpr int kLineVariant256x256 = 7;      // direct-to-LDS, 128-byte rows, 256 x 256, 8 waves (K % 64 == 0)
 constexpr int kLineVariant128x128 = 8;      // direct-to-LDS, 128-byte rows, 128 x 128, 4 waves, 2 per CU
 constexpr int kLineVariant128x256 = 9;      // direct-to-LDS, 128-byte rows, 128 x 256, 8 waves
+constexpr int kLineVariant128x128Deep = 10; // direct-to-LDS, 128-byte rows, 128 x 128, 4 waves, 4-stage ring
+constexpr int kGemvVariant = 11;            // M <= 32: 16 weight rows x all K per 8-wave workgroup, no split-K
 
 constexpr int kMaxSplits = 32;
 constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget
