@@ -247,11 +247,36 @@ typedef enum rl_option {
                                 else a multiple of 32 in [32, 65536]; doubled
                                 as needed so no sequence has more than 64
                                 chunks                                         */
-    RL_OPT_PROFILE = 2       /* bit mask over rl_kernel_class: launches of the
+    RL_OPT_PROFILE = 2,      /* bit mask over rl_kernel_class: launches of the
                                 selected classes are timed with HIP events on
                                 the context's stream; 0 = off (default),
                                 -1 = every class                              */
+    RL_OPT_GEMM_PLAN = 3     /* bf16 GEMM kernel override (testing every tile
+                                kernel on small models): 0 = the cost-model
+                                planner (default); else
+                                  bits 0-7:   rl_gemm_kernel of all columns
+                                              (or of the first half, below),
+                                  bits 8-15:  split-K count (0 or 1 = none,
+                                              else a power of two <= 32),
+                                  bits 16-23: rl_gemm_kernel of the second
+                                              half of the output columns
+                                              (0 = one segment; no split-K).
+                                A GEMM the override cannot serve (GEMV with
+                                M > 32, direct-load with M > 64, a tile kernel
+                                with K not a multiple of 64) keeps the
+                                planner's choice.  Results stay within the
+                                parity tolerances for every choice; the bits
+                                differ (fp32 summation order).               */
 } rl_option;
+
+typedef enum rl_gemm_kernel {
+    RL_GEMM_DIRECT = 1,      /* direct-load MFMA kernel (M <= 64)            */
+    RL_GEMM_GEMV = 2,        /* 16 weight rows x all K per workgroup (M <= 32) */
+    RL_GEMM_T256 = 3,        /* 256 x 256 tiles, 8 waves                      */
+    RL_GEMM_T128X256 = 4,    /* 128 x 256 tiles, 8 waves                      */
+    RL_GEMM_T128 = 5,        /* 128 x 128 tiles, 4 waves, two per CU          */
+    RL_GEMM_T128_DEEP = 6    /* 128 x 128 tiles, 4 waves, 4-stage ring        */
+} rl_gemm_kernel;
 
 rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value);
 

@@ -111,6 +111,7 @@ struct rl_decode_ctx {
     bool stage_used[kStages] = {false, false, false};
     int stage_next = 0;
     int64_t opt_chunk = 0;
+    int64_t opt_gemm = 0;             // RL_OPT_GEMM_PLAN
     uint32_t profile = 0;             // bit mask over kernel classes
     struct Pending { int kc; hipEvent_t a, b; };
     std::vector<Pending> pending;
@@ -279,7 +280,9 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
     hipError_t e;
     *splits = 0;
     if (c->bf16()) {
-        GemmPlan p = plan_gemm_bf16(M, Nw, K, epi, cf.ffn);
+        GemmPlan p;
+        if (c->opt_gemm == 0 || !plan_gemm_forced(M, Nw, K, epi, cf.ffn, c->opt_gemm, &p))
+            p = plan_gemm_bf16(M, Nw, K, epi, cf.ffn);
         {
             Prof pr(c, kc);
             e = launch_gemm_bf16(a, p, c->stream);
@@ -952,6 +955,16 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
                 return fail(ctx, RL_ERR_INVALID_ARG, "attention chunk must be 0 or a multiple of 32 in [32, 65536]");
             ctx->opt_chunk = value;
             return RL_OK;
+        case RL_OPT_GEMM_PLAN: {
+            const int64_t k1 = value & 0xff, sp = (value >> 8) & 0xff, k2 = (value >> 16) & 0xff;
+            const bool ok = value == 0 ||
+                            (value >= 0 && (value >> 24) == 0 && k1 >= RL_GEMM_DIRECT && k1 <= RL_GEMM_T128_DEEP &&
+                             (sp == 0 || (sp <= 32 && (sp & (sp - 1)) == 0)) &&
+                             (k2 == 0 || (k2 >= RL_GEMM_T128X256 && k2 <= RL_GEMM_T128_DEEP)));
+            if (!ok) return fail(ctx, RL_ERR_INVALID_ARG, "invalid GEMM plan override");
+            ctx->opt_gemm = value;
+            return RL_OK;
+        }
         case RL_OPT_PROFILE:
             if (value < -1 || value >= (int64_t(1) << RL_K_COUNT))
                 return fail(ctx, RL_ERR_INVALID_ARG, "profile must be a class bit mask or -1");

@@ -12,6 +12,7 @@
 // (k_gemm_lds.hip).
 //
 // fp32: a plain LDS-tiled VALU kernel (the tiny fp32 decoder only).
+#include "rl_decode.h"
 #include "rl_device.h"
 #include "rl_internal.h"
 
@@ -179,6 +180,70 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
         }
     }
     return best_p;
+}
+
+bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPlan* out) {
+    const int k1 = static_cast<int>(code & 0xff), s = static_cast<int>((code >> 8) & 0xff);
+    const int k2 = static_cast<int>((code >> 16) & 0xff);
+    const int n_out = epi == EPI_SWIGLU ? F : Nw;
+    auto tile = [](int k) {
+        switch (k) {
+            case RL_GEMM_T256: return kLineVariant256x256;
+            case RL_GEMM_T128X256: return kLineVariant128x256;
+            case RL_GEMM_T128: return kLineVariant128x128;
+            case RL_GEMM_T128_DEEP: return kLineVariant128x128Deep;
+            default: return -1;
+        }
+    };
+    auto out_width = [&](int v) {
+        const int bn = v == kLineVariant128x128 || v == kLineVariant128x128Deep ? 128 : 256;
+        return epi == EPI_SWIGLU ? bn / 2 : bn;
+    };
+    if (s != 0 && (s & (s - 1)) != 0) return false;
+    GemmPlan p{};
+    if (k1 == RL_GEMM_DIRECT) {
+        if (M > 64 || k2 != 0) return false;
+        p = plan_direct(M, Nw, K, epi, F);
+        if (s > 1) {
+            const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+            if (static_cast<size_t>(ceil_div(K, ks)) * M * Nw > kPartCapFloats) return false;
+            p.ksplit = ks;
+            p.splits = ceil_div(K, ks);
+        } else if (s == 1) {
+            p.ksplit = K;
+            p.splits = 1;
+        }
+        *out = p;
+        return true;
+    }
+    if (k1 == RL_GEMM_GEMV) {
+        if (M > 32 || K % 64 != 0 || k2 != 0) return false;
+        p.variant = kGemvVariant; p.splits = 1; p.ksplit = K;
+        *out = p;
+        return true;
+    }
+    const int v1 = tile(k1);
+    if (v1 < 0 || K % 64 != 0) return false;
+    p.variant = v1;
+    p.splits = 1;
+    p.ksplit = K;
+    if (k2 != 0) {
+        const int v2 = tile(k2);
+        if (v2 < 0) return false;
+        const int w = out_width(v1);
+        const int n_split = (n_out / 2) / w * w;
+        if (n_split <= 0) return false;
+        p.n_split = n_split;
+        p.variant2 = v2;
+    } else if (s > 1) {
+        const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+        const int splits = ceil_div(K, ks);
+        if (static_cast<size_t>(splits) * M * Nw > kPartCapFloats) return false;
+        p.ksplit = ks;
+        p.splits = splits;
+    }
+    *out = p;
+    return true;
 }
 
 // ---------------------------------------------------------------------------

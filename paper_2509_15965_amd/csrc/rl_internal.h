@@ -75,6 +75,8 @@ constexpr int kMaxSplits = 32;
 constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget
 
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F);
+// RL_OPT_GEMM_PLAN override; false when it cannot serve this GEMM
+bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPlan* p);
 
 // ---- launchers (enqueue only; return hipGetLastError()) -----------------
 // x = embedding rows; h = first-layer attention norm of x when h != nullptr

@@ -12,7 +12,9 @@ from harness import (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL, LOGIT_REL_TOL, LOGP_AB
                      build_models, check_token, inject_random_kv, row_rel_err)
 from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 from paper_2509_15965_amd.inputs import rollout_plan, uniform_tokens
-from paper_2509_15965_amd.rl_decode import RL_OPT_ATTN_CHUNK, Engine
+from paper_2509_15965_amd.rl_decode import (RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T128, RL_GEMM_T128_DEEP,
+                                           RL_GEMM_T128X256, RL_GEMM_T256, RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN,
+                                           Engine, gemm_plan_code)
 
 pytestmark = pytest.mark.gpu
 
@@ -31,7 +33,7 @@ def _free_memory():
 
 
 def teacher_forced_run(shape, seed, prompts, group, n_steps, T=1.0, sample_seed=5, max_ctx=None,
-                       embed_rows=None):
+                       embed_rows=None, gemm_plan=0):
     """Prefill `prompts` (group slots each), then n_steps decode steps that feed
     seeded forced tokens.  Returns per-step (gpu logits, oracle logits, gpu
     logp, oracle logp, gpu tokens, oracle sampled tokens)."""
@@ -40,6 +42,8 @@ def teacher_forced_run(shape, seed, prompts, group, n_steps, T=1.0, sample_seed=
     plens = [len(p) for p in prompts]
     max_ctx = max_ctx or (max(plens) + n_steps + 2)
     eng = Engine(shape, w_dev, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=sum(plens))
+    if gemm_plan:
+        eng.set_option(RL_OPT_GEMM_PLAN, gemm_plan)
     slots = list(range(n_seq))
     uids = [1000 + i for i in range(n_seq)]
     offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
@@ -304,3 +308,32 @@ def test_large_batch_gemm_tiles_match_oracle(n_prompts, plen):
     for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
         assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
         assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+
+
+_FORCED_PLANS = [
+    ("gemv", gemm_plan_code(RL_GEMM_GEMV)),
+    ("direct_s4", gemm_plan_code(RL_GEMM_DIRECT, 4)),
+    ("t256", gemm_plan_code(RL_GEMM_T256)),
+    ("t256_s4", gemm_plan_code(RL_GEMM_T256, 4)),
+    ("t128x256_s2", gemm_plan_code(RL_GEMM_T128X256, 2)),
+    ("t128", gemm_plan_code(RL_GEMM_T128)),
+    ("t128deep_s8", gemm_plan_code(RL_GEMM_T128_DEEP, 8)),
+    ("t256+t128", gemm_plan_code(RL_GEMM_T256, 0, RL_GEMM_T128)),
+    ("t256+t128x256", gemm_plan_code(RL_GEMM_T256, 0, RL_GEMM_T128X256)),
+    ("t128x256+t128deep", gemm_plan_code(RL_GEMM_T128X256, 0, RL_GEMM_T128_DEEP)),
+]
+
+
+@pytest.mark.parametrize("name,code", _FORCED_PLANS, ids=[n for n, _ in _FORCED_PLANS])
+def test_every_gemm_kernel_matches_oracle(name, code):
+    """Each bf16 GEMM tile kernel, split-K count and two-segment launch, forced
+    for every projection of a model whose dimensions are multiples of 64
+    (vocab ragged): prefill of 144 rows (tile kernels; the GEMV and direct-load
+    overrides fall back to the planner there) and decode at 24 rows."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e6, "bf16")
+    rng = np.random.default_rng(77)
+    prompts = [rng.integers(0, shape.vocab, size=6).astype(np.int32) for _ in range(24)]
+    res = teacher_forced_run(shape, 91, prompts, group=1, n_steps=2, T=1.0, gemm_plan=code)
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, (name, k)
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, (name, k)
