@@ -76,9 +76,64 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
         Elem<T>::store(orow, i, xr[i] * r * Elem<T>::load(g, i));
 }
 
+// The same norm with 16-byte accesses (H a multiple of 4): the row is read
+// once into registers (PER float4 per thread) and reused for the output.
+template <typename T, int PER>
+__global__ void __launch_bounds__(256) rmsnorm4_kernel(const float* __restrict__ x,
+        const int32_t* __restrict__ sel, int H, const T* __restrict__ g, float eps,
+        T* __restrict__ out) {
+    __shared__ float red[4];
+    const int o = blockIdx.x;
+    const int row = sel ? sel[o] : o;
+    const f32x4* xr = reinterpret_cast<const f32x4*>(x + static_cast<size_t>(row) * H);
+    const int H4 = H / 4;
+    f32x4 v[PER];
+    float ss = 0.0f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        v[j] = c < H4 ? xr[c] : f32x4{0.f, 0.f, 0.f, 0.f};
+        ss = fmaf(v[j][0], v[j][0], ss);
+        ss = fmaf(v[j][1], v[j][1], ss);
+        ss = fmaf(v[j][2], v[j][2], ss);
+        ss = fmaf(v[j][3], v[j][3], ss);
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    ss = red[0] + red[1] + red[2] + red[3];
+    const float r = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+    T* orow = out + static_cast<size_t>(o) * H;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        if (c < H4) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) Elem<T>::store(orow, 4 * c + e, v[j][e] * r * Elem<T>::load(g, 4 * c + e));
+        }
+    }
+}
+
 hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int H,
                           const void* g, float eps, void* out, hipStream_t s) {
     if (n <= 0) return hipSuccess;
+    const int per = (H / 4 + 255) / 256;
+    if (H % 4 == 0 && per <= 8) {
+#define RL_N4(P)                                                                                          \
+        do {                                                                                              \
+            if (dt == DT_BF16)                                                                            \
+                hipLaunchKernelGGL((rmsnorm4_kernel<uint16_t, P>), dim3(n), dim3(256), 0, s, x, sel, H,  \
+                                   static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(out));   \
+            else                                                                                          \
+                hipLaunchKernelGGL((rmsnorm4_kernel<float, P>), dim3(n), dim3(256), 0, s, x, sel, H,     \
+                                   static_cast<const float*>(g), eps, static_cast<float*>(out));         \
+        } while (0)
+        if (per <= 2) RL_N4(2);
+        else if (per <= 4) RL_N4(4);
+        else RL_N4(8);
+#undef RL_N4
+        return hipGetLastError();
+    }
     if (dt == DT_BF16)
         hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(n), dim3(256), 0, s, x, sel, H,
                            static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(out));

@@ -547,19 +547,68 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs p, int spli
     }
 }
 
+// Four consecutive columns per thread (n_out, Nw and the output strides
+// multiples of 4): 16-byte loads of every slice, issued before the in-order sum.
+template <typename T>
+__global__ void __launch_bounds__(256) splitk_reduce4_kernel(GemmArgs p, int splits,
+        const float* __restrict__ part) {
+    const int n_out = p.epi == EPI_SWIGLU ? p.F : p.Nw;
+    const size_t total4 = static_cast<size_t>(p.M) * n_out / 4;
+    const size_t slice = static_cast<size_t>(p.M) * p.Nw;
+    for (size_t i4 = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i4 < total4;
+         i4 += static_cast<size_t>(gridDim.x) * blockDim.x) {
+        const size_t idx = 4 * i4;
+        const int m = static_cast<int>(idx / n_out);
+        const int c = static_cast<int>(idx - static_cast<size_t>(m) * n_out);
+        const float* src = part + static_cast<size_t>(m) * p.Nw + c;
+        auto sum = [&](const float* b) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            int z = 0;
+            for (; z + 4 <= splits; z += 4) {
+                const f32x4 a0 = *reinterpret_cast<const f32x4*>(b + (z + 0) * slice);
+                const f32x4 a1 = *reinterpret_cast<const f32x4*>(b + (z + 1) * slice);
+                const f32x4 a2 = *reinterpret_cast<const f32x4*>(b + (z + 2) * slice);
+                const f32x4 a3 = *reinterpret_cast<const f32x4*>(b + (z + 3) * slice);
+                acc += a0; acc += a1; acc += a2; acc += a3;
+            }
+            for (; z < splits; ++z) acc += *reinterpret_cast<const f32x4*>(b + z * slice);
+            return acc;
+        };
+        const f32x4 v = sum(src);
+        if (p.epi == EPI_F32) {
+            *reinterpret_cast<f32x4*>(p.out_f32 + static_cast<size_t>(m) * p.ldo + c) = v;
+        } else if (p.epi == EPI_RESID) {
+            f32x4* r = reinterpret_cast<f32x4*>(p.resid + static_cast<size_t>(m) * p.ldr + c);
+            *r = *r + v;
+        } else {
+            const f32x4 u = sum(src + p.F);
+            T* act = static_cast<T*>(p.act) + static_cast<size_t>(m) * p.ld_act + c;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float silu = v[e] / (1.0f + expf(-v[e]));
+                Elem<T>::store(act, e, silu * u[e]);
+            }
+        }
+    }
+}
+
 hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const float* partial,
                                 hipStream_t s) {
     const int n_out = a.epi == EPI_SWIGLU ? a.F : a.Nw;
     const size_t total = static_cast<size_t>(a.M) * n_out;
     if (total == 0) return hipSuccess;
-    size_t blocks = (total + 255) / 256;
+    const int ld = a.epi == EPI_F32 ? a.ldo : a.epi == EPI_RESID ? a.ldr : a.ld_act;
+    const bool vec = n_out % 4 == 0 && a.Nw % 4 == 0 && ld % 4 == 0;
+    size_t blocks = ((vec ? total / 4 : total) + 255) / 256;
     if (blocks > 16384) blocks = 16384;
-    if (dt == DT_BF16)
-        hipLaunchKernelGGL(splitk_reduce_kernel<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                           a, splits, partial);
-    else
-        hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                           a, splits, partial);
+    const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+    if (vec) {
+        if (dt == DT_BF16) hipLaunchKernelGGL(splitk_reduce4_kernel<uint16_t>, grid, block, 0, s, a, splits, partial);
+        else hipLaunchKernelGGL(splitk_reduce4_kernel<float>, grid, block, 0, s, a, splits, partial);
+    } else {
+        if (dt == DT_BF16) hipLaunchKernelGGL(splitk_reduce_kernel<uint16_t>, grid, block, 0, s, a, splits, partial);
+        else hipLaunchKernelGGL(splitk_reduce_kernel<float>, grid, block, 0, s, a, splits, partial);
+    }
     return hipGetLastError();
 }
 
