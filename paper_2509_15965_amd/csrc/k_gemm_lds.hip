@@ -401,23 +401,42 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma_kernel(GemmArgs p, int kspli
 // serves full lines markedly faster than the half lines of the 64-byte-row
 // ring).  Chunk c of row r sits at c ^ ((r / 2) % 8), which keeps the 32x32
 // fragment reads free of bank conflicts.  A stage is 64 k (four 16-wide
-// sub-steps); the ring has S stages and the slot of stage kt takes stage
-// kt + S as soon as every wave has read all of stage kt.
+// sub-steps).  The activation tile (re-read by every weight tile, so mostly
+// L2 hits) and the weight tile (streamed from HBM) have rings of SA and
+// SW >= SA stages: the slot of stage kt takes stage kt + SA (kt + SW) as soon
+// as every wave has read all of stage kt, the activation DMA issued first so
+// that the in-order load counter lets the weight stream stay in flight
+// across the barrier (SW - 1 stages of lookahead for the weights).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int NW, int S, int EPI, bool SPLIT>
+// s_waitcnt vmcnt(<= n): rounded down to one of a few immediates (waiting for
+// fewer outstanding loads than allowed is always safe)
+__device__ __forceinline__ void wait_vm_atmost(int n) {
+    if (n >= 48) wait_vm<48>();
+    else if (n >= 32) wait_vm<32>();
+    else if (n >= 24) wait_vm<24>();
+    else if (n >= 16) wait_vm<16>();
+    else if (n >= 12) wait_vm<12>();
+    else if (n >= 8) wait_vm<8>();
+    else if (n >= 6) wait_vm<6>();
+    else if (n >= 4) wait_vm<4>();
+    else if (n >= 2) wait_vm<2>();
+    else wait_vm<0>();
+}
+
+template <int BM, int BN, int WM, int NW, int SA, int SW, int EPI, bool SPLIT>
 __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ksplit, int m_tiles, int n_tiles, int n0,
                                                               int gm) {
     constexpr int BK = 64, ROWB = 128;
     constexpr int WN = NW / WM;
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int MT = TM / 32, NT = TN / 32;
-    constexpr int STAGE = (BM + BN) * ROWB;
+    constexpr int ASTAGE = BM * ROWB, BSTAGE = BN * ROWB;
     constexpr int AQ = BM / (8 * NW), BQ = BN / (8 * NW);   // DMA instructions (8 rows each) per wave per stage
-    constexpr int Q = AQ + BQ;
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows must fill whole DMA instructions");
     static_assert(TM % 32 == 0 && TN % 64 == 0, "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
-    static_assert(S >= 2 && S - 1 <= 5, "ring depth");
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[S * STAGE];
+    static_assert(SA >= 2 && SW >= SA && SW <= 6, "ring depths");
+    static_assert(SA * AQ + SW * BQ < 64, "vmcnt range (most loads ever in flight)");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[SA * ASTAGE + SW * BSTAGE];
 
     const int w = blockIdx.x;
     const int xcd = w & 7, j = w >> 3;
@@ -474,13 +493,39 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         const int ch = (lane & 7) ^ (((8 * g + lrow) >> 1) & 7);
         boff[q] = static_cast<uint32_t>(n) * static_cast<uint32_t>(p.ldw) + 8u * ch;
     }
-    auto issue = [&](int stage, int k0) {
-        uint8_t* abase = smem + (stage % S) * STAGE;
-        uint8_t* bbase = abase + BM * ROWB;
+    uint8_t* const abuf = smem;
+    uint8_t* const bbuf = smem + SA * ASTAGE;
+    auto issue_a = [&](int stage) {
+        uint8_t* base = abuf + (stage % SA) * ASTAGE;
+        const int k0 = kb + stage * BK;
 #pragma unroll
-        for (int q = 0; q < AQ; ++q) dma16(A + aoff[q] + k0, abase + (wave * AQ + q) * 1024);
+        for (int q = 0; q < AQ; ++q) dma16(A + aoff[q] + k0, base + (wave * AQ + q) * 1024);
+    };
+    auto issue_w = [&](int stage) {
+        uint8_t* base = bbuf + (stage % SW) * BSTAGE;
+        const int k0 = kb + stage * BK;
 #pragma unroll
-        for (int q = 0; q < BQ; ++q) dma16(W + boff[q] + k0, bbase + (wave * BQ + q) * 1024);
+        for (int q = 0; q < BQ; ++q) dma16(W + boff[q] + k0, base + (wave * BQ + q) * 1024);
+    };
+    // Issue schedule: in (real or prologue) iteration i, A(i + SA) if in range,
+    // then W(i + SW) if in range; the prologue is iterations -SW .. -1.
+    auto issue_iter = [&](int i) {
+        if (i + SA >= 0 && i + SA < nk) issue_a(i + SA);
+        if (i + SW >= 0 && i + SW < nk) issue_w(i + SW);
+    };
+    // DMA instructions issued after the later of A(s), W(s), up to iteration `last`
+    auto after_stage = [&](int s, int last) {
+        const int ia = s - SA, iw = s - SW;   // issuing iterations
+        int n = 0, i0;
+        if (ia > iw) {                           // A(s) is issued after W(s): count W of its iteration
+            i0 = ia;
+            n += (i0 + SW >= 0 && i0 + SW < nk) ? BQ : 0;
+        } else {                                 // same iteration, W(s) last
+            i0 = iw;
+        }
+        for (int i = i0 + 1; i <= last; ++i)
+            n += ((i + SA >= 0 && i + SA < nk) ? AQ : 0) + ((i + SW >= 0 && i + SW < nk) ? BQ : 0);
+        return n;
     };
 
     f32x16 acc[MT][NT];
@@ -493,11 +538,11 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
 
     // every fragment row is r32 plus a multiple of 32, so the swizzle depends on r32 only
     const int swz = (r32 >> 1) & 7;
-    const uint32_t la = (wm * TM + r32) * ROWB, lb = (BM + wn * TN + r32) * ROWB;
+    const uint32_t la = (wm * TM + r32) * ROWB, lb = (wn * TN + r32) * ROWB;
     auto load_sub = [&](int stage, int ks, u32x4 (&fa)[MT], u32x4 (&fb)[NT]) {
-        const uint32_t so = static_cast<uint32_t>(stage % S) * STAGE + (((2 * ks + kh) ^ swz) << 4);
-        const uint8_t* pa = smem + so + la;
-        const uint8_t* pb = smem + so + lb;
+        const uint32_t ch = ((2 * ks + kh) ^ swz) << 4;
+        const uint8_t* pa = abuf + (stage % SA) * ASTAGE + ch + la;
+        const uint8_t* pb = bbuf + (stage % SW) * BSTAGE + ch + lb;
 #pragma unroll
         for (int i = 0; i < MT; ++i) fa[i] = *reinterpret_cast<const u32x4*>(pa + 32 * i * ROWB);
 #pragma unroll
@@ -518,17 +563,15 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         }
     };
 
-#pragma unroll
-    for (int st = 0; st < S; ++st)
-        if (st < nk) issue(st, kb + st * BK);
-    wait_stages<Q, S - 1>(min(S - 1, nk - 1));
+    for (int i = -SW; i < 0; ++i) issue_iter(i);
+    if (nk > 0) wait_vm_atmost(after_stage(0, -1));
     __syncthreads();
     u32x4 f0a[MT], f0b[NT], f1a[MT], f1b[NT];
     load_sub(0, 0, f0a, f0b);
 
     // sub-steps 0..3 of stage kt alternate register sets; before the read of
     // stage kt+1 (under the MFMAs of sub-step 3) stage kt+1 must be resident
-    // and every wave done with stage kt, whose slot then takes stage kt+S.
+    // and every wave done with stage kt, whose slots then take A(kt+SA), W(kt+SW).
     for (int kt = 0; kt < nk; ++kt) {
         load_sub(kt, 1, f1a, f1b);
         mma_sub(f0a, f0b);
@@ -536,10 +579,9 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         mma_sub(f1a, f1b);
         load_sub(kt, 3, f1a, f1b);
         mma_sub(f0a, f0b);
-        const int left = nk - 2 - kt;
-        wait_stages<Q, S - 1>(left < 0 ? 0 : left < S - 2 ? left : S - 2);   // stage kt+1 resident
+        wait_vm_atmost(kt + 1 < nk ? after_stage(kt + 1, kt - 1) : 0);   // stage kt+1 resident
         __syncthreads();
-        if (kt + S < nk) issue(kt + S, kb + (kt + S) * BK);
+        issue_iter(kt);
         load_sub(kt + 1 < nk ? kt + 1 : kt, 0, f0a, f0b);
         mma_sub(f1a, f1b);
     }
@@ -582,7 +624,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     }
 }
 
-template <int BM, int BN, int WM, int NW, int S>
+template <int BM, int BN, int WM, int NW, int SA, int SW>
 hipError_t launch_dma128(const GemmArgs& a, const GemmPlan& p, int n0, int n1, hipStream_t s) {
     const int m_tiles = (a.M + BM - 1) / BM;
     const int n_out = n1 - n0;
@@ -594,15 +636,15 @@ hipError_t launch_dma128(const GemmArgs& a, const GemmPlan& p, int n0, int n1, h
     dim3 grid(8 * ntx * groups * gm, p.splits), block(64 * NW);
     if (p.splits > 1) {
         if (a.epi == EPI_SWIGLU)
-            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
         else
-            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_F32) {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_RESID) {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, S, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     }
     return hipGetLastError();
 }
@@ -661,10 +703,10 @@ hipError_t launch_tile_variant(int variant, const GemmArgs& a, const GemmPlan& p
     switch (variant) {
         case kDmaVariant256x256: return launch_dma<256, 256, 2, 8, 5>(a, p, n0, n1, s);
         case kDmaVariant128x256: return launch_dma<128, 256, 2, 8, 6>(a, p, n0, n1, s);
-        case kLineVariant256x256: return launch_dma128<256, 256, 2, 8, 2>(a, p, n0, n1, s);
-        case kLineVariant128x128: return launch_dma128<128, 128, 2, 4, 2>(a, p, n0, n1, s);
-        case kLineVariant128x256: return launch_dma128<128, 256, 2, 8, 3>(a, p, n0, n1, s);
-        case kLineVariant128x128Deep: return launch_dma128<128, 128, 2, 4, 4>(a, p, n0, n1, s);
+        case kLineVariant256x256: return launch_dma128<256, 256, 2, 8, 2, 3>(a, p, n0, n1, s);
+        case kLineVariant128x128: return launch_dma128<128, 128, 2, 4, 2, 3>(a, p, n0, n1, s);
+        case kLineVariant128x256: return launch_dma128<128, 256, 2, 8, 3, 3>(a, p, n0, n1, s);
+        case kLineVariant128x128Deep: return launch_dma128<128, 128, 2, 4, 4, 4>(a, p, n0, n1, s);
         default:   // register-staged tiles cover the whole output only
             if (n0 != 0) return hipErrorInvalidValue;
             return variant == kLdsVariant256 ? launch_tile<256, 128>(a, p, s) : launch_tile<128, 128>(a, p, s);
