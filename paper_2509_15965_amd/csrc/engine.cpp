@@ -383,16 +383,14 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         rl_status st = run_gemm(c, RL_K_GEMM_QKV, h, H, wqkv, n, L.nqkv, H, EPI_F32, qkv, L.nqkv,
                                 nullptr, 0, nullptr, 0, true, &splits);
         if (st != RL_OK) return st;
-        if (splits > 1) {   // wide split-K reduction into q|k|v
-            st = reduce_splits(c, EPI_F32, n, L.nqkv, splits, qkv, L.nqkv, nullptr);
-            if (st != RL_OK) return st;
-        }
-        {
+        {   // RoPE + KV append; with split K it sums the fp32 slices itself
+            const int qs = splits > 1 ? splits : 1;
+            const float* src = splits > 1 ? c->wsp<float>(L.off_part) : qkv;
             Prof pr(c, RL_K_ROPE_APPEND);
-            e = launch_rope_append(dt, qkv, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride, Hq, Hkv,
-                                   D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
+            e = launch_rope_append(dt, src, qs, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride, Hq,
+                                   Hkv, D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "rope/append launch");
-            pr.done(n * (L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
+            pr.done(n * (qs * L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
         }
         {
             Prof pr(c, RL_K_ATTENTION);

@@ -143,78 +143,83 @@ hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int
     return hipGetLastError();
 }
 
-// Rotate-half RoPE on q and k of one row (pairs i, i + D/2 rotated by the
-// angle of position pos at frequency i), storage rounding, and the KV append.
+// Rotate-half RoPE on q and k (pairs i, i + D/2 rotated by the angle of the
+// row's position at frequency i), storage rounding, and the KV append.  One
+// thread per (row, head of q|k|v, pair i): it reads elements i and i + D/2 of
+// the projection -- the sum, in split order, of `splits` fp32 split-K slices
+// when the projection was split (no separate reduction pass) -- and writes q
+// or the K / V cache entries of every destination slot.
 // cs: cos table [cap][D/2] followed by the sin table [cap][D/2].
 // K cache element (l, s, h, t, i): (((l*S + s)*Hkv + h)*cap + t)*D + i.
 // V cache element: ((((l*S + s)*Hkv + h)*(cap/8) + t/8)*D + i)*8 + t%8.
 template <typename T>
-__global__ void __launch_bounds__(256) rope_append_kernel(const float* __restrict__ qkv,
-        const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_dst, int n_dst,
-        const int32_t* __restrict__ dst_slots, const float* __restrict__ cs, int cs_stride,
-        int Hq, int Hkv, int D, int S, int cap, int layer, T* __restrict__ q_out,
-        T* __restrict__ kc, T* __restrict__ vc) {
-    const int r = blockIdx.x;
-    const int pos = row_pos[r];
+__global__ void __launch_bounds__(256) rope_append_kernel(const float* __restrict__ qkv, int splits,
+        size_t slice, int n_rows, const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_dst,
+        int n_dst, const int32_t* __restrict__ dst_slots, const float* __restrict__ cs, int cs_stride, int Hq,
+        int Hkv, int D, int S, int cap, int layer, T* __restrict__ q_out, T* __restrict__ kc,
+        T* __restrict__ vc) {
     const int half = D / 2;
-    const int nqkv = (Hq + 2 * Hkv) * D;
-    const float* src = qkv + static_cast<size_t>(r) * nqkv;
-    auto val = [&](int c) { return src[c]; };
-    const float* cosr = cs + static_cast<size_t>(pos) * half;
-    const float* sinr = cs + static_cast<size_t>(cs_stride) + static_cast<size_t>(pos) * half;
+    const int nh = Hq + 2 * Hkv;
+    const size_t gid = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (gid >= static_cast<size_t>(n_rows) * nh * half) return;
+    const int i = static_cast<int>(gid % half);
+    const int h = static_cast<int>((gid / half) % nh);
+    const int r = static_cast<int>(gid / (static_cast<size_t>(half) * nh));
+    const int nqkv = nh * D;
+    const float* src = qkv + static_cast<size_t>(r) * nqkv + h * D + i;
+    float a = src[0], b = src[half];
+    for (int z = 1; z < splits; ++z) {
+        a += src[z * slice];
+        b += src[z * slice + half];
+    }
+    const int pos = row_pos[r];
+    if (h < Hq + Hkv) {
+        const float c = cs[static_cast<size_t>(pos) * half + i];
+        const float sn = cs[static_cast<size_t>(cs_stride) + static_cast<size_t>(pos) * half + i];
+        const float x0 = a * c - b * sn, x1 = b * c + a * sn;
+        if (h < Hq) {
+            T* qo = q_out + (static_cast<size_t>(r) * Hq + h) * D;
+            Elem<T>::store(qo, i, x0);
+            Elem<T>::store(qo, i + half, x1);
+            return;
+        }
+        const int d0 = row_dst[r];
+        for (int g = 0; g < n_dst; ++g) {
+            const int slot = dst_slots[d0 + g];
+            T* kr = kc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq)) * static_cast<size_t>(cap) * D +
+                    static_cast<size_t>(pos) * D;
+            Elem<T>::store(kr, i, x0);
+            Elem<T>::store(kr, i + half, x1);
+        }
+        return;
+    }
     const int d0 = row_dst[r];
-
-    // q heads
-    for (int idx = threadIdx.x; idx < Hq * half; idx += blockDim.x) {
-        const int h = idx / half, i = idx - h * half;
-        const float a = val(h * D + i), b = val(h * D + i + half);
-        const float c = cosr[i], s = sinr[i];
-        T* qo = q_out + (static_cast<size_t>(r) * Hq + h) * D;
-        Elem<T>::store(qo, i, a * c - b * s);
-        Elem<T>::store(qo, i + half, b * c + a * s);
-    }
-    // k heads -> cache
-    for (int idx = threadIdx.x; idx < Hkv * half; idx += blockDim.x) {
-        const int h = idx / half, i = idx - h * half;
-        const float a = val((Hq + h) * D + i), b = val((Hq + h) * D + i + half);
-        const float c = cosr[i], s = sinr[i];
-        const float k0 = a * c - b * s, k1 = b * c + a * s;
-        for (int g = 0; g < n_dst; ++g) {
-            const int slot = dst_slots[d0 + g];
-            T* kr = kc + ((static_cast<size_t>(layer) * S + slot) * Hkv + h) * static_cast<size_t>(cap) * D
-                    + static_cast<size_t>(pos) * D;
-            Elem<T>::store(kr, i, k0);
-            Elem<T>::store(kr, i + half, k1);
-        }
-    }
-    // v heads -> cache (8-position blocks)
-    for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-        const int h = idx / D, i = idx - h * D;
-        const float v = val((Hq + Hkv + h) * D + i);
-        for (int g = 0; g < n_dst; ++g) {
-            const int slot = dst_slots[d0 + g];
-            T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + h) * static_cast<size_t>(cap) * D;
-            Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i) * 8 + (pos & 7), v);
-        }
+    for (int g = 0; g < n_dst; ++g) {
+        const int slot = dst_slots[d0 + g];
+        T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq - Hkv)) * static_cast<size_t>(cap) * D;
+        Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i) * 8 + (pos & 7), a);
+        Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i + half) * 8 + (pos & 7), b);
     }
 }
 
-hipError_t launch_rope_append(int dt, const float* qkv, int n_rows, const int32_t* row_pos,
+hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, const int32_t* row_pos,
                               const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
                               const float* cs, int cs_stride, int Hq, int Hkv, int D,
                               int max_seqs, int cap, int layer,
                               void* q_out, void* kc, void* vc, hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
+    const size_t threads = static_cast<size_t>(n_rows) * (Hq + 2 * Hkv) * (D / 2);
+    const size_t slice = static_cast<size_t>(n_rows) * (Hq + 2 * Hkv) * D;
+    const dim3 grid(static_cast<unsigned>((threads + 255) / 256)), block(256);
+    const int sp = splits < 1 ? 1 : splits;
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(rope_append_kernel<uint16_t>, dim3(n_rows), dim3(256), 0, s, qkv,
-                           row_pos, row_dst, n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D,
-                           max_seqs, cap, layer, static_cast<uint16_t*>(q_out),
-                           static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc));
+        hipLaunchKernelGGL(rope_append_kernel<uint16_t>, grid, block, 0, s, qkv, sp, slice, n_rows, row_pos, row_dst,
+                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, max_seqs, cap, layer,
+                           static_cast<uint16_t*>(q_out), static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc));
     else
-        hipLaunchKernelGGL(rope_append_kernel<float>, dim3(n_rows), dim3(256), 0, s, qkv,
-                           row_pos, row_dst, n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D,
-                           max_seqs, cap, layer, static_cast<float*>(q_out),
-                           static_cast<float*>(kc), static_cast<float*>(vc));
+        hipLaunchKernelGGL(rope_append_kernel<float>, grid, block, 0, s, qkv, sp, slice, n_rows, row_pos, row_dst,
+                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, max_seqs, cap, layer,
+                           static_cast<float*>(q_out), static_cast<float*>(kc), static_cast<float*>(vc));
     return hipGetLastError();
 }
 

@@ -96,7 +96,9 @@ hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const flo
 // RoPE on q and k of fp32 q|k|v rows, q stored to q_out [rows][Hq][d]; k and
 // v appended to the cache of every destination slot of the row
 // (dst_slots[row_dst[r] + g], g < n_dst) at position row_pos[r].
-hipError_t launch_rope_append(int dt, const float* qkv, int n_rows, const int32_t* row_pos,
+// qkv: `splits` fp32 split-K slices [splits][n_rows][(Hq + 2 Hkv) D] summed in
+// order (splits <= 1: the finished projection)
+hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, const int32_t* row_pos,
                               const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
                               const float* cs, int cs_stride, int Hq, int Hkv, int D,
                               int max_seqs, int cap, int layer,
