@@ -335,6 +335,32 @@ rl_status reduce_splits(rl_decode_ctx* c, int epi, int M, int N, int splits, flo
     return RL_OK;
 }
 
+// x += the split-K slices of a deferred RESID GEMM (splits > 0), then
+// h = rmsnorm(x) * g.  From kResidNormMinRows rows one fused pass per row
+// (enough rows to fill the CUs); below, the wide reduction and the norm.
+constexpr int kResidNormMinRows = 64;
+rl_status resid_then_norm(rl_decode_ctx* c, int dt, int splits, float* x, int n, int H, const void* g, float eps,
+                          void* h) {
+    const double es = c->lay.es;
+    hipError_t e;
+    if (splits > 0 && n >= kResidNormMinRows && H % 4 == 0 && H <= 8192) {
+        Prof pr(c, RL_K_SPLITK_REDUCE);
+        e = launch_resid_norm(dt, c->wsp<float>(c->lay.off_part), splits, x, n, H, g, eps, h, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "residual + rmsnorm launch");
+        pr.done(n * H * (4.0 * splits + 8.0 + es) + H * es, 0.0);
+        return RL_OK;
+    }
+    if (splits > 0) {
+        rl_status st = reduce_splits(c, EPI_RESID, n, H, splits, nullptr, 0, x);
+        if (st != RL_OK) return st;
+    }
+    Prof pr(c, RL_K_RMSNORM);
+    e = launch_rmsnorm(dt, x, nullptr, n, H, g, eps, h, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+    pr.done(n * H * (4.0 + es) + H * es, 0.0);
+    return RL_OK;
+}
+
 rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
     const rl_model_config& cf = c->cfg;
     const Layout& L = c->lay;
@@ -415,31 +441,20 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         st = run_gemm(c, RL_K_GEMM_O, attn, HqD, wo, n, H, HqD, EPI_RESID, nullptr, 0, x, H, nullptr, 0,
                       true, &splits);
         if (st != RL_OK) return st;
-        if (splits > 0) {   // wide split-K reduction into the residual
-            st = reduce_splits(c, EPI_RESID, n, H, splits, nullptr, 0, x);
-            if (st != RL_OK) return st;
-        }
-        {   // MLP norm
-            Prof pr(c, RL_K_RMSNORM);
-            e = launch_rmsnorm(dt, x, nullptr, n, H, mn, eps, h, c->stream);
-            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
-            pr.done(n * H * (4.0 + es) + H * es, 0.0);
-        }
+        st = resid_then_norm(c, dt, splits, x, n, H, mn, eps, h);   // MLP norm
+        if (st != RL_OK) return st;
         st = run_gemm(c, RL_K_GEMM_GATE_UP, h, H, wgu, n, 2 * F, H, EPI_SWIGLU, nullptr, 0, nullptr, 0, mlp, F,
                       false, &splits);
         if (st != RL_OK) return st;
         st = run_gemm(c, RL_K_GEMM_DOWN, mlp, F, wd, n, H, F, EPI_RESID, nullptr, 0, x, H, nullptr, 0, true,
                       &splits);
         if (st != RL_OK) return st;
-        if (splits > 0) {
+        if (norm_after_down) {   // next layer's attention norm, or the final norm (decode)
+            st = resid_then_norm(c, dt, splits, x, n, H, next_norm, eps, h);
+            if (st != RL_OK) return st;
+        } else if (splits > 0) {
             st = reduce_splits(c, EPI_RESID, n, H, splits, nullptr, 0, x);
             if (st != RL_OK) return st;
-        }
-        if (norm_after_down) {   // next layer's attention norm, or the final norm (decode)
-            Prof pr(c, RL_K_RMSNORM);
-            e = launch_rmsnorm(dt, x, nullptr, n, H, next_norm, eps, h, c->stream);
-            if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
-            pr.done(n * H * (4.0 + es) + H * es, 0.0);
         }
     }
     const int nf = f.final_sel ? f.n_final : n;

@@ -143,6 +143,97 @@ hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int
     return hipGetLastError();
 }
 
+// Split-K sum + residual + RMSNorm of one row per workgroup (H a multiple of 4):
+//   x[r] += sum_{z < splits} part[z][r]   (in order z = 0, 1, ...)
+//   out[r] = storage(x[r] / sqrt(mean(x[r]^2) + eps) * g)
+// Each thread owns PER float4 of the row; the slices are loaded four at a
+// time (every load of a group in flight together) and added in order, so the
+// result equals the wide reduction followed by the norm.
+template <typename T, int PER>
+__global__ void __launch_bounds__(256) resid_norm4_kernel(const float* __restrict__ part, int splits,
+        size_t slice, float* __restrict__ x, int H, const T* __restrict__ g, float eps, T* __restrict__ out) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    const int H4 = H / 4;
+    f32x4* xr = reinterpret_cast<f32x4*>(x + static_cast<size_t>(r) * H);
+    const f32x4* pr = reinterpret_cast<const f32x4*>(part + static_cast<size_t>(r) * H);
+    const size_t sl4 = slice / 4;
+    f32x4 v[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) v[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int z = 0;
+    for (; z + 4 <= splits; z += 4) {
+        f32x4 t[4][PER];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                const int c = threadIdx.x + 256 * j;
+                t[u][j] = c < H4 ? pr[(z + u) * sl4 + c] : f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int j = 0; j < PER; ++j) v[j] += t[u][j];
+    }
+    for (; z < splits; ++z)
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int c = threadIdx.x + 256 * j;
+            if (c < H4) v[j] += pr[z * sl4 + c];
+        }
+    float ss = 0.0f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        if (c < H4) {
+            const f32x4 nv = xr[c] + v[j];
+            xr[c] = nv;
+            v[j] = nv;
+            ss = fmaf(nv[0], nv[0], ss);
+            ss = fmaf(nv[1], nv[1], ss);
+            ss = fmaf(nv[2], nv[2], ss);
+            ss = fmaf(nv[3], nv[3], ss);
+        }
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    ss = red[0] + red[1] + red[2] + red[3];
+    const float rs = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+    T* orow = out + static_cast<size_t>(r) * H;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        if (c < H4) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) Elem<T>::store(orow, 4 * c + e, v[j][e] * rs * Elem<T>::load(g, 4 * c + e));
+        }
+    }
+}
+
+hipError_t launch_resid_norm(int dt, const float* part, int splits, float* x, int n, int H, const void* g,
+                             float eps, void* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int per = (H / 4 + 255) / 256;
+    if (H % 4 != 0 || per > 8) return hipErrorInvalidValue;
+    const size_t slice = static_cast<size_t>(n) * H;
+#define RL_RN(P)                                                                                            \
+    do {                                                                                                    \
+        if (dt == DT_BF16)                                                                                  \
+            hipLaunchKernelGGL((resid_norm4_kernel<uint16_t, P>), dim3(n), dim3(256), 0, s, part, splits,  \
+                               slice, x, H, static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(out)); \
+        else                                                                                                \
+            hipLaunchKernelGGL((resid_norm4_kernel<float, P>), dim3(n), dim3(256), 0, s, part, splits,     \
+                               slice, x, H, static_cast<const float*>(g), eps, static_cast<float*>(out));   \
+    } while (0)
+    if (per <= 2) RL_RN(2);
+    else if (per <= 4) RL_RN(4);
+    else RL_RN(8);
+#undef RL_RN
+    return hipGetLastError();
+}
+
 // Rotate-half RoPE on q and k (pairs i, i + D/2 rotated by the angle of the
 // row's position at frequency i), storage rounding, and the KV append.  One
 // thread per (row, head of q|k|v, pair i): it reads elements i and i + D/2 of

@@ -87,6 +87,11 @@ hipError_t launch_embed(int dt, const int32_t* tok, int n, const void* table, in
 hipError_t launch_rmsnorm(int dt, const float* x, const int32_t* sel, int n, int H,
                           const void* g, float eps, void* out, hipStream_t s);
 
+// x[r] += sum of `splits` split-K slices [splits][n][H] (in order), then
+// out[r] = storage(rmsnorm(x[r]) * g); one workgroup per row (H % 4 == 0, H <= 8192)
+hipError_t launch_resid_norm(int dt, const float* part, int splits, float* x, int n, int H, const void* g,
+                             float eps, void* out, hipStream_t s);
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);   // writes a.out_f32 [M][Nw]
