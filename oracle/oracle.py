@@ -53,6 +53,8 @@ def load():
     lib.orc_gumbel_argmax_u.argtypes = [_fp, _dp, C.c_int32, C.c_float]
     lib.orc_sample.argtypes = [_fp, C.c_int32, C.c_float, C.c_uint64, C.c_uint64, C.c_int32,
                                C.c_int32, C.POINTER(C.c_int32), _dp]
+    lib.orc_logprob.restype = C.c_double
+    lib.orc_logprob.argtypes = [_fp, C.c_int32, C.c_float, C.c_int32]
     lib.orc_sample_margin.argtypes = [_fp, C.c_int32, C.c_float, C.c_uint64, C.c_uint64, C.c_int32,
                                       C.POINTER(C.c_int32), C.POINTER(C.c_int32), _dp]
     lib.orc_rmsnorm.argtypes = [_dp, C.c_int, C.c_void_p, C.c_size_t, C.c_int32, C.c_double, C.c_int, _dp]
@@ -132,6 +134,12 @@ def sample(z, T: float, seed: int, uid: int, pos_new: int, forced: int = -1):
     lp = C.c_double()
     load().orc_sample(_f(z), len(z), T, seed, uid, pos_new, forced, C.byref(tok), C.byref(lp))
     return int(tok.value), float(lp.value)
+
+
+def logprob(z, T: float, y: int) -> float:
+    """log softmax(fl32(z / T))[y] for fp32 logits z (T == 0: the T = 1 value)."""
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    return float(load().orc_logprob(_f(z), len(z), T, int(y)))
 
 
 def sample_margin(z, T: float, seed: int, uid: int, pos_new: int):
@@ -293,3 +301,26 @@ class OracleSeq:
         v = np.empty(D, dtype=np.float64)
         self.lib.orc_seq_get_kv(C.byref(self.model.m), self.h, layer, pos, kvh, _d(k), _d(v))
         return k, v
+
+
+def score(model: OracleModel, prompt, response, T: float, embeds=None):
+    """Inference-stage log-probabilities of one response (Sec. 2.1, GRPO:
+    after generation the log-probabilities of the responses are computed by a
+    forward pass over them).
+
+    Entry j is log softmax(z_j / T)[response[j]], where z_j are the logits
+    after prompt + response[:j].  The sequence is fed one token at a time
+    through the oracle's KV-cached forward; prompt ids < 0 select rows of
+    `embeds` (row -id-1).  Returns a float64 array of len(response)."""
+    response = [int(t) for t in response]
+    seq = model.new_seq(len(prompt) + len(response))
+    z = None
+    for t in prompt:
+        t = int(t)
+        z = seq.forward(t, None if t >= 0 else embeds[-t - 1])
+    out = np.empty(len(response), dtype=np.float64)
+    for j, y in enumerate(response):
+        out[j] = logprob(z.astype(np.float32), T, y)
+        if j + 1 < len(response):
+            z = seq.forward(y)
+    return out

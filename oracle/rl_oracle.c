@@ -195,6 +195,30 @@ void orc_sample(const float* z, int32_t V, float T, uint64_t seed, uint64_t uid,
     *logp_out = (double)(z[r] / T) - lse;
 }
 
+/* Log-probability of token y under temperature T: fl32(z_y / T) - LSE(fl32(z / T)),
+ * the same quantity the sampler reports, with no draw.  This is what the
+ * inference stage computes for every generated token (Sec. 2.1, GRPO: the
+ * log-probabilities of the responses, from a forward pass over them).
+ * T == 0 reports the T = 1 value (as the arg-max sampler does).
+ * y outside [0, V) returns NaN. */
+double orc_logprob(const float* z, int32_t V, float T, int32_t y)
+{
+    if (y < 0 || y >= V) return NAN;
+    const int scaled = T != 0.0f;
+    double m = -INFINITY;
+    for (int32_t v = 0; v < V; ++v) {
+        double zt = scaled ? (double)(z[v] / T) : (double)z[v];
+        if (zt > m) m = zt;
+    }
+    double s = 0.0;
+    for (int32_t v = 0; v < V; ++v) {
+        double zt = scaled ? (double)(z[v] / T) : (double)z[v];
+        s += exp(zt - m);
+    }
+    double zy = scaled ? (double)(z[y] / T) : (double)z[y];
+    return zy - (m + log(s));
+}
+
 /* Top-two perturbed scores of a draw (used to excuse near-tie flips). */
 void orc_sample_margin(const float* z, int32_t V, float T, uint64_t seed, uint64_t uid,
                        int32_t pos_new, int32_t* first, int32_t* second, double* margin)

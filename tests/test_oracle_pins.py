@@ -386,3 +386,70 @@ def test_kv_injection_then_decode_matches_natural_cache():
             b.set_kv_block(l, g, K, V)
     b.set_length(4)
     assert np.array_equal(a.forward(toks[-1]), b.forward(toks[-1]))
+
+
+# --------------------------------------------------------------------------
+# Inference stage: log-probabilities of given responses
+# --------------------------------------------------------------------------
+
+def test_logprob_closed_forms():
+    V = 1000
+    assert oracle.logprob(np.zeros(V, np.float32), 1.0, 17) == pytest.approx(-math.log(V), abs=1e-12)
+    z = np.array([0.0, 0.0, math.log(2.0)], dtype=np.float32)
+    zf = z.astype(np.float64)
+    assert oracle.logprob(z, 1.0, 2) == pytest.approx(zf[2] - math.log(2.0 + math.exp(zf[2])), abs=1e-12)
+    # two entries: log-sigmoid of the difference / T
+    a, b, T = 1.25, -0.5, 0.5
+    z2 = np.array([a, b], dtype=np.float32)
+    assert oracle.logprob(z2, T, 0) == pytest.approx(-math.log1p(math.exp(-(a - b) / T)), abs=1e-12)
+    # T == 0 reports the T = 1 value; ids outside the vocabulary give NaN
+    rng = np.random.default_rng(21)
+    z3 = rng.normal(0, 2, size=50).astype(np.float32)
+    assert oracle.logprob(z3, 0.0, 7) == oracle.logprob(z3, 1.0, 7)
+    assert math.isnan(oracle.logprob(z3, 1.0, 50)) and math.isnan(oracle.logprob(z3, 1.0, -1))
+
+
+def test_logprob_normalises_and_matches_sampler_report():
+    rng = np.random.default_rng(22)
+    for T in (1.0, 0.6):
+        z = rng.normal(0, 3, size=301).astype(np.float32)
+        lps = np.array([oracle.logprob(z, T, v) for v in range(len(z))])
+        assert np.all(lps <= 0.0)
+        assert abs(np.exp(lps).sum() - 1.0) < 1e-12
+        # exactly the quantity the sampler reports for a forced token
+        for v in (0, 150, 300):
+            assert oracle.logprob(z, T, v) == oracle.sample(z, T, 3, 4, 5, forced=v)[1]
+
+
+@pytest.mark.parametrize("T", [1.0, 0.6])
+@pytest.mark.parametrize("shape", [
+    SMALL,
+    ModelShape(2, 64, 8, 1, 8, 64, 64, 1e-6, 1e6, "fp32"),       # MQA (group 8)
+])
+def test_score_equals_bruteforce_log_softmax(shape, T):
+    """score() = log-softmax of the full causal forward over prompt +
+    response, read at each response token (fp64 storage, no cache)."""
+    from scipy.special import logsumexp
+    m, w, s = small_model(oracle.MODE_FP64, "fp32", seed=23, shape=shape)
+    rng = np.random.default_rng(24)
+    prompt = [int(t) for t in rng.integers(0, s.vocab, size=9)]
+    resp = [int(t) for t in rng.integers(0, s.vocab, size=14)]
+    got = oracle.score(m, prompt, resp, T)
+    ref = forward_all(s.as_dict(), w, prompt + resp)
+    P = len(prompt)
+    for j, y in enumerate(resp):
+        zt = ref[P - 1 + j] / T
+        exp = zt[y] - logsumexp(zt)
+        assert got[j] == pytest.approx(exp, abs=2e-5), (j, got[j], exp)
+
+
+def test_score_embedding_prompt_rows():
+    """Prompt ids < 0 read rows of the caller's embedding table: with rows
+    equal to token rows the scores are identical."""
+    m, w, s = small_model(oracle.MODE_BF16, "bf16", seed=25)
+    rng = np.random.default_rng(26)
+    prompt = [int(t) for t in rng.integers(0, s.vocab, size=6)]
+    resp = [int(t) for t in rng.integers(0, s.vocab, size=5)]
+    embeds = w["embed"][np.array(prompt[:3])]
+    mixed = [-1, -2, -3] + prompt[3:]
+    assert np.array_equal(oracle.score(m, prompt, resp, 1.0), oracle.score(m, mixed, resp, 1.0, embeds=embeds))
