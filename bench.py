@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=0, help="decode steps to time (0 = the whole rollout)")
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="qwen7b")
+    ap.add_argument("--stage", choices=("rollout", "score"), default="rollout",
+                    help="rollout: the decode hot path (default); score: the inference stage "
+                         "(log-probabilities of given responses, one GRPO group per call)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true",
                     help="time every kernel class (adds event overhead; diagnostics only)")
@@ -100,6 +103,163 @@ def cpu_baseline(shape, weights, seconds: float):
                       f"(one token per sequence, fp64 accumulation), {el:.1f} s"}
 
 
+def cpu_baseline_score(shape, weights, seconds: float):
+    """Oracle inference-stage tokens/s on this host's cores: score() of a
+    short prompt + response, fed one token at a time, until `seconds`."""
+    import numpy as np
+
+    import oracle
+    from paper_2509_15965_amd.inputs import weights_to_host
+    cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(cores)
+    host = weights_to_host(weights)
+    om = oracle.OracleModel(shape.as_dict(), host, oracle.MODE_BF16)
+    rng = np.random.default_rng(5)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        prompt = rng.integers(0, shape.vocab, size=4)
+        resp = rng.integers(0, shape.vocab, size=4)
+        oracle.score(om, prompt, resp, 1.0)
+        n += 7                                    # forwards: prompt + response - 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 512:
+            break
+    del om, host
+    return {"value": n / el, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n} scored-sequence tokens of the 7B-shape decoder (4-token prompts + 4-token "
+                      f"responses, KV-cached one token at a time, fp64 accumulation), {el:.1f} s"}
+
+
+def roofline_of(stats, classes):
+    """Roofline entry of the class with the largest measured time."""
+    dom = max(classes, key=lambda c: stats[c]["total_ms"])
+    d = stats[dom]
+    avg_ms = d["total_ms"] / max(1, d["launches"])
+    gbs = d["alg_bytes"] / (d["total_ms"] * 1e-3) / 1e9
+    tflops = d["alg_flops"] / (d["total_ms"] * 1e-3) / 1e12
+    intensity = d["alg_flops"] / max(1.0, d["alg_bytes"])
+    if intensity > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    roof.update({"kernel": dom, "launches": d["launches"], "avg_launch_ms": round(avg_ms, 5),
+                 "alg_bytes_per_launch": round(d["alg_bytes"] / max(1, d["launches"])),
+                 "alg_flops_per_launch": round(d["alg_flops"] / max(1, d["launches"]))})
+    return dom, roof
+
+
+def score_main(args):
+    """Inference stage on the 7B-shape rollout: every step scores one GRPO
+    group (its prompt once + its 16 responses) with rl_score."""
+    import numpy as np
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights, rollout_plan
+    from paper_2509_15965_amd.rl_decode import KERNEL_CLASSES, RL_OPT_PROFILE, Engine
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    plan = rollout_plan(wl)
+    G = wl.group
+    steps = args.steps if args.steps > 0 else 4
+    warm = max(0, min(args.warmup, 1))
+    n_groups = min(wl.n_prompts, steps + warm)
+    plens, resp = plan["prompt_lens"], plan["response_lens"]
+    rng = np.random.default_rng(wl.seed + 7)
+    groups = []
+    for p in range(n_groups):
+        rl = resp[p * G:(p + 1) * G]
+        rt = rng.integers(0, shape.vocab, size=int(rl.sum())).astype(np.int32)
+        groups.append({"prompt": torch.as_tensor(plan["prompts"][p], device=dev),
+                       "poffs": np.array([0, plens[p]], dtype=np.int32),
+                       "roffs": np.concatenate([[0], np.cumsum(rl)]).astype(np.int32),
+                       "resp": torch.as_tensor(rt, device=dev),
+                       "out": torch.empty(int(rl.sum()), dtype=torch.float32, device=dev),
+                       "tokens": int(plens[p] + rl.sum()), "scored": int(rl.sum())})
+    weights = make_weights(shape, wl.seed, device=dev)
+    max_ctx = max(int(plens[p] + resp[p * G:(p + 1) * G].max()) for p in range(n_groups))
+    max_tok = max(g["tokens"] for g in groups)
+    eng = Engine(shape, weights, max_seqs=G, max_ctx=max_ctx, max_prefill_tokens=max_tok, device=dev)
+    stream = eng.stream
+    slots = list(range(G))
+
+    def run(g):
+        eng.score(slots, g["poffs"], g["prompt"], g["roffs"], g["resp"], g["out"], group=G,
+                  temperature=wl.temperature)
+
+    for g in groups[:warm]:
+        run(g)
+    torch.cuda.synchronize()
+    timed = groups[warm:warm + steps]
+    prof_classes = ("attention", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "sample")
+    mask = 0
+    for c in prof_classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    eng.reset_stats()
+    eng.set_option(RL_OPT_PROFILE, mask)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i, g in enumerate(timed):
+        run(g)
+        print(f"[bench] score step {i + 1}/{len(timed)} enqueued", file=sys.stderr, flush=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    stats = eng.kernel_stats()
+    eng.set_option(RL_OPT_PROFILE, 0)
+    finite = all(bool(torch.isfinite(g["out"]).all()) for g in timed)
+    tokens = sum(g["tokens"] for g in timed)
+    scored = sum(g["scored"] for g in timed)
+    dom, roof = roofline_of(stats, prof_classes)
+    gemm_flops = sum(stats[c]["alg_flops"] for c in prof_classes if c.startswith("gemm"))
+    gemm_ms = sum(stats[c]["total_ms"] for c in prof_classes if c.startswith("gemm"))
+    classes = {c: {"launches": stats[c]["launches"], "ms": round(stats[c]["total_ms"], 3),
+                   "TFLOP/s": round(stats[c]["alg_flops"] / (stats[c]["total_ms"] * 1e9), 1)
+                   if stats[c]["total_ms"] > 0 and stats[c]["alg_flops"] > 0 else None}
+               for c in prof_classes}
+    out = {
+        "metric": "inference-stage tokens/sec (1 GPU) at 7B shape: prompt + response tokens through the "
+                  "scoring forward",
+        "value": round(tokens / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": len(timed),
+        "warmup": warm,
+        "ms_per_step": round(wall * 1e3 / max(1, len(timed)), 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, uniform prompt and response tokens)",
+        "config": {"workload": f"{wl.name} inference stage: one GRPO group ({G} responses of one prompt) per "
+                               f"rl_score call; prompts U[{wl.prompt_len[0]},{wl.prompt_len[1]}], lognormal "
+                               f"responses (median {wl.response_median}, cap {wl.response_cap})",
+                   "tokens_timed": tokens, "scored_tokens_timed": scored},
+        "scored_tokens_per_s": round(scored / wall, 1),
+        "gpu_ms_timed": round(gpu_ms, 2),
+        "gemm_TFLOPs": round(gemm_flops / (gemm_ms * 1e9), 1) if gemm_ms > 0 else None,
+        "all_finite": finite,
+        "roofline": roof,
+        "timed_classes": classes,
+    }
+    eng.close()
+    del eng
+    torch.cuda.synchronize()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_score(shape, weights, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe_mib > 0:
@@ -108,6 +268,9 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
+    if args.stage == "score":
+        score_main(args)
+        return
     import numpy as np
     import torch
 
@@ -221,22 +384,11 @@ def main():
     eng.set_option(RL_OPT_PROFILE, 0)
 
     # dominant kernel (largest measured time among the timed classes)
-    dom = max(prof_classes, key=lambda c: stats[c]["total_ms"])
+    dom, roof = roofline_of(stats, prof_classes)
+    roof.pop("alg_flops_per_launch")
     d = stats[dom]
-    avg_ms = d["total_ms"] / max(1, d["launches"])
-    gbs = d["alg_bytes"] / (d["total_ms"] * 1e-3) / 1e9
-    tflops = d["alg_flops"] / (d["total_ms"] * 1e-3) / 1e12
-    intensity = d["alg_flops"] / max(1.0, d["alg_bytes"])
-    if intensity > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None}
-    else:
-        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}
     if dom == "attention" and ATTN_TRAFFIC_PER_ALG_BYTE is not None:
         roof["traffic"] = round(ATTN_TRAFFIC_PER_ALG_BYTE * d["alg_bytes"] / max(1, d["launches"]))
-    roof.update({"kernel": dom, "launches": d["launches"], "avg_launch_ms": round(avg_ms, 5),
-                 "alg_bytes_per_launch": round(d["alg_bytes"] / max(1, d["launches"]))})
 
     classes = {c: {"launches": stats[c]["launches"],
                    "avg_launch_ms": round(stats[c]["total_ms"] / max(1, stats[c]["launches"]), 5),

@@ -192,6 +192,38 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group,
                      int32_t* out_tok, float* out_logp, float* out_logits);
 
 /* ---------------------------------------------------------------------
+ * Inference stage: log-probabilities of given responses (Sec. 2.1, GRPO:
+ * after generation the per-token log-probabilities of the responses are
+ * computed by a forward pass over prompt + response, with no sampling).
+ *
+ * Sequence s (< n_prompts*group) is prompt p = s / group followed by
+ * response s.  One causal forward over all tokens: each prompt is computed
+ * once and its K/V written to all `group` slots of its group; the response
+ * tokens of sequence s continue its slot at positions P, P+1, ...
+ *  n_prompts, group, slots, prompt_offsets, prompt_tokens, embeds,
+ *                 n_embed_rows: as rl_prefill.
+ *  resp_offsets   host [n_prompts*group + 1], CSR offsets into resp_tokens;
+ *                 resp_offsets[0] = 0; every response length m >= 1 with
+ *                 P + m <= max_ctx.  All prompt plus all response tokens
+ *                 <= max_prefill_tokens.
+ *  resp_tokens    device int32 [resp_offsets[n]].
+ *  temperature    >= 0; 0 reports the T = 1 value (as the arg-max sampler).
+ *  out_logp       device float [resp_offsets[n]]:
+ *                 out_logp[resp_offsets[s] + j] = fl32(z_y / T) - LSE(fl32(z / T))
+ *                 with y = response token j and z the logits after the
+ *                 prompt and response tokens 0..j-1; NaN when y is outside
+ *                 [0, vocab).
+ * The slots serve as scratch: their K/V is overwritten and they are empty
+ * (length 0) afterwards.  The LM head runs in chunks of rows whose fp32
+ * logits fit the workspace (max_seqs rows, or more when the MLP activation
+ * buffer, free by then, holds more). */
+rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const int32_t* slots,
+                   const int32_t* prompt_offsets, const int32_t* prompt_tokens,
+                   const void* embeds, int32_t n_embed_rows,
+                   const int32_t* resp_offsets, const int32_t* resp_tokens,
+                   float temperature, float* out_logp);
+
+/* ---------------------------------------------------------------------
  * One decode step (the rollout's hot loop).
  *
  * For each row i < n: appends in_tok[i] to slot slots[i] at position

@@ -32,7 +32,7 @@ struct Layout {
     size_t kv_bytes = 0, ws_bytes = 0;
     size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
     size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
-    size_t off_cnt = 0, cnt_bytes = 0, off_spart = 0;
+    size_t off_cnt = 0, cnt_bytes = 0, off_spart = 0, off_tok = 0;
     size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
 };
 
@@ -71,8 +71,11 @@ Layout make_layout(const rl_model_config& c) {
     L.part_floats = kPartCapFloats;
     if (c.dtype == RL_DTYPE_FP32) L.part_floats = std::max(L.part_floats, R * std::max(H, 2 * F));
     L.apart_floats = static_cast<size_t>(kPartItems) * c.n_kv_heads * 16 * (c.head_dim + 2);
-    L.meta_bytes = 4 * (3 * R + 4 * static_cast<size_t>(c.max_seqs)) + 8 * static_cast<size_t>(c.max_seqs) +
-                   sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + 4 * R + 4096;
+    // per-row index arrays (position, KV destination, slot read, LM-head
+    // selection, log-prob item offsets and targets), per-sequence arrays,
+    // attention work items
+    L.meta_bytes = 4 * (7 * R + 4 * static_cast<size_t>(c.max_seqs)) + 8 * static_cast<size_t>(c.max_seqs) +
+                   sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + 4096;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     L.off_x = take(R * H * 4);
@@ -86,6 +89,7 @@ Layout make_layout(const rl_model_config& c) {
     L.off_logits = take(static_cast<size_t>(c.max_seqs) * V * 4);
     L.off_rope = take(static_cast<size_t>(L.cap) * (c.head_dim / 2) * 2 * 4);
     L.off_meta = take(L.meta_bytes);
+    L.off_tok = take(R * 4);   // packed token ids of a scoring pass
     // sampler completion counters (one per row): zero between launches
     L.cnt_bytes = 4 * static_cast<size_t>(c.max_seqs);
     L.off_cnt = take(L.cnt_bytes);
@@ -256,6 +260,14 @@ struct Fwd {
     float T = 1.0f;
     int32_t* out_tok = nullptr;
     float* out_logp = nullptr;
+    // scoring pass (inference stage): instead of sampling, log-probabilities
+    // of given tokens for the LM-head rows; row i of final_sel owns items
+    // [score_items[i], score_items[i+1]) of score_idx, each an index into
+    // score_targets and out_logp
+    const int32_t* score_items = nullptr;
+    const int32_t* score_idx = nullptr;
+    const int32_t* score_targets = nullptr;
+    int score_chunk = 0;                    // LM-head rows per chunk (rows of f.logits)
 };
 
 // Y = A . W^T with the given epilogue.  When the plan splits K, fp32 partials
@@ -463,6 +475,23 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         e = launch_rmsnorm(dt, x, f.final_sel, nf, H, c->w.final_norm, eps, h, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "final rmsnorm launch");
         pr.done(nf * H * (4.0 + es) + H * es, 0.0);
+    }
+    if (f.score_items) {   // LM head and log-probabilities in chunks of score_chunk rows
+        const int V = cf.vocab;
+        for (int r0 = 0; r0 < nf; r0 += f.score_chunk) {
+            const int nc = std::min(f.score_chunk, nf - r0);
+            int sp = 0;
+            const uint8_t* hr = static_cast<const uint8_t*>(h) + static_cast<size_t>(r0) * H * esz;
+            rl_status st = run_gemm(c, RL_K_GEMM_LM_HEAD, hr, H, c->w.lm_head, nc, V, H, EPI_F32, f.logits, V,
+                                    nullptr, 0, nullptr, 0, false, &sp);
+            if (st != RL_OK) return st;
+            Prof pr(c, RL_K_SAMPLE);
+            e = launch_logprob(f.logits, V, nc, V, f.score_items + r0, f.score_idx, f.score_targets, f.T,
+                               f.out_logp, c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "log-prob launch");
+            pr.done(nc * V * 4.0, 0.0);
+        }
+        return RL_OK;
     }
     int splits = 0;
     rl_status st = run_gemm(c, RL_K_GEMM_LM_HEAD, h, H, c->w.lm_head, nf, cf.vocab, H, EPI_F32, f.logits,
@@ -819,6 +848,157 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     for (int p = 0; p < n_prompts; ++p)
         for (int k = 0; k < group; ++k) c->len[slots[p * group + k]] = prompt_offsets[p + 1] - prompt_offsets[p];
     return RL_OK;
+}
+
+rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const int32_t* slots,
+                   const int32_t* prompt_offsets, const int32_t* prompt_tokens, const void* embeds,
+                   int32_t n_embed_rows, const int32_t* resp_offsets, const int32_t* resp_tokens,
+                   float temperature, float* out_logp) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    const rl_model_config& cf = c->cfg;
+    if (n_prompts < 1 || group < 1) return fail(c, RL_ERR_INVALID_ARG, "n_prompts and group must be >= 1");
+    if (static_cast<int64_t>(n_prompts) * group > cf.max_seqs)
+        return fail(c, RL_ERR_CAPACITY, "n_prompts * group exceeds max_seqs");
+    if (!slots || !prompt_offsets || !prompt_tokens || !resp_offsets || !resp_tokens || !out_logp)
+        return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    if (n_embed_rows < 0 || (n_embed_rows > 0 && !embeds)) return fail(c, RL_ERR_INVALID_ARG, "bad embedding rows");
+    if (embeds && !aligned(embeds, 16)) return fail(c, RL_ERR_INVALID_ARG, "embeds must be 16-byte aligned");
+    if (!(temperature >= 0.0f) || !std::isfinite(temperature))
+        return fail(c, RL_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+    const int n_seq = n_prompts * group;
+    std::vector<char> seen;
+    rl_status st = check_slots(c, n_seq, slots, &seen);
+    if (st != RL_OK) return st;
+    if (prompt_offsets[0] != 0) return fail(c, RL_ERR_INVALID_ARG, "prompt_offsets[0] must be 0");
+    if (resp_offsets[0] != 0) return fail(c, RL_ERR_INVALID_ARG, "resp_offsets[0] must be 0");
+    int64_t r1 = 0, r2 = 0;
+    for (int p = 0; p < n_prompts; ++p) {
+        const int64_t len = static_cast<int64_t>(prompt_offsets[p + 1]) - prompt_offsets[p];
+        if (len < 1) return fail(c, RL_ERR_INVALID_ARG, "empty prompt");
+        if (len > cf.max_ctx - 1) return fail(c, RL_ERR_CAPACITY, "prompt longer than max_ctx - 1");
+        r1 += len;
+        for (int k = 0; k < group; ++k) {
+            const int sq = p * group + k;
+            const int64_t m = static_cast<int64_t>(resp_offsets[sq + 1]) - resp_offsets[sq];
+            if (m < 1) return fail(c, RL_ERR_INVALID_ARG, "empty response");
+            if (len + m > cf.max_ctx) return fail(c, RL_ERR_CAPACITY, "prompt + response longer than max_ctx");
+            r2 += m;
+        }
+    }
+    if (r1 + r2 > cf.max_prefill_tokens)
+        return fail(c, RL_ERR_CAPACITY, "prompt + response tokens exceed max_prefill_tokens");
+    const int R1 = static_cast<int>(r1), R = static_cast<int>(r1 + r2);
+    const int n_sel = n_prompts + static_cast<int>(r2) - n_seq;   // LM-head rows
+    DeviceGuard g(c->device);
+
+    Meta m{};
+    int stage = 0;
+    st = begin_meta(c, &m, &stage);
+    if (st != RL_OK) return st;
+    int32_t *d_row_pos, *d_row_dst, *d_row_slot, *d_dst, *d_sel, *d_items, *d_idx;
+    int32_t* row_pos = m.take<int32_t>(R, &d_row_pos);
+    int32_t* row_dst = m.take<int32_t>(R, &d_row_dst);
+    int32_t* row_slot = m.take<int32_t>(R, &d_row_slot);
+    int32_t* dst = m.take<int32_t>(n_seq, &d_dst);
+    int32_t* sel = m.take<int32_t>(n_sel, &d_sel);
+    int32_t* items = m.take<int32_t>(static_cast<size_t>(n_sel) + 1, &d_items);
+    int32_t* idx = m.take<int32_t>(static_cast<size_t>(r2), &d_idx);
+    if (m.overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    // rows [0, R1): prompts, K/V written to every slot of the group; rows
+    // [R1, R): response tokens of each sequence, K/V written to its own slot
+    // at positions P, P+1, ...  LM-head rows: each prompt's last row (it
+    // scores response token 0 of every member), then response rows j < m-1
+    // (row j scores token j+1).
+    std::vector<Block> blocks;
+    const int G = cf.n_q_heads / cf.n_kv_heads;
+    const int tq = std::max(1, 16 / G);
+    double kvpos = 0, scorepos = 0;
+    int ns = 0, ni = 0;
+    for (int p = 0; p < n_prompts; ++p) {
+        const int b = prompt_offsets[p], len = prompt_offsets[p + 1] - b;
+        for (int t = 0; t < len; ++t) {
+            row_pos[b + t] = t;
+            row_dst[b + t] = p * group;
+            row_slot[b + t] = slots[p * group];
+        }
+        for (int k = 0; k < group; ++k) dst[p * group + k] = slots[p * group + k];
+        for (int t = 0; t < len; t += tq) blocks.push_back(Block{b + t, std::min(tq, len - t), slots[p * group], t});
+        kvpos += len;
+        scorepos += 0.5 * len * (len + 1.0);
+        sel[ns] = b + len - 1;
+        items[ns++] = ni;
+        for (int k = 0; k < group; ++k) idx[ni++] = resp_offsets[p * group + k];
+    }
+    for (int p = 0; p < n_prompts; ++p) {
+        const int P = prompt_offsets[p + 1] - prompt_offsets[p];
+        for (int k = 0; k < group; ++k) {
+            const int sq = p * group + k;
+            const int o = resp_offsets[sq], mlen = resp_offsets[sq + 1] - o;
+            const int b = R1 + o;
+            for (int j = 0; j < mlen; ++j) {
+                row_pos[b + j] = P + j;
+                row_dst[b + j] = -(slots[sq] + 1);
+                row_slot[b + j] = slots[sq];
+            }
+            for (int j = 0; j < mlen; j += tq) blocks.push_back(Block{b + j, std::min(tq, mlen - j), slots[sq], P + j});
+            kvpos += P + mlen;
+            scorepos += mlen * (P + 0.5 * (mlen + 1.0));
+            for (int j = 0; j + 1 < mlen; ++j) {
+                sel[ns] = b + j;
+                items[ns++] = ni;
+                idx[ni++] = o + j + 1;
+            }
+        }
+    }
+    items[ns] = ni;
+    Fwd f;
+    f.rows = R;
+    f.tok = c->wsp<int32_t>(c->lay.off_tok);
+    f.embeds = embeds;
+    f.n_embed_rows = n_embed_rows;
+    f.row_pos = d_row_pos;
+    f.row_dst = d_row_dst;
+    f.n_dst = group;
+    f.dst_slots = d_dst;
+    f.row_slot = d_row_slot;
+    f.attn_kv_positions = kvpos;
+    if (c->bf16()) {
+        const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, kPrefillChunk, c->lay.items_cap, false);
+        st = build_items(c, &m, blocks, C, &f);
+        if (st != RL_OK) return st;
+    } else {
+        f.attn_score_positions = scorepos;
+    }
+    f.final_sel = d_sel;
+    f.n_final = n_sel;
+    // LM-head chunks: the fp32 logits go to the SwiGLU activation region when
+    // it holds more rows than the logits buffer (it is free once the last
+    // layer's down projection has run)
+    const size_t mlp_rows = static_cast<size_t>(c->lay.R) * cf.ffn * c->lay.es / (4 * static_cast<size_t>(cf.vocab));
+    if (mlp_rows > static_cast<size_t>(cf.max_seqs)) {
+        f.logits = c->wsp<float>(c->lay.off_mlp);
+        f.score_chunk = static_cast<int>(std::min<size_t>(mlp_rows, 1 << 20));
+    } else {
+        f.logits = c->wsp<float>(c->lay.off_logits);
+        f.score_chunk = cf.max_seqs;
+    }
+    f.T = temperature > 0.0f ? temperature : 1.0f;
+    f.out_logp = out_logp;
+    f.score_items = d_items;
+    f.score_idx = d_idx;
+    f.score_targets = resp_tokens;
+    st = upload_meta(c, &m, stage);
+    if (st != RL_OK) return st;
+    int32_t* tok = c->wsp<int32_t>(c->lay.off_tok);
+    hipError_t e = hipMemcpyAsync(tok, prompt_tokens, sizeof(int32_t) * R1, hipMemcpyDeviceToDevice, c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(tok + R1, resp_tokens, sizeof(int32_t) * static_cast<size_t>(r2), hipMemcpyDeviceToDevice,
+                           c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "token copy");
+    st = run_forward(c, f);
+    for (int i = 0; i < n_seq; ++i) c->len[slots[i]] = 0;   // the slots were scratch
+    return st;
 }
 
 rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, const uint64_t* seq_uids,

@@ -239,7 +239,8 @@ hipError_t launch_resid_norm(int dt, const float* part, int splits, float* x, in
 // thread per (row, head of q|k|v, pair i): it reads elements i and i + D/2 of
 // the projection -- the sum, in split order, of `splits` fp32 split-K slices
 // when the projection was split (no separate reduction pass) -- and writes q
-// or the K / V cache entries of every destination slot.
+// or the K / V cache entries of every destination slot (a negative row_dst
+// entry names a single slot directly).
 // cs: cos table [cap][D/2] followed by the sin table [cap][D/2].
 // K cache element (l, s, h, t, i): (((l*S + s)*Hkv + h)*cap + t)*D + i.
 // V cache element: ((((l*S + s)*Hkv + h)*(cap/8) + t/8)*D + i)*8 + t%8.
@@ -275,8 +276,9 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
             return;
         }
         const int d0 = row_dst[r];
-        for (int g = 0; g < n_dst; ++g) {
-            const int slot = dst_slots[d0 + g];
+        const int nd = d0 < 0 ? 1 : n_dst;
+        for (int g = 0; g < nd; ++g) {
+            const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
             T* kr = kc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq)) * static_cast<size_t>(cap) * D +
                     static_cast<size_t>(pos) * D;
             Elem<T>::store(kr, i, x0);
@@ -285,8 +287,9 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
         return;
     }
     const int d0 = row_dst[r];
-    for (int g = 0; g < n_dst; ++g) {
-        const int slot = dst_slots[d0 + g];
+    const int nd = d0 < 0 ? 1 : n_dst;
+    for (int g = 0; g < nd; ++g) {
+        const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
         T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq - Hkv)) * static_cast<size_t>(cap) * D;
         Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i) * 8 + (pos & 7), a);
         Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i + half) * 8 + (pos & 7), b);

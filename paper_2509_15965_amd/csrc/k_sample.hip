@@ -141,4 +141,53 @@ hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_
     return hipGetLastError();
 }
 
+// Inference-stage log-probabilities of given tokens, one workgroup per logits
+// row: the row's LSE of fl32(z / T) (online max / sum-exp per lane, merged in
+// a fixed lane and wave order), then every item of the row.  No noise.
+__global__ void __launch_bounds__(256) logprob_kernel(const float* __restrict__ logits, int ld, int V,
+        const int32_t* __restrict__ row_items, const int32_t* __restrict__ item_idx,
+        const int32_t* __restrict__ targets, float T, float* __restrict__ out) {
+    __shared__ Lse sl[4];
+    const int r = blockIdx.x;
+    const float* z = logits + static_cast<size_t>(r) * ld;
+    Lse acc{-INFINITY, 0.0f};
+    for (int v4 = threadIdx.x; 4 * v4 < V; v4 += blockDim.x) {
+        const float4 zz = *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4));
+        const float zv[4] = {zz.x / T, zz.y / T, zz.z / T, zz.w / T};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float zt = zv[w];
+            if (zt > acc.m) {
+                acc.s = acc.s * expf(acc.m - zt) + 1.0f;
+                acc.m = zt;
+            } else {
+                acc.s += expf(zt - acc.m);
+            }
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        Lse o{__shfl_xor(acc.m, off, 64), __shfl_xor(acc.s, off, 64)};
+        acc = lse_merge(acc, o);
+    }
+    if ((threadIdx.x & 63) == 0) sl[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    Lse a = sl[0];
+    for (int w = 1; w < 4; ++w) a = lse_merge(a, sl[w]);
+    const float lse = a.m + logf(a.s);
+    for (int k = row_items[r] + threadIdx.x; k < row_items[r + 1]; k += blockDim.x) {
+        const int idx = item_idx[k];
+        const int y = targets[idx];
+        out[idx] = (y >= 0 && y < V) ? z[y] / T - lse : __builtin_nanf("");
+    }
+}
+
+hipError_t launch_logprob(const float* logits, int ld, int n_rows, int V, const int32_t* row_items,
+                          const int32_t* item_idx, const int32_t* targets, float T, float* out,
+                          hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(logprob_kernel, dim3(n_rows), dim3(256), 0, s, logits, ld, V, row_items, item_idx,
+                       targets, T, out);
+    return hipGetLastError();
+}
+
 }  // namespace rl

@@ -100,7 +100,8 @@ hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const flo
 
 // RoPE on q and k of fp32 q|k|v rows, q stored to q_out [rows][Hq][d]; k and
 // v appended to the cache of every destination slot of the row
-// (dst_slots[row_dst[r] + g], g < n_dst) at position row_pos[r].
+// (dst_slots[row_dst[r] + g], g < n_dst) at position row_pos[r]; a negative
+// row_dst[r] names one slot, -(row_dst[r] + 1).
 // qkv: `splits` fp32 split-K slices [splits][n_rows][(Hq + 2 Hkv) D] summed in
 // order (splits <= 1: the finished projection)
 hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, const int32_t* row_pos,
@@ -132,6 +133,14 @@ struct SamplePart { float best_s; int best_v; float m; float s; };
 constexpr int kSampleMaxChunks = 64;
 
 // parts: [n][kSampleMaxChunks]; counters: [n] ints, zero between launches.
+// Inference-stage log-probabilities: for logits row r < n_rows and every item
+// k in [row_items[r], row_items[r+1]), out[item_idx[k]] = fl32(z_y / T) -
+// LSE(fl32(z / T)) with y = targets[item_idx[k]] (NaN when y is outside
+// [0, V)).  T > 0.
+hipError_t launch_logprob(const float* logits, int ld, int n_rows, int V, const int32_t* row_items,
+                          const int32_t* item_idx, const int32_t* targets, float T, float* out,
+                          hipStream_t s);
+
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
                          uint64_t seed, float T, SamplePart* parts, int* counters,

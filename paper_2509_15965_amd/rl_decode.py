@@ -30,7 +30,7 @@ KERNEL_CLASSES = ("embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "a
                   "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample")
 
 EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create", "rl_decode_destroy",
-           "rl_prefill", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
+           "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
            "rl_set_slot_lengths", "rl_slot_length", "rl_decode_set_option", "rl_decode_kernel_stats",
            "rl_decode_reset_stats", "rl_probe_copy", "rl_status_string", "rl_decode_last_error")
 
@@ -80,6 +80,8 @@ def lib():
     L.rl_decode_destroy.argtypes = [vp]
     L.rl_prefill.restype = C.c_int
     L.rl_prefill.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, C.POINTER(SampleParams), vp, vp, vp]
+    L.rl_score.restype = C.c_int
+    L.rl_score.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, vp, vp, C.c_float, vp]
     L.rl_decode_step.restype = C.c_int
     L.rl_decode_step.argtypes = [vp, i32, vp, vp, vp, vp, C.POINTER(SampleParams), vp, vp, vp]
     L.rl_sample_logits.restype = C.c_int
@@ -199,6 +201,16 @@ class Engine:
                               offs.ctypes.data, _p(tokens), _p(embeds), n_rows, _p(forced), C.byref(sp),
                               _p(out_tok), _p(out_logp), _p(out_logits))
         self._check(st, "rl_prefill")
+
+    def score(self, slots: Sequence[int], prompt_offsets: Sequence[int], prompt_tokens: torch.Tensor,
+              resp_offsets: Sequence[int], resp_tokens: torch.Tensor, out_logp: torch.Tensor, *,
+              group: int = 1, embeds: Optional[torch.Tensor] = None, temperature: float = 1.0):
+        slots, poffs, roffs = _host_i32(slots), _host_i32(prompt_offsets), _host_i32(resp_offsets)
+        n_rows = 0 if embeds is None else int(embeds.shape[0])
+        st = lib().rl_score(self.h, len(poffs) - 1, group, slots.ctypes.data, poffs.ctypes.data,
+                            _p(prompt_tokens), _p(embeds), n_rows, roffs.ctypes.data, _p(resp_tokens),
+                            float(temperature), _p(out_logp))
+        self._check(st, "rl_score")
 
     def step(self, slots: Sequence[int], uids: Sequence[int], in_tok: torch.Tensor, out_tok: torch.Tensor,
              out_logp: torch.Tensor, *, forced: Optional[torch.Tensor] = None, seed: int = 0,

@@ -8,7 +8,11 @@ host, so every check samples what it can compute one by one:
     written through the documented pool layout, same rows given to the
     oracle), then decode steps: the split-KV path at full length;
   - for the 7B shape, one decode step of the 512-sequence ragged batch the
-    benchmark times, checked on sampled rows.
+    benchmark times, checked on sampled rows;
+  - the inference stage (rl_score) at the 7B shape: short prompts and
+    responses against the oracle, and one whole GRPO group of the rollout
+    workload (the launch configuration its benchmark times) against
+    prefill + teacher-forced decoding of the same sequences.
 """
 import gc
 
@@ -294,4 +298,111 @@ def test_benchmark_batch_sampled_rows():
 @pytest.fixture(autouse=True)
 def _release_after():
     yield
+    _free()
+
+
+@pytest.mark.timeout(1500)
+def test_score_7b_short_sequences_match_oracle():
+    """rl_score at the 7B shape on 2 prompts (5 and 9 tokens) x 2 responses
+    of 4 tokens, every log-probability against the oracle."""
+    wl = WORKLOADS["qwen7b"]
+    shape = wl.model
+    oracle.set_threads(max(1, min(16, len(__import__("os").sched_getaffinity(0)))))
+    w_dev, w_host, om = build_models(shape, wl.seed)
+    rng = np.random.default_rng(17)
+    prompts = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in (5, 9)]
+    resp = [rng.integers(0, shape.vocab, size=4).astype(np.int32) for _ in range(4)]
+    eng = Engine(shape, w_dev, max_seqs=4, max_ctx=16, max_prefill_tokens=32)
+    out = torch.empty(16, dtype=torch.float32, device=DEV)
+    eng.score([3, 1, 0, 2], [0, 5, 14], _i32(np.concatenate(prompts)), [0, 4, 8, 12, 16],
+              _i32(np.concatenate(resp)), out, group=2)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    eng.close()
+    ref = np.concatenate([oracle.score(om, prompts[s // 2], resp[s], 1.0) for s in range(4)])
+    lerr = np.abs(got - ref)
+    # the oracle's own sensitivity: response 0 scored with one bf16 ulp
+    # flipped in the first prompt row (as the decode checks above)
+    row = w_host["embed"][int(prompts[0][0])].copy()
+    row[7] ^= 1
+    pert = oracle.score(om, np.concatenate([[-1], prompts[0][1:]]), resp[0], 1.0, embeds=row[None])
+    lsens = float(np.abs(pert - ref[:4]).max())
+    _record("qwen7b", "score_short_sequences", [0.0], lerr, 0.0, lsens)
+    assert np.isfinite(got).all()
+    assert lerr.max() < max(LOGP_ABS_TOL, 2 * lsens), (lerr, lsens)
+    del om
+    _free()
+
+
+@pytest.mark.timeout(1500)
+def test_score_benchmark_group_matches_teacher_forced_decode():
+    """rl_score over the first GRPO group of the 7B-shape rollout workload
+    (prompt + 16 lognormal responses, one call, as the score benchmark runs
+    it) against prefill + teacher-forced decode steps of the same 16
+    sequences.  Both are bf16 paths checked against the oracle elsewhere.
+    The depth-28 random-init decoder is ill-conditioned: the same scoring
+    call with one bf16 ulp flipped in the prompt's first input row moves the
+    log-probabilities by (sens_max, sens_mean).  Bar: the maximum difference
+    below max(2 x tolerance, 2 x sens_max), the mean below
+    max(tolerance / 10, 2 x sens_mean)."""
+    from paper_2509_15965_amd.inputs import make_weights, rollout_plan
+    wl = WORKLOADS["qwen7b"]
+    shape = wl.model
+    G = wl.group
+    plan = rollout_plan(wl)
+    P = int(plan["prompt_lens"][0])
+    rl = plan["response_lens"][:G].astype(np.int64)
+    rng = np.random.default_rng(wl.seed + 7)
+    rt = rng.integers(0, shape.vocab, size=int(rl.sum())).astype(np.int32)
+    w_dev = make_weights(shape, wl.seed, device=DEV)
+    max_ctx = P + int(rl.max())
+    eng = Engine(shape, w_dev, max_seqs=G, max_ctx=max_ctx, max_prefill_tokens=P + int(rl.sum()))
+    roffs = np.concatenate([[0], np.cumsum(rl)]).astype(np.int32)
+    out = torch.empty(int(rl.sum()), dtype=torch.float32, device=DEV)
+    prompt = _i32(plan["prompts"][0])
+    eng.score(list(range(G)), [0, P], prompt, roffs, _i32(rt), out, group=G, temperature=wl.temperature)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    # self-sensitivity: first prompt row given as an embedding row with one
+    # ulp flipped in element 7
+    row = w_dev["embed"][int(plan["prompts"][0][0])].clone().view(torch.int16)
+    row[7] ^= 1
+    pprompt = prompt.clone()
+    pprompt[0] = -1
+    eng.score(list(range(G)), [0, P], pprompt, roffs, _i32(rt), out, group=G, temperature=wl.temperature,
+              embeds=row.view(torch.bfloat16).reshape(1, -1).contiguous())
+    torch.cuda.synchronize()
+    sens = np.abs(out.cpu().numpy().astype(np.float64) - got)
+    # teacher-forced decoding of the same sequences: sequence s sits in slot
+    # pos[s], slots ordered longest response first so the active rows of
+    # every step are a prefix
+    order = np.argsort(-rl, kind="stable")
+    pos = np.empty(G, dtype=np.int64)
+    pos[order] = np.arange(G)
+    M = int(rl.max())
+    R = np.zeros((G, M), dtype=np.int32)
+    for q in range(G):
+        R[q, :rl[q]] = rt[roffs[q]:roffs[q + 1]]
+    Rs = torch.as_tensor(R[order], device=DEV)
+    ot = torch.empty(G, dtype=torch.int32, device=DEV)
+    lp0 = torch.empty(G, dtype=torch.float32, device=DEV)
+    lp = torch.zeros((M, G), dtype=torch.float32, device=DEV)
+    eng.prefill([int(x) for x in pos], list(range(G)), [0, P], prompt, ot, lp0, group=G,
+                forced=_i32(R[:, 0]), temperature=wl.temperature)
+    slots = list(range(G))
+    for j in range(1, M):
+        n = int((rl > j).sum())
+        eng.step(slots[:n], [int(x) for x in order[:n]], Rs[:n, j - 1].contiguous(), ot[:n], lp[j, :n],
+                 forced=Rs[:n, j].contiguous(), temperature=wl.temperature)
+    torch.cuda.synchronize()
+    dec = lp.cpu().numpy()
+    first = lp0.cpu().numpy()
+    eng.close()
+    ref = np.concatenate([np.concatenate([[first[q]], dec[1:rl[q], pos[q]]]) for q in range(G)])
+    assert np.isfinite(got).all() and np.all(got <= 1e-6)
+    d = np.abs(got - ref)
+    _record("qwen7b", "score_group_vs_teacher_forced_decode: diff max, diff mean, ulp-flip max, ulp-flip mean",
+            [0.0], [float(d.max()), float(d.mean()), float(sens.max()), float(sens.mean())])
+    assert d.max() < max(2 * LOGP_ABS_TOL, 2 * sens.max()), (d.max(), d.mean(), sens.max(), sens.mean())
+    assert d.mean() < max(0.1 * LOGP_ABS_TOL, 2 * sens.mean()), (d.max(), d.mean(), sens.max(), sens.mean())
     _free()
