@@ -34,13 +34,11 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
 # HBM traffic of the attention kernel per algorithmic byte, from two
-# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over the first 48 decode
-# steps of this workload, each counter scaled by what it reads for the
-# library's plain copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x
-# 1.0): 713.8 MB fetched + 3.7 MB written per launch against 700.9 MB
-# algorithmic.  Valid for the attention kernel as of that measurement; set to
-# None when the kernel changes until the counters are taken again.
-ATTN_TRAFFIC_PER_ALG_BYTE = 1.0235
+# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over decode steps of this
+# workload, each counter scaled by what it reads for the library's plain copy
+# kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  None until the
+# counters are taken for the current kernel and work-item layout.
+ATTN_TRAFFIC_PER_ALG_BYTE = None
 
 
 def parse():

@@ -183,7 +183,12 @@ rl_status rl_decode_destroy(rl_decode_ctx* ctx);
  *  out_logits     device float [n_prompts][vocab] (logits of each prompt's
  *                 last position) or NULL.
  * Afterwards each slot's length is its prompt length; the sampled token
- * takes position `length` and is fed back through rl_decode_step. */
+ * takes position `length` and is fed back through rl_decode_step.
+ * With group > 1 the slots of a group share the prompt for decode attention
+ * (RL_OPT_SHARED_PREFIX) until one of them is released, prefilled or scored
+ * again, or has its length set: then that slot and every slot reading
+ * through it go back to their own copies.  K/V the caller writes into the
+ * pool must be declared with rl_set_slot_lengths. */
 rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group,
                      const int32_t* slots, const uint64_t* seq_uids,
                      const int32_t* prompt_offsets, const int32_t* tokens,
@@ -283,7 +288,7 @@ typedef enum rl_option {
                                 selected classes are timed with HIP events on
                                 the context's stream; 0 = off (default),
                                 -1 = every class                              */
-    RL_OPT_GEMM_PLAN = 3     /* bf16 GEMM kernel override (testing every tile
+    RL_OPT_GEMM_PLAN = 3,    /* bf16 GEMM kernel override (testing every tile
                                 kernel on small models): 0 = the cost-model
                                 planner (default); else
                                   bits 0-7:   rl_gemm_kernel of all columns
@@ -299,6 +304,14 @@ typedef enum rl_option {
                                 planner's choice.  Results stay within the
                                 parity tolerances for every choice; the bits
                                 differ (fp32 summation order).               */
+    RL_OPT_SHARED_PREFIX = 4 /* 1 (default): decode attention of the slots of
+                                one rl_prefill group reads the prompt's K/V
+                                from the group's first slot (every slot of
+                                the group holds the same copy), in 32-position
+                                steps, and keeps the readers of one prompt
+                                chunk on one XCD, so each prompt chunk is read
+                                from HBM about once per group; 0: every slot
+                                reads its own copy.  Results are identical. */
 } rl_option;
 
 typedef enum rl_gemm_kernel {

@@ -110,11 +110,16 @@ struct rl_decode_ctx {
     hipStream_t stream = nullptr;
     int device = 0;
     std::vector<int32_t> len;
+    // shared GRPO prompt: decode attention over positions [0, share_len[s])
+    // of slot s reads slot share_src[s] (the group's first slot, holding the
+    // same K/V); -1 = no sharing
+    std::vector<int32_t> share_src, share_len;
     uint8_t* staging[kStages] = {nullptr, nullptr, nullptr};
     hipEvent_t stage_ev[kStages] = {nullptr, nullptr, nullptr};
     bool stage_used[kStages] = {false, false, false};
     int stage_next = 0;
     int64_t opt_chunk = 0;
+    bool opt_shared = true;           // RL_OPT_SHARED_PREFIX
     int64_t opt_gemm = 0;             // RL_OPT_GEMM_PLAN
     uint32_t profile = 0;             // bit mask over kernel classes
     struct Pending { int kc; hipEvent_t a, b; };
@@ -509,81 +514,197 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
 }
 
 // Split-KV work items for a set of query blocks.  Each block: nq tokens at
-// positions pos0 .. pos0+nq-1 of a slot, keys [0, pos0 + nq).
-struct Block { int qrow, nq, slot, pos0; };
+// positions pos0 .. pos0+nq-1 of a slot, keys [0, pos0 + nq).  With src >= 0
+// the keys [0, plen) (plen a multiple of 32, <= pos0) are read from slot src
+// instead (a shared prompt) and the rest from the block's own slot.
+struct Block {
+    int qrow, nq, slot, pos0;
+    int src = -1, plen = 0;
+};
+
+int block_items(const Block& b, int C) {
+    const int hi = b.pos0 + b.nq;
+    if (b.src >= 0 && b.plen > 0) return ceil_div(b.plen, C) + ceil_div(hi - b.plen, C);
+    return ceil_div(hi, C);
+}
 
 int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int default_min,
                  int items_cap, bool decode) {
-    auto count = [&](int C, long* items, long* multi) {
-        *items = 0; *multi = 0;
+    auto count = [&](int C, long* items, long* multi, int* most) {
+        *items = 0; *multi = 0; *most = 0;
         for (const Block& b : blocks) {
-            long k = ceil_div(b.pos0 + b.nq, C);
+            const long k = block_items(b, C);
             *items += k;
             if (k > 1) *multi += k;
+            *most = std::max<int>(*most, static_cast<int>(k));
         }
     };
     long items, multi;
-    int C;
+    int most, C;
     if (forced > 0) {
         C = static_cast<int>(forced);
     } else if (decode) {
         C = 64;
         while (C < (1 << 16)) {
-            count(2 * C, &items, &multi);
+            count(2 * C, &items, &multi, &most);
             if (items * Hkv < kAttnWaveTarget) break;
             C *= 2;
         }
     } else {
         C = default_min;
     }
-    int longest = 0;
-    for (const Block& b : blocks) longest = std::max(longest, b.pos0 + b.nq);
     for (;;) {
-        count(C, &items, &multi);
-        const bool fits = items <= items_cap && multi <= kPartItems && ceil_div(longest, C) <= kMaxCombine;
+        count(C, &items, &multi, &most);
+        const bool fits = items <= items_cap && multi <= kPartItems && most <= kMaxCombine;
         if (fits || C >= (1 << 20)) break;
         C *= 2;
     }
     return C;
 }
 
+// Work-item order for shared prompts.  The attention grid is (items / 4,
+// Hkv) with the x extent a multiple of 8, so workgroup x runs on XCD x % 8
+// for every kv-head.  Items that read the same shared chunk (the prompt of
+// one group) are kept together and their workgroups placed on one XCD, so
+// the chunk comes from HBM once and the other reads hit that XCD's L2.
+// Workgroup units go to the least-loaded XCD queue (load = key positions)
+// unless they continue the previous unit's chunk.  Returns the item order
+// (new position -> old index, -1 = empty padding item).
+std::vector<int> place_shared(const std::vector<AttnItem>& its, const std::vector<int64_t>& key) {
+    std::vector<int> idx(its.size());
+    for (size_t i = 0; i < idx.size(); ++i) idx[i] = static_cast<int>(i);
+    std::stable_sort(idx.begin(), idx.end(), [&](int a, int b) {
+        const bool sa = key[a] >= 0, sb = key[b] >= 0;
+        if (sa != sb) return sa;
+        return sa && key[a] < key[b];
+    });
+    const int nu = static_cast<int>((idx.size() + 3) / 4);
+    std::vector<std::vector<int>> q(8);
+    double load[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int prev_q = -1;
+    int64_t prev_key = -1;
+    for (int u = 0; u < nu; ++u) {
+        const int b0 = 4 * u, b1 = std::min<int>(4 * u + 4, static_cast<int>(idx.size()));
+        const int64_t k = key[idx[b0]];
+        int qq = 0;
+        if (k >= 0 && k == prev_key) {
+            qq = prev_q;
+        } else {
+            for (int j = 1; j < 8; ++j) if (load[j] < load[qq]) qq = j;
+        }
+        q[qq].push_back(u);
+        for (int i = b0; i < b1; ++i) load[qq] += its[idx[i]].kv_hi - its[idx[i]].kv_lo;
+        prev_q = qq;
+        prev_key = key[idx[b1 - 1]];
+    }
+    size_t L = 0;
+    for (int j = 0; j < 8; ++j) L = std::max(L, q[j].size());
+    std::vector<int> order(32 * L, -1);
+    for (int j = 0; j < 8; ++j)
+        for (size_t i = 0; i < q[j].size(); ++i) {
+            const int u = q[j][i];
+            const size_t x = 8 * i + j;
+            for (int t = 0; t < 4 && 4 * u + t < static_cast<int>(idx.size()); ++t) order[4 * x + t] = idx[4 * u + t];
+        }
+    return order;
+}
+
 rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& blocks, int C, Fwd* f) {
-    long total = 0;
-    for (const Block& b : blocks) total += ceil_div(b.pos0 + b.nq, C);
-    if (total > c->lay.items_cap) return fail(c, RL_ERR_CAPACITY, "too many attention work items");
-    AttnItem* dItems = nullptr;
-    AttnItem* items = m->take<AttnItem>(static_cast<size_t>(total), &dItems);
-    int32_t* dSplit = nullptr;
-    int32_t* split = m->take<int32_t>(blocks.size(), &dSplit);
-    if (!items || !split) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
-    int k = 0, part = 0, nsplit = 0;
-    double scorepos = 0;
+    std::vector<AttnItem> its;
+    std::vector<int64_t> key;
+    std::vector<int> split_first;
+    int part = 0;
+    bool any_shared = false;
+    double scorepos = 0, kvpos = 0;
     for (const Block& b : blocks) {
         const int hi_all = b.pos0 + b.nq;
-        const int nch = ceil_div(hi_all, C);
+        const bool sh = b.src >= 0 && b.plen > 0;
+        const int n_sh = sh ? ceil_div(b.plen, C) : 0;
+        const int lo_own = sh ? b.plen : 0;
+        const int nch = n_sh + ceil_div(hi_all - lo_own, C);
         const int part0 = nch > 1 ? part : -1;
         if (nch > kMaxCombine) return fail(c, RL_ERR_CAPACITY, "too many split-KV chunks in one block");
-        if (nch > 1) split[nsplit++] = k;
+        if (nch > 1) split_first.push_back(static_cast<int>(its.size()));
         for (int ch = 0; ch < nch; ++ch) {
-            AttnItem& it = items[k++];
+            AttnItem it;
             std::memset(&it, 0, sizeof(it));
-            it.qrow = b.qrow; it.nq = b.nq; it.slot = b.slot; it.pos0 = b.pos0;
-            it.kv_lo = ch * C;
-            it.kv_hi = std::min(hi_all, (ch + 1) * C);
+            it.qrow = b.qrow; it.nq = b.nq; it.pos0 = b.pos0;
+            if (ch < n_sh) {
+                it.slot = b.src;
+                it.kv_lo = ch * C;
+                it.kv_hi = std::min(b.plen, (ch + 1) * C);
+                key.push_back((static_cast<int64_t>(b.src) << 32) | ch);
+                any_shared = true;
+            } else {
+                const int j = ch - n_sh;
+                it.slot = b.slot;
+                it.kv_lo = lo_own + j * C;
+                it.kv_hi = std::min(hi_all, lo_own + (j + 1) * C);
+                key.push_back(-1);
+            }
             it.part = nch > 1 ? part++ : -1;
             it.part0 = part0;
             it.nparts = nch;
+            its.push_back(it);
         }
         for (int t = 0; t < b.nq; ++t) scorepos += b.pos0 + t + 1;
+        kvpos += sh ? hi_all - b.plen : hi_all;
     }
     if (part > kPartItems) return fail(c, RL_ERR_CAPACITY, "too many split-KV partials");
+    std::vector<int> order;
+    if (any_shared) {
+        order = place_shared(its, key);
+        if (order.size() > static_cast<size_t>(c->lay.items_cap)) order.clear();   // keep the plain order
+        // algorithmic KV positions: the own parts plus each shared chunk once
+        std::vector<std::pair<int64_t, int>> sh;
+        for (size_t i = 0; i < its.size(); ++i)
+            if (key[i] >= 0) sh.emplace_back(key[i], its[i].kv_hi - its[i].kv_lo);
+        std::sort(sh.begin(), sh.end());
+        for (size_t i = 0; i < sh.size(); ++i)
+            if (i == 0 || sh[i].first != sh[i - 1].first) kvpos += sh[i].second;
+        f->attn_kv_positions = kvpos;
+    }
+    if (order.empty()) {
+        order.resize(its.size());
+        for (size_t i = 0; i < its.size(); ++i) order[i] = static_cast<int>(i);
+    }
+    if (order.size() > static_cast<size_t>(c->lay.items_cap)) return fail(c, RL_ERR_CAPACITY, "too many attention work items");
+    AttnItem* dItems = nullptr;
+    AttnItem* items = m->take<AttnItem>(order.size(), &dItems);
+    int32_t* dSplit = nullptr;
+    int32_t* split = m->take<int32_t>(std::max<size_t>(split_first.size(), 1), &dSplit);
+    if (!items || !split) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    std::vector<int> newpos(its.size(), 0);
+    for (size_t x = 0; x < order.size(); ++x) {
+        if (order[x] < 0) {   // padding: no query columns, no keys
+            std::memset(&items[x], 0, sizeof(AttnItem));
+            items[x].part = -1;
+        } else {
+            items[x] = its[order[x]];
+            newpos[order[x]] = static_cast<int>(x);
+        }
+    }
+    for (size_t i = 0; i < split_first.size(); ++i) split[i] = newpos[split_first[i]];
     f->items = dItems;
-    f->n_items = k;
+    f->n_items = static_cast<int>(order.size());
     f->n_partial_items = part;
     f->split_blocks = dSplit;
-    f->n_split_blocks = nsplit;
+    f->n_split_blocks = static_cast<int>(split_first.size());
     f->attn_score_positions = scorepos;
     return RL_OK;
+}
+
+// Drop prompt sharing of the given slots, and of every slot that reads its
+// prompt from one of them (their own copies stay valid).
+void unshare(rl_decode_ctx* c, int n, const int32_t* slots) {
+    const int S = c->cfg.max_seqs;
+    std::vector<char> hit(static_cast<size_t>(S), 0);
+    for (int i = 0; i < n; ++i) hit[slots[i]] = 1;
+    for (int s = 0; s < S; ++s)
+        if (hit[s] || (c->share_src[s] >= 0 && hit[c->share_src[s]])) {
+            c->share_src[s] = -1;
+            c->share_len[s] = 0;
+        }
 }
 
 void fill_rope_table(const rl_model_config& c, int cap, std::vector<float>* out) {
@@ -692,6 +813,8 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
     c->ws = static_cast<uint8_t*>(workspace);
     c->stream = static_cast<hipStream_t>(stream);
     c->len.assign(static_cast<size_t>(cfg->max_seqs), 0);
+    c->share_src.assign(static_cast<size_t>(cfg->max_seqs), -1);
+    c->share_len.assign(static_cast<size_t>(cfg->max_seqs), 0);
     auto cleanup = [&](rl_status s) {
         for (int i = 0; i < kStages; ++i) {
             if (c->staging[i]) (void)hipHostFree(c->staging[i]);
@@ -845,8 +968,18 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     if (st != RL_OK) return st;
     st = run_forward(c, f);
     if (st != RL_OK) return st;
-    for (int p = 0; p < n_prompts; ++p)
-        for (int k = 0; k < group; ++k) c->len[slots[p * group + k]] = prompt_offsets[p + 1] - prompt_offsets[p];
+    unshare(c, n_out, slots);
+    for (int p = 0; p < n_prompts; ++p) {
+        const int len = prompt_offsets[p + 1] - prompt_offsets[p];
+        for (int k = 0; k < group; ++k) {
+            const int s = slots[p * group + k];
+            c->len[s] = len;
+            if (group > 1) {   // every slot of the group holds the same prompt K/V
+                c->share_src[s] = slots[p * group];
+                c->share_len[s] = len;
+            }
+        }
+    }
     return RL_OK;
 }
 
@@ -996,6 +1129,7 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
         e = hipMemcpyAsync(tok + R1, resp_tokens, sizeof(int32_t) * static_cast<size_t>(r2), hipMemcpyDeviceToDevice,
                            c->stream);
     if (e != hipSuccess) return hip_fail(c, e, "token copy");
+    unshare(c, n_seq, slots);
     st = run_forward(c, f);
     for (int i = 0; i < n_seq; ++i) c->len[slots[i]] = 0;   // the slots were scratch
     return st;
@@ -1044,6 +1178,11 @@ rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, co
         posn[i] = p + 1;
         uid[i] = seq_uids[i];
         blocks[i] = Block{i, 1, slots[i], p};
+        const int src = c->opt_shared ? c->share_src[slots[i]] : -1;
+        if (src >= 0) {   // a shared prompt: whole 32-position steps of it come from the group's first slot
+            blocks[i].src = src;
+            blocks[i].plen = c->share_len[slots[i]] / 32 * 32;
+        }
         kvpos += p + 1;
     }
     Fwd f;
@@ -1121,6 +1260,7 @@ rl_status rl_release_slots(rl_decode_ctx* ctx, int32_t n, const int32_t* slots) 
     for (int i = 0; i < n; ++i)
         if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return fail(ctx, RL_ERR_INVALID_ARG, "slot out of range");
     for (int i = 0; i < n; ++i) ctx->len[slots[i]] = 0;
+    unshare(ctx, n, slots);
     return RL_OK;
 }
 
@@ -1132,6 +1272,7 @@ rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slot
         if (lengths[i] < 0 || lengths[i] > ctx->cfg.max_ctx) return fail(ctx, RL_ERR_INVALID_ARG, "length out of range");
     }
     for (int i = 0; i < n; ++i) ctx->len[slots[i]] = lengths[i];
+    unshare(ctx, n, slots);
     return RL_OK;
 }
 
@@ -1158,6 +1299,10 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
             ctx->opt_gemm = value;
             return RL_OK;
         }
+        case RL_OPT_SHARED_PREFIX:
+            if (value != 0 && value != 1) return fail(ctx, RL_ERR_INVALID_ARG, "shared prefix option must be 0 or 1");
+            ctx->opt_shared = value == 1;
+            return RL_OK;
         case RL_OPT_PROFILE:
             if (value < -1 || value >= (int64_t(1) << RL_K_COUNT))
                 return fail(ctx, RL_ERR_INVALID_ARG, "profile must be a class bit mask or -1");

@@ -1,0 +1,141 @@
+"""Shared GRPO prompts in decode attention (RL_OPT_SHARED_PREFIX), through
+the C ABI (needs an MI355X).
+
+After rl_prefill with group > 1 every slot of a group holds the same prompt
+K/V; decode attention then reads the prompt part from the group's first slot.
+These tests check the results against the oracle while the sharing is set
+up, used, and torn down again (the first slot released and refilled with
+another prompt, a group re-prefilled over part of another), and that the
+sharing is really in effect (the attention's algorithmic bytes count each
+group's prompt once).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import LOGIT_REL_TOL, LOGP_ABS_TOL, OracleRollout, build_models, row_rel_err
+from paper_2509_15965_amd.configs import ModelShape
+from paper_2509_15965_amd.inputs import uniform_tokens
+from paper_2509_15965_amd.rl_decode import (KERNEL_CLASSES, RL_OPT_ATTN_CHUNK, RL_OPT_PROFILE,
+                                           RL_OPT_SHARED_PREFIX, Engine)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+GQA = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e4, "bf16")
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _i32(a):
+    return torch.as_tensor(np.asarray(a, dtype=np.int32), device=DEV)
+
+
+class Run:
+    """GPU engine plus oracle sequences keyed by slot, stepped together with
+    seeded forced tokens; every step is compared with the oracle."""
+
+    def __init__(self, shared: int, chunk: int = 0):
+        self.w_dev, _, self.om = build_models(GQA, 51)
+        self.eng = Engine(GQA, self.w_dev, max_seqs=10, max_ctx=160, max_prefill_tokens=256)
+        self.eng.set_option(RL_OPT_SHARED_PREFIX, shared)
+        if chunk:
+            self.eng.set_option(RL_OPT_ATTN_CHUNK, chunk)
+        self.orc = OracleRollout(self.om, 160)
+        self.step_no = 0
+        self.errs = []
+
+    def prefill(self, slots, prompts, group):
+        n = len(slots)
+        offs = np.concatenate([[0], np.cumsum([len(p) for p in prompts])]).astype(np.int32)
+        ot = torch.empty(n, dtype=torch.int32, device=DEV)
+        ol = torch.empty(n, dtype=torch.float32, device=DEV)
+        self.eng.release(slots)
+        self.eng.prefill(slots, slots, offs, _i32(np.concatenate(prompts)), ot, ol, group=group)
+        for p, pr in enumerate(prompts):
+            self.orc.prefill(slots[p * group], pr)
+            for k in range(1, group):
+                self.orc.seqs[slots[p * group + k]] = self.orc.seqs[slots[p * group]].clone()
+
+    def step(self, slots):
+        n = len(slots)
+        self.step_no += 1
+        tin = uniform_tokens(n, GQA.vocab, 1000 + self.step_no)
+        tf = uniform_tokens(n, GQA.vocab, 2000 + self.step_no)
+        ot = torch.empty(n, dtype=torch.int32, device=DEV)
+        ol = torch.empty(n, dtype=torch.float32, device=DEV)
+        lg = torch.empty((n, GQA.vocab), dtype=torch.float32, device=DEV)
+        self.eng.step(slots, slots, _i32(tin), ot, ol, forced=_i32(tf), out_logits=lg)
+        torch.cuda.synchronize()
+        zg, lp = lg.cpu().numpy(), ol.cpu().numpy()
+        for i, s in enumerate(slots):
+            z = self.orc.step(s, tin[i])
+            e = row_rel_err(zg[i], z)
+            le = abs(lp[i] - oracle.logprob(z.astype(np.float32), 1.0, int(tf[i])))
+            self.errs.append((self.step_no, s, e, le))
+            assert e < LOGIT_REL_TOL, (self.step_no, s, e)
+            assert le < LOGP_ABS_TOL, (self.step_no, s, le)
+
+
+@pytest.mark.parametrize("shared,chunk", [(1, 0), (1, 32), (0, 0)], ids=["shared", "shared-chunk32", "off"])
+def test_shared_prompt_through_leader_reuse(shared, chunk):
+    rng = np.random.default_rng(52)
+    pr = [rng.integers(0, GQA.vocab, size=n).astype(np.int32) for n in (70, 45, 50, 66, 33)]
+    r = Run(shared, chunk)
+    r.prefill(list(range(8)), [pr[0], pr[1]], group=4)      # groups {0,1,2,3} and {4,5,6,7}
+    for _ in range(3):
+        r.step(list(range(8)))
+    # the first slot of group 0 takes a new prompt: slots 1..3 must fall back
+    # to their own copies of the old prompt
+    r.prefill([0], [pr[2]], group=1)
+    for _ in range(2):
+        r.step(list(range(8)))
+    # a new group over the old group 1's first slot and a free slot: slots
+    # 5..7 lose their source, slots 4 and 8 share the new prompt
+    r.prefill([4, 8], [pr[3]], group=2)
+    for _ in range(2):
+        r.step([1, 2, 3, 5, 6, 7, 0, 4, 8])
+    # a group whose members decode without their first slot
+    r.prefill([9, 6], [pr[4]], group=2)
+    r.eng.release([9])
+    for _ in range(2):
+        r.step([6, 0, 4])
+    r.eng.close()
+
+
+def test_shared_prompt_counts_each_prompt_once():
+    """The attention's algorithmic bytes of a decode step: with sharing, each
+    group's prompt (whole 32-position steps of it) once plus every row's own
+    part; without, every row's whole context."""
+    rng = np.random.default_rng(53)
+    plens = (70, 45)
+    prompts = [rng.integers(0, GQA.vocab, size=n).astype(np.int32) for n in plens]
+    out = {}
+    for shared in (0, 1):
+        w_dev, _, _ = build_models(GQA, 54)
+        eng = Engine(GQA, w_dev, max_seqs=8, max_ctx=128, max_prefill_tokens=128)
+        eng.set_option(RL_OPT_SHARED_PREFIX, shared)
+        offs = np.array([0, 70, 115], dtype=np.int32)
+        ot = torch.empty(8, dtype=torch.int32, device=DEV)
+        ol = torch.empty(8, dtype=torch.float32, device=DEV)
+        eng.prefill(list(range(8)), list(range(8)), offs, _i32(np.concatenate(prompts)), ot, ol, group=4)
+        eng.reset_stats()
+        eng.set_option(RL_OPT_PROFILE, 1 << KERNEL_CLASSES.index("attention"))
+        eng.step(list(range(8)), list(range(8)), ot.clone(), ot, ol)
+        torch.cuda.synchronize()
+        st = eng.kernel_stats()["attention"]
+        out[shared] = (st["alg_bytes"], st["launches"])
+        eng.close()
+    L, Hkv, D, Hq = GQA.n_layers, GQA.n_kv_heads, GQA.head_dim, GQA.n_q_heads
+    per_pos = Hkv * 2 * D * 2
+    q_bytes = 2 * 8 * Hq * D * 2
+    full = sum(4 * (p + 1) for p in plens)
+    shared_pos = sum(p // 32 * 32 + 4 * (p + 1 - p // 32 * 32) for p in plens)
+    assert out[0] == (L * (full * per_pos + q_bytes), L)
+    assert out[1] == (L * (shared_pos * per_pos + q_bytes), L)
