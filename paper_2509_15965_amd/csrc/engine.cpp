@@ -564,12 +564,15 @@ int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int 
 
 // Work-item order for shared prompts.  The attention grid is (items / 4,
 // Hkv) with the x extent a multiple of 8, so workgroup x runs on XCD x % 8
-// for every kv-head.  Items that read the same shared chunk (the prompt of
-// one group) are kept together and their workgroups placed on one XCD, so
-// the chunk comes from HBM once and the other reads hit that XCD's L2.
-// Workgroup units go to the least-loaded XCD queue (load = key positions)
-// unless they continue the previous unit's chunk.  Returns the item order
-// (new position -> old index, -1 = empty padding item).
+// for every kv-head, and workgroups start in x order.  Items that read the
+// same shared chunk (the prompt of one group) are kept together and their
+// workgroups placed on one XCD, so the chunk comes from HBM once and the
+// other reads hit that XCD's L2.  Workgroups (4 consecutive items; a run of
+// up to kMaxRunUnits of them for one chunk stays whole) are dealt longest first to the XCD with
+// the least work, so each XCD also starts its longest ones first.  Returns
+// the item order (new position -> old index, -1 = empty padding item).
+constexpr int kMaxRunUnits = 4;   // a chunk read by more workgroups spreads over several XCDs
+
 std::vector<int> place_shared(const std::vector<AttnItem>& its, const std::vector<int64_t>& key) {
     std::vector<int> idx(its.size());
     for (size_t i = 0; i < idx.size(); ++i) idx[i] = static_cast<int>(i);
@@ -579,23 +582,31 @@ std::vector<int> place_shared(const std::vector<AttnItem>& its, const std::vecto
         return sa && key[a] < key[b];
     });
     const int nu = static_cast<int>((idx.size() + 3) / 4);
-    std::vector<std::vector<int>> q(8);
-    double load[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    int prev_q = -1;
-    int64_t prev_key = -1;
+    // unit time: its longest item; runs: consecutive units of one chunk
+    std::vector<int> utime(nu, 0);
+    struct Run { int u0, u1, t; };
+    std::vector<Run> runs;
     for (int u = 0; u < nu; ++u) {
         const int b0 = 4 * u, b1 = std::min<int>(4 * u + 4, static_cast<int>(idx.size()));
+        for (int i = b0; i < b1; ++i) utime[u] = std::max(utime[u], its[idx[i]].kv_hi - its[idx[i]].kv_lo);
         const int64_t k = key[idx[b0]];
-        int qq = 0;
-        if (k >= 0 && k == prev_key) {
-            qq = prev_q;
+        if (u > 0 && k >= 0 && k == key[idx[4 * u - 1]] && runs.back().u1 - runs.back().u0 < kMaxRunUnits) {
+            runs.back().u1 = u + 1;
+            runs.back().t = std::max(runs.back().t, utime[u]);
         } else {
-            for (int j = 1; j < 8; ++j) if (load[j] < load[qq]) qq = j;
+            runs.push_back(Run{u, u + 1, utime[u]});
         }
-        q[qq].push_back(u);
-        for (int i = b0; i < b1; ++i) load[qq] += its[idx[i]].kv_hi - its[idx[i]].kv_lo;
-        prev_q = qq;
-        prev_key = key[idx[b1 - 1]];
+    }
+    std::stable_sort(runs.begin(), runs.end(), [](const Run& a, const Run& b) { return a.t > b.t; });
+    std::vector<std::vector<int>> q(8);
+    double load[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (const Run& r : runs) {
+        int qq = 0;
+        for (int j = 1; j < 8; ++j) if (load[j] < load[qq]) qq = j;
+        for (int u = r.u0; u < r.u1; ++u) {
+            q[qq].push_back(u);
+            load[qq] += utime[u];
+        }
     }
     size_t L = 0;
     for (int j = 0; j < 8; ++j) L = std::max(L, q[j].size());
@@ -624,11 +635,14 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
         const int nch = n_sh + ceil_div(hi_all - lo_own, C);
         const int part0 = nch > 1 ? part : -1;
         if (nch > kMaxCombine) return fail(c, RL_ERR_CAPACITY, "too many split-KV chunks in one block");
-        if (nch > 1) split_first.push_back(static_cast<int>(its.size()));
+        // the combine reads the block's rows and partial range from its last
+        // item (an own-slot item: never merged into a pair)
+        if (nch > 1) split_first.push_back(static_cast<int>(its.size()) + nch - 1);
         for (int ch = 0; ch < nch; ++ch) {
             AttnItem it;
             std::memset(&it, 0, sizeof(it));
             it.qrow = b.qrow; it.nq = b.nq; it.pos0 = b.pos0;
+            it.qrow_b = -1; it.part_b = -1;
             if (ch < n_sh) {
                 it.slot = b.src;
                 it.kv_lo = ch * C;
@@ -652,6 +666,36 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
     }
     if (part > kPartItems) return fail(c, RL_ERR_CAPACITY, "too many split-KV partials");
     std::vector<int> order;
+    const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    if (any_shared && 2 * G <= 16) {
+        // single-token readers of one shared chunk go two to an item
+        std::vector<int> sidx;
+        for (size_t i = 0; i < its.size(); ++i)
+            if (key[i] >= 0 && its[i].nq == 1) sidx.push_back(static_cast<int>(i));
+        std::stable_sort(sidx.begin(), sidx.end(), [&](int a, int b) { return key[a] < key[b]; });
+        std::vector<char> drop(its.size(), 0);
+        for (size_t k = 0; k + 1 < sidx.size();) {
+            const int a = sidx[k], b = sidx[k + 1];
+            if (key[a] != key[b]) { ++k; continue; }
+            its[a].nq = 2;
+            its[a].qrow_b = its[b].qrow;
+            its[a].part_b = its[b].part;
+            drop[b] = 1;
+            k += 2;
+        }
+        std::vector<int> remap(its.size(), -1);
+        size_t w = 0;
+        for (size_t i = 0; i < its.size(); ++i) {
+            if (drop[i]) continue;
+            remap[i] = static_cast<int>(w);
+            its[w] = its[i];
+            key[w] = key[i];
+            ++w;
+        }
+        for (int& f0 : split_first) f0 = remap[f0];
+        its.resize(w);
+        key.resize(w);
+    }
     if (any_shared) {
         order = place_shared(its, key);
         if (order.size() > static_cast<size_t>(c->lay.items_cap)) order.clear();   // keep the plain order
@@ -679,6 +723,8 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
         if (order[x] < 0) {   // padding: no query columns, no keys
             std::memset(&items[x], 0, sizeof(AttnItem));
             items[x].part = -1;
+            items[x].qrow_b = -1;
+            items[x].part_b = -1;
         } else {
             items[x] = its[order[x]];
             newpos[order[x]] = static_cast<int>(x);

@@ -3,7 +3,9 @@
 // bf16 path (split-KV, MFMA).  One wave owns one work item: up to 16 query
 // columns (query tokens x the q-heads of one kv-head) against one chunk of
 // key positions of one KV slot.  Every K and V byte of the chunk is read
-// once for all q-heads of the group.
+// once for all q-heads of the group.  A pair item serves the single decode
+// tokens of two sequences that read the same shared prompt chunk (2 x group
+// columns), so that chunk is read once for both.
 //   scores   S^T[t][c] = K[t] . Q[c]     (A = 16 key rows, B = 16 columns)
 //   output   O^T[d][c] += V^T[d][t] P^T[t][c]
 // Key rows of the two 16-row score tiles of a 32-position step are permuted
@@ -55,7 +57,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
     const bool cvalid = col < ncols;
     const int tau = cvalid ? col / G : 0;
     const int head = kvh * G + (cvalid ? col - tau * G : 0);
-    const int qrow = it.qrow + tau;
+    const bool second = it.qrow_b >= 0 && tau == 1;   // second sequence of a pair item
+    const int qrow = second ? it.qrow_b : it.qrow + tau;
     const int limit = cvalid ? it.pos0 + tau : -1;   // last key this column sees
 
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -176,7 +179,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
     }
     // split block: (m, l, unnormalised o) partials, merged by attn_combine
     if (!cvalid) return;
-    float* pp = part + ((static_cast<size_t>(it.part) * Hkv + kvh) * 16 + col) * (D + 2);
+    // a pair item's second sequence owns its own partial slot (columns from 0)
+    const int pidx = second ? it.part_b : it.part;
+    const int pcol = second ? col - G : col;
+    float* pp = part + ((static_cast<size_t>(pidx) * Hkv + kvh) * 16 + pcol) * (D + 2);
 #pragma unroll
     for (int i = 0; i < DT; ++i)
 #pragma unroll

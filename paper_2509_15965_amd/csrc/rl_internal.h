@@ -32,7 +32,12 @@ struct AttnItem {
                     // its tokens see (it then writes the final output)
     int32_t part0;  // first partial index of the block's items (they are consecutive)
     int32_t nparts; // items of the block (>= 2 when part >= 0)
-    int32_t pad[3];
+    int32_t qrow_b; // >= 0: a pair item over a shared prompt chunk -- columns
+                    // [G, 2G) are the single token of a second sequence,
+                    // workspace row qrow_b, partial index part_b (nq = 2,
+                    // no key of the chunk is masked for either); -1: none
+    int32_t part_b;
+    int32_t pad;
 };
 
 struct GemmArgs {
