@@ -50,9 +50,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=0, help="decode steps to time (0 = the whole rollout)")
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="qwen7b")
-    ap.add_argument("--stage", choices=("rollout", "score"), default="rollout",
+    ap.add_argument("--stage", choices=("rollout", "score", "switch"), default="rollout",
                     help="rollout: the decode hot path (default); score: the inference stage "
-                         "(log-probabilities of given responses, one GRPO group per call)")
+                         "(log-probabilities of given responses, one GRPO group per call); switch: "
+                         "context-switch cost (weights and live K/V to pinned host memory and back)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true",
                     help="time every kernel class (adds event overhead; diagnostics only)")
@@ -261,6 +262,96 @@ def score_main(args):
     print(json.dumps(out), flush=True)
 
 
+PCIE_PEAK_GBS = 64.0           # PCIe 5.0 x16, one direction
+
+
+def switch_main(args):
+    """Temporal-mode context switch of the 7B-shape rollout engine: the
+    weights (caller tensors) and the live K/V of the 512 sequences right
+    after the rollout's prefill go to pinned host memory and come back."""
+    import numpy as np
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights, rollout_plan
+    from paper_2509_15965_amd.rl_decode import Engine
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    plan = rollout_plan(wl)
+    P, G = wl.n_prompts, wl.group
+    n = P * G
+    plens = plan["prompt_lens"]
+    weights = make_weights(shape, wl.seed, device=dev)
+    eng = Engine(shape, weights, max_seqs=n, max_ctx=int(plens.max() + plan["response_lens"].max()),
+                 max_prefill_tokens=int(plens.sum()), device=dev)
+    slots = np.arange(n, dtype=np.int32)
+    offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
+    tok = torch.as_tensor(np.concatenate(plan["prompts"]), dtype=torch.int32, device=dev)
+    ot = torch.empty(n, dtype=torch.int32, device=dev)
+    ol = torch.empty(n, dtype=torch.float32, device=dev)
+    eng.prefill(slots, plan["uids"], offs, tok, ot, ol, group=G, seed=1)
+    torch.cuda.synchronize()
+    kv_bytes = eng.kv_offload_bytes(slots)
+    host_kv = torch.empty(kv_bytes, dtype=torch.uint8, pin_memory=True)
+    host_w = {k: torch.empty(v.shape, dtype=v.dtype, pin_memory=True) for k, v in weights.items()}
+    w_bytes = sum(v.numel() * v.element_size() for v in weights.values())
+    stream = eng.stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    res = []
+    reps = max(1, args.steps if args.steps > 0 else 3)
+    for r in range(reps + 1):
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        with torch.cuda.stream(stream):
+            for k, v in weights.items():
+                host_w[k].copy_(v, non_blocking=True)
+        ev[1].record(stream)
+        eng.kv_offload(slots, host_kv)
+        ev[2].record(stream)
+        with torch.cuda.stream(stream):
+            for k, v in weights.items():
+                v.copy_(host_w[k], non_blocking=True)
+        ev[3].record(stream)
+        eng.kv_onload(slots, [eng.slot_length(int(s)) for s in slots], host_kv)
+        ev[4].record(stream)
+        torch.cuda.synchronize()
+        if r > 0:                                 # the first round is warm-up
+            res.append([ev[i].elapsed_time(ev[i + 1]) for i in range(4)])
+        print(f"[bench] switch round {r + 1}/{reps + 1}", file=sys.stderr, flush=True)
+    ms = np.median(np.array(res), axis=0)
+    gbs = [w_bytes / (ms[0] * 1e6), kv_bytes / (ms[1] * 1e6), w_bytes / (ms[2] * 1e6), kv_bytes / (ms[3] * 1e6)]
+    out = {
+        "metric": "context-switch time (1 GPU) at 7B shape: weights + live K/V offloaded to pinned host memory "
+                  "and reloaded",
+        "value": round(float(ms.sum()) / 1e3, 4),
+        "unit": "s",
+        "n_gpus": 1,
+        "steps": reps,
+        "warmup": 1,
+        "ms_per_step": round(float(ms.sum()), 2),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, the rollout's prefilled K/V)",
+        "config": {"workload": f"{wl.name}: weights {w_bytes / 1e9:.2f} GB; live K/V of {n} sequences after the "
+                               f"prefill ({int(plens.sum())} prompt tokens) {kv_bytes / 1e9:.3f} GB"},
+        "ms": {"weights_offload": round(float(ms[0]), 2), "kv_offload": round(float(ms[1]), 2),
+               "weights_onload": round(float(ms[2]), 2), "kv_onload": round(float(ms[3]), 2)},
+        "GBps": {"weights_offload": round(gbs[0], 1), "kv_offload": round(gbs[1], 1),
+                 "weights_onload": round(gbs[2], 1), "kv_onload": round(gbs[3], 1)},
+        "roofline": {"bound": "pcie", "achieved": round((2 * w_bytes + 2 * kv_bytes) / (float(ms.sum()) * 1e6), 1),
+                     "peak": PCIE_PEAK_GBS, "unit": "GB/s",
+                     "frac": round((2 * w_bytes + 2 * kv_bytes) / (float(ms.sum()) * 1e6) / PCIE_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    eng.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe_mib > 0:
@@ -271,6 +362,9 @@ def main():
         sys.exit(2)
     if args.stage == "score":
         score_main(args)
+        return
+    if args.stage == "switch":
+        switch_main(args)
         return
     import numpy as np
     import torch

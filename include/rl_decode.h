@@ -276,6 +276,49 @@ rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slot
 int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot);
 
 /* ---------------------------------------------------------------------
+ * Context switching (Sec. 3: in temporal mode a worker's GPU state is
+ * offloaded so that the next stage can use the devices, and reloaded when
+ * it runs again; Sec. 5.1.1 counts that cost in "Others").
+ *
+ * Packed K/V of slot s (length n = its current length, E = element size):
+ * for every layer l and kv-head h (index l*Hkv + h): n K rows of head_dim
+ * elements, then ceil(n/8) V blocks of 8 positions (the pool's own layouts),
+ * i.e. n_layers * Hkv * (n + ceil8(n)) * head_dim * E bytes; slots follow
+ * one another in the order given.  The copies go through the workspace (a
+ * chunk of whole slots at a time); the host buffer should be pinned
+ * (hipHostMalloc) for full PCIe speed.  Weights are the caller's tensors and
+ * are moved by the caller.
+ * ------------------------------------------------------------------- */
+
+/* Bytes rl_kv_offload writes for these slots; 0 for an invalid context or
+ * slot. */
+size_t rl_kv_offload_bytes(const rl_decode_ctx* ctx, int32_t n, const int32_t* slots);
+
+/* Copy the live K/V of n distinct slots to host_dst (host_bytes >= the size
+ * above).  Asynchronous: host_dst is complete once the stream is
+ * synchronised.  Slot state is unchanged (release the slots to reuse them).
+ * RL_ERR_CAPACITY when one slot's K/V exceeds the workspace's staging region
+ * (the activation buffers). */
+rl_status rl_kv_offload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, void* host_dst,
+                        size_t host_bytes);
+
+/* Copy packed K/V from host_src into n distinct slots and set their
+ * lengths (lengths[i] in [0, max_ctx]; the layout above for these
+ * lengths).  The slots need not be those it was offloaded from.  They read
+ * their own copies afterwards (no prompt sharing). */
+rl_status rl_kv_onload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* lengths,
+                       const void* host_src, size_t host_bytes);
+
+/* Point the context at new device buffers (same sizes and alignment rules
+ * as rl_decode_create), e.g. after the caller freed the old ones during a
+ * context switch.  Waits for the context's outstanding work, then writes the
+ * RoPE table and sampler counters into the new workspace (synchronises the
+ * stream).  Slot lengths are kept: reload their K/V with rl_kv_onload, or
+ * release them. */
+rl_status rl_decode_rebind(rl_decode_ctx* ctx, const rl_weights* w, void* kv_pool, size_t kv_bytes,
+                           void* workspace, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------
  * Options and measurement.
  * ------------------------------------------------------------------- */
 

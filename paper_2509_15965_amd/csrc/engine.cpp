@@ -33,6 +33,7 @@ struct Layout {
     size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
     size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
     size_t off_cnt = 0, cnt_bytes = 0, off_spart = 0, off_tok = 0;
+    size_t off_stage = 0, stage_bytes = 0;   // KV offload staging: the activation buffers x .. split-K partials
     size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
 };
 
@@ -85,6 +86,8 @@ Layout make_layout(const rl_model_config& c) {
     L.off_attn = take(R * HqD * es);
     L.off_mlp = take(R * F * es);
     L.off_part = take(L.part_floats * 4);
+    L.off_stage = L.off_x;
+    L.stage_bytes = o - L.off_x;
     L.off_apart = take(L.apart_floats * 4);
     L.off_logits = take(static_cast<size_t>(c.max_seqs) * V * 4);
     L.off_rope = take(static_cast<size_t>(L.cap) * (c.head_dim / 2) * 2 * 4);
@@ -832,6 +835,32 @@ size_t rl_decode_workspace_bytes(const rl_model_config* cfg) {
     return make_layout(*cfg).ws_bytes;
 }
 
+namespace {
+
+// RoPE table and zeroed sampler counters in the workspace; synchronises the stream.
+hipError_t init_workspace(rl_decode_ctx* c) {
+    std::vector<float> table;
+    fill_rope_table(c->cfg, c->lay.cap, &table);
+    hipError_t e = hipMemcpyAsync(c->ws + c->lay.off_rope, table.data(), table.size() * sizeof(float),
+                                  hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->ws + c->lay.off_cnt, 0, c->lay.cnt_bytes, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    return e;
+}
+
+bool weights_ok(const rl_weights* w) {
+    if (!w || !w->embed || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up ||
+        !w->w_down || !w->final_norm || !w->lm_head)
+        return false;
+    const void* wp[9] = {w->embed, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm, w->w_gate_up, w->w_down,
+                         w->final_norm, w->lm_head};
+    for (const void* p : wp)
+        if (!aligned(p, 16)) return false;
+    return true;
+}
+
+}  // namespace
+
 rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void* kv_pool,
                            size_t kv_bytes, void* workspace, size_t ws_bytes, void* stream,
                            rl_decode_ctx** out) {
@@ -839,13 +868,7 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
     *out = nullptr;
     rl_status code; std::string why;
     if (!cfg_check(cfg, &code, &why)) return code;
-    if (!w || !w->embed || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up ||
-        !w->w_down || !w->final_norm || !w->lm_head)
-        return RL_ERR_INVALID_ARG;
-    const void* wp[9] = {w->embed, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm, w->w_gate_up, w->w_down,
-                         w->final_norm, w->lm_head};
-    for (const void* p : wp)
-        if (!aligned(p, 16)) return RL_ERR_INVALID_ARG;
+    if (!weights_ok(w)) return RL_ERR_INVALID_ARG;
     if (!kv_pool || !workspace || !aligned(kv_pool, 256) || !aligned(workspace, 256)) return RL_ERR_INVALID_ARG;
     Layout L = make_layout(*cfg);
     if (kv_bytes < L.kv_bytes || ws_bytes < L.ws_bytes) return RL_ERR_CAPACITY;
@@ -876,13 +899,7 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
         if (hipEventCreateWithFlags(&c->stage_ev[i], hipEventDisableTiming) != hipSuccess)
             return cleanup(RL_ERR_HIP);
     }
-    std::vector<float> table;
-    fill_rope_table(*cfg, L.cap, &table);
-    if (hipMemcpyAsync(c->ws + L.off_rope, table.data(), table.size() * sizeof(float), hipMemcpyHostToDevice,
-                       c->stream) != hipSuccess)
-        return cleanup(RL_ERR_HIP);
-    if (hipMemsetAsync(c->ws + L.off_cnt, 0, L.cnt_bytes, c->stream) != hipSuccess) return cleanup(RL_ERR_HIP);
-    if (hipStreamSynchronize(c->stream) != hipSuccess) return cleanup(RL_ERR_HIP);
+    if (init_workspace(c) != hipSuccess) return cleanup(RL_ERR_HIP);
     for (int i = 0; i < RL_K_COUNT; ++i)
         std::snprintf(c->stats[i].name, sizeof(c->stats[i].name), "%s", kClassNames[i]);
     *out = c;
@@ -1297,6 +1314,138 @@ rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits, c
                                  c->stream);
     if (e != hipSuccess) return hip_fail(c, e, "sample launch");
     pr.done(n * (c->cfg.vocab * 4.0 + 8.0), 0.0);
+    return RL_OK;
+}
+
+namespace {
+
+size_t kv_slot_packed_bytes(const rl_decode_ctx* c, int len) {
+    const rl_model_config& cf = c->cfg;
+    const size_t len8 = (static_cast<size_t>(len) + 7) / 8 * 8;
+    return static_cast<size_t>(cf.n_layers) * cf.n_kv_heads * (len + len8) * cf.head_dim * c->lay.es;
+}
+
+// Offload (dir 0) or onload (dir 1) the packed live K/V of slots through the
+// workspace staging region, a chunk of whole slots at a time.
+rl_status kv_transfer(rl_decode_ctx* c, int dir, int n, const int32_t* slots, const int32_t* lens, uint8_t* host) {
+    const rl_model_config& cf = c->cfg;
+    const Layout& L = c->lay;
+    size_t host_off = 0;
+    int i0 = 0;
+    while (i0 < n) {
+        size_t bytes = 0;
+        int i1 = i0;
+        while (i1 < n && bytes + kv_slot_packed_bytes(c, lens[i1]) <= L.stage_bytes) bytes += kv_slot_packed_bytes(c, lens[i1++]);
+        if (i1 == i0) return fail(c, RL_ERR_CAPACITY, "one slot's K/V exceeds the workspace staging region");
+        Meta m{};
+        int stage = 0;
+        rl_status st = begin_meta(c, &m, &stage);
+        if (st != RL_OK) return st;
+        int32_t *d_slots, *d_lens;
+        int64_t* d_base;
+        int32_t* hs = m.take<int32_t>(i1 - i0, &d_slots);
+        int32_t* hl = m.take<int32_t>(i1 - i0, &d_lens);
+        int64_t* hb = m.take<int64_t>(i1 - i0, &d_base);
+        if (m.overflow) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+        size_t b = 0;
+        for (int i = i0; i < i1; ++i) {
+            hs[i - i0] = slots[i];
+            hl[i - i0] = lens[i];
+            hb[i - i0] = static_cast<int64_t>(b);
+            b += kv_slot_packed_bytes(c, lens[i]);
+        }
+        st = upload_meta(c, &m, stage);
+        if (st != RL_OK) return st;
+        uint8_t* stg = c->ws + L.off_stage;
+        hipError_t e = hipSuccess;
+        if (dir == 1) e = hipMemcpyAsync(stg, host + host_off, bytes, hipMemcpyHostToDevice, c->stream);
+        if (e == hipSuccess)
+            e = launch_kv_pack(dir, d_slots, d_lens, d_base, i1 - i0, cf.n_layers, cf.max_seqs, cf.n_kv_heads, L.cap,
+                               cf.head_dim * L.es, c->kslab(), c->vslab(), stg, c->stream);
+        if (e == hipSuccess && dir == 0) e = hipMemcpyAsync(host + host_off, stg, bytes, hipMemcpyDeviceToHost, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, dir == 0 ? "KV offload" : "KV onload");
+        host_off += bytes;
+        i0 = i1;
+    }
+    return RL_OK;
+}
+
+}  // namespace
+
+size_t rl_kv_offload_bytes(const rl_decode_ctx* ctx, int32_t n, const int32_t* slots) {
+    if (!ctx_ok(ctx) || n < 0 || (n > 0 && !slots)) return 0;
+    size_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return 0;
+        total += kv_slot_packed_bytes(ctx, ctx->len[slots[i]]);
+    }
+    return total;
+}
+
+rl_status rl_kv_offload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, void* host_dst, size_t host_bytes) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    if (n < 0) return fail(c, RL_ERR_INVALID_ARG, "n must be >= 0");
+    if (n == 0) return RL_OK;
+    if (!slots || !host_dst) return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    std::vector<char> seen;
+    rl_status st = check_slots(c, n, slots, &seen);
+    if (st != RL_OK) return st;
+    std::vector<int32_t> lens(static_cast<size_t>(n));
+    size_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        lens[i] = c->len[slots[i]];
+        const size_t b = kv_slot_packed_bytes(c, lens[i]);
+        if (b > c->lay.stage_bytes) return fail(c, RL_ERR_CAPACITY, "one slot's K/V exceeds the workspace staging region");
+        total += b;
+    }
+    if (total > host_bytes) return fail(c, RL_ERR_CAPACITY, "host buffer smaller than rl_kv_offload_bytes");
+    DeviceGuard g(c->device);
+    return kv_transfer(c, 0, n, slots, lens.data(), static_cast<uint8_t*>(host_dst));
+}
+
+rl_status rl_kv_onload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* lengths,
+                       const void* host_src, size_t host_bytes) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    if (n < 0) return fail(c, RL_ERR_INVALID_ARG, "n must be >= 0");
+    if (n == 0) return RL_OK;
+    if (!slots || !lengths || !host_src) return fail(c, RL_ERR_INVALID_ARG, "required pointer is NULL");
+    std::vector<char> seen;
+    rl_status st = check_slots(c, n, slots, &seen);
+    if (st != RL_OK) return st;
+    size_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        if (lengths[i] < 0 || lengths[i] > c->cfg.max_ctx) return fail(c, RL_ERR_INVALID_ARG, "length out of range");
+        const size_t b = kv_slot_packed_bytes(c, lengths[i]);
+        if (b > c->lay.stage_bytes) return fail(c, RL_ERR_CAPACITY, "one slot's K/V exceeds the workspace staging region");
+        total += b;
+    }
+    if (total > host_bytes) return fail(c, RL_ERR_CAPACITY, "host buffer smaller than the packed K/V of these lengths");
+    DeviceGuard g(c->device);
+    st = kv_transfer(c, 1, n, slots, lengths, static_cast<uint8_t*>(const_cast<void*>(host_src)));
+    if (st != RL_OK) return st;
+    for (int i = 0; i < n; ++i) c->len[slots[i]] = lengths[i];
+    unshare(c, n, slots);
+    return RL_OK;
+}
+
+rl_status rl_decode_rebind(rl_decode_ctx* ctx, const rl_weights* w, void* kv_pool, size_t kv_bytes,
+                           void* workspace, size_t ws_bytes) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    rl_decode_ctx* c = ctx;
+    if (!weights_ok(w)) return fail(c, RL_ERR_INVALID_ARG, "weights: NULL or misaligned pointer");
+    if (!kv_pool || !workspace || !aligned(kv_pool, 256) || !aligned(workspace, 256))
+        return fail(c, RL_ERR_INVALID_ARG, "KV pool and workspace must be 256-byte aligned device pointers");
+    if (kv_bytes < c->lay.kv_bytes || ws_bytes < c->lay.ws_bytes) return fail(c, RL_ERR_CAPACITY, "buffer too small");
+    DeviceGuard g(c->device);
+    hipError_t e = hipStreamSynchronize(c->stream);   // nothing may still use the old buffers
+    if (e != hipSuccess) return hip_fail(c, e, "rebind wait");
+    c->w = *w;
+    c->kv = static_cast<uint8_t*>(kv_pool);
+    c->ws = static_cast<uint8_t*>(workspace);
+    e = init_workspace(c);
+    if (e != hipSuccess) return hip_fail(c, e, "rebind workspace setup");
     return RL_OK;
 }
 

@@ -317,6 +317,39 @@ hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, 
     return hipGetLastError();
 }
 
+// Live K/V of slots <-> a packed staging buffer (dir 0: pool -> stage, dir 1:
+// stage -> pool).  One workgroup per (slot i, layer * Hkv + head, K|V): the
+// slot's K rows [len][d] and its V blocks [ceil8(len)/8][d][8] are contiguous
+// in the pool and are copied as they are, 16 bytes per lane.  Packed layout
+// of slot i at byte base[i]: for l, h: K rows then V blocks.
+__global__ void __launch_bounds__(256) kv_pack_kernel(int dir, const int32_t* __restrict__ slots,
+        const int32_t* __restrict__ lens, const int64_t* __restrict__ base, int S, int Hkv, int cap,
+        int rowbytes, uint8_t* __restrict__ kslab, uint8_t* __restrict__ vslab, uint8_t* __restrict__ stage) {
+    const int i = blockIdx.x, lh = blockIdx.y, kv = blockIdx.z;
+    const int l = lh / Hkv, h = lh - l * Hkv;
+    const int len = lens[i], len8 = (len + 7) / 8 * 8;
+    const size_t pool_off = ((static_cast<size_t>(l) * S + slots[i]) * Hkv + h) * static_cast<size_t>(cap) * rowbytes;
+    const size_t st_off = static_cast<size_t>(base[i]) +
+                          (static_cast<size_t>(lh) * (len + len8) + (kv ? len : 0)) * rowbytes;
+    u32x4* pool = reinterpret_cast<u32x4*>((kv ? vslab : kslab) + pool_off);
+    u32x4* st = reinterpret_cast<u32x4*>(stage + st_off);
+    const size_t n16 = static_cast<size_t>(kv ? len8 : len) * rowbytes / 16;
+    for (size_t j = threadIdx.x; j < n16; j += blockDim.x) {
+        if (dir == 0) st[j] = pool[j];
+        else pool[j] = st[j];
+    }
+}
+
+hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
+                          int S, int Hkv, int cap, int rowbytes, void* kslab, void* vslab, void* stage,
+                          hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(kv_pack_kernel, dim3(n, L * Hkv, 2), dim3(256), 0, s, dir, slots, lens, base, S, Hkv, cap,
+                       rowbytes, static_cast<uint8_t*>(kslab), static_cast<uint8_t*>(vslab),
+                       static_cast<uint8_t*>(stage));
+    return hipGetLastError();
+}
+
 // Plain streaming copy: 16 bytes per lane per iteration, grid-stride.
 __global__ void __launch_bounds__(256) copy16_kernel(u32x4* __restrict__ dst,
         const u32x4* __restrict__ src, size_t n16) {

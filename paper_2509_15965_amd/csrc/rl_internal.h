@@ -151,6 +151,15 @@ hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_
                          uint64_t seed, float T, SamplePart* parts, int* counters,
                          int32_t* out_tok, float* out_logp, hipStream_t s);
 
+// Copy the live K/V of n slots between the pool and a packed staging buffer
+// (dir 0: pool -> stage, dir 1: stage -> pool).  Slot i (lens[i] positions)
+// starts at byte base[i] of the stage: for layer l, kv-head h (index
+// l*Hkv + h): lens[i] K rows of rowbytes, then ceil8(lens[i]) / 8 V blocks of
+// 8 * rowbytes (the pool's own layouts).  rowbytes = head_dim * element size.
+hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
+                          int S, int Hkv, int cap, int rowbytes, void* kslab, void* vslab, void* stage,
+                          hipStream_t s);
+
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
 
 }  // namespace rl

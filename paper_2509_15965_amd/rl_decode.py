@@ -31,7 +31,8 @@ KERNEL_CLASSES = ("embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "a
 
 EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create", "rl_decode_destroy",
            "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
-           "rl_set_slot_lengths", "rl_slot_length", "rl_decode_set_option", "rl_decode_kernel_stats",
+           "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
+           "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
            "rl_decode_reset_stats", "rl_probe_copy", "rl_status_string", "rl_decode_last_error")
 
 
@@ -92,6 +93,14 @@ def lib():
     L.rl_set_slot_lengths.argtypes = [vp, i32, vp, vp]
     L.rl_slot_length.restype = i32
     L.rl_slot_length.argtypes = [vp, i32]
+    L.rl_kv_offload_bytes.restype = sz
+    L.rl_kv_offload_bytes.argtypes = [vp, i32, vp]
+    L.rl_kv_offload.restype = C.c_int
+    L.rl_kv_offload.argtypes = [vp, i32, vp, vp, sz]
+    L.rl_kv_onload.restype = C.c_int
+    L.rl_kv_onload.argtypes = [vp, i32, vp, vp, vp, sz]
+    L.rl_decode_rebind.restype = C.c_int
+    L.rl_decode_rebind.argtypes = [vp, C.POINTER(Weights), vp, sz, vp, sz]
     L.rl_decode_set_option.restype = C.c_int
     L.rl_decode_set_option.argtypes = [vp, i32, C.c_int64]
     L.rl_decode_kernel_stats.restype = C.c_int
@@ -241,6 +250,30 @@ class Engine:
 
     def slot_length(self, slot: int) -> int:
         return int(lib().rl_slot_length(self.h, slot))
+
+    def kv_offload_bytes(self, slots: Sequence[int]) -> int:
+        s = _host_i32(slots)
+        return int(lib().rl_kv_offload_bytes(self.h, len(s), s.ctypes.data))
+
+    def kv_offload(self, slots: Sequence[int], host: torch.Tensor):
+        """Live K/V of `slots` into `host` (a pinned uint8 CPU tensor)."""
+        s = _host_i32(slots)
+        self._check(lib().rl_kv_offload(self.h, len(s), s.ctypes.data, host.data_ptr(), host.numel()),
+                    "rl_kv_offload")
+
+    def kv_onload(self, slots: Sequence[int], lengths: Sequence[int], host: torch.Tensor):
+        s, l = _host_i32(slots), _host_i32(lengths)
+        self._check(lib().rl_kv_onload(self.h, len(s), s.ctypes.data, l.ctypes.data, host.data_ptr(),
+                                       host.numel()), "rl_kv_onload")
+
+    def rebind(self, weights: Dict[str, torch.Tensor], kv: torch.Tensor, ws: torch.Tensor):
+        """Point the context at new device buffers (weights, KV pool, workspace)."""
+        w = Weights()
+        for name, _ in Weights._fields_:
+            setattr(w, name, weights[name].data_ptr())
+        self._check(lib().rl_decode_rebind(self.h, C.byref(w), kv.data_ptr(), kv.numel(), ws.data_ptr(),
+                                           ws.numel()), "rl_decode_rebind")
+        self.weights, self.kv, self.ws = weights, kv, ws
 
     def set_option(self, option: int, value: int):
         self._check(lib().rl_decode_set_option(self.h, option, value), "rl_decode_set_option")
