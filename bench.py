@@ -50,10 +50,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=0, help="decode steps to time (0 = the whole rollout)")
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="qwen7b")
-    ap.add_argument("--stage", choices=("rollout", "score", "switch"), default="rollout",
+    ap.add_argument("--slots", type=int, default=256, help="--stage continuous: KV slots (sequences in flight)")
+    ap.add_argument("--emit-every", type=int, default=64, help="--stage continuous: responses per emitted chunk")
+    ap.add_argument("--stage", choices=("rollout", "score", "switch", "continuous"), default="rollout",
                     help="rollout: the decode hot path (default); score: the inference stage "
                          "(log-probabilities of given responses, one GRPO group per call); switch: "
-                         "context-switch cost (weights and live K/V to pinned host memory and back)")
+                         "context-switch cost (weights and live K/V to pinned host memory and back); "
+                         "continuous: the rollout's 512 sequences through fewer slots, continuous batching "
+                         "with chunked emission against static batches of the same size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true",
                     help="time every kernel class (adds event overhead; diagnostics only)")
@@ -352,6 +356,91 @@ def switch_main(args):
     print(json.dumps(out), flush=True)
 
 
+def continuous_main(args):
+    """The 7B rollout's 512 sequences (32 GRPO groups of 16) through
+    args.slots slots: static batches one after another (each runs until its
+    longest response ends) against continuous batching (groups admitted as
+    slots free up), which also hands finished responses downstream in chunks
+    of args.emit_every."""
+    import numpy as np
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights, rollout_plan
+    from paper_2509_15965_amd.rl_decode import Engine
+    from paper_2509_15965_amd.rollout import ContinuousRollout, StaticRollout
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    plan = rollout_plan(wl)
+    P, G = wl.n_prompts, wl.group
+    S = args.slots
+    if S % G or S < G:
+        raise SystemExit("--slots must be a multiple of the group size")
+    plens, resp, uids = plan["prompt_lens"], plan["response_lens"], plan["uids"]
+    weights = make_weights(shape, wl.seed, device=dev)
+    per = S // G                                          # prompts per static batch
+    eng = Engine(shape, weights, max_seqs=S, max_ctx=int(plens.max() + resp.max()),
+                 max_prefill_tokens=int(max(plens[i:i + per].sum() for i in range(0, P, per))), device=dev)
+    seed, T = 20250919, wl.temperature
+    # warm-up: a short static run
+    w = StaticRollout(eng, plan["prompts"][:per], G, np.minimum(resp[:S], 16), uids[:S], seed, T)
+    w.run()
+    torch.cuda.synchronize()
+    # static batches of S sequences, one after another
+    t0 = time.perf_counter()
+    gen_static = 0
+    for b in range(0, P, per):
+        ro = StaticRollout(eng, plan["prompts"][b:b + per], G, resp[b * G:(b + per) * G], uids[b * G:(b + per) * G],
+                           seed, T)
+        gen_static += ro.run() + ro.n
+        print(f"[bench] static batch {b // per + 1}/{-(-P // per)} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t_static = time.perf_counter() - t0
+    # continuous batching over the same slots
+    marks = []
+    t0 = time.perf_counter()
+
+    def on_emit(chunk):
+        marks.append((time.perf_counter() - t0, len(chunk)))
+        if len(marks) % 4 == 1:
+            print(f"[bench] continuous: chunk {len(marks)} emitted", file=sys.stderr, flush=True)
+
+    ro = ContinuousRollout(eng, plan["prompts"], G, resp, uids, seed, T, n_slots=S, emit_every=args.emit_every,
+                           on_emit=on_emit)
+    gen_cont = ro.run()
+    torch.cuda.synchronize()
+    t_cont = time.perf_counter() - t0
+    eng.close()
+    out = {
+        "metric": f"continuous-batching rollout tokens/sec (1 GPU) at 7B shape, {P * G} sequences through {S} slots",
+        "value": round(gen_cont / t_cont, 1),
+        "unit": "generated tokens/s",
+        "n_gpus": 1,
+        "steps": ro.steps,
+        "warmup": 16,
+        "ms_per_step": round(t_cont * 1e3 / max(1, ro.steps), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights and uniform prompt tokens)",
+        "config": {"workload": f"{wl.name}: {P} prompts x {G} samples, lognormal responses (median "
+                               f"{wl.response_median}, cap {wl.response_cap}); {S} slots; chunks of "
+                               f"{args.emit_every} responses",
+                   "generated_tokens": int(gen_cont)},
+        "static_batches": {"batches": -(-P // per), "seconds": round(t_static, 3),
+                           "tokens_per_s": round(gen_static / t_static, 1)},
+        "continuous": {"seconds": round(t_cont, 3), "decode_steps": ro.steps},
+        "speedup_vs_static": round(t_static / t_cont, 3),
+        "first_chunk_s": round(marks[0][0], 3) if marks else None,
+        "chunk_times_s": [round(m[0], 2) for m in marks],
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe_mib > 0:
@@ -366,12 +455,16 @@ def main():
     if args.stage == "switch":
         switch_main(args)
         return
+    if args.stage == "continuous":
+        continuous_main(args)
+        return
     import numpy as np
     import torch
 
     from paper_2509_15965_amd.configs import WORKLOADS
     from paper_2509_15965_amd.inputs import make_weights, rollout_plan
     from paper_2509_15965_amd.rl_decode import KERNEL_CLASSES, RL_OPT_PROFILE, Engine
+    from paper_2509_15965_amd.rollout import StaticRollout
 
     wl = WORKLOADS[args.workload]
     shape = wl.model
@@ -388,43 +481,14 @@ def main():
                  device=dev)
     stream = eng.stream
 
-    # sequences ordered by response length (longest first): the active set of
-    # decode step t is always a prefix of this order
-    seq_prompt = np.repeat(np.arange(P), G)
-    order = np.argsort(-resp, kind="stable")
-    slot_of = np.empty(n_seq, dtype=np.int64)
-    slot_of[order] = np.arange(n_seq)
-    uids_sorted = plan["uids"][order].astype(np.uint64)
-    resp_sorted = resp[order]
-    # prefill wants slots grouped by prompt: slots[p*G + k] = slot of sample k of prompt p
-    pre_slots = slot_of.astype(np.int32)
-    pre_uids = plan["uids"].astype(np.uint64)
-    offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
-    prompt_tok = torch.as_tensor(np.concatenate(plan["prompts"]), dtype=torch.int32, device=dev)
-    max_steps = int(resp.max()) - 1
-    active = np.array([(resp_sorted > t + 1).sum() for t in range(max_steps)], dtype=np.int64)
-    steps = max_steps if args.steps <= 0 else min(args.steps, max_steps)
+    # the rollout driver orders slots by response length (longest first), so
+    # the active set of decode step t is always a prefix of that order
     seed, T = 20250919, wl.temperature
-
-    toks = torch.zeros((max_steps + 1, n_seq), dtype=torch.int32, device=dev)
-    logps = torch.zeros((max_steps + 1, n_seq), dtype=torch.float32, device=dev)
-    first_tok = torch.empty(n_seq, dtype=torch.int32, device=dev)
-    first_lp = torch.empty(n_seq, dtype=torch.float32, device=dev)
-    slots_sorted = np.arange(n_seq, dtype=np.int32)
-
-    def prefill():
-        eng.release(slots_sorted)
-        eng.prefill(pre_slots, pre_uids, offs, prompt_tok, first_tok, first_lp, group=G, seed=seed,
-                    temperature=T)
-        # row 0 of the token table in slot order
-        toks[0].index_copy_(0, torch.as_tensor(pre_slots.astype(np.int64), device=dev), first_tok)
-        logps[0].index_copy_(0, torch.as_tensor(pre_slots.astype(np.int64), device=dev), first_lp)
-
-    def decode(t):
-        n = int(active[t])
-        eng.step(slots_sorted[:n], uids_sorted[:n], toks[t, :n], toks[t + 1, :n], logps[t + 1, :n],
-                 seed=seed, temperature=T)
-        return n
+    ro = StaticRollout(eng, plan["prompts"], G, resp, plan["uids"], seed=seed, temperature=T)
+    max_steps = ro.max_steps
+    steps = max_steps if args.steps <= 0 else min(args.steps, max_steps)
+    prefill = ro.prefill
+    decode = ro.step
 
     # ---- warm-up rollout (untimed) ----
     prefill()
