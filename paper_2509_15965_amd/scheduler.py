@@ -21,7 +21,8 @@ Readings (the paper leaves these open):
   - a pipeline's micro-batch times are the subgraphs' own estimates at batch
     m on their devices, t_s and t_t; T_critical = t_s + t_t (one micro-batch
     through both stages) and T_bottleneck = max(t_s, t_t);
-  - m ranges over the powers of two dividing the batch M, and M itself;
+  - m ranges over the powers of two dividing the batch M that are at least
+    a given minimum (1 by default), and M itself;
   - N_s ranges over 1 .. N-1 for N <= 64 and over the multiples of N/64
     above (keeps the search under seconds at 1024 devices);
   - a collapsed cycle's estimate is the sum of its members' estimates;
@@ -153,11 +154,11 @@ class Schedule:
         return f"({a} | {b} m={self.micro_batch})"
 
 
-def micro_batches(M: int) -> List[int]:
+def micro_batches(M: int, min_micro: int = 1) -> List[int]:
     out = []
     m = 1
     while m < M:
-        if M % m == 0:
+        if M % m == 0 and m >= min_micro:
             out.append(m)
         m *= 2
     out.append(M)
@@ -180,9 +181,10 @@ class Scheduler:
     """FindSchedule over a workflow; switch_bw = host link bytes/s per
     device for the temporal mode's offload + reload."""
 
-    def __init__(self, wf: Workflow, switch_bw: float = INF):
+    def __init__(self, wf: Workflow, switch_bw: float = INF, min_micro: int = 1):
         self.wf = collapse_cycles(wf)
         self.switch_bw = switch_bw
+        self.min_micro = min_micro
         self.memo: Dict[Tuple[FrozenSet[str], int, int], Tuple[float, Optional[Schedule]]] = {}
 
     def switch_cost(self, S: FrozenSet[str], T: FrozenSet[str]) -> float:
@@ -215,7 +217,7 @@ class Scheduler:
                 best, sched = t, Schedule("temporal", N, M, parts=(ss, st))
             for Ns in device_splits(N):
                 Nt = N - Ns
-                for m in micro_batches(M):
+                for m in micro_batches(M, self.min_micro):
                     a, sa = self.find(S, Ns, m)
                     if a == INF:
                         continue
@@ -232,10 +234,10 @@ class Scheduler:
         return self.find(frozenset(self.wf.components), N, M)
 
 
-def brute_force(wf: Workflow, N: int, M: int, switch_bw: float = INF) -> float:
+def brute_force(wf: Workflow, N: int, M: int, switch_bw: float = INF, min_micro: int = 1) -> float:
     """Best time by exhaustive enumeration of the same schedule space, with no
     memo and no pruning (small graphs and device counts only)."""
-    sch = Scheduler(wf, switch_bw)
+    sch = Scheduler(wf, switch_bw, min_micro)
     g = sch.wf
 
     def all_times(nodes, n, b):
@@ -248,7 +250,7 @@ def brute_force(wf: Workflow, N: int, M: int, switch_bw: float = INF) -> float:
                 for tt in all_times(T, n, b):
                     yield ts + tt + sch.switch_cost(S, T)
             for Ns in device_splits(n):
-                for m in micro_batches(b):
+                for m in micro_batches(b, min_micro):
                     for a in all_times(S, Ns, m):
                         for c in all_times(T, n - Ns, m):
                             if a < INF and c < INF:

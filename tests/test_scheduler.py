@@ -43,6 +43,7 @@ def test_pipelining_time_formula():
     assert pipelining_time(2.0, 3.0, 8, 2) == pytest.approx(14.0)
     assert micro_batches(12) == [1, 2, 4, 12]
     assert micro_batches(8) == [1, 2, 4, 8]
+    assert micro_batches(512, 16) == [16, 32, 64, 128, 256, 512]
 
 
 def test_single_node_is_its_estimate():
@@ -115,3 +116,43 @@ def test_search_time_stays_small_at_many_devices():
     t, s = Scheduler(wf, switch_bw=50e9).schedule(256, 512)
     assert time.perf_counter() - t0 < 60.0
     assert math.isfinite(t) and s is not None
+
+
+def test_profiler_fit_recovers_the_model_form():
+    import numpy as np
+
+    from paper_2509_15965_amd.profiler import fit_inverse_poly
+    ns = [1, 2, 4]
+    ts = [3.0 + 8.0 / n + 0.5 / n ** 2 for n in ns]
+    coef, f = fit_inverse_poly(ns, ts, deg=2)
+    assert np.allclose(coef, [3.0, 8.0, 0.5])
+    assert f(8) == pytest.approx(3.0 + 1.0 + 0.5 / 64)
+    coef2, f2 = fit_inverse_poly([1, 2, 4, 8], [1.0 + 2.0 / n for n in (1, 2, 4, 8)])
+    assert np.allclose(coef2, [1.0, 2.0], atol=1e-12)
+    assert f2(16) == pytest.approx(1.125)
+    # no negative parts: data below the proportional line clamps the fixed part at 0
+    coef3, _ = fit_inverse_poly([1, 2, 4], [10.0, 4.9, 2.4])
+    assert coef3[0] == 0.0 and coef3[1] > 0
+
+
+def test_profiler_schedules_use_the_policy():
+    from paper_2509_15965_amd.profiler import schedules
+    E = {"rollout": lambda n: 40.0 / n + 2.0, "inference": lambda n: 10.0 / n + 0.5,
+         "training": lambda n: 30.0 / n + 1.5}
+    out = schedules(E, 512, {"rollout": 15e9, "inference": 15e9, "training": 120e9}, 56.5e9, [1, 4, 16])
+    assert [o["devices"] for o in out] == [1, 4, 16]
+    assert out[0]["schedule"] == "((rollout@1 ; inference@1) ; training@1)"
+    for o in out:
+        assert o["estimate_s"] > 0 and o["search_s"] >= 0
+
+
+def test_search_with_a_minimum_micro_batch_equals_enumeration():
+    wf = Workflow({
+        "rollout": Component("rollout", lambda n, b: 0.3 + 2.0 * b / n ** 0.9, state_bytes=3e9),
+        "inference": Component("inference", lambda n, b: 0.01 + 0.5 * b / n, state_bytes=1e9),
+        "training": Component("training", lambda n, b: 0.02 + 1.5 * b / n, state_bytes=5e9),
+    }, [("rollout", "inference"), ("inference", "training")])
+    for N in (3, 5):
+        t, s = Scheduler(wf, switch_bw=2e9, min_micro=4).schedule(N, 16)
+        assert t == pytest.approx(brute_force(wf, N, 16, switch_bw=2e9, min_micro=4), rel=1e-12)
+        assert all(p.micro_batch == 0 or p.micro_batch >= 4 for p in (s,) + s.parts)
