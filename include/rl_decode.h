@@ -347,14 +347,21 @@ typedef enum rl_option {
                                 planner's choice.  Results stay within the
                                 parity tolerances for every choice; the bits
                                 differ (fp32 summation order).               */
-    RL_OPT_SHARED_PREFIX = 4 /* 1 (default): decode attention of the slots of
+    RL_OPT_SHARED_PREFIX = 4, /* 1 (default): decode attention of the slots of
                                 one rl_prefill group reads the prompt's K/V
                                 from the group's first slot (every slot of
                                 the group holds the same copy), in 32-position
                                 steps, and keeps the readers of one prompt
                                 chunk on one XCD, so each prompt chunk is read
                                 from HBM about once per group; 0: every slot
-                                reads its own copy.  Results are identical. */
+                                reads its own copy.  The same function; the
+                                bits differ (fp32 summation order).        */
+    RL_OPT_PREFILL_ATTENTION = 5 /* attention of rl_prefill and rl_score: 0
+                                (default) workgroups of consecutive query
+                                tokens sharing each K/V step through LDS; 1:
+                                the decode kernel's split-KV work items
+                                (RL_OPT_ATTN_CHUNK applies).  Results agree
+                                within the parity tolerances.             */
 } rl_option;
 
 typedef enum rl_gemm_kernel {

@@ -123,6 +123,7 @@ struct rl_decode_ctx {
     int stage_next = 0;
     int64_t opt_chunk = 0;
     bool opt_shared = true;           // RL_OPT_SHARED_PREFIX
+    bool opt_prefill_items = false;   // RL_OPT_PREFILL_ATTENTION = 1: split-KV work items
     int64_t opt_gemm = 0;             // RL_OPT_GEMM_PLAN
     uint32_t profile = 0;             // bit mask over kernel classes
     struct Pending { int kc; hipEvent_t a, b; };
@@ -252,6 +253,8 @@ struct Fwd {
     const AttnItem* items = nullptr;
     int n_items = 0;
     int n_partial_items = 0;
+    const PrefillTile* tiles = nullptr;     // prefill / scoring: shared-LDS tiles instead of items
+    int n_tiles = 0;
     const int32_t* split_blocks = nullptr;   // first item of every split block
     int n_split_blocks = 0;
     double attn_kv_positions = 0;           // algorithmic KV positions read per kv-head
@@ -440,7 +443,10 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         }
         {
             Prof pr(c, RL_K_ATTENTION);
-            if (c->bf16())
+            if (c->bf16() && f.tiles)
+                e = launch_attention_prefill(f.tiles, f.n_tiles, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv, D,
+                                             L.cap, l, attn, c->stream);
+            else if (c->bf16())
                 e = launch_attention_bf16(f.items, f.n_items, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv,
                                           D, L.cap, l, attn, apart, c->stream);
             else
@@ -743,6 +749,44 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
     return RL_OK;
 }
 
+// Prefill / scoring tiles: each block run of consecutive query tokens of one
+// sequence (blocks of one slot with consecutive rows and positions) split
+// into tiles of kPrefillWaves * (16 / G) tokens, longest key range first.
+rl_status build_tiles(rl_decode_ctx* c, Meta* m, const std::vector<Block>& blocks, Fwd* f) {
+    const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    const int T = kPrefillWaves * std::max(1, 16 / G);
+    std::vector<PrefillTile> tl;
+    size_t i = 0;
+    while (i < blocks.size()) {
+        // a run: consecutive blocks continuing the same sequence segment
+        size_t j = i + 1;
+        while (j < blocks.size() && blocks[j].slot == blocks[i].slot &&
+               blocks[j].qrow == blocks[j - 1].qrow + blocks[j - 1].nq &&
+               blocks[j].pos0 == blocks[j - 1].pos0 + blocks[j - 1].nq)
+            ++j;
+        const int qrow0 = blocks[i].qrow, pos0 = blocks[i].pos0, slot = blocks[i].slot;
+        const int n = blocks[j - 1].qrow + blocks[j - 1].nq - qrow0;
+        for (int t = 0; t < n; t += T) tl.push_back(PrefillTile{qrow0 + t, std::min(T, n - t), slot, pos0 + t});
+        i = j;
+    }
+    std::stable_sort(tl.begin(), tl.end(), [](const PrefillTile& a, const PrefillTile& b) {
+        return a.pos0 + a.ntok > b.pos0 + b.ntok;
+    });
+    PrefillTile* d = nullptr;
+    PrefillTile* h = m->take<PrefillTile>(std::max<size_t>(tl.size(), 1), &d);
+    if (!h) return fail(c, RL_ERR_CAPACITY, "per-call metadata exceeds its workspace region");
+    std::copy(tl.begin(), tl.end(), h);
+    double scorepos = 0;
+    for (const Block& b : blocks)
+        for (int t = 0; t < b.nq; ++t) scorepos += b.pos0 + t + 1;
+    f->tiles = d;
+    f->n_tiles = static_cast<int>(tl.size());
+    f->n_items = 0;
+    f->n_split_blocks = 0;
+    f->attn_score_positions = scorepos;
+    return RL_OK;
+}
+
 // Drop prompt sharing of the given slots, and of every slot that reads its
 // prompt from one of them (their own copies stay valid).
 void unshare(rl_decode_ctx* c, int n, const int32_t* slots) {
@@ -1003,9 +1047,12 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     f.dst_slots = d_dst;
     f.row_slot = d_row_slot;
     f.attn_kv_positions = kvpos;
-    if (c->bf16()) {
+    if (c->bf16() && c->opt_prefill_items) {
         const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, kPrefillChunk, c->lay.items_cap, false);
         st = build_items(c, &m, blocks, C, &f);
+        if (st != RL_OK) return st;
+    } else if (c->bf16()) {
+        st = build_tiles(c, &m, blocks, &f);
         if (st != RL_OK) return st;
     } else {
         double sp_ = 0;
@@ -1159,9 +1206,12 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     f.dst_slots = d_dst;
     f.row_slot = d_row_slot;
     f.attn_kv_positions = kvpos;
-    if (c->bf16()) {
+    if (c->bf16() && c->opt_prefill_items) {
         const int C = choose_chunk(blocks, cf.n_kv_heads, c->opt_chunk, kPrefillChunk, c->lay.items_cap, false);
         st = build_items(c, &m, blocks, C, &f);
+        if (st != RL_OK) return st;
+    } else if (c->bf16()) {
+        st = build_tiles(c, &m, blocks, &f);
         if (st != RL_OK) return st;
     } else {
         f.attn_score_positions = scorepos;
@@ -1494,6 +1544,10 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
             ctx->opt_gemm = value;
             return RL_OK;
         }
+        case RL_OPT_PREFILL_ATTENTION:
+            if (value != 0 && value != 1) return fail(ctx, RL_ERR_INVALID_ARG, "prefill attention option must be 0 or 1");
+            ctx->opt_prefill_items = value == 1;
+            return RL_OK;
         case RL_OPT_SHARED_PREFIX:
             if (value != 0 && value != 1) return fail(ctx, RL_ERR_INVALID_ARG, "shared prefix option must be 0 or 1");
             ctx->opt_shared = value == 1;

@@ -218,6 +218,188 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
 }
 
 
+// ---------------------------------------------------------------------------
+// Prefill / scoring attention: a 4-wave workgroup shares each K/V step
+// through LDS.  Per 32-position step the workgroup DMAs the step's K rows
+// ([32][D], 16-byte chunks permuted by row so that the fragment reads below
+// are free of bank conflicts) and its four V blocks ([4][D][8], contiguous in
+// the cache) into one of two LDS buffers with global_load_lds; every wave
+// then runs the decode kernel's MFMA step on its own 16 query columns from
+// LDS.  The next step's DMA is issued right after the barrier that retires
+// the previous step, so it overlaps the current step's math.
+// ---------------------------------------------------------------------------
+
+// 16-byte chunk permutation of K row r in LDS (logical chunk c sits at c ^ kswz(r)).
+template <int D>
+__device__ __forceinline__ int kswz(int r) {
+    return D == 128 ? ((r & 3) | ((r >> 1) & 12)) : (((r >> 1) & 1) | ((r >> 2) & 6));
+}
+
+__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds_wave_base), 16, 0, 0);
+}
+
+template <int D>
+__global__ void __launch_bounds__(256, 2) attn_prefill_kernel(const PrefillTile* __restrict__ tiles,
+        const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int S,
+        int Hq, int Hkv, int cap, int layer, float scale_log2, uint16_t* __restrict__ out) {
+    constexpr int KG = D / 32, DT = D / 16;
+    constexpr int STEPB = 32 * D * 2;               // bytes of K (and of V) per 32-position step
+    constexpr int NDMA = STEPB / 1024 / kPrefillWaves;   // 1 KB DMA instructions per wave per step, K and V each
+    static_assert(NDMA >= 1 && NDMA * kPrefillWaves * 1024 == STEPB, "step split over the waves");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[2][2][STEPB];   // [buffer][K | V]
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int kvh = blockIdx.y;
+    const int G = Hq / Hkv;
+    const int tq = 16 / G;
+    const PrefillTile tl = tiles[blockIdx.x];
+    const int tok0 = wave * tq;
+    const int nq = max(0, min(tq, tl.ntok - tok0));
+    const int col = lane & 15, kq = lane >> 4;
+    const bool cvalid = col < nq * G;
+    const int tau = cvalid ? col / G : 0;
+    const int head = kvh * G + (cvalid ? col - tau * G : 0);
+    const int qrow = cvalid ? tl.qrow0 + tok0 + tau : tl.qrow0;
+    const int limit = cvalid ? tl.pos0 + tok0 + tau : -1;
+    const int hi = tl.pos0 + tl.ntok;               // keys [0, hi)
+    const int wave_last = tl.pos0 + tok0 + nq - 1;  // last key any column of this wave sees
+    const int nsteps = (hi + 31) / 32;
+
+    const size_t base = ((static_cast<size_t>(layer) * S + tl.slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
+    const uint16_t* kb = kc + base;
+    const uint16_t* vb = vc + base;
+
+    // DMA of step s into buffer s & 1: wave w moves K bytes and V bytes
+    // [w * NDMA KB, (w + 1) * NDMA KB) of the step
+    auto issue = [&](int s) {
+        uint8_t* kl = lds[s & 1][0];
+        uint8_t* vl = lds[s & 1][1];
+        const int t0 = 32 * s;
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) {
+            const int kb_ = wave * NDMA + j;          // which KB of the step
+            constexpr int RPK = 1024 / (D * 2);       // K rows per KB
+            constexpr int CPR = D / 8;                // 16-byte chunks per row
+            const int r = kb_ * RPK + lane / CPR;
+            const int c = (lane % CPR) ^ kswz<D>(r);
+            lds_dma16(kb + static_cast<size_t>(t0 + r) * D + 8 * c, kl + kb_ * 1024);
+            lds_dma16(reinterpret_cast<const uint8_t*>(vb + static_cast<size_t>(t0) * D) + kb_ * 1024 + lane * 16,
+                      vl + kb_ * 1024);
+        }
+    };
+
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 qf[KG];
+    {
+        const uint16_t* qp = q + (static_cast<size_t>(qrow) * Hq + head) * D + 8 * kq;
+#pragma unroll
+        for (int j = 0; j < KG; ++j) qf[j] = cvalid ? ld16(qp + 32 * j) : zero;
+    }
+    float m = -INFINITY, l = 0.0f;
+    f32x4 o[DT];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int krow = 8 * (col >> 2) + (col & 3);
+
+    if (nsteps > 0) issue(0);
+    for (int s = 0; s < nsteps; ++s) {
+        // vmcnt(0) (expcnt, lgkmcnt untouched): this wave's DMAs and q loads landed
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+        __syncthreads();                               // every wave's part of step s is in LDS; step s-1 retired
+        if (s + 1 < nsteps) issue(s + 1);
+        const int t0 = 32 * s;
+        if (nq == 0 || t0 > wave_last) continue;       // wave-uniform: nothing of this step is visible
+        const uint8_t* kl = lds[s & 1][0];
+        const uint8_t* vl = lds[s & 1][1];
+        u32x4 k0[KG], k1[KG], vf[DT];
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+            const int c = kq + 4 * j;
+            k0[j] = *reinterpret_cast<const u32x4*>(kl + krow * (2 * D) + 16 * (c ^ kswz<D>(krow)));
+            k1[j] = *reinterpret_cast<const u32x4*>(kl + (krow + 4) * (2 * D) + 16 * (c ^ kswz<D>(krow + 4)));
+        }
+#pragma unroll
+        for (int i = 0; i < DT; ++i) vf[i] = *reinterpret_cast<const u32x4*>(vl + (kq * D + col + 16 * i) * 16);
+        const int pb = t0 + 8 * kq;
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+            s0 = mfma16x16x32(as_bf16x8(k0[j]), as_bf16x8(qf[j]), s0);
+            s1 = mfma16x16x32(as_bf16x8(k1[j]), as_bf16x8(qf[j]), s1);
+        }
+        const int lim = min(hi - 1, limit);
+        float sv[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sv[e] = (pb + e <= lim) ? s0[e] * scale_log2 : -INFINITY;
+            sv[4 + e] = (pb + 4 + e <= lim) ? s1[e] * scale_log2 : -INFINITY;
+        }
+        float mx = sv[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m, mx);
+        const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+        const float alpha = exp2f(m - m_use);
+        float psum = 0.0f;
+        uint32_t ph[4], pl[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float p0 = exp2f(sv[2 * w] - m_use);
+            const float p1 = exp2f(sv[2 * w + 1] - m_use);
+            psum += p0 + p1;
+            const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+            const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
+            ph[w] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+            pl[w] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+        }
+        l = l * alpha + psum;
+        m = m_new;
+        const u32x4 pfh = {ph[0], ph[1], ph[2], ph[3]};
+        const u32x4 pfl = {pl[0], pl[1], pl[2], pl[3]};
+        const int nvalid = hi - pb;   // keys past the last query carry no data
+#pragma unroll
+        for (int i = 0; i < DT; ++i) {
+            u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
+            o[i] = o[i] * alpha;
+            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
+            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
+        }
+    }
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (!cvalid) return;
+    const float inv = 1.0f / l;
+    uint16_t* op = out + (static_cast<size_t>(qrow) * Hq + head) * D + 4 * kq;
+#pragma unroll
+    for (int i = 0; i < DT; ++i) {
+        const uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(o[i][0] * inv)) |
+                            (static_cast<uint32_t>(f32_to_bf16(o[i][1] * inv)) << 16);
+        const uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(o[i][2] * inv)) |
+                            (static_cast<uint32_t>(f32_to_bf16(o[i][3] * inv)) << 16);
+        *reinterpret_cast<uint2*>(op + 16 * i) = make_uint2(w0, w1);
+    }
+}
+
+hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const void* q, const void* kc,
+                                    const void* vc, int max_seqs, int Hq, int Hkv, int D, int cap, int layer,
+                                    void* out, hipStream_t s) {
+    if (n_tiles <= 0) return hipSuccess;
+    const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
+    dim3 grid(n_tiles, Hkv), block(64 * kPrefillWaves);
+    if (D == 128)
+        hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, block, 0, s, tiles, static_cast<const uint16_t*>(q),
+                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
+                           cap, layer, scale_log2, static_cast<uint16_t*>(out));
+    else
+        hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, block, 0, s, tiles, static_cast<const uint16_t*>(q),
+                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
+                           cap, layer, scale_log2, static_cast<uint16_t*>(out));
+    return hipGetLastError();
+}
+
 // Merge the split partials of one query block and q-head: one workgroup per
 // (split block, q-head), one thread per (token, d).  The block's per-item
 // (m, l) go through LDS; the weighted sums issue their loads 8 at a time.

@@ -127,6 +127,24 @@ constexpr int kMaxCombine = 64;
 hipError_t launch_attn_combine(const int32_t* blocks, int n_blocks, const AttnItem* items, const float* part,
                                int Hq, int Hkv, int D, void* out, hipStream_t s);
 
+// Prefill / scoring attention tile: up to kPrefillWaves * (16 / G) consecutive
+// query tokens of one sequence (workspace rows qrow0 .., positions pos0 ..)
+// against every key they see, [0, pos0 + ntok), of one KV slot.
+struct PrefillTile {
+    int32_t qrow0;
+    int32_t ntok;
+    int32_t slot;
+    int32_t pos0;
+};
+constexpr int kPrefillWaves = 4;
+
+// One 4-wave workgroup per (tile, kv-head): each 32-position K/V step is
+// loaded once into LDS and used by every wave (wave w takes the tile's tokens
+// [w * 16/G, (w+1) * 16/G)); outputs are final (no split partials).
+hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const void* q, const void* kc,
+                                    const void* vc, int max_seqs, int Hq, int Hkv, int D, int cap, int layer,
+                                    void* out, hipStream_t s);
+
 // fp32 model dtype: one workgroup per (row, q-head), keys 0..row_pos[r].
 hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
                                 const float* q, const float* kc, const float* vc, int max_seqs,

@@ -17,8 +17,8 @@ import oracle
 from harness import F32_LOGP_ABS_TOL, LOGP_ABS_TOL, build_models
 from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 from paper_2509_15965_amd.inputs import patch_rows, uniform_tokens
-from paper_2509_15965_amd.rl_decode import RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN, RL_GEMM_T128, Engine, \
-    gemm_plan_code
+from paper_2509_15965_amd.rl_decode import RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN, RL_OPT_PREFILL_ATTENTION, \
+    RL_GEMM_T128, Engine, gemm_plan_code
 
 pytestmark = pytest.mark.gpu
 
@@ -49,7 +49,7 @@ def make_case(shape, n_prompts, group, plens, rlens, seed):
 
 
 def run_score(shape, w_dev, prompts, group, resp, T, *, embeds=None, chunk=0, gemm_plan=0, max_seqs=None,
-              slots=None):
+              slots=None, prefill_items=False):
     n_seq = len(prompts) * group
     plens = [len(p) for p in prompts]
     rlens = [len(r) for r in resp]
@@ -60,6 +60,8 @@ def run_score(shape, w_dev, prompts, group, resp, T, *, embeds=None, chunk=0, ge
         eng.set_option(RL_OPT_ATTN_CHUNK, chunk)
     if gemm_plan:
         eng.set_option(RL_OPT_GEMM_PLAN, gemm_plan)
+    if prefill_items:
+        eng.set_option(RL_OPT_PREFILL_ATTENTION, 1)
     slots = slots if slots is not None else list(reversed(range(n_seq)))
     poffs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
     roffs = np.concatenate([[0], np.cumsum(rlens)]).astype(np.int32)
@@ -123,13 +125,25 @@ def test_score_head_groupings_match_oracle(shape):
     _check(got, ref, LOGP_ABS_TOL, shape)
 
 
+@pytest.mark.parametrize("shape", [GQA, G7, MHA], ids=["group4", "group7", "mha"])
+def test_score_both_prefill_attention_kernels(shape):
+    """The LDS-shared tile kernel (default) and the split-KV item kernel
+    both match the oracle, over tiles cut short at sequence ends."""
+    w_dev, _, om = build_models(shape, 47)
+    prompts, resp = make_case(shape, 2, 2, [33, 70], [45, 2, 64, 29], 48)
+    ref = oracle_scores(om, prompts, 2, resp, 1.0)
+    for items in (False, True):
+        got = run_score(shape, w_dev, prompts, 2, resp, 1.0, prefill_items=items)
+        _check(got, ref, LOGP_ABS_TOL, (shape, items))
+
+
 def test_score_split_kv_chunks_and_forced_tile_kernel():
     """32-position split-KV chunks (every long row combines several partial
     sums) and a forced 128x128 tile GEMM give the same scores."""
     w_dev, _, om = build_models(GQA, 37)
     prompts, resp = make_case(GQA, 2, 2, [90, 41], [120, 3, 77, 150], 38)
     ref = oracle_scores(om, prompts, 2, resp, 1.0)
-    got = run_score(GQA, w_dev, prompts, 2, resp, 1.0, chunk=32)
+    got = run_score(GQA, w_dev, prompts, 2, resp, 1.0, chunk=32, prefill_items=True)
     _check(got, ref, LOGP_ABS_TOL, "chunk 32")
     got2 = run_score(GQA, w_dev, prompts, 2, resp, 1.0, gemm_plan=gemm_plan_code(RL_GEMM_T128))
     _check(got2, ref, LOGP_ABS_TOL, "tile 128")
