@@ -740,6 +740,13 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
         }
     }
     for (size_t i = 0; i < split_first.size(); ++i) split[i] = newpos[split_first[i]];
+    if (any_shared) {   // workgroups whose four items read one shared chunk stage it through LDS
+        for (size_t x = 0; x + 3 < order.size(); x += 4) {
+            bool same = order[x] >= 0 && key[order[x]] >= 0;
+            for (int t = 1; t < 4 && same; ++t) same = order[x + t] >= 0 && key[order[x + t]] == key[order[x]];
+            if (same) items[x].pad = 1;
+        }
+    }
     f->items = dItems;
     f->n_items = static_cast<int>(order.size());
     f->n_partial_items = part;

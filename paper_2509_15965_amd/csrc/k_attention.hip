@@ -38,6 +38,119 @@ __device__ __forceinline__ u32x4 mask_tail8(u32x4 v, int nvalid) {
     return v;
 }
 
+// One 32-position step of the online-softmax attention of a wave's 16 query
+// columns: scores of positions t0..t0+31 from the K rows (k0: tile 0, k1:
+// tile 1), positions past min(hi - 1, limit) masked, running max / sum / output
+// updated with the V blocks vf (positions >= hi zeroed).
+template <int D>
+__device__ __forceinline__ void attn_step(const u32x4 (&k0)[D / 32], const u32x4 (&k1)[D / 32],
+                                          const u32x4 (&vf)[D / 16], const u32x4 (&qf)[D / 32], int t0, int hi,
+                                          int limit, int kq, float scale_log2, float& m, float& l,
+                                          f32x4 (&o)[D / 16]) {
+    constexpr int KG = D / 32, DT = D / 16;
+    const int pb = t0 + 8 * kq;
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KG; ++j) {
+        s0 = mfma16x16x32(as_bf16x8(k0[j]), as_bf16x8(qf[j]), s0);
+        s1 = mfma16x16x32(as_bf16x8(k1[j]), as_bf16x8(qf[j]), s1);
+    }
+    // this lane now holds the scores of its column at positions pb + 0..7
+    const int lim = min(hi - 1, limit);
+    float sv[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        sv[e] = (pb + e <= lim) ? s0[e] * scale_log2 : -INFINITY;
+        sv[4 + e] = (pb + 4 + e <= lim) ? s1[e] * scale_log2 : -INFINITY;
+    }
+    float mx = sv[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m, mx);
+    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+    const float alpha = exp2f(m - m_use);
+    // probabilities as a bf16 pair hi + lo (hi = rne(p), lo = rne(p - hi)):
+    // the P.V product then carries ~16 significant bits of p, so the only
+    // storage rounding left is the one of the attention output
+    float psum = 0.0f;
+    uint32_t ph[4], pl[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const float p0 = exp2f(sv[2 * w] - m_use);
+        const float p1 = exp2f(sv[2 * w + 1] - m_use);
+        psum += p0 + p1;
+        const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+        const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
+        ph[w] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+        pl[w] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+    }
+    l = l * alpha + psum;
+    m = m_new;
+    const u32x4 pfh = {ph[0], ph[1], ph[2], ph[3]};
+    const u32x4 pfl = {pl[0], pl[1], pl[2], pl[3]};
+    const int nvalid = hi - pb;   // keys past the chunk end carry no data
+#pragma unroll
+    for (int i = 0; i < DT; ++i) {
+        u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
+        o[i] = o[i] * alpha;
+        o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
+        o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
+    }
+}
+
+// 16-byte chunk permutation of K row r (of a 32-position step) in LDS:
+// logical chunk c sits at c ^ kswz(r), which makes the fragment reads of one
+// 16-lane group hit 16 different 16-byte bank groups.
+template <int D>
+__device__ __forceinline__ int kswz(int r) {
+    return D == 128 ? ((r & 3) | ((r >> 1) & 12)) : (((r >> 1) & 1) | ((r >> 2) & 6));
+}
+
+__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds_wave_base), 16, 0, 0);
+}
+
+// The K rows and V blocks of positions t0..t0+31 of one (slot, kv-head) into
+// an LDS step buffer (K [32][D] chunk-permuted, V [4][D][8]), spread over the
+// kWaves waves of the workgroup: wave w moves KB [w * NDMA, (w+1) * NDMA) of
+// each.  One global_load_lds per KB per lane.
+template <int D, int kWaves>
+__device__ __forceinline__ void step_dma(const uint16_t* kb, const uint16_t* vb, int t0, int wave, int lane,
+                                         uint8_t* kl, uint8_t* vl) {
+    constexpr int STEPB = 32 * D * 2;
+    constexpr int NDMA = STEPB / 1024 / kWaves;
+    constexpr int RPK = 1024 / (D * 2);   // K rows per KB
+    constexpr int CPR = D / 8;            // 16-byte chunks per row
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) {
+        const int kb_ = wave * NDMA + j;
+        const int r = kb_ * RPK + lane / CPR;
+        const int c = (lane % CPR) ^ kswz<D>(r);
+        lds_dma16(kb + static_cast<size_t>(t0 + r) * D + 8 * c, kl + kb_ * 1024);
+        lds_dma16(reinterpret_cast<const uint8_t*>(vb + static_cast<size_t>(t0) * D) + kb_ * 1024 + lane * 16,
+                  vl + kb_ * 1024);
+    }
+}
+
+// A wave's K / V fragments of one step from an LDS step buffer.
+template <int D>
+__device__ __forceinline__ void step_frags(const uint8_t* kl, const uint8_t* vl, int krow, int kq, int col,
+                                           u32x4 (&k0)[D / 32], u32x4 (&k1)[D / 32], u32x4 (&vf)[D / 16]) {
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) {
+        const int c = kq + 4 * j;
+        k0[j] = *reinterpret_cast<const u32x4*>(kl + krow * (2 * D) + 16 * (c ^ kswz<D>(krow)));
+        k1[j] = *reinterpret_cast<const u32x4*>(kl + (krow + 4) * (2 * D) + 16 * (c ^ kswz<D>(krow + 4)));
+    }
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) vf[i] = *reinterpret_cast<const u32x4*>(vl + (kq * D + col + 16 * i) * 16);
+}
+
+// vmcnt(0) with expcnt and lgkmcnt left alone (gfx9 encoding)
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
 template <int D, bool PF>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __restrict__ items,
         int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
@@ -45,8 +158,14 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
         float scale_log2, uint16_t* __restrict__ out, float* __restrict__ part) {
     constexpr int KG = D / 32;   // 32-wide k groups of a head
     constexpr int DT = D / 16;   // 16-wide d tiles of the output
-    const int lane = threadIdx.x & 63;
-    const int item_id = blockIdx.x * 4 + (threadIdx.x >> 6);
+    constexpr int STEPB = 32 * D * 2;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[2][2][STEPB];   // [buffer][K | V], shared-chunk units
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int item_id = blockIdx.x * 4 + wave;
+    // a unit of four items over one shared prompt chunk (same slot and key
+    // range; the host sets pad = 1 on its first item): every K/V step goes
+    // through LDS once for the four waves
+    const bool wg_lds = blockIdx.x * 4 + 3 < n_items && items[blockIdx.x * 4].pad == 1;
     if (item_id >= n_items) return;
     const int kvh = blockIdx.y;
     const int G = Hq / Hkv;
@@ -96,62 +215,26 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
 #pragma unroll
         for (int i = 0; i < DT; ++i) vv[i] = ld16(vp + 16 * 8 * i);
     };
-    if (it.kv_lo < hi) load_step(it.kv_lo, k0, k1, vf);
-    for (int t0 = it.kv_lo; t0 < hi; t0 += 32) {
+    if (wg_lds) {
+        const int nsteps = (hi - it.kv_lo + 31) / 32;
+        if (nsteps > 0) step_dma<D, 4>(kb, vb, it.kv_lo, wave, lane, lds[0][0], lds[0][1]);
+        for (int s = 0; s < nsteps; ++s) {
+            wait_vm0();        // this wave's DMAs (and q loads) landed
+            __syncthreads();   // every wave's part of step s is in LDS; step s-1 retired
+            if (s + 1 < nsteps)
+                step_dma<D, 4>(kb, vb, it.kv_lo + 32 * (s + 1), wave, lane, lds[(s + 1) & 1][0], lds[(s + 1) & 1][1]);
+            step_frags<D>(lds[s & 1][0], lds[s & 1][1], krow, kq, col, k0, k1, vf);
+            attn_step<D>(k0, k1, vf, qf, it.kv_lo + 32 * s, hi, limit, kq, scale_log2, m, l, o);
+        }
+    } else if (it.kv_lo < hi) {
+        load_step(it.kv_lo, k0, k1, vf);
+    }
+    for (int t0 = it.kv_lo; !wg_lds && t0 < hi; t0 += 32) {
         u32x4 nk0[KG], nk1[KG], nvf[DT];
         const bool more = PF && t0 + 32 < hi;
         if (more) load_step(t0 + 32, nk0, nk1, nvf);
         if (!PF && t0 != it.kv_lo) load_step(t0, k0, k1, vf);
-        const int pb = t0 + 8 * kq;
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < KG; ++j) {
-            s0 = mfma16x16x32(as_bf16x8(k0[j]), as_bf16x8(qf[j]), s0);
-            s1 = mfma16x16x32(as_bf16x8(k1[j]), as_bf16x8(qf[j]), s1);
-        }
-        // this lane now holds the scores of column col at positions pb + 0..7
-        const int lim = min(hi - 1, limit);
-        float sv[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            sv[e] = (pb + e <= lim) ? s0[e] * scale_log2 : -INFINITY;
-            sv[4 + e] = (pb + 4 + e <= lim) ? s1[e] * scale_log2 : -INFINITY;
-        }
-        float mx = sv[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m, mx);
-        const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-        const float alpha = exp2f(m - m_use);
-        // probabilities as a bf16 pair hi + lo (hi = rne(p), lo = rne(p - hi)):
-        // the P.V product then carries ~16 significant bits of p, so the
-        // only storage rounding left is the one of the attention output
-        float psum = 0.0f;
-        uint32_t ph[4], pl[4];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const float p0 = exp2f(sv[2 * w] - m_use);
-            const float p1 = exp2f(sv[2 * w + 1] - m_use);
-            psum += p0 + p1;
-            const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
-            const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
-            ph[w] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-            pl[w] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
-        }
-        l = l * alpha + psum;
-        m = m_new;
-        const u32x4 pfh = {ph[0], ph[1], ph[2], ph[3]};
-        const u32x4 pfl = {pl[0], pl[1], pl[2], pl[3]};
-        const int nvalid = hi - pb;   // keys past the chunk end carry no data
-#pragma unroll
-        for (int i = 0; i < DT; ++i) {
-            u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
-            o[i] = o[i] * alpha;
-            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
-            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
-        }
+        attn_step<D>(k0, k1, vf, qf, t0, hi, limit, kq, scale_log2, m, l, o);
         if (more) {
 #pragma unroll
             for (int j = 0; j < KG; ++j) { k0[j] = nk0[j]; k1[j] = nk1[j]; }
@@ -229,16 +312,6 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
 // the previous step, so it overlaps the current step's math.
 // ---------------------------------------------------------------------------
 
-// 16-byte chunk permutation of K row r in LDS (logical chunk c sits at c ^ kswz(r)).
-template <int D>
-__device__ __forceinline__ int kswz(int r) {
-    return D == 128 ? ((r & 3) | ((r >> 1) & 12)) : (((r >> 1) & 1) | ((r >> 2) & 6));
-}
-
-__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds_wave_base) {
-    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds_wave_base), 16, 0, 0);
-}
-
 template <int D>
 __global__ void __launch_bounds__(256, 2) attn_prefill_kernel(const PrefillTile* __restrict__ tiles,
         const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int S,
@@ -270,25 +343,6 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_kernel(const PrefillTile*
     const uint16_t* kb = kc + base;
     const uint16_t* vb = vc + base;
 
-    // DMA of step s into buffer s & 1: wave w moves K bytes and V bytes
-    // [w * NDMA KB, (w + 1) * NDMA KB) of the step
-    auto issue = [&](int s) {
-        uint8_t* kl = lds[s & 1][0];
-        uint8_t* vl = lds[s & 1][1];
-        const int t0 = 32 * s;
-#pragma unroll
-        for (int j = 0; j < NDMA; ++j) {
-            const int kb_ = wave * NDMA + j;          // which KB of the step
-            constexpr int RPK = 1024 / (D * 2);       // K rows per KB
-            constexpr int CPR = D / 8;                // 16-byte chunks per row
-            const int r = kb_ * RPK + lane / CPR;
-            const int c = (lane % CPR) ^ kswz<D>(r);
-            lds_dma16(kb + static_cast<size_t>(t0 + r) * D + 8 * c, kl + kb_ * 1024);
-            lds_dma16(reinterpret_cast<const uint8_t*>(vb + static_cast<size_t>(t0) * D) + kb_ * 1024 + lane * 16,
-                      vl + kb_ * 1024);
-        }
-    };
-
     const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 qf[KG];
     {
@@ -302,71 +356,17 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_kernel(const PrefillTile*
     for (int i = 0; i < DT; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int krow = 8 * (col >> 2) + (col & 3);
 
-    if (nsteps > 0) issue(0);
+    if (nsteps > 0) step_dma<D, kPrefillWaves>(kb, vb, 0, wave, lane, lds[0][0], lds[0][1]);
     for (int s = 0; s < nsteps; ++s) {
-        // vmcnt(0) (expcnt, lgkmcnt untouched): this wave's DMAs and q loads landed
-        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
-        __syncthreads();                               // every wave's part of step s is in LDS; step s-1 retired
-        if (s + 1 < nsteps) issue(s + 1);
+        wait_vm0();        // this wave's DMAs (and q loads) landed
+        __syncthreads();   // every wave's part of step s is in LDS; step s-1 retired
+        if (s + 1 < nsteps)
+            step_dma<D, kPrefillWaves>(kb, vb, 32 * (s + 1), wave, lane, lds[(s + 1) & 1][0], lds[(s + 1) & 1][1]);
         const int t0 = 32 * s;
         if (nq == 0 || t0 > wave_last) continue;       // wave-uniform: nothing of this step is visible
-        const uint8_t* kl = lds[s & 1][0];
-        const uint8_t* vl = lds[s & 1][1];
         u32x4 k0[KG], k1[KG], vf[DT];
-#pragma unroll
-        for (int j = 0; j < KG; ++j) {
-            const int c = kq + 4 * j;
-            k0[j] = *reinterpret_cast<const u32x4*>(kl + krow * (2 * D) + 16 * (c ^ kswz<D>(krow)));
-            k1[j] = *reinterpret_cast<const u32x4*>(kl + (krow + 4) * (2 * D) + 16 * (c ^ kswz<D>(krow + 4)));
-        }
-#pragma unroll
-        for (int i = 0; i < DT; ++i) vf[i] = *reinterpret_cast<const u32x4*>(vl + (kq * D + col + 16 * i) * 16);
-        const int pb = t0 + 8 * kq;
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < KG; ++j) {
-            s0 = mfma16x16x32(as_bf16x8(k0[j]), as_bf16x8(qf[j]), s0);
-            s1 = mfma16x16x32(as_bf16x8(k1[j]), as_bf16x8(qf[j]), s1);
-        }
-        const int lim = min(hi - 1, limit);
-        float sv[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            sv[e] = (pb + e <= lim) ? s0[e] * scale_log2 : -INFINITY;
-            sv[4 + e] = (pb + 4 + e <= lim) ? s1[e] * scale_log2 : -INFINITY;
-        }
-        float mx = sv[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m, mx);
-        const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-        const float alpha = exp2f(m - m_use);
-        float psum = 0.0f;
-        uint32_t ph[4], pl[4];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const float p0 = exp2f(sv[2 * w] - m_use);
-            const float p1 = exp2f(sv[2 * w + 1] - m_use);
-            psum += p0 + p1;
-            const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
-            const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
-            ph[w] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-            pl[w] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
-        }
-        l = l * alpha + psum;
-        m = m_new;
-        const u32x4 pfh = {ph[0], ph[1], ph[2], ph[3]};
-        const u32x4 pfl = {pl[0], pl[1], pl[2], pl[3]};
-        const int nvalid = hi - pb;   // keys past the last query carry no data
-#pragma unroll
-        for (int i = 0; i < DT; ++i) {
-            u32x4 v = nvalid < 8 ? mask_tail8(vf[i], nvalid < 0 ? 0 : nvalid) : vf[i];
-            o[i] = o[i] * alpha;
-            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfh), o[i]);
-            o[i] = mfma16x16x32(as_bf16x8(v), as_bf16x8(pfl), o[i]);
-        }
+        step_frags<D>(lds[s & 1][0], lds[s & 1][1], krow, kq, col, k0, k1, vf);
+        attn_step<D>(k0, k1, vf, qf, t0, hi, limit, kq, scale_log2, m, l, o);
     }
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);

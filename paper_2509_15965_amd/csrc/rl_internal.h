@@ -37,7 +37,9 @@ struct AttnItem {
                     // workspace row qrow_b, partial index part_b (nq = 2,
                     // no key of the chunk is masked for either); -1: none
     int32_t part_b;
-    int32_t pad;
+    int32_t pad;    // 1 on the first item of a workgroup whose four items read
+                    // the same shared prompt chunk (same slot and key range):
+                    // the workgroup stages each K/V step through LDS once
 };
 
 struct GemmArgs {
