@@ -15,6 +15,8 @@
 #include "rl_device.h"
 #include "rl_internal.h"
 
+#include <algorithm>
+
 namespace rl {
 
 namespace {
@@ -193,6 +195,13 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ void dma16(const uint16_t* g, uint8_t* lds_wave_base) {
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(g), (lds_void_t*)(lds_wave_base), 16, 0, 0);
+}
+
+// Same, from a wave-uniform base plus a 32-bit per-lane byte offset: the
+// address then stays in the scalar-base form of the instruction (no 64-bit
+// per-lane address arithmetic per issue).
+__device__ __forceinline__ void dma16_off(const uint8_t* base, uint32_t off, uint8_t* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(base + off), (lds_void_t*)(lds_wave_base), 16, 0, 0);
 }
 
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding)
@@ -447,7 +456,8 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     const int n_tile = (rem / gm) * 8 + xcd;
     if (m_tile >= m_tiles || n_tile >= n_tiles) return;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
     const int r32 = lane & 31, kh = lane >> 5;
     const int M = p.M, Nw = p.Nw, K = p.K;
@@ -475,14 +485,14 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     const uint16_t* W = static_cast<const uint16_t*>(p.W);
     // DMA lane l of block g: row 8g + l/8, LDS chunk l%8 <- source chunk (l%8) ^ ((row/2)%8)
     const int lrow = lane >> 3;
-    uint32_t aoff[AQ], boff[BQ];
+    uint32_t aoff[AQ], boff[BQ];   // byte offsets (the launcher keeps them below 4 GiB)
 #pragma unroll
     for (int q = 0; q < AQ; ++q) {
         const int g = wave * AQ + q;
         int m = m0 + 8 * g + lrow;
         m = m < M ? m : M - 1;
         const int ch = (lane & 7) ^ (((8 * g + lrow) >> 1) & 7);
-        aoff[q] = static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda) + 8u * ch;
+        aoff[q] = 2u * (static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda) + 8u * ch);
     }
 #pragma unroll
     for (int q = 0; q < BQ; ++q) {
@@ -491,21 +501,21 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         int n = wrow(8 * g + lrow, &ok);
         n = ok ? n : 0;
         const int ch = (lane & 7) ^ (((8 * g + lrow) >> 1) & 7);
-        boff[q] = static_cast<uint32_t>(n) * static_cast<uint32_t>(p.ldw) + 8u * ch;
+        boff[q] = 2u * (static_cast<uint32_t>(n) * static_cast<uint32_t>(p.ldw) + 8u * ch);
     }
     uint8_t* const abuf = smem;
     uint8_t* const bbuf = smem + SA * ASTAGE;
     auto issue_a = [&](int stage) {
         uint8_t* base = abuf + (stage % SA) * ASTAGE;
-        const int k0 = kb + stage * BK;
+        const uint8_t* src = reinterpret_cast<const uint8_t*>(A + kb + stage * BK);
 #pragma unroll
-        for (int q = 0; q < AQ; ++q) dma16(A + aoff[q] + k0, base + (wave * AQ + q) * 1024);
+        for (int q = 0; q < AQ; ++q) dma16_off(src, aoff[q], base + (wave * AQ + q) * 1024);
     };
     auto issue_w = [&](int stage) {
         uint8_t* base = bbuf + (stage % SW) * BSTAGE;
-        const int k0 = kb + stage * BK;
+        const uint8_t* src = reinterpret_cast<const uint8_t*>(W + kb + stage * BK);
 #pragma unroll
-        for (int q = 0; q < BQ; ++q) dma16(W + boff[q] + k0, base + (wave * BQ + q) * 1024);
+        for (int q = 0; q < BQ; ++q) dma16_off(src, boff[q], base + (wave * BQ + q) * 1024);
     };
     // Issue schedule: in (real or prologue) iteration i, A(i + SA) if in range,
     // then W(i + SW) if in range; the prologue is iterations -SW .. -1.
@@ -562,6 +572,28 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
             __builtin_amdgcn_sched_group_barrier(0x008, R, 0);
         }
     };
+    // The last sub-step of stage kt with the DMA issues of iteration kt,
+    // A(kt + SA) then W(kt + SW) (both in range), spread between its MFMAs:
+    // a wave held at a full load queue then still has matrix work queued.
+    auto mma_sub_dma = [&](const u32x4 (&fa)[MT], const u32x4 (&fb)[NT], int kt) {
+        constexpr int NMF = MT * NT, ND = AQ + BQ;
+        const uint8_t* srca = reinterpret_cast<const uint8_t*>(A + kb + (kt + SA) * BK);
+        const uint8_t* srcw = reinterpret_cast<const uint8_t*>(W + kb + (kt + SW) * BK);
+        uint8_t* ldsa = abuf + ((kt + SA) % SA) * ASTAGE + wave * AQ * 1024;
+        uint8_t* ldsw = bbuf + ((kt + SW) % SW) * BSTAGE + wave * BQ * 1024;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int g = 0; g < NMF; ++g) {
+            const int i = g / NT, t = g % NT;
+            acc[i][t] = mfma32x32x16(as_bf16x8(fa[i]), as_bf16x8(fb[t]), acc[i][t]);
+#pragma unroll
+            for (int d = (ND * g) / NMF; d < (ND * (g + 1)) / NMF; ++d) {
+                if (d < AQ) dma16_off(srca, aoff[d], ldsa + d * 1024);
+                else dma16_off(srcw, boff[d - AQ], ldsw + (d - AQ) * 1024);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
 
     for (int i = -SW; i < 0; ++i) issue_iter(i);
     if (nk > 0) wait_vm_atmost(after_stage(0, -1));
@@ -572,14 +604,27 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     // sub-steps 0..3 of stage kt alternate register sets; before the read of
     // stage kt+1 (under the MFMAs of sub-step 3) stage kt+1 must be resident
     // and every wave done with stage kt, whose slots then take A(kt+SA), W(kt+SW).
-    for (int kt = 0; kt < nk; ++kt) {
+    int kt = 0;
+    for (; kt + SW < nk; ++kt) {   // steady state: both issues in range
         load_sub(kt, 1, f1a, f1b);
         mma_sub(f0a, f0b);
         load_sub(kt, 2, f0a, f0b);
         mma_sub(f1a, f1b);
         load_sub(kt, 3, f1a, f1b);
         mma_sub(f0a, f0b);
-        wait_vm_atmost(kt + 1 < nk ? after_stage(kt + 1, kt - 1) : 0);   // stage kt+1 resident
+        wait_vm_atmost(after_stage(kt + 1, kt - 1));   // stage kt+1 resident
+        __syncthreads();
+        load_sub(kt + 1, 0, f0a, f0b);
+        mma_sub_dma(f1a, f1b, kt);
+    }
+    for (; kt < nk; ++kt) {
+        load_sub(kt, 1, f1a, f1b);
+        mma_sub(f0a, f0b);
+        load_sub(kt, 2, f0a, f0b);
+        mma_sub(f1a, f1b);
+        load_sub(kt, 3, f1a, f1b);
+        mma_sub(f0a, f0b);
+        wait_vm_atmost(kt + 1 < nk ? after_stage(kt + 1, kt - 1) : 0);
         __syncthreads();
         issue_iter(kt);
         load_sub(kt + 1 < nk ? kt + 1 : kt, 0, f0a, f0b);
@@ -715,8 +760,7 @@ hipError_t launch_tile_variant(int variant, const GemmArgs& a, const GemmPlan& p
 
 }  // namespace
 
-hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
-    if (a.M <= 0) return hipSuccess;
+static hipError_t launch_segments(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     const int n_out = a.epi == EPI_SWIGLU ? a.F : a.Nw;
     const int n_split = p.n_split > 0 && p.n_split < n_out ? p.n_split : n_out;
     hipError_t e = launch_tile_variant(p.variant, a, p, 0, n_split, s);
@@ -725,6 +769,31 @@ hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_
     q.splits = 1;
     q.ksplit = a.K;
     return launch_tile_variant(p.variant2, a, q, n_split, n_out, s);
+}
+
+// The tile kernels address A and W with 32-bit per-lane byte offsets: the
+// weight rows must span less than 4 GiB, and larger M is run in row blocks
+// that each do (split-K partials, laid out over the whole M, are never that
+// large: their budget is far below).
+hipError_t launch_gemm_bf16_lds(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    if (a.M <= 0) return hipSuccess;
+    constexpr uint64_t kOffLimit = 0xFFFFFFFFull;
+    const uint64_t wrows = a.epi == EPI_SWIGLU ? 2ull * a.F : static_cast<uint64_t>(a.Nw);
+    if (wrows * a.ldw * 2 > kOffLimit) return hipErrorInvalidValue;
+    const uint64_t rows_max = kOffLimit / (2ull * a.lda) / 256 * 256;
+    if (static_cast<uint64_t>(a.M) <= rows_max) return launch_segments(a, p, s);
+    if (p.splits > 1 || rows_max == 0) return hipErrorInvalidValue;
+    for (int m0 = 0; m0 < a.M; m0 += static_cast<int>(rows_max)) {
+        GemmArgs b = a;
+        b.M = static_cast<int>(std::min<uint64_t>(rows_max, static_cast<uint64_t>(a.M - m0)));
+        b.A = static_cast<const uint16_t*>(a.A) + static_cast<size_t>(m0) * a.lda;
+        if (b.out_f32) b.out_f32 += static_cast<size_t>(m0) * a.ldo;
+        if (b.resid) b.resid += static_cast<size_t>(m0) * a.ldr;
+        if (b.act) b.act = static_cast<uint16_t*>(a.act) + static_cast<size_t>(m0) * a.ld_act;
+        const hipError_t e = launch_segments(b, p, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace rl
