@@ -20,8 +20,9 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         if (r > 0) { k0 += W0; k1 += W1; }
-        const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
-        const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+        const uint64_t p0 = static_cast<uint64_t>(M0) * c[0], p1 = static_cast<uint64_t>(M1) * c[2];
+        const uint32_t hi0 = static_cast<uint32_t>(p0 >> 32), lo0 = static_cast<uint32_t>(p0);
+        const uint32_t hi1 = static_cast<uint32_t>(p1 >> 32), lo1 = static_cast<uint32_t>(p1);
         const uint32_t n0 = hi1 ^ c[1] ^ k0;
         const uint32_t n2 = hi0 ^ c[3] ^ k1;
         c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
@@ -31,6 +32,21 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
 __device__ __forceinline__ float gumbel_of_word(uint32_t x) {
     const double u = (static_cast<double>(x) + 0.5) * 2.3283064365386963e-10;
     return static_cast<float>(-log(-log(u)));
+}
+
+// Upper bounds of g(x) = gumbel_of_word(x).  g grows with x: g < 5.56 for
+// x < 0xFF000000 (u < 1 - 2^-8, g(0xFEFFFFFF) = 5.5433) and g <= 22.874 for
+// every x (u = 1 - 2^-33).  Below 0xFF000000 a tighter bound comes from fp32
+// hardware logarithms: rounding u to fp32 (relative error <= 2^-23) moves
+// L = -ln u (>= 3.9e-3) by a relative 3.1e-5 at most, the two logarithms and
+// the products add ~1e-6 each, so the fp32 value is within 1e-4 of -ln L;
+// 0.01 is added on top.
+constexpr uint32_t kGumbelLowWords = 0xFF000000u;
+constexpr float kGumbelLowMax = 5.56f, kGumbelMax = 22.9f;
+__device__ __forceinline__ float gumbel_upper_low(uint32_t x) {
+    const float u = (static_cast<float>(x) + 0.5f) * 2.3283064365386963e-10f;
+    const float L = -__log2f(u) * 0.69314718f;
+    return -__log2f(L) * 0.69314718f + 0.01f;
 }
 
 struct Best { float s; int v; };
@@ -62,12 +78,23 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
     const uint64_t u64 = uid[o];
     const uint32_t pos = static_cast<uint32_t>(pos_new[o]);
     const bool greedy = T == 0.0f;
+    const bool unit_t = T == 1.0f;   // z / 1 == z exactly: no division
     const int vbeg = c * chunk, vend = min(V, vbeg + chunk);
 
+    // The exact fp64 noise is evaluated only where the score could still
+    // reach the wave's best so far: with an upper bound b >= g(x) and rounding
+    // monotonic, fl32(z/T + b) < thr implies fl32(z/T + g) < thr, and thr
+    // is the score of an entry already seen, so the skipped entry can neither
+    // win nor tie.  The sample is therefore the same as scoring every entry.
     Best best{-INFINITY, 0x7FFFFFFF};
     Lse acc{-INFINITY, 0.0f};
-    for (int v4 = vbeg / 4 + threadIdx.x; 4 * v4 < vend; v4 += blockDim.x) {
-        const float4 zz = *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4));
+    float thr = -INFINITY;
+    // every lane runs the same number of iterations (the wave-wide threshold
+    // reads every lane); lanes past the chunk's end score nothing
+    for (int b4 = vbeg / 4; 4 * b4 < vend; b4 += blockDim.x) {
+        const int v4 = b4 + threadIdx.x;
+        const float4 zz = 4 * v4 < vend ? *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4))
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
         const float zv[4] = {zz.x, zz.y, zz.z, zz.w};
         uint32_t cw[4] = {static_cast<uint32_t>(v4), pos, static_cast<uint32_t>(u64),
                           static_cast<uint32_t>(u64 >> 32)};
@@ -76,16 +103,27 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
         for (int w = 0; w < 4; ++w) {
             const int v = 4 * v4 + w;
             if (v >= vend) break;
-            const float zt = greedy ? zv[w] : zv[w] / T;
-            const float sc = greedy ? zt : zt + gumbel_of_word(cw[w]);
-            best = better(best, Best{sc, v});
+            const float zt = greedy || unit_t ? zv[w] : zv[w] / T;
+            if (greedy) {
+                best = better(best, Best{zt, v});
+            } else {
+                const uint32_t x = cw[w];
+                const bool cand = x >= kGumbelLowWords
+                                      ? !(zt + kGumbelMax < thr)
+                                      : !(zt + kGumbelLowMax < thr) && !(zt + gumbel_upper_low(x) < thr);
+                if (cand) best = better(best, Best{zt + gumbel_of_word(x), v});
+            }
             if (zt > acc.m) {
-                acc.s = acc.s * expf(acc.m - zt) + 1.0f;
+                acc.s = acc.s * __expf(acc.m - zt) + 1.0f;
                 acc.m = zt;
             } else {
-                acc.s += expf(zt - acc.m);
+                acc.s += __expf(zt - acc.m);
             }
         }
+        float t = best.s;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) t = fmaxf(t, __shfl_xor(t, off, 64));
+        thr = t;
     }
     for (int off = 32; off > 0; off >>= 1) {
         Best ob{__shfl_xor(best.s, off, 64), __shfl_xor(best.v, off, 64)};
