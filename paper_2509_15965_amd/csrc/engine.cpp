@@ -359,14 +359,15 @@ rl_status reduce_splits(rl_decode_ctx* c, int epi, int M, int N, int splits, flo
 }
 
 // x += the split-K slices of a deferred RESID GEMM (splits > 0), then
-// h = rmsnorm(x) * g.  From kResidNormMinRows rows one fused pass per row
-// (enough rows to fill the CUs); below, the wide reduction and the norm.
+// h = rmsnorm(x) * g in one fused pass per row: at any batch size when a row
+// fits one float4 per thread (H <= 4096), else from kResidNormMinRows rows
+// (enough rows to hide the grouped loads); below, the wide reduction and the norm.
 constexpr int kResidNormMinRows = 64;
 rl_status resid_then_norm(rl_decode_ctx* c, int dt, int splits, float* x, int n, int H, const void* g, float eps,
                           void* h) {
     const double es = c->lay.es;
     hipError_t e;
-    if (splits > 0 && n >= kResidNormMinRows && H % 4 == 0 && H <= 8192) {
+    if (splits > 0 && H % 4 == 0 && (H <= 4096 || (n >= kResidNormMinRows && H <= 8192))) {
         Prof pr(c, RL_K_SPLITK_REDUCE);
         e = launch_resid_norm(dt, c->wsp<float>(c->lay.off_part), splits, x, n, H, g, eps, h, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "residual + rmsnorm launch");

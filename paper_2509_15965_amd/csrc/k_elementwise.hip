@@ -212,9 +212,68 @@ __global__ void __launch_bounds__(256) resid_norm4_kernel(const float* __restric
     }
 }
 
+// The same pass with one float4 of the row per thread (H <= 4096, up to
+// 1024 threads): every slice's load of a group of eight is in flight at
+// once, so a row costs one or two memory round trips -- for batches too
+// small to hide the latency of the grouped loads above.  Same order of
+// additions; the sum of squares is reduced over the workgroup's waves.
+template <typename T>
+__global__ void __launch_bounds__(1024) resid_norm_wide_kernel(const float* __restrict__ part, int splits,
+        size_t slice, float* __restrict__ x, int H, const T* __restrict__ g, float eps, T* __restrict__ out) {
+    __shared__ float red[16];
+    const int r = blockIdx.x, c = threadIdx.x;
+    const int H4 = H / 4;
+    const bool on = c < H4;
+    f32x4* xr = reinterpret_cast<f32x4*>(x + static_cast<size_t>(r) * H);
+    const f32x4* pr = reinterpret_cast<const f32x4*>(part + static_cast<size_t>(r) * H);
+    const size_t sl4 = slice / 4;
+    f32x4 v{0.f, 0.f, 0.f, 0.f};
+    for (int z = 0; z < splits; z += 8) {
+        f32x4 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            t[u] = on && z + u < splits ? pr[(z + u) * sl4 + c] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (z + u < splits) v += t[u];
+    }
+    float ss = 0.0f;
+    if (on) {
+        v = xr[c] + v;
+        xr[c] = v;
+        ss = fmaf(v[0], v[0], ss);
+        ss = fmaf(v[1], v[1], ss);
+        ss = fmaf(v[2], v[2], ss);
+        ss = fmaf(v[3], v[3], ss);
+    }
+    ss = wave_sum(ss);
+    const int nw = (blockDim.x + 63) >> 6;
+    if ((c & 63) == 0) red[c >> 6] = ss;
+    __syncthreads();
+    ss = 0.0f;
+    for (int w = 0; w < nw; ++w) ss += red[w];
+    const float rs = 1.0f / sqrtf(ss / static_cast<float>(H) + eps);
+    if (on) {
+        T* orow = out + static_cast<size_t>(r) * H;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Elem<T>::store(orow, 4 * c + e, v[e] * rs * Elem<T>::load(g, 4 * c + e));
+    }
+}
+
 hipError_t launch_resid_norm(int dt, const float* part, int splits, float* x, int n, int H, const void* g,
                              float eps, void* out, hipStream_t s) {
     if (n <= 0) return hipSuccess;
+    if (H % 4 == 0 && H / 4 <= 1024) {
+        const size_t slice = static_cast<size_t>(n) * H;
+        const int threads = (H / 4 + 63) / 64 * 64;
+        if (dt == DT_BF16)
+            hipLaunchKernelGGL(resid_norm_wide_kernel<uint16_t>, dim3(n), dim3(threads), 0, s, part, splits, slice,
+                               x, H, static_cast<const uint16_t*>(g), eps, static_cast<uint16_t*>(out));
+        else
+            hipLaunchKernelGGL(resid_norm_wide_kernel<float>, dim3(n), dim3(threads), 0, s, part, splits, slice,
+                               x, H, static_cast<const float*>(g), eps, static_cast<float*>(out));
+        return hipGetLastError();
+    }
     const int per = (H / 4 + 255) / 256;
     if (H % 4 != 0 || per > 8) return hipErrorInvalidValue;
     const size_t slice = static_cast<size_t>(n) * H;
