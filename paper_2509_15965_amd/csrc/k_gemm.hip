@@ -374,8 +374,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmArgs p, int ksplit) 
                     const int c = wrow[t] + r16;
                     if (!wok[t]) continue;
                     const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
-                    const float silu = g / (1.0f + expf(-g));
-                    act[static_cast<size_t>(m) * p.ld_act + c] = f32_to_bf16(silu * u);
+                    act[static_cast<size_t>(m) * p.ld_act + c] = f32_to_bf16(swiglu_bf16(g, u));
                 }
             }
         }
@@ -491,8 +490,7 @@ __global__ void __launch_bounds__(512) gemv_kernel(GemmArgs p, int kw) {
         if (EPI == EPI_SWIGLU) {
             const float up = __shfl(val, (lane & ~15) | ((r16 + 8) & 15), 64);
             if (r16 < 8 && ok && m < M) {
-                const float silu = val / (1.0f + expf(-val));
-                static_cast<uint16_t*>(p.act)[static_cast<size_t>(m) * p.ld_act + n] = f32_to_bf16(silu * up);
+                static_cast<uint16_t*>(p.act)[static_cast<size_t>(m) * p.ld_act + n] = f32_to_bf16(swiglu_bf16(val, up));
             }
         } else if (ok && m < M) {
             if (EPI == EPI_F32) p.out_f32[static_cast<size_t>(m) * p.ldo + n] = val;
@@ -541,8 +539,7 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs p, int spli
         } else {
             float u = 0.0f;
             for (int z = 0; z < splits; ++z) u += src[z * slice + p.F];
-            const float silu = v / (1.0f + expf(-v));
-            Elem<T>::store(static_cast<T*>(p.act), static_cast<size_t>(m) * p.ld_act + c, silu * u);
+            Elem<T>::store(static_cast<T*>(p.act), static_cast<size_t>(m) * p.ld_act + c, swiglu<T>(v, u));
         }
     }
 }
@@ -585,8 +582,7 @@ __global__ void __launch_bounds__(256) splitk_reduce4_kernel(GemmArgs p, int spl
             T* act = static_cast<T*>(p.act) + static_cast<size_t>(m) * p.ld_act + c;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float silu = v[e] / (1.0f + expf(-v[e]));
-                Elem<T>::store(act, e, silu * u[e]);
+                Elem<T>::store(act, e, swiglu<T>(v[e], u[e]));
             }
         }
     }

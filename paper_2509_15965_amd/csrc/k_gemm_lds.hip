@@ -16,6 +16,7 @@
 #include "rl_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace rl {
 
@@ -168,8 +169,7 @@ __global__ void __launch_bounds__(256) gemm_lds_kernel(GemmArgs p, int ksplit, i
                 for (int t = 0; t < NT / 2; ++t) {
                     if (!nok[t]) continue;
                     const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
-                    const float silu = g / (1.0f + expf(-g));
-                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(silu * u);
+                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(swiglu_bf16(g, u));
                 }
             }
         }
@@ -396,8 +396,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma_kernel(GemmArgs p, int kspli
                 for (int t = 0; t < NT / 2; ++t) {
                     if (!nok[t]) continue;
                     const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
-                    const float silu = g / (1.0f + expf(-g));
-                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(silu * u);
+                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(swiglu_bf16(g, u));
                 }
             }
         }
@@ -636,37 +635,46 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     bool nok[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) nrow[t] = wrow(wn * TN + 32 * t + r32, &nok[t]);
+    // CHECKED: per-element row and column bounds (edge tiles); interior tiles
+    // store without them
+    auto store_tile = [&](auto checked) {
+        constexpr bool CHECKED = decltype(checked)::value;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
+        for (int i = 0; i < MT; ++i) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int m = m0 + wm * TM + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
-            if (m >= M) continue;
-            if (SPLIT) {
-                float* dst = p.partial + (static_cast<size_t>(blockIdx.y) * M + m) * Nw;
+            for (int e = 0; e < 16; ++e) {
+                const int m = m0 + wm * TM + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
+                if (CHECKED && m >= M) continue;
+                if (SPLIT) {
+                    float* dst = p.partial + (static_cast<size_t>(blockIdx.y) * M + m) * Nw;
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    if (nok[t]) dst[nrow[t]] = acc[i][t][e];
-            } else if (EPI == EPI_F32) {
+                    for (int t = 0; t < NT; ++t)
+                        if (!CHECKED || nok[t]) dst[nrow[t]] = acc[i][t][e];
+                } else if (EPI == EPI_F32) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    if (nok[t]) p.out_f32[static_cast<size_t>(m) * p.ldo + nrow[t]] = acc[i][t][e];
-            } else if (EPI == EPI_RESID) {
+                    for (int t = 0; t < NT; ++t)
+                        if (!CHECKED || nok[t]) p.out_f32[static_cast<size_t>(m) * p.ldo + nrow[t]] = acc[i][t][e];
+                } else if (EPI == EPI_RESID) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    if (nok[t]) p.resid[static_cast<size_t>(m) * p.ldr + nrow[t]] += acc[i][t][e];
-            } else {
-                uint16_t* act = static_cast<uint16_t*>(p.act);
+                    for (int t = 0; t < NT; ++t)
+                        if (!CHECKED || nok[t]) p.resid[static_cast<size_t>(m) * p.ldr + nrow[t]] += acc[i][t][e];
+                } else {
+                    uint16_t* act = static_cast<uint16_t*>(p.act);
 #pragma unroll
-                for (int t = 0; t < NT / 2; ++t) {
-                    if (!nok[t]) continue;
-                    const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
-                    const float silu = g / (1.0f + expf(-g));
-                    act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(silu * u);
+                    for (int t = 0; t < NT / 2; ++t) {
+                        if (CHECKED && !nok[t]) continue;
+                        const float g = acc[i][t][e], u = acc[i][t + NT / 2][e];
+                        act[static_cast<size_t>(m) * p.ld_act + nrow[t]] = f32_to_bf16(swiglu_bf16(g, u));
+                    }
                 }
             }
         }
-    }
+    };
+    bool inside = m0 + BM <= M;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) inside = inside && nok[t];
+    if (inside) store_tile(std::false_type{});
+    else store_tile(std::true_type{});
 }
 
 template <int BM, int BN, int WM, int NW, int SA, int SW>

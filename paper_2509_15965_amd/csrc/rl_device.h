@@ -23,6 +23,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // Model-dtype element access.
+// silu(g) * u for bf16-stored activations: hardware exponential and
+// reciprocal (a few fp32 ulp; the value is rounded to bf16 right after).
+__device__ __forceinline__ float swiglu_bf16(float g, float u) {
+    return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
+// The same for fp32 storage: IEEE division and the accurate exponential.
+__device__ __forceinline__ float swiglu_f32(float g, float u) {
+    return g / (1.0f + expf(-g)) * u;
+}
+template <typename T> __device__ __forceinline__ float swiglu(float g, float u);
+template <> __device__ __forceinline__ float swiglu<uint16_t>(float g, float u) { return swiglu_bf16(g, u); }
+template <> __device__ __forceinline__ float swiglu<float>(float g, float u) { return swiglu_f32(g, u); }
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
     static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
