@@ -604,7 +604,8 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     // stage kt+1 (under the MFMAs of sub-step 3) stage kt+1 must be resident
     // and every wave done with stage kt, whose slots then take A(kt+SA), W(kt+SW).
     int kt = 0;
-    for (; kt + SW < nk; ++kt) {   // steady state: both issues in range
+    constexpr int SMAX = SA > SW ? SA : SW;
+    for (; kt + SMAX < nk; ++kt) {   // steady state: both issues in range
         load_sub(kt, 1, f1a, f1b);
         mma_sub(f0a, f0b);
         load_sub(kt, 2, f0a, f0b);
