@@ -410,11 +410,12 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma_kernel(GemmArgs p, int kspli
 // ring).  Chunk c of row r sits at c ^ ((r / 2) % 8), which keeps the 32x32
 // fragment reads free of bank conflicts.  A stage is 64 k (four 16-wide
 // sub-steps).  The activation tile (re-read by every weight tile, so mostly
-// L2 hits) and the weight tile (streamed from HBM) have rings of SA and
-// SW >= SA stages: the slot of stage kt takes stage kt + SA (kt + SW) as soon
-// as every wave has read all of stage kt, the activation DMA issued first so
-// that the in-order load counter lets the weight stream stay in flight
-// across the barrier (SW - 1 stages of lookahead for the weights).
+// L2 hits) and the weight tile (streamed from HBM) have rings of SA and SW
+// stages (any pair; the kernels use SW >= SA): the slot of stage kt takes
+// stage kt + SA (kt + SW) as soon as every wave has read all of stage kt, the
+// activation DMA issued first so that the in-order load counter lets the
+// weight stream stay in flight across the barrier (SW - 1 stages of
+// lookahead for the weights).
 // ---------------------------------------------------------------------------
 // s_waitcnt vmcnt(<= n): rounded down to one of a few immediates (waiting for
 // fewer outstanding loads than allowed is always safe)
@@ -442,7 +443,8 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     constexpr int AQ = BM / (8 * NW), BQ = BN / (8 * NW);   // DMA instructions (8 rows each) per wave per stage
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows must fill whole DMA instructions");
     static_assert(TM % 32 == 0 && TN % 64 == 0, "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
-    static_assert(SA >= 2 && SW >= SA && SW <= 6, "ring depths");
+    static_assert(SA >= 2 && SW >= 2 && SA <= 6 && SW <= 6, "ring depths");
+    constexpr int SMAX = SA > SW ? SA : SW;   // the prologue covers iterations -SMAX .. -1
     static_assert(SA * AQ + SW * BQ < 64, "vmcnt range (most loads ever in flight)");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[SA * ASTAGE + SW * BSTAGE];
 
@@ -517,7 +519,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         for (int q = 0; q < BQ; ++q) dma16_off(src, boff[q], base + (wave * BQ + q) * 1024);
     };
     // Issue schedule: in (real or prologue) iteration i, A(i + SA) if in range,
-    // then W(i + SW) if in range; the prologue is iterations -SW .. -1.
+    // then W(i + SW) if in range; the prologue is iterations -SMAX .. -1.
     auto issue_iter = [&](int i) {
         if (i + SA >= 0 && i + SA < nk) issue_a(i + SA);
         if (i + SW >= 0 && i + SW < nk) issue_w(i + SW);
@@ -594,7 +596,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         }
     };
 
-    for (int i = -SW; i < 0; ++i) issue_iter(i);
+    for (int i = -SMAX; i < 0; ++i) issue_iter(i);
     if (nk > 0) wait_vm_atmost(after_stage(0, -1));
     __syncthreads();
     u32x4 f0a[MT], f0b[NT], f1a[MT], f1b[NT];
@@ -604,7 +606,6 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     // stage kt+1 (under the MFMAs of sub-step 3) stage kt+1 must be resident
     // and every wave done with stage kt, whose slots then take A(kt+SA), W(kt+SW).
     int kt = 0;
-    constexpr int SMAX = SA > SW ? SA : SW;
     for (; kt + SMAX < nk; ++kt) {   // steady state: both issues in range
         load_sub(kt, 1, f1a, f1b);
         mma_sub(f0a, f0b);
