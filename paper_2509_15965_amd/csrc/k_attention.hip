@@ -401,64 +401,85 @@ hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const
 }
 
 // Merge the split partials of one query block and q-head: one workgroup per
-// (split block, q-head), one thread per (token, d).  The block's per-item
-// (m, l) go through LDS; the weighted sums issue their loads 8 at a time.
+// (split block, q-head), one thread per d, the block's tokens in turn.  Each
+// thread loads every item's (m, l) itself (broadcast reads) together with its
+// own column of the partial outputs, so up to 8 items take one memory round
+// trip and no workgroup barrier; more items take a max pass and then groups
+// of 8.  Weights 2^(m_j - M) (M: the token's max), sums in item order.
 template <int D>
-__global__ void __launch_bounds__(256) attn_combine_kernel(const int32_t* __restrict__ blocks,
+__global__ void __launch_bounds__(D) attn_combine_kernel(const int32_t* __restrict__ blocks,
         const AttnItem* __restrict__ items, const float* __restrict__ part, int Hq, int Hkv,
         uint16_t* __restrict__ out) {
-    __shared__ float wsh[16][kMaxCombine];
-    __shared__ float lsh[16][kMaxCombine];
-    __shared__ float lsum[16];
     const AttnItem it = items[blocks[blockIdx.x]];
     const int h = blockIdx.y;
     const int G = Hq / Hkv;
     const int kvh = h / G, g = h - kvh * G;
     const int np = it.nparts;
+    const int d = threadIdx.x;
     const size_t pstride = static_cast<size_t>(Hkv) * 16 * (D + 2);
     const float* pb0 = part + (static_cast<size_t>(it.part0) * Hkv + kvh) * 16 * (D + 2);
-    // every item's (m, l) for every token, loaded in parallel
-    for (int p = threadIdx.x; p < it.nq * np; p += blockDim.x) {
-        const int t = p / np, j = p - t * np;
-        const float* pc = pb0 + j * pstride + static_cast<size_t>(t * G + g) * (D + 2);
-        wsh[t][j] = pc[D];
-        lsh[t][j] = pc[D + 1];
-    }
-    __syncthreads();
-    // weights 2^(m_j - M) (M: the token's max) and the total sum
-    for (int t = threadIdx.x; t < it.nq; t += blockDim.x) {
-        float M = -INFINITY;
-        for (int j = 0; j < np; ++j) M = fmaxf(M, wsh[t][j]);
-        float L = 0.0f;
-        for (int j = 0; j < np; ++j) {
-            const float w = exp2f(wsh[t][j] - M);
-            wsh[t][j] = w;
-            L += w * lsh[t][j];
-        }
-        lsum[t] = L;
-    }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < it.nq * D; idx += blockDim.x) {
-        const int t = idx / D, d = idx - t * D;
-        const float* pc = pb0 + static_cast<size_t>(t * G + g) * (D + 2) + d;
-        float acc = 0.0f;
-        int j = 0;
-        for (; j + 8 <= np; j += 8) {
-            float v[8];
+    for (int t = 0; t < it.nq; ++t) {
+        const float* pc = pb0 + static_cast<size_t>(t * G + g) * (D + 2);
+        float acc = 0.0f, L = 0.0f;
+        if (np <= 8) {
+            float m[8], l[8], v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = pc[(j + u) * pstride];
+            for (int u = 0; u < 8; ++u) {
+                if (u < np) {
+                    m[u] = pc[u * pstride + D];
+                    l[u] = pc[u * pstride + D + 1];
+                    v[u] = pc[u * pstride + d];
+                }
+            }
+            float M = -INFINITY;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) acc += wsh[t][j + u] * v[u];
+            for (int u = 0; u < 8; ++u)
+                if (u < np) M = fmaxf(M, m[u]);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                if (u < np) {
+                    const float w = exp2f(m[u] - M);
+                    L += w * l[u];
+                    acc += w * v[u];
+                }
+            }
+        } else {
+            float M = -INFINITY;
+            for (int j = 0; j < np; j += 16) {
+                float m[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) m[u] = j + u < np ? pc[(j + u) * pstride + D] : -INFINITY;
+#pragma unroll
+                for (int u = 0; u < 16; ++u) M = fmaxf(M, m[u]);
+            }
+            for (int j = 0; j < np; j += 8) {
+                float m[8], l[8], v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    if (j + u < np) {
+                        m[u] = pc[(j + u) * pstride + D];
+                        l[u] = pc[(j + u) * pstride + D + 1];
+                        v[u] = pc[(j + u) * pstride + d];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    if (j + u < np) {
+                        const float w = exp2f(m[u] - M);
+                        L += w * l[u];
+                        acc += w * v[u];
+                    }
+                }
+            }
         }
-        for (; j < np; ++j) acc += wsh[t][j] * pc[j * pstride];
-        out[(static_cast<size_t>(it.qrow + t) * Hq + h) * D + d] = f32_to_bf16(acc / lsum[t]);
+        out[(static_cast<size_t>(it.qrow + t) * Hq + h) * D + d] = f32_to_bf16(acc / L);
     }
 }
 
 hipError_t launch_attn_combine(const int32_t* blocks, int n_blocks, const AttnItem* items, const float* part,
                                int Hq, int Hkv, int D, void* out, hipStream_t s) {
     if (n_blocks <= 0) return hipSuccess;
-    dim3 grid(n_blocks, Hq), block(128);
+    dim3 grid(n_blocks, Hq), block(D);
     if (D == 128)
         hipLaunchKernelGGL(attn_combine_kernel<128>, grid, block, 0, s, blocks, items, part, Hq, Hkv,
                            static_cast<uint16_t*>(out));
