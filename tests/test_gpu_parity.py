@@ -337,3 +337,19 @@ def test_every_gemm_kernel_matches_oracle(name, code):
     for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
         assert row_rel_err(zg, zo) < LOGIT_REL_TOL, (name, k)
         assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, (name, k)
+
+
+@pytest.mark.parametrize("n_prompts", [64, 20])
+def test_wide_hidden_residual_norm_paths(n_prompts):
+    """hidden 4608 > 4096 (more than one float4 per thread of a 1024-wide
+    workgroup): the split-K o / down slices are summed with the residual and
+    normed in one grouped pass per row from 64 rows, by the wide reduction and
+    a separate norm below (split-K 4 forced for every projection)."""
+    shape = ModelShape(1, 4608, 36, 6, 128, 640, 512, 1e-6, 1e6, "bf16")
+    rng = np.random.default_rng(n_prompts)
+    prompts = [rng.integers(0, shape.vocab, size=2).astype(np.int32) for _ in range(n_prompts)]
+    res = teacher_forced_run(shape, 90 + n_prompts, prompts, group=1, n_steps=1, T=1.0,
+                             gemm_plan=gemm_plan_code(RL_GEMM_T256, 4))
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
