@@ -1,5 +1,6 @@
 // k_sample.hip -- temperature log-softmax, Gumbel-max sampling and the
-// per-token log-probability, one workgroup per output row.
+// per-token log-probability, one workgroup per (output row, vocabulary
+// chunk); the exact noise is evaluated only where an entry can still win.
 //
 // Noise: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit seed with
 // counter (v / 4, position of the new token, uid lo, uid hi); word v % 4 of
