@@ -57,8 +57,9 @@ typedef enum rl_dtype {
 
 /* Decoder shape and capacity.
  * Supported: head_dim in {64, 128}; n_q_heads a multiple of n_kv_heads with
- * n_q_heads / n_kv_heads <= 16; hidden, ffn and vocab multiples of 8.
- * rms_eps > 0, rope_theta > 1.  Capacity: max_seqs KV slots (also the most
+ * n_q_heads / n_kv_heads <= 16; hidden, ffn and vocab multiples of 8; in
+ * bf16 every weight matrix (the LM head, gate|up, q|k|v, o, down) under
+ * 4 GiB.  rms_eps > 0, rope_theta > 1.  Capacity: max_seqs KV slots (also the most
  * rows one rl_decode_step takes), max_ctx positions per slot, and
  * max_prefill_tokens packed prompt tokens per rl_prefill call. */
 typedef struct rl_model_config {

@@ -56,6 +56,14 @@ bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
     if (c->n_q_heads % c->n_kv_heads != 0) return bad(RL_ERR_UNSUPPORTED, "n_q_heads must be a multiple of n_kv_heads");
     if (c->n_q_heads / c->n_kv_heads > 16) return bad(RL_ERR_UNSUPPORTED, "more than 16 q-heads per kv-head");
     if (c->hidden % 8 || c->ffn % 8 || c->vocab % 8) return bad(RL_ERR_UNSUPPORTED, "hidden, ffn and vocab must be multiples of 8");
+    if (c->dtype == RL_DTYPE_BF16) {
+        // the bf16 GEMM kernels address a weight matrix with 32-bit byte offsets
+        const uint64_t H = static_cast<uint64_t>(c->hidden), F = static_cast<uint64_t>(c->ffn);
+        const uint64_t qkv = static_cast<uint64_t>(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+        const uint64_t widest = std::max({static_cast<uint64_t>(c->vocab) * H, 2 * F * H, qkv * H, H * F,
+                                          H * static_cast<uint64_t>(c->n_q_heads) * c->head_dim});
+        if (2 * widest > 0xFFFFFFFFull) return bad(RL_ERR_UNSUPPORTED, "a bf16 weight matrix spans 4 GiB or more");
+    }
     return true;
 }
 

@@ -72,6 +72,21 @@ def test_invalid_configs_rejected_before_any_device_call(field, value, status):
     assert not h.value
 
 
+def test_bf16_weight_matrix_of_4_gib_rejected():
+    """The bf16 GEMMs address a weight matrix with 32-bit byte offsets: an LM
+    head of 600000 x 3584 bf16 (4.3 GB) is refused at create, 590000 is not."""
+    c = cfg_for("qwen7b")
+    c.vocab = 600000
+    assert R.kv_bytes(c) == 0
+    h = C.c_void_p(123)
+    w = R.Weights(*([256] * 9))
+    st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
+    assert st == R.RL_ERR_UNSUPPORTED
+    assert not h.value
+    c.vocab = 590000
+    assert R.kv_bytes(c) > 0
+
+
 def test_create_validates_pointers_and_sizes_first():
     lib = R.lib()
     c = cfg_for("tiny")
