@@ -313,8 +313,7 @@ rl_status rl_kv_onload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, cons
 /* Point the context at new device buffers (same sizes and alignment rules
  * as rl_decode_create), e.g. after the caller freed the old ones during a
  * context switch.  Waits for the context's outstanding work, then writes the
- * RoPE table and sampler counters into the new workspace (synchronises the
- * stream).  Slot lengths are kept: reload their K/V with rl_kv_onload, or
+ * RoPE table into the new workspace (synchronises the stream).  Slot lengths are kept: reload their K/V with rl_kv_onload, or
  * release them. */
 rl_status rl_decode_rebind(rl_decode_ctx* ctx, const rl_weights* w, void* kv_pool, size_t kv_bytes,
                            void* workspace, size_t ws_bytes);

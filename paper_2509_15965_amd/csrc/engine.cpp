@@ -32,7 +32,7 @@ struct Layout {
     size_t kv_bytes = 0, ws_bytes = 0;
     size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
     size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
-    size_t off_cnt = 0, cnt_bytes = 0, off_spart = 0, off_tok = 0;
+    size_t off_spart = 0, off_tok = 0;
     size_t off_stage = 0, stage_bytes = 0;   // KV offload staging: the activation buffers x .. split-K partials
     size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
 };
@@ -101,9 +101,6 @@ Layout make_layout(const rl_model_config& c) {
     L.off_rope = take(static_cast<size_t>(L.cap) * (c.head_dim / 2) * 2 * 4);
     L.off_meta = take(L.meta_bytes);
     L.off_tok = take(R * 4);   // packed token ids of a scoring pass
-    // sampler completion counters (one per row): zero between launches
-    L.cnt_bytes = 4 * static_cast<size_t>(c.max_seqs);
-    L.off_cnt = take(L.cnt_bytes);
     L.off_spart = take(sizeof(SamplePart) * static_cast<size_t>(c.max_seqs) * kSampleMaxChunks);
     L.ws_bytes = o;
     return L;
@@ -143,7 +140,6 @@ struct rl_decode_ctx {
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
     uint8_t* kslab() const { return kv; }
     uint8_t* vslab() const { return kv + lay.kv_bytes / 2; }
-    int* sample_counters() const { return reinterpret_cast<int*>(ws + lay.off_cnt); }
     SamplePart* sample_parts() const { return reinterpret_cast<SamplePart*>(ws + lay.off_spart); }
     bool bf16() const { return cfg.dtype == RL_DTYPE_BF16; }
 };
@@ -523,7 +519,7 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
     {
         Prof pr(c, RL_K_SAMPLE);
         e = launch_sample(f.logits, cf.vocab, f.n_out, cf.vocab, f.logit_row, f.uid, f.pos_new, f.forced,
-                          f.seed, f.T, c->sample_parts(), c->sample_counters(), f.out_tok, f.out_logp,
+                          f.seed, f.T, c->sample_parts(), f.out_tok, f.out_logp,
                           c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "sample launch");
         pr.done(f.n_out * (cf.vocab * 4.0 + 8.0), 0.0);
@@ -897,13 +893,12 @@ size_t rl_decode_workspace_bytes(const rl_model_config* cfg) {
 
 namespace {
 
-// RoPE table and zeroed sampler counters in the workspace; synchronises the stream.
+// RoPE table in the workspace; synchronises the stream.
 hipError_t init_workspace(rl_decode_ctx* c) {
     std::vector<float> table;
     fill_rope_table(c->cfg, c->lay.cap, &table);
     hipError_t e = hipMemcpyAsync(c->ws + c->lay.off_rope, table.data(), table.size() * sizeof(float),
                                   hipMemcpyHostToDevice, c->stream);
-    if (e == hipSuccess) e = hipMemsetAsync(c->ws + c->lay.off_cnt, 0, c->lay.cnt_bytes, c->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     return e;
 }
@@ -1376,7 +1371,7 @@ rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits, c
     if (st != RL_OK) return st;
     Prof pr(c, RL_K_SAMPLE);
     hipError_t e = launch_sample(logits, c->cfg.vocab, n, c->cfg.vocab, nullptr, d_uid, d_posn, forced, sp->seed,
-                                 sp->temperature, c->sample_parts(), c->sample_counters(), out_tok, out_logp,
+                                 sp->temperature, c->sample_parts(), out_tok, out_logp,
                                  c->stream);
     if (e != hipSuccess) return hip_fail(c, e, "sample launch");
     pr.done(n * (c->cfg.vocab * 4.0 + 8.0), 0.0);

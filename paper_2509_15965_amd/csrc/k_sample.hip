@@ -63,13 +63,25 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
     return Lse{m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
 }
 
+// The row's token (the arg-max) and the log-probability of the token, or of
+// `forced` when it is a vocabulary index.
+__device__ __forceinline__ void sample_finish(Best b, Lse a, const float* z, int V, int forced, float T, int o,
+                                              int32_t* out_tok, float* out_logp) {
+    const float lse = a.m + logf(a.s);
+    const int r = (forced >= 0 && forced < V) ? forced : b.v;
+    const float zr = T == 0.0f ? z[r] : z[r] / T;
+    out_tok[o] = b.v;
+    out_logp[o] = zr - lse;
+}
+
 // One workgroup per (row, vocabulary chunk).  With several chunks per row,
-// each writes its (best score, index, max, sum-exp) and the last chunk of the
-// row to finish (device-scope counter) merges them in chunk order.
+// each writes its (best score, index, max, sum-exp) and sample_merge_kernel
+// merges them in chunk order (a kernel boundary instead of device-scope
+// fences: on this multi-XCD part a fence writes back the whole L2).
 __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ logits, int ld,
         int V, const int32_t* __restrict__ logit_row, const uint64_t* __restrict__ uid,
         const int32_t* __restrict__ pos_new, const int32_t* __restrict__ forced, uint32_t seed_lo,
-        uint32_t seed_hi, float T, int chunk, SamplePart* __restrict__ parts, int* __restrict__ counters,
+        uint32_t seed_hi, float T, int chunk, SamplePart* __restrict__ parts,
         int32_t* __restrict__ out_tok, float* __restrict__ out_logp) {
     __shared__ Best sb[4];
     __shared__ Lse sl[4];
@@ -92,10 +104,17 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
     float thr = -INFINITY;
     // every lane runs the same number of iterations (the wave-wide threshold
     // reads every lane); lanes past the chunk's end score nothing
+    // (the next iteration's logits are loaded before this one's math)
+    auto load4 = [&](int bb) {
+        const int v4 = bb + static_cast<int>(threadIdx.x);
+        return 4 * v4 < vend ? *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4))
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    float4 znext = load4(vbeg / 4);
     for (int b4 = vbeg / 4; 4 * b4 < vend; b4 += blockDim.x) {
         const int v4 = b4 + threadIdx.x;
-        const float4 zz = 4 * v4 < vend ? *reinterpret_cast<const float4*>(z + 4 * static_cast<size_t>(v4))
-                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 zz = znext;
+        if (4 * (b4 + static_cast<int>(blockDim.x)) < vend) znext = load4(b4 + blockDim.x);
         const float zv[4] = {zz.x, zz.y, zz.z, zz.w};
         uint32_t cw[4] = {static_cast<uint32_t>(v4), pos, static_cast<uint32_t>(u64),
                           static_cast<uint32_t>(u64 >> 32)};
@@ -139,34 +158,37 @@ __global__ void __launch_bounds__(256) sample_kernel(const float* __restrict__ l
     Best b = sb[0];
     Lse a = sl[0];
     for (int w = 1; w < 4; ++w) { b = better(b, sb[w]); a = lse_merge(a, sl[w]); }
-    if (nchunks > 1) {
+    if (nchunks > 1) {   // merged by sample_merge_kernel
         parts[static_cast<size_t>(o) * nchunks + c] = SamplePart{b.s, b.v, a.m, a.s};
-        __threadfence();
-        if (atomicAdd(&counters[o], 1) != nchunks - 1) return;
-        __threadfence();
-        const SamplePart* pr = parts + static_cast<size_t>(o) * nchunks;
-        b = Best{pr[0].best_s, pr[0].best_v};
-        a = Lse{pr[0].m, pr[0].s};
-        for (int k = 1; k < nchunks; ++k) {
-            b = better(b, Best{pr[k].best_s, pr[k].best_v});
-            a = lse_merge(a, Lse{pr[k].m, pr[k].s});
-        }
-        counters[o] = 0;
+        return;
     }
-    const float lse = a.m + logf(a.s);
-    int r = b.v;
-    if (forced) {
-        const int f = forced[o];
-        r = (f >= 0 && f < V) ? f : b.v;
+    sample_finish(b, a, z, V, forced ? forced[o] : -1, T, o, out_tok, out_logp);
+}
+
+// One 64-lane workgroup per row: lane k loads chunk k's partial (all in one
+// memory round trip), then lane 0 merges them in chunk order.
+__global__ void __launch_bounds__(64) sample_merge_kernel(const SamplePart* __restrict__ parts, int nchunks,
+        const float* __restrict__ logits, int ld, int V, const int32_t* __restrict__ logit_row,
+        const int32_t* __restrict__ forced, float T, int32_t* __restrict__ out_tok, float* __restrict__ out_logp) {
+    __shared__ SamplePart sp[kSampleMaxChunks];
+    const int o = blockIdx.x;
+    const SamplePart* pr = parts + static_cast<size_t>(o) * nchunks;
+    for (int k = threadIdx.x; k < nchunks; k += blockDim.x) sp[k] = pr[k];
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    Best b{sp[0].best_s, sp[0].best_v};
+    Lse a{sp[0].m, sp[0].s};
+    for (int k = 1; k < nchunks; ++k) {
+        b = better(b, Best{sp[k].best_s, sp[k].best_v});
+        a = lse_merge(a, Lse{sp[k].m, sp[k].s});
     }
-    const float zr = greedy ? z[r] : z[r] / T;
-    out_tok[o] = b.v;
-    out_logp[o] = zr - lse;
+    const int row = logit_row ? logit_row[o] : o;
+    sample_finish(b, a, logits + static_cast<size_t>(row) * ld, V, forced ? forced[o] : -1, T, o, out_tok, out_logp);
 }
 
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
-                         uint64_t seed, float T, SamplePart* parts, int* counters,
+                         uint64_t seed, float T, SamplePart* parts,
                          int32_t* out_tok, float* out_logp, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     int nchunks = (2048 + n - 1) / n;
@@ -176,7 +198,10 @@ hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_
     nchunks = (V + chunk - 1) / chunk;
     hipLaunchKernelGGL(sample_kernel, dim3(n, nchunks), dim3(256), 0, s, logits, ld, V, logit_row, uid,
                        pos_new, forced, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
-                       T, chunk, parts, counters, out_tok, out_logp);
+                       T, chunk, parts, out_tok, out_logp);
+    if (nchunks > 1)
+        hipLaunchKernelGGL(sample_merge_kernel, dim3(n), dim3(64), 0, s, parts, nchunks, logits, ld, V, logit_row,
+                           forced, T, out_tok, out_logp);
     return hipGetLastError();
 }
 

@@ -153,11 +153,11 @@ hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32
                                 int Hq, int Hkv, int D, int cap, int layer, float* out,
                                 hipStream_t s);
 
-// Per-chunk partial of the sampler (merged by the row's last chunk).
+// Per-chunk partial of the sampler (merged in chunk order by a second kernel).
 struct SamplePart { float best_s; int best_v; float m; float s; };
 constexpr int kSampleMaxChunks = 64;
 
-// parts: [n][kSampleMaxChunks]; counters: [n] ints, zero between launches.
+// parts: [n][kSampleMaxChunks].
 // Inference-stage log-probabilities: for logits row r < n_rows and every item
 // k in [row_items[r], row_items[r+1]), out[item_idx[k]] = fl32(z_y / T) -
 // LSE(fl32(z / T)) with y = targets[item_idx[k]] (NaN when y is outside
@@ -168,7 +168,7 @@ hipError_t launch_logprob(const float* logits, int ld, int n_rows, int V, const 
 
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
-                         uint64_t seed, float T, SamplePart* parts, int* counters,
+                         uint64_t seed, float T, SamplePart* parts,
                          int32_t* out_tok, float* out_logp, hipStream_t s);
 
 // Copy the live K/V of n slots between the pool and a packed staging buffer
