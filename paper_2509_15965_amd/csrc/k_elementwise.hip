@@ -20,10 +20,35 @@ __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ 
     else if (t < 0 && rows != nullptr && -(t + 1) < n_rows) src = rows + static_cast<size_t>(-(t + 1)) * H;
     float* dst = x + static_cast<size_t>(r) * H;
     float ss = 0.0f;
-    for (int i = threadIdx.x; i < H; i += blockDim.x) {
-        const float v = src ? Elem<T>::load(src, i) : 0.0f;
-        dst[i] = v;
-        ss = fmaf(v, v, ss);
+    bool vec = false;
+    if constexpr (sizeof(T) == 2)
+        vec = H % 8 == 0 && H <= 8 * 4 * 256 && (reinterpret_cast<uintptr_t>(src) & 15) == 0;
+    if (vec) {
+        // 16-byte loads, every one of the thread's loads in flight at once
+        constexpr int P = 4;
+        u32x4 raw[P];
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+            const int c = threadIdx.x + 256 * j;
+            raw[j] = src && 8 * c < H ? ld16(src + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+            const int c = threadIdx.x + 256 * j;
+            if (8 * c >= H) continue;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = bf16_to_f32(static_cast<uint16_t>(raw[j][e >> 1] >> (16 * (e & 1))));
+                dst[8 * c + e] = v;
+                ss = fmaf(v, v, ss);
+            }
+        }
+    } else {
+        for (int i = threadIdx.x; i < H; i += blockDim.x) {
+            const float v = src ? Elem<T>::load(src, i) : 0.0f;
+            dst[i] = v;
+            ss = fmaf(v, v, ss);
+        }
     }
     if (h == nullptr) return;
     ss = wave_sum(ss);
