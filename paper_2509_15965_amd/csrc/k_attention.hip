@@ -114,18 +114,20 @@ __device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds_wave_base)
 
 // The K rows and V blocks of positions t0..t0+31 of one (slot, kv-head) into
 // an LDS step buffer (K [32][D] chunk-permuted, V [4][D][8]), spread over the
-// kWaves waves of the workgroup: wave w moves KB [w * NDMA, (w+1) * NDMA) of
-// each.  One global_load_lds per KB per lane.
+// kWaves waves of the workgroup: wave w moves KB w, w + kWaves, ... of each
+// (waves past the step's KB count move none).  One global_load_lds per KB per
+// lane.
 template <int D, int kWaves>
 __device__ __forceinline__ void step_dma(const uint16_t* kb, const uint16_t* vb, int t0, int wave, int lane,
                                          uint8_t* kl, uint8_t* vl) {
     constexpr int STEPB = 32 * D * 2;
-    constexpr int NDMA = STEPB / 1024 / kWaves;
+    constexpr int NKB = STEPB / 1024;     // KB of K (and of V) per step
     constexpr int RPK = 1024 / (D * 2);   // K rows per KB
     constexpr int CPR = D / 8;            // 16-byte chunks per row
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) {
-        const int kb_ = wave * NDMA + j;
+    for (int j = 0; j < (NKB + kWaves - 1) / kWaves; ++j) {
+        const int kb_ = wave + kWaves * j;
+        if (kb_ >= NKB) break;
         const int r = kb_ * RPK + lane / CPR;
         const int c = (lane % CPR) ^ kswz<D>(r);
         lds_dma16(kb + static_cast<size_t>(t0 + r) * D + 8 * c, kl + kb_ * 1024);
@@ -302,8 +304,8 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
 
 
 // ---------------------------------------------------------------------------
-// Prefill / scoring attention: a 4-wave workgroup shares each K/V step
-// through LDS.  Per 32-position step the workgroup DMAs the step's K rows
+// Prefill / scoring attention: a workgroup of kPrefillWaves waves shares each
+// K/V step through LDS.  Per 32-position step the workgroup DMAs the step's K rows
 // ([32][D], 16-byte chunks permuted by row so that the fragment reads below
 // are free of bank conflicts) and its four V blocks ([4][D][8], contiguous in
 // the cache) into one of two LDS buffers with global_load_lds; every wave
@@ -313,13 +315,12 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
 // ---------------------------------------------------------------------------
 
 template <int D>
-__global__ void __launch_bounds__(256, 2) attn_prefill_kernel(const PrefillTile* __restrict__ tiles,
+__global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const PrefillTile* __restrict__ tiles,
         const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int S,
         int Hq, int Hkv, int cap, int layer, float scale_log2, uint16_t* __restrict__ out) {
     constexpr int KG = D / 32, DT = D / 16;
     constexpr int STEPB = 32 * D * 2;               // bytes of K (and of V) per 32-position step
-    constexpr int NDMA = STEPB / 1024 / kPrefillWaves;   // 1 KB DMA instructions per wave per step, K and V each
-    static_assert(NDMA >= 1 && NDMA * kPrefillWaves * 1024 == STEPB, "step split over the waves");
+    static_assert(STEPB % 1024 == 0, "whole 1 KB DMA instructions per step");
     __shared__ __attribute__((aligned(1024))) uint8_t lds[2][2][STEPB];   // [buffer][K | V]
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -138,7 +138,7 @@ struct PrefillTile {
     int32_t slot;
     int32_t pos0;
 };
-constexpr int kPrefillWaves = 4;
+constexpr int kPrefillWaves = 8;
 
 // One 4-wave workgroup per (tile, kv-head): each 32-position K/V step is
 // loaded once into LDS and used by every wave (wave w takes the tile's tokens
