@@ -402,74 +402,51 @@ hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const
 }
 
 // Merge the split partials of one query block and q-head: one workgroup per
-// (split block, q-head), one thread per d, the block's tokens in turn.  Each
-// thread loads every item's (m, l) itself (broadcast reads) together with its
-// own column of the partial outputs, so up to 8 items take one memory round
-// trip and no workgroup barrier; more items take a max pass and then groups
-// of 8.  Weights 2^(m_j - M) (M: the token's max), sums in item order.
+// (split block, q-head), one thread per d, the block's tokens in turn.  Lane
+// j of each wave loads item j's (m, l) (at most 64 items), the token's max
+// comes from a wave reduction, and each thread sums its own column of the
+// partial outputs in item order, 8 loads in flight at a time, reading the
+// items' (m, l) from their lanes.  Weights 2^(m_j - M).
 template <int D>
 __global__ void __launch_bounds__(D) attn_combine_kernel(const int32_t* __restrict__ blocks,
         const AttnItem* __restrict__ items, const float* __restrict__ part, int Hq, int Hkv,
         uint16_t* __restrict__ out) {
+    static_assert(kMaxCombine <= 64, "one item per lane");
     const AttnItem it = items[blocks[blockIdx.x]];
     const int h = blockIdx.y;
     const int G = Hq / Hkv;
     const int kvh = h / G, g = h - kvh * G;
     const int np = it.nparts;
-    const int d = threadIdx.x;
+    const int d = threadIdx.x, lane = threadIdx.x & 63;
     const size_t pstride = static_cast<size_t>(Hkv) * 16 * (D + 2);
     const float* pb0 = part + (static_cast<size_t>(it.part0) * Hkv + kvh) * 16 * (D + 2);
+    auto lane_f = [](float v, int src) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), src));
+    };
     for (int t = 0; t < it.nq; ++t) {
         const float* pc = pb0 + static_cast<size_t>(t * G + g) * (D + 2);
+        const float mv = lane < np ? pc[lane * pstride + D] : -INFINITY;
+        const float lv = lane < np ? pc[lane * pstride + D + 1] : 0.0f;
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (u < np) v[u] = pc[u * pstride + d];
+        float M = mv;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
         float acc = 0.0f, L = 0.0f;
-        if (np <= 8) {
-            float m[8], l[8], v[8];
+        for (int j = 0; j < np; j += 8) {
+            if (j > 0) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (u < np) {
-                    m[u] = pc[u * pstride + D];
-                    l[u] = pc[u * pstride + D + 1];
-                    v[u] = pc[u * pstride + d];
-                }
+                for (int u = 0; u < 8; ++u)
+                    if (j + u < np) v[u] = pc[(j + u) * pstride + d];
             }
-            float M = -INFINITY;
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (u < np) M = fmaxf(M, m[u]);
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                if (u < np) {
-                    const float w = exp2f(m[u] - M);
-                    L += w * l[u];
+                if (j + u < np) {
+                    const float w = exp2f(lane_f(mv, j + u) - M);
+                    L += w * lane_f(lv, j + u);
                     acc += w * v[u];
-                }
-            }
-        } else {
-            float M = -INFINITY;
-            for (int j = 0; j < np; j += 16) {
-                float m[16];
-#pragma unroll
-                for (int u = 0; u < 16; ++u) m[u] = j + u < np ? pc[(j + u) * pstride + D] : -INFINITY;
-#pragma unroll
-                for (int u = 0; u < 16; ++u) M = fmaxf(M, m[u]);
-            }
-            for (int j = 0; j < np; j += 8) {
-                float m[8], l[8], v[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    if (j + u < np) {
-                        m[u] = pc[(j + u) * pstride + D];
-                        l[u] = pc[(j + u) * pstride + D + 1];
-                        v[u] = pc[(j + u) * pstride + d];
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    if (j + u < np) {
-                        const float w = exp2f(m[u] - M);
-                        L += w * l[u];
-                        acc += w * v[u];
-                    }
                 }
             }
         }
