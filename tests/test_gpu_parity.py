@@ -121,6 +121,29 @@ def test_sampler_matches_oracle_on_given_logits():
     eng.close()
 
 
+def test_sampler_single_chunk_rows_match_oracle():
+    """From 2048 rows each row's vocabulary is one chunk: the sampling
+    workgroup finishes the row itself (no merge kernel)."""
+    shape = WORKLOADS["tiny"].model
+    w_dev, _, _ = build_models(shape, 4)
+    n, V = 2048, shape.vocab
+    eng = Engine(shape, w_dev, max_seqs=n, max_ctx=16, max_prefill_tokens=16)
+    rng = np.random.default_rng(1)
+    z = rng.normal(0, 2.0, size=(n, V)).astype(np.float32)
+    uids = [int(u) for u in rng.integers(0, 2 ** 63, size=n, dtype=np.int64)]
+    pos = [int(p) for p in rng.integers(0, 5000, size=n)]
+    out_tok = torch.empty(n, dtype=torch.int32, device=DEV)
+    out_lp = torch.empty(n, dtype=torch.float32, device=DEV)
+    eng.sample_logits(torch.from_numpy(z).to(DEV), uids, pos, out_tok, out_lp, seed=77, temperature=0.8)
+    torch.cuda.synchronize()
+    gt, gl = out_tok.cpu().numpy(), out_lp.cpu().numpy()
+    for i in range(0, n, 7):
+        ot, ol = oracle.sample(z[i], 0.8, 77, uids[i], pos[i])
+        assert gt[i] == ot, i
+        assert abs(gl[i] - ol) < 1e-5, (i, gl[i], ol)
+    eng.close()
+
+
 def test_tiny_fp32_rollout_bit_exact_tokens():
     """The tiny fp32 workload end to end: 2 prompts x 4 samples, 32 prompt
     tokens, 32 generated tokens, seeded Gumbel noise at T = 1.  Every GPU token
