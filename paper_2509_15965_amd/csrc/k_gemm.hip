@@ -38,7 +38,6 @@ constexpr TileKernel kLineTiles[] = {   // ties go to the earlier entry (weights
     {kLineVariant128x128, 128, 128, 2, 20.3, 15.0},
     {kLineVariant128x256, 128, 256, 1, 19.5, 19.5},
     {kLineVariant128x128Deep, 128, 128, 1, 12.0, 12.0},
-    {kLineVariant128x128W8, 128, 128, 1, 10.8, 10.8},   // no SwiGLU epilogue
 };
 constexpr int kCUs = 256;
 
@@ -144,7 +143,6 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     }
     const double fixed = M <= 64 ? 5.0 : 0.0;
     for (const TileKernel& t : kLineTiles) {
-        if (t.variant == kLineVariant128x128W8 && epi == EPI_SWIGLU) continue;
         const long tiles = tiles_of(t, M, n_out, epi);
         for (int s = 1; s <= kMaxSplits; s *= 2) {
             const int ks = ceil_div(ceil_div(K, s), 64) * 64;
@@ -194,7 +192,6 @@ bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPl
             case RL_GEMM_T128X256: return kLineVariant128x256;
             case RL_GEMM_T128: return kLineVariant128x128;
             case RL_GEMM_T128_DEEP: return kLineVariant128x128Deep;
-            case RL_GEMM_T128_W8: return kLineVariant128x128W8;
             default: return -1;
         }
     };
@@ -227,13 +224,12 @@ bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPl
     }
     const int v1 = tile(k1);
     if (v1 < 0 || K % 64 != 0) return false;
-    if (v1 == kLineVariant128x128W8 && epi == EPI_SWIGLU) return false;
     p.variant = v1;
     p.splits = 1;
     p.ksplit = K;
     if (k2 != 0) {
         const int v2 = tile(k2);
-        if (v2 < 0 || (v2 == kLineVariant128x128W8 && epi == EPI_SWIGLU)) return false;
+        if (v2 < 0) return false;
         const int w = out_width(v1);
         const int n_split = (n_out / 2) / w * w;
         if (n_split <= 0) return false;

@@ -442,8 +442,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
     constexpr int ASTAGE = BM * ROWB, BSTAGE = BN * ROWB;
     constexpr int AQ = BM / (8 * NW), BQ = BN / (8 * NW);   // DMA instructions (8 rows each) per wave per stage
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows must fill whole DMA instructions");
-    static_assert(TM % 32 == 0 && TN % 32 == 0 && (EPI != EPI_SWIGLU || TN % 64 == 0),
-                  "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
+    static_assert(TM % 32 == 0 && TN % 64 == 0, "wave tile must hold whole 32x32 tiles (and gate/up pairs)");
     static_assert(SA >= 2 && SW >= 2 && SA <= 6 && SW <= 6, "ring depths");
     constexpr int SMAX = SA > SW ? SA : SW;   // the prologue covers iterations -SMAX .. -1
     static_assert(SA * AQ + SW * BQ < 64, "vmcnt range (most loads ever in flight)");
@@ -690,23 +689,17 @@ hipError_t launch_dma128(const GemmArgs& a, const GemmPlan& p, int n0, int n1, h
     const int ntx = (n_tiles + 7) / 8;
     const int groups = (m_tiles + gm - 1) / gm;
     dim3 grid(8 * ntx * groups * gm, p.splits), block(64 * NW);
-    constexpr bool kSwiglu = (BN / (NW / WM)) % 64 == 0;   // wave tiles hold gate/up pairs
-    if (!kSwiglu && a.epi == EPI_SWIGLU) return hipErrorInvalidValue;
     if (p.splits > 1) {
-        if constexpr (kSwiglu) {
-            if (a.epi == EPI_SWIGLU) {
-                hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
-                return hipGetLastError();
-            }
-        }
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        if (a.epi == EPI_SWIGLU)
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        else
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_F32) {
         hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else if (a.epi == EPI_RESID) {
         hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     } else {
-        if constexpr (kSwiglu)
-            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
     }
     return hipGetLastError();
 }
@@ -769,7 +762,6 @@ hipError_t launch_tile_variant(int variant, const GemmArgs& a, const GemmPlan& p
         case kLineVariant128x128: return launch_dma128<128, 128, 2, 4, 2, 3>(a, p, n0, n1, s);
         case kLineVariant128x256: return launch_dma128<128, 256, 2, 8, 3, 3>(a, p, n0, n1, s);
         case kLineVariant128x128Deep: return launch_dma128<128, 128, 2, 4, 4, 4>(a, p, n0, n1, s);
-        case kLineVariant128x128W8: return launch_dma128<128, 128, 2, 8, 4, 4>(a, p, n0, n1, s);
         default:   // register-staged tiles cover the whole output only
             if (n0 != 0) return hipErrorInvalidValue;
             return variant == kLdsVariant256 ? launch_tile<256, 128>(a, p, s) : launch_tile<128, 128>(a, p, s);

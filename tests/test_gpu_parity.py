@@ -13,8 +13,8 @@ from harness import (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL, LOGIT_REL_TOL, LOGP_AB
 from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 from paper_2509_15965_amd.inputs import rollout_plan, uniform_tokens
 from paper_2509_15965_amd.rl_decode import (RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T128, RL_GEMM_T128_DEEP,
-                                           RL_GEMM_T128_W8, RL_GEMM_T128X256, RL_GEMM_T256, RL_OPT_ATTN_CHUNK,
-                                           RL_OPT_GEMM_PLAN, Engine, gemm_plan_code)
+                                           RL_GEMM_T128X256, RL_GEMM_T256, RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN,
+                                           Engine, gemm_plan_code)
 
 pytestmark = pytest.mark.gpu
 
@@ -341,8 +341,6 @@ _FORCED_PLANS = [
     ("t128x256_s2", gemm_plan_code(RL_GEMM_T128X256, 2)),
     ("t128", gemm_plan_code(RL_GEMM_T128)),
     ("t128deep_s8", gemm_plan_code(RL_GEMM_T128_DEEP, 8)),
-    ("t128w8", gemm_plan_code(RL_GEMM_T128_W8)),          # gate|up keeps the planner's kernel
-    ("t128w8_s4", gemm_plan_code(RL_GEMM_T128_W8, 4)),
     ("t256+t128", gemm_plan_code(RL_GEMM_T256, 0, RL_GEMM_T128)),
     ("t256+t128x256", gemm_plan_code(RL_GEMM_T256, 0, RL_GEMM_T128X256)),
     ("t128x256+t128deep", gemm_plan_code(RL_GEMM_T128X256, 0, RL_GEMM_T128_DEEP)),
