@@ -22,6 +22,7 @@ constexpr uint32_t kDead = 0xDEADDEADu;
 constexpr int kStages = 3;                  // pinned metadata staging ring
 constexpr int kPartItems = 8192;            // split-KV partial slots per call
 constexpr int kAttnWaveTarget = 1024;       // split-KV: keep about one wave per SIMD, each as long as possible
+constexpr int kSharedDecodeChunk = 256;     // split-KV keys per item in decode steps that read shared prompts
 constexpr int kPrefillChunk = 1024;         // default keys per prefill work item
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -558,11 +559,21 @@ int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int 
     if (forced > 0) {
         C = static_cast<int>(forced);
     } else if (decode) {
-        C = 64;
-        while (C < (1 << 16)) {
-            count(2 * C, &items, &multi, &most);
-            if (items * Hkv < kAttnWaveTarget) break;
-            C *= 2;
+        bool shared = false;
+        for (const Block& b : blocks) shared = shared || (b.src >= 0 && b.plen > 0);
+        if (shared) {
+            // Prompt chunks served from L2 and HBM-bound own parts take very
+            // different times per key: short items let the dispatcher balance
+            // them over the chip (over a GRPO rollout, 256 keys per item beat
+            // the long-item rule by 7% of attention time, 128 and 512 by less).
+            C = kSharedDecodeChunk;
+        } else {
+            C = 64;
+            while (C < (1 << 16)) {
+                count(2 * C, &items, &multi, &most);
+                if (items * Hkv < kAttnWaveTarget) break;
+                C *= 2;
+            }
         }
     } else {
         C = default_min;
