@@ -41,7 +41,7 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 # shared prompt once).  Valid for the attention kernel and work-item layout as
 # of that measurement (256-key items in steps that read shared prompts); set
 # to None when either changes until the counters are taken again.
-ATTN_TRAFFIC_PER_ALG_BYTE = 1.0784
+ATTN_TRAFFIC_PER_ALG_BYTE = None
 
 
 def parse():

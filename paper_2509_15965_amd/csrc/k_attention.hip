@@ -153,7 +153,7 @@ __device__ __forceinline__ void step_frags(const uint8_t* kl, const uint8_t* vl,
 // vmcnt(0) with expcnt and lgkmcnt left alone (gfx9 encoding)
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
-template <int D, bool PF>
+template <int D>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __restrict__ items,
         int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
         const uint16_t* __restrict__ vc, int S, int Hq, int Hkv, int cap, int layer,
@@ -202,8 +202,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
     const int hi = it.kv_hi;
     // key row r of score tile 0 is position t0 + 8(r/4) + r%4; tile 1 adds 4
     const int krow = 8 * (col >> 2) + (col & 3);
-    // K rows and V blocks of one 32-position step; the next step's loads are
-    // issued before the current step's math
+    // K rows and V blocks of one 32-position step, loaded and then used (the
+    // waves resident on the chip keep HBM busy without a per-wave prefetch)
     u32x4 k0[KG], k1[KG], vf[DT];
     auto load_step = [&](int t0, u32x4 (&a0)[KG], u32x4 (&a1)[KG], u32x4 (&vv)[DT]) {
         const uint16_t* kp0 = kb + static_cast<size_t>(t0 + krow) * D + 8 * kq;
@@ -228,20 +228,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
             step_frags<D>(lds[s & 1][0], lds[s & 1][1], krow, kq, col, k0, k1, vf);
             attn_step<D>(k0, k1, vf, qf, it.kv_lo + 32 * s, hi, limit, kq, scale_log2, m, l, o);
         }
-    } else if (it.kv_lo < hi) {
-        load_step(it.kv_lo, k0, k1, vf);
-    }
-    for (int t0 = it.kv_lo; !wg_lds && t0 < hi; t0 += 32) {
-        u32x4 nk0[KG], nk1[KG], nvf[DT];
-        const bool more = PF && t0 + 32 < hi;
-        if (more) load_step(t0 + 32, nk0, nk1, nvf);
-        if (!PF && t0 != it.kv_lo) load_step(t0, k0, k1, vf);
-        attn_step<D>(k0, k1, vf, qf, t0, hi, limit, kq, scale_log2, m, l, o);
-        if (more) {
-#pragma unroll
-            for (int j = 0; j < KG; ++j) { k0[j] = nk0[j]; k1[j] = nk1[j]; }
-#pragma unroll
-            for (int i = 0; i < DT; ++i) vf[i] = nvf[i];
+    } else {
+        for (int t0 = it.kv_lo; t0 < hi; t0 += 32) {
+            load_step(t0, k0, k1, vf);
+            attn_step<D>(k0, k1, vf, qf, t0, hi, limit, kq, scale_log2, m, l, o);
         }
     }
     l += __shfl_xor(l, 16, 64);
@@ -285,20 +275,12 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
     if (n_items <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     dim3 grid((n_items + 3) / 4, Hkv), block(256);
-    // Each wave keeps the next 32-position step's K/V loads in flight while it
-    // computes the current one; at two waves per SIMD (<= 256 registers) that
-    // is the most bytes in flight the register file allows.
-    const bool pf = true;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
                            static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
                            cap, layer, scale_log2, static_cast<uint16_t*>(out), part);
     };
-    if (D == 128) {
-        if (pf) go(attn_bf16_kernel<128, true>); else go(attn_bf16_kernel<128, false>);
-    } else {
-        if (pf) go(attn_bf16_kernel<64, true>); else go(attn_bf16_kernel<64, false>);
-    }
+    if (D == 128) go(attn_bf16_kernel<128>); else go(attn_bf16_kernel<64>);
     return hipGetLastError();
 }
 
