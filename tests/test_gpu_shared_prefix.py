@@ -41,13 +41,13 @@ class Run:
     """GPU engine plus oracle sequences keyed by slot, stepped together with
     seeded forced tokens; every step is compared with the oracle."""
 
-    def __init__(self, shared: int, chunk: int = 0):
+    def __init__(self, shared: int, chunk: int = 0, max_ctx: int = 160, max_prefill: int = 256):
         self.w_dev, _, self.om = build_models(GQA, 51)
-        self.eng = Engine(GQA, self.w_dev, max_seqs=10, max_ctx=160, max_prefill_tokens=256)
+        self.eng = Engine(GQA, self.w_dev, max_seqs=10, max_ctx=max_ctx, max_prefill_tokens=max_prefill)
         self.eng.set_option(RL_OPT_SHARED_PREFIX, shared)
         if chunk:
             self.eng.set_option(RL_OPT_ATTN_CHUNK, chunk)
-        self.orc = OracleRollout(self.om, 160)
+        self.orc = OracleRollout(self.om, max_ctx)
         self.step_no = 0
         self.errs = []
 
@@ -106,6 +106,21 @@ def test_shared_prompt_through_leader_reuse(shared, chunk):
     r.eng.release([9])
     for _ in range(2):
         r.step([6, 0, 4])
+    r.eng.close()
+
+
+def test_shared_prompt_longer_than_one_item():
+    """Prompts longer than the 256-key items that decode steps over shared
+    prompts use by default: each group's prompt part spans several pair items
+    (the last one partial), the own part starts inside a 32-position step, and
+    the combine merges up to four partials per row."""
+    rng = np.random.default_rng(55)
+    pr = [rng.integers(0, GQA.vocab, size=n).astype(np.int32) for n in (600, 290)]
+    r = Run(1, max_ctx=640, max_prefill=1024)
+    r.prefill(list(range(8)), pr, group=4)
+    for _ in range(3):
+        r.step(list(range(8)))
+    r.step([5, 1, 6, 2])
     r.eng.close()
 
 
