@@ -323,10 +323,14 @@ rl_status rl_decode_rebind(rl_decode_ctx* ctx, const rl_weights* w, void* kv_poo
  * ------------------------------------------------------------------- */
 
 typedef enum rl_option {
-    RL_OPT_ATTN_CHUNK = 1,   /* positions per split-KV chunk: 0 = automatic,
-                                else a multiple of 32 in [32, 65536]; doubled
-                                as needed so no sequence has more than 64
-                                chunks                                         */
+    RL_OPT_ATTN_CHUNK = 1,   /* positions per split-KV chunk: 0 = automatic
+                                (decode steps that read shared prompts: 256;
+                                other decode steps: the largest power of two
+                                that still gives about 1024 work items;
+                                prefill and scoring: 1024), else a multiple of
+                                32 in [32, 65536]; doubled as needed so no
+                                sequence has more than 64 chunks and the work
+                                items fit the workspace                        */
     RL_OPT_PROFILE = 2,      /* bit mask over rl_kernel_class: launches of the
                                 selected classes are timed with HIP events on
                                 the context's stream; 0 = off (default),
