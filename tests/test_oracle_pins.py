@@ -167,6 +167,44 @@ def test_uniform_logits_uniform_frequencies():
     assert float(((counts - e) ** 2 / e).sum()) < 31.3   # 7 dof, p = 1e-4
 
 
+def test_sample_margin_hand_cases():
+    """Top-two perturbed scores of a draw (what excuses a near-tie token flip
+    in fp32 parity): at T = 0 the scores are the logits themselves, so the
+    best, runner-up and margin are read off by hand."""
+    cases = [
+        ([0.5, 3.0, -1.0, 2.0], (1, 3, 1.0)),
+        ([0.5, 3.0, -1.0, 3.0], (1, 3, 0.0)),      # exact tie: lowest index first, the other second
+        ([4.0, 1.0, 2.0], (0, 2, 2.0)),             # runner-up found after the best
+        ([1.0, 2.0, 3.0], (2, 1, 1.0)),             # each new best pushes the old one to second
+        ([-2.0, -2.0], (0, 1, 0.0)),
+    ]
+    for z, exp in cases:
+        assert oracle.sample_margin(np.array(z, dtype=np.float32), 0.0, 1, 2, 3) == exp, z
+
+
+@pytest.mark.parametrize("T", [1.0, 0.6])
+def test_sample_margin_matches_sorted_scores(T):
+    """With noise: the perturbed scores fl32(fl32(z/T) + g_v) formed here in
+    NumPy from the noise words, sorted by (score desc, index asc); the top two
+    and their fp64 difference equal sample_margin, and its best is the
+    sampler's token."""
+    rng = np.random.default_rng(33)
+    for trial in range(40):
+        V = int(rng.integers(2, 400))
+        z = rng.normal(0, 2, size=V).astype(np.float32)
+        if trial % 4 == 0:
+            z[:] = np.float32(0.25)                   # equal logits: the noise decides alone
+        seed, uid, pos = 1000 + trial, 7 * trial, trial % 5
+        g = np.array([oracle.gumbel_of_word(oracle.noise_word(seed, uid, pos, v)) for v in range(V)],
+                     dtype=np.float32)
+        sc = (z / np.float32(T)).astype(np.float32) + g
+        order = np.lexsort((np.arange(V), -sc.astype(np.float64)))
+        a, b, m = oracle.sample_margin(z, T, seed, uid, pos)
+        assert (a, b) == (int(order[0]), int(order[1]))
+        assert m == float(sc[order[0]]) - float(sc[order[1]])
+        assert a == oracle.sample(z, T, seed, uid, pos)[0]
+
+
 def test_noise_depends_on_uid_and_position():
     z = np.zeros(512, dtype=np.float32)
     a = [oracle.sample(z, 1.0, 1, uid, 0)[0] for uid in range(8)]
@@ -323,6 +361,44 @@ def test_kv_cached_decode_equals_recompute(mode, dtype):
         for t in toks[:k]:
             last = fresh.forward(t)
         assert np.array_equal(last, inc[k - 1])
+
+
+MHA = ModelShape(1, 48, 3, 3, 16, 80, 96, 1e-5, 1e4, "fp32")
+MQA = ModelShape(2, 64, 8, 1, 8, 64, 64, 1e-6, 1e6, "fp32")
+
+
+def test_bruteforce_round_bf16_matches_torch():
+    """The brute force's own bf16 rounding (frexp/rint) against torch's
+    fp32 -> bf16 conversion on fp32-exact values, ties and subnormals included."""
+    from bruteforce import round_bf16
+    rng = np.random.default_rng(30)
+    x = rng.normal(0, 10, size=20000).astype(np.float32)
+    x[:10] = [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 3.0e38, -7.5e-39, 1e-40, 0.0, 2.0 ** -130,
+              65504.0, 255.5]
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(round_bf16(x.astype(np.float64)), ref)
+
+
+@pytest.mark.parametrize("shape", [SMALL, MHA, MQA], ids=["gqa", "mha", "mqa"])
+@pytest.mark.parametrize("mode,dtype,bmode", [(oracle.MODE_FP32, "fp32", "fp32"), (oracle.MODE_BF16, "bf16", "bf16")],
+                         ids=["fp32", "bf16"])
+def test_storage_modes_equal_bruteforce_with_same_rounding(shape, mode, dtype, bmode):
+    """The oracle's storage modes against the brute-force full-sequence
+    forward that rounds at the same declared sites (normed projection inputs,
+    q and k after RoPE, v, attention output, SwiGLU product; fp32 residual
+    and logits), written independently in NumPy.  Both accumulate in fp64, so
+    they agree to fp64 round-off; a storage rounding missing on either side
+    moves the logits by about one storage ulp (~1e-3 in bf16, ~1e-7 in fp32)."""
+    m, w, s = small_model(mode, dtype, seed=31, shape=shape)
+    toks = [int(t) for t in np.random.default_rng(32).integers(0, s.vocab, size=24)]
+    seq = m.new_seq(32)
+    inc = np.stack([seq.forward(t) for t in toks])
+    ref = forward_all(s.as_dict(), w, toks, mode=bmode)
+    scale = np.abs(ref).max()
+    assert np.abs(inc - ref).max() / scale < 1e-10
+    # the rounding is visible at this size: the fp64 forward differs
+    ref64 = forward_all(s.as_dict(), w, toks, mode="fp64")
+    assert np.abs(ref - ref64).max() / scale > (1e-4 if dtype == "bf16" else 1e-8)
 
 
 def test_storage_rounding_is_small_against_fp64():
