@@ -8,15 +8,23 @@ o-projection / SwiGLU MLP, final norm, LM head, log-softmax + Gumbel-max
 sampling + log-probability) over the sequences still generating.  The
 workload is the GRPO rollout of 32 prompts x 16 samples (uniform prompt
 lengths in [256, 1024], lognormal response lengths around 1500 capped at
-4096) on a randomly initialised bf16 decoder; by default every decode step of
-the rollout is timed (K = longest response - 1), after W warm-up steps of a
-separate warm-up rollout.  Inputs and weights are resident in HBM before
-timing starts; the prefill that opens the rollout is timed and reported
-separately.
+4096) on a randomly initialised bf16 decoder.
 
-Prints one JSON line: generated tokens/s over the timed steps, the roofline
-of the dominant kernel measured with HIP events on the library's stream, and
-the CPU oracle timed on a bounded sample on this host.
+After W warm-up steps of a separate rollout, the whole rollout runs twice.
+The first pass is the measurement: nothing is instrumented, and K decode
+steps spread evenly over the rollout (every step with K = 0) are each timed
+between device synchronisations; the whole pass is timed as well.  `value`
+is the generated tokens of the K steps over their wall time.  The second pass
+times the kernel classes with HIP events on the library's stream during the
+same K steps, for the roofline of the dominant kernel.  Inputs and weights
+are resident in HBM before timing starts; the prefill that opens the rollout
+is timed and reported separately.
+
+Prints one JSON line: generated tokens/s over the timed steps, their
+algorithmic HBM GB/s (nominal: every row's whole context; unique: each GRPO
+group's shared prompt once) with the fraction of the 8 TB/s peak, the same
+time-weighted over the whole rollout, the roofline of the dominant kernel,
+and the CPU oracle timed on a bounded sample on this host.
 """
 import argparse
 import json
@@ -47,7 +55,9 @@ ATTN_TRAFFIC_PER_ALG_BYTE = 1.0913
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=0, help="decode steps to time (0 = the whole rollout)")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="rollout: decode steps to time, spread evenly over the whole rollout (default 32, 0 = "
+                         "every step); score: GRPO groups (default 4); switch: rounds (default 3)")
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="qwen7b")
     ap.add_argument("--slots", type=int, default=256, help="--stage continuous: KV slots (sequences in flight)")
@@ -59,9 +69,7 @@ def parse():
                          "continuous: the rollout's 512 sequences through fewer slots, continuous batching "
                          "with chunked emission against static batches of the same size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--breakdown", action="store_true",
-                    help="time every kernel class (adds event overhead; diagnostics only)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run the library's plain copy kernel over this many MiB, 4 times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters against a known size)")
@@ -81,32 +89,6 @@ def copy_probe(mib: int):
     torch.cuda.synchronize()
     assert torch.equal(dst, src)
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 4}), flush=True)
-
-
-def cpu_baseline(shape, weights, seconds: float):
-    """Oracle decode tokens/s on this host's cores: one new token per sequence
-    at the rollout's mean starting context, until `seconds` have elapsed."""
-    import oracle
-    from paper_2509_15965_amd.inputs import weights_to_host
-    cores = len(os.sched_getaffinity(0))
-    oracle.set_threads(cores)
-    host = weights_to_host(weights)
-    om = oracle.OracleModel(shape.as_dict(), host, oracle.MODE_BF16)
-    ctx = 640
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        s = om.new_seq(ctx + 1)
-        s.set_length(ctx)            # cache rows are zeros: the arithmetic per token is the same
-        s.forward(1 + n)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or n >= 256:
-            break
-    del om, host
-    return {"value": n / el, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{n} decode tokens of the 7B-shape decoder at context {ctx + 1} "
-                      f"(one token per sequence, fp64 accumulation), {el:.1f} s"}
 
 
 def cpu_baseline_score(shape, weights, seconds: float):
@@ -173,7 +155,7 @@ def score_main(args):
     torch.cuda.set_device(dev)
     plan = rollout_plan(wl)
     G = wl.group
-    steps = args.steps if args.steps > 0 else 4
+    steps = args.steps if args.steps else 4
     warm = max(0, min(args.warmup, 1))
     n_groups = min(wl.n_prompts, steps + warm)
     plens, resp = plan["prompt_lens"], plan["response_lens"]
@@ -188,7 +170,7 @@ def score_main(args):
                        "resp": torch.as_tensor(rt, device=dev),
                        "out": torch.empty(int(rl.sum()), dtype=torch.float32, device=dev),
                        "tokens": int(plens[p] + rl.sum()), "scored": int(rl.sum())})
-    weights = make_weights(shape, wl.seed, device=dev)
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     max_ctx = max(int(plens[p] + resp[p * G:(p + 1) * G].max()) for p in range(n_groups))
     max_tok = max(g["tokens"] for g in groups)
     eng = Engine(shape, weights, max_seqs=G, max_ctx=max_ctx, max_prefill_tokens=max_tok, device=dev)
@@ -288,7 +270,7 @@ def switch_main(args):
     P, G = wl.n_prompts, wl.group
     n = P * G
     plens = plan["prompt_lens"]
-    weights = make_weights(shape, wl.seed, device=dev)
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     eng = Engine(shape, weights, max_seqs=n, max_ctx=int(plens.max() + plan["response_lens"].max()),
                  max_prefill_tokens=int(plens.sum()), device=dev)
     slots = np.arange(n, dtype=np.int32)
@@ -305,7 +287,7 @@ def switch_main(args):
     stream = eng.stream
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
     res = []
-    reps = max(1, args.steps if args.steps > 0 else 3)
+    reps = max(1, args.steps if args.steps else 3)
     for r in range(reps + 1):
         torch.cuda.synchronize()
         ev[0].record(stream)
@@ -380,7 +362,7 @@ def continuous_main(args):
     if S % G or S < G:
         raise SystemExit("--slots must be a multiple of the group size")
     plens, resp, uids = plan["prompt_lens"], plan["response_lens"], plan["uids"]
-    weights = make_weights(shape, wl.seed, device=dev)
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     per = S // G                                          # prompts per static batch
     eng = Engine(shape, weights, max_seqs=S, max_ctx=int(plens.max() + resp.max()),
                  max_prefill_tokens=int(max(plens[i:i + per].sum() for i in range(0, P, per))), device=dev)
@@ -441,6 +423,103 @@ def continuous_main(args):
     print(json.dumps(out), flush=True)
 
 
+def rollout_step_bytes(shape, plens, resp, group, steps):
+    """Algorithmic HBM bytes of every decode step of a static rollout (the
+    sequences ordered longest first, decode step t appending position
+    plen + t): the decode-read parameters, every active row's K/V context and
+    new K/V row, its embedding row and 12 bytes of token / log-probability.
+    Returns (nominal, unique): nominal counts every row's whole context;
+    unique counts each GRPO group's shared prompt (whole 32-position steps,
+    as the attention reads it) once per step while any member is active."""
+    import numpy as np
+    es = shape.elem_bytes
+    kv_tok = shape.kv_bytes_per_token()
+    fixed = shape.decode_params() * es
+    plens = np.asarray(plens, dtype=np.int64)
+    resp = np.asarray(resp, dtype=np.int64)
+    n_seq = len(resp)
+    seq_plen = np.repeat(plens, group)
+    grp = np.arange(n_seq) // group
+    shared = seq_plen // 32 * 32
+    nominal = np.zeros(steps)
+    unique = np.zeros(steps)
+    for t in range(steps):
+        act = resp > t + 1
+        n = int(act.sum())
+        ctx = seq_plen[act] + t + 1
+        per_row = n * (kv_tok + shape.hidden * es + 12)
+        nominal[t] = fixed + per_row + float(ctx.sum()) * kv_tok
+        own = ctx - (shared[act] if group > 1 else 0)
+        groups_live = np.unique(grp[act]) if group > 1 else np.array([], dtype=np.int64)
+        prompt_once = float(shared[groups_live * group].sum()) if group > 1 else 0.0
+        unique[t] = fixed + per_row + (float(own.sum()) + prompt_once) * kv_tok
+    return nominal, unique
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline_rollout(shape, weights, seconds: float):
+    """Oracle decode tokens/s on this host: one new token per sequence at
+    the 7B rollout's mean starting context (641), with a seeded N(0, 1) K/V
+    cache of 640 positions, first on all host cores, then on one thread."""
+    import numpy as np
+
+    import oracle
+    from paper_2509_15965_amd.inputs import weights_to_host
+    cores = len(os.sched_getaffinity(0))
+    host = weights_to_host(weights)
+    om = oracle.OracleModel(shape.as_dict(), host, oracle.MODE_BF16)
+    ctx = 640
+    rng = np.random.default_rng(11)
+    base = om.new_seq(ctx + 1)
+    for l in range(shape.n_layers):
+        for g in range(shape.n_kv_heads):
+            K = rng.standard_normal((ctx, shape.head_dim))
+            V = rng.standard_normal((ctx, shape.head_dim))
+            base.set_kv_block(l, g, K, V)
+    base.set_length(ctx)
+
+    def timed(threads, budget, cap):
+        oracle.set_threads(threads)
+        n, el = 0, 0.0
+        while el < budget and n < cap:
+            s = base.clone()
+            t0 = time.perf_counter()
+            s.forward(1 + n)
+            el += time.perf_counter() - t0
+            n += 1
+            del s
+        return n, el, oracle.num_threads()
+
+    n, el, used = timed(cores, seconds, 256)
+    n1, el1, _ = timed(1, max(1.0, seconds * 0.6), 2)
+    del om, host, base
+    return {"value": round(n / el, 4), "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": f"{n} decode tokens of the 7B-shape decoder at context {ctx + 1} (seeded N(0,1) K/V "
+                      f"cache, one token per sequence, fp64 accumulation) in {el:.1f} s on {used} threads; "
+                      f"single thread: {n1} tokens in {el1:.1f} s",
+            "single_thread_value": round(n1 / el1, 4), "cpu_model": cpu_model()}
+
+
+def sample_steps(max_steps: int, k: int):
+    """k decode steps spread evenly over the rollout (all steps when k <= 0
+    or k >= max_steps)."""
+    if k <= 0 or k >= max_steps:
+        return list(range(max_steps))
+    if k == 1:
+        return [0]
+    return sorted({round(j * (max_steps - 1) / (k - 1)) for j in range(k)})
+
+
 def main():
     args = parse()
     if args.copy_probe_mib > 0:
@@ -475,7 +554,7 @@ def main():
     n_seq = P * G
     plens = plan["prompt_lens"]
     resp = plan["response_lens"]
-    weights = make_weights(shape, wl.seed, device=dev)
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     max_ctx = int(plens.max() + resp.max())
     eng = Engine(shape, weights, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=int(plens.sum()),
                  device=dev)
@@ -486,111 +565,145 @@ def main():
     seed, T = 20250919, wl.temperature
     ro = StaticRollout(eng, plan["prompts"], G, resp, plan["uids"], seed=seed, temperature=T)
     max_steps = ro.max_steps
-    steps = max_steps if args.steps <= 0 else min(args.steps, max_steps)
-    prefill = ro.prefill
-    decode = ro.step
+    sampled = sample_steps(max_steps, 32 if args.steps is None else args.steps)
+    is_sampled = np.zeros(max_steps, dtype=bool)
+    is_sampled[sampled] = True
+    nominal, unique = rollout_step_bytes(shape, plens, resp, G, max_steps)
 
-    # ---- warm-up rollout (untimed) ----
-    prefill()
+    # ---- warm-up (untimed) ----
+    ro.prefill()
     for t in range(min(args.warmup, max_steps)):
-        decode(t)
+        ro.step(t)
     torch.cuda.synchronize()
+    print(f"[bench] warm-up done; timing {len(sampled)} of {max_steps} decode steps", file=sys.stderr, flush=True)
 
-    # ---- optional per-class breakdown on a few sampled steps (untimed) ----
-    breakdown = None
-    if args.breakdown:
-        eng.reset_stats()
-        eng.set_option(RL_OPT_PROFILE, -1)
-        prefill()
-        for t in range(min(64, max_steps)):
-            decode(t)
-        st = eng.kernel_stats()
-        eng.set_option(RL_OPT_PROFILE, 0)
-        breakdown = {k: {"ms": round(v["total_ms"], 3), "launches": v["launches"],
-                         "GB/s": round(v["alg_bytes"] / (v["total_ms"] * 1e6), 1) if v["total_ms"] > 0 else None}
-                     for k, v in st.items() if v["launches"]}
-        print(json.dumps({"breakdown_first_64_steps": breakdown}), file=sys.stderr, flush=True)
+    # ---- pass 1: the whole rollout, profiling off; the sampled steps are
+    # each bracketed by device synchronisation and timed ----
+    t_pf0 = time.perf_counter()
+    ro.prefill()
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t_pf0
+    ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e_all0, e_all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall_t, gpu_t, gen_t = [], [], []
+    gen_all = 0
+    torch.cuda.synchronize()
+    t_all0 = time.perf_counter()
+    e_all0.record(stream)
+    last_print = t_all0
+    for t in range(max_steps):
+        if is_sampled[t]:
+            torch.cuda.synchronize()
+            w0 = time.perf_counter()
+            ea.record(stream)
+            n = ro.step(t)
+            eb.record(stream)
+            torch.cuda.synchronize()
+            wall_t.append(time.perf_counter() - w0)
+            gpu_t.append(ea.elapsed_time(eb) * 1e-3)
+            gen_t.append(n)
+        else:
+            n = ro.step(t)
+        gen_all += n
+        now = time.perf_counter()
+        if now - last_print > 20.0:
+            print(f"[bench] measured pass: step {t + 1}/{max_steps}", file=sys.stderr, flush=True)
+            last_print = now
+    e_all1.record(stream)
+    torch.cuda.synchronize()
+    rollout_wall = time.perf_counter() - t_all0
+    rollout_gpu = e_all0.elapsed_time(e_all1) * 1e-3
 
-    # ---- timed rollout ----
+    # ---- pass 2: the same rollout again, kernel classes timed with HIP
+    # events on the library's stream during the sampled steps only ----
     prof_classes = ("attention", "gemm_gate_up", "gemm_down", "gemm_lm_head", "gemm_qkv", "gemm_o")
     mask = 0
     for c in prof_classes:
         mask |= 1 << KERNEL_CLASSES.index(c)
-    t_pf0 = time.perf_counter()
-    prefill()
+    ro.prefill()
     torch.cuda.synchronize()
-    prefill_s = time.perf_counter() - t_pf0
     eng.reset_stats()
-    eng.set_option(RL_OPT_PROFILE, mask)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    gen = 0
-    last_print = t0
-    for t in range(steps):
-        gen += decode(t)
+    last_print = time.perf_counter()
+    for t in range(max_steps):
+        if is_sampled[t]:
+            eng.set_option(RL_OPT_PROFILE, mask)
+            ro.step(t)
+            eng.set_option(RL_OPT_PROFILE, 0)
+        else:
+            ro.step(t)
         now = time.perf_counter()
         if now - last_print > 20.0:
-            print(f"[bench] step {t + 1}/{steps}", file=sys.stderr, flush=True)
+            print(f"[bench] profiled pass: step {t + 1}/{max_steps}", file=sys.stderr, flush=True)
             last_print = now
-    ev1.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = ev0.elapsed_time(ev1)
     stats = eng.kernel_stats()
-    eng.set_option(RL_OPT_PROFILE, 0)
 
-    # dominant kernel (largest measured time among the timed classes)
     dom, roof = roofline_of(stats, prof_classes)
     roof.pop("alg_flops_per_launch")
     d = stats[dom]
     if dom == "attention" and ATTN_TRAFFIC_PER_ALG_BYTE is not None:
         roof["traffic"] = round(ATTN_TRAFFIC_PER_ALG_BYTE * d["alg_bytes"] / max(1, d["launches"]))
-
     classes = {c: {"launches": stats[c]["launches"],
                    "avg_launch_ms": round(stats[c]["total_ms"] / max(1, stats[c]["launches"]), 5),
-                   "alg_bytes_per_launch": round(stats[c]["alg_bytes"] / max(1, stats[c]["launches"]))}
+                   "alg_bytes_per_launch": round(stats[c]["alg_bytes"] / max(1, stats[c]["launches"])),
+                   "frac_of_peak": round(stats[c]["alg_flops"] / (stats[c]["total_ms"] * 1e9) / BF16_PEAK_TFLOPS, 4)
+                   if c.startswith("gemm") and stats[c]["total_ms"] > 0 else
+                   round(stats[c]["alg_bytes"] / (stats[c]["total_ms"] * 1e6) / HBM_PEAK_GBS, 4)
+                   if stats[c]["total_ms"] > 0 else None}
                for c in prof_classes}
-    all_bytes = sum(v["alg_bytes"] for k, v in stats.items() if k not in ("splitk_reduce", "attn_combine"))
+
+    wall_s, gpu_s, gen = sum(wall_t), sum(gpu_t), sum(gen_t)
+    nom_b = float(nominal[is_sampled].sum())
+    uni_b = float(unique[is_sampled].sum())
+    step_gbs = nom_b / gpu_s / 1e9
+    step_gbs_u = uni_b / gpu_s / 1e9
+    roll_gbs = float(nominal.sum()) / rollout_gpu / 1e9
+    roll_gbs_u = float(unique.sum()) / rollout_gpu / 1e9
     prompt_tokens = int(plens.sum())
-    gen_total = gen
-    value = gen_total / wall
     out = {
         "metric": "rollout tokens/sec (1 GPU) at 7B shape; decode-step HBM GB/s vs peak",
-        "value": round(value, 1),
+        "value": round(gen / wall_s, 1),
         "unit": "generated tokens/s",
         "n_gpus": 1,
-        "steps": steps,
+        "steps": len(sampled),
         "warmup": args.warmup,
-        "ms_per_step": round(wall * 1e3 / max(1, steps), 4),
+        "ms_per_step": round(wall_s * 1e3 / len(sampled), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded random-init weights and uniform prompt tokens)",
+        "data": f"synthetic (seeded random-init weights, {wl.init} init, and uniform prompt tokens)",
         "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped decoder (28 layers, hidden 3584, 28 q / 4 kv heads, "
                                f"ffn 18944, vocab 152064); {P} prompts x {G} samples, prompts U[{wl.prompt_len[0]},"
                                f"{wl.prompt_len[1]}], lognormal responses (median {wl.response_median}, sigma "
-                               f"{wl.response_sigma}, cap {wl.response_cap})",
-                   "n_seqs": n_seq, "prompt_tokens": prompt_tokens,
-                   "generated_tokens_timed": gen_total, "decode_steps_in_rollout": max_steps},
-        "gpu_ms_timed": round(gpu_ms, 2),
-        "decode_step_alg_GBps": round(all_bytes / (gpu_ms * 1e-3) / 1e9, 1) if steps == max_steps else None,
-        "prefill_s": round(prefill_s, 4),
-        "paper_style_tokens_per_s": round((prompt_tokens + gen_total + n_seq) / (wall + prefill_s), 1)
-        if steps == max_steps else None,
+                               f"{wl.response_sigma}, cap {wl.response_cap}); the timed steps are spread evenly "
+                               f"over the whole rollout",
+                   "n_seqs": n_seq, "prompt_tokens": prompt_tokens, "decode_steps_in_rollout": max_steps,
+                   "timed_steps": sampled if len(sampled) <= 64 else f"all {len(sampled)}",
+                   "generated_tokens_timed": gen},
+        "gpu_ms_timed": round(gpu_s * 1e3, 3),
+        "decode_step_alg_GBps": round(step_gbs, 1),
+        "decode_step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        "decode_step_unique_GBps": round(step_gbs_u, 1),
+        "decode_step_unique_hbm_frac": round(step_gbs_u / HBM_PEAK_GBS, 4),
+        "rollout": {"decode_s": round(rollout_wall, 3), "gpu_s": round(rollout_gpu, 3),
+                    "generated_tokens": gen_all, "tokens_per_s": round(gen_all / rollout_wall, 1),
+                    "alg_GBps": round(roll_gbs, 1), "hbm_frac": round(roll_gbs / HBM_PEAK_GBS, 4),
+                    "unique_alg_GBps": round(roll_gbs_u, 1),
+                    "unique_hbm_frac": round(roll_gbs_u / HBM_PEAK_GBS, 4),
+                    "alg_TB": round(float(nominal.sum()) / 1e12, 2),
+                    "unique_alg_TB": round(float(unique.sum()) / 1e12, 2),
+                    "prefill_s": round(prefill_s, 4),
+                    "paper_style_tokens_per_s": round((prompt_tokens + gen_all + n_seq) /
+                                                      (rollout_wall + prefill_s), 1)},
         "roofline": roof,
         "timed_classes": classes,
     }
-    if breakdown:
-        out["breakdown_first_64_steps"] = breakdown
     eng.close()
-    del eng
+    del eng, ro
     torch.cuda.synchronize()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, weights, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline_rollout(shape, weights, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -140,7 +140,10 @@ size_t rl_decode_workspace_bytes(const rl_model_config* cfg);
  * Life cycle.
  * ------------------------------------------------------------------- */
 
-/* Create a context on the current HIP device.
+/* Create a context on the current HIP device.  The context is the rollout
+ * engine's state for one policy model: its KV capacity (max_seqs slots of
+ * max_ctx positions) bounds how many responses generate at once, which is
+ * what sets rollout speed (Sec. 5.1.1, larger KV-cache allocations).
  *  cfg        host; copied.
  *  w          host struct of device pointers; copied (the memory is borrowed).
  *  kv_pool    device, kv_bytes >= rl_decode_kv_bytes(cfg), 256-byte aligned.
@@ -230,7 +233,10 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
                    float temperature, float* out_logp);
 
 /* ---------------------------------------------------------------------
- * One decode step (the rollout's hot loop).
+ * One decode step (the rollout's hot loop: Sec. 2.1, generation extends every
+ * unfinished response by one token and the RL loss later consumes each
+ * token's log-probability; Sec. 5.1.2, the token and its log-probability come
+ * from the same forward pass; Sec. 5.2, temperature).
  *
  * For each row i < n: appends in_tok[i] to slot slots[i] at position
  * p = length(slot), attends over positions 0..p, and samples the token of
@@ -398,12 +404,45 @@ typedef struct rl_kernel_stats {
 } rl_kernel_stats;
 
 rl_status rl_decode_kernel_stats(rl_decode_ctx* ctx, int32_t kclass, rl_kernel_stats* out);
+
+/* Shape of the decode attention's work-item plans, summed over the
+ * rl_decode_step calls since the last reset (one plan serves every layer of
+ * a call).  Host-side counters, always collected; nothing is synchronised.
+ * A work item is one wave's key range for up to 16 query columns; a pair
+ * item serves two sequences that read the same shared prompt chunk
+ * (RL_OPT_SHARED_PREFIX); an LDS workgroup is a workgroup of four items over
+ * one shared chunk that stages each K/V step through LDS once. */
+typedef struct rl_attn_plan_stats {
+    int64_t steps;            /* rl_decode_step calls counted               */
+    int64_t items;            /* work items (padding excluded)              */
+    int64_t shared_items;     /* items over a shared prompt chunk           */
+    int64_t pair_items;       /* items serving two sequences                */
+    int64_t lds_workgroups;   /* workgroups staging a shared chunk in LDS   */
+} rl_attn_plan_stats;
+
+rl_status rl_decode_attn_plan_stats(const rl_decode_ctx* ctx, rl_attn_plan_stats* out);
+
+/* Zero the kernel-class figures and the attention plan counters. */
 rl_status rl_decode_reset_stats(rl_decode_ctx* ctx);
 
 /* Plain device-to-device copy kernel (16-byte vector loads and stores) of
  * `bytes` bytes (a multiple of 16; both pointers 16-byte aligned) on
  * `stream`.  Used to calibrate hardware byte counters against a known size. */
 rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream);
+
+/* Check of the two upper bounds of the Gumbel noise g(x) = fl32(-log(-log u)),
+ * u = (x + 1/2) 2^-32, that the sampler uses to skip the exact fp64 noise of
+ * entries that cannot win (the sample stays the exhaustive arg-max only if
+ * both hold), evaluated with the sampler's own device code over the noise
+ * words [lo, lo + count), count <= 2^32 and lo + count <= 2^32:
+ *   x <  0xFF000000: the fp32 hardware-logarithm bound >= g(x), 5.56 >= g(x);
+ *   x >= 0xFF000000: 22.9 >= g(x).
+ * viol and min_margin are device arrays of n_blocks (1..65536) entries; each
+ * workgroup writes its count of violations and the smallest margin of the
+ * fp32 bound over its words (+inf if it saw none below 0xFF000000).
+ * Asynchronous on `stream`.  A test probe, not part of the decode path. */
+rl_status rl_probe_gumbel_bound(uint32_t lo, uint64_t count, int32_t n_blocks, uint32_t* viol, float* min_margin,
+                                void* stream);
 
 /* Static description of a status code. */
 const char* rl_status_string(rl_status s);

@@ -61,6 +61,7 @@ class Workload:
     patch_rows: int = 0                 # embodied workload: caller-provided embedding rows
     env_steps: int = 0                  # embodied workload: env steps per rollout
     seed: int = 20250919
+    init: str = "fanin"                 # weight initialisation (inputs.make_weights)
 
     @property
     def n_seqs(self) -> int:
@@ -83,7 +84,7 @@ QWEN_32B = ModelShape(64, 5120, 40, 8, 128, 27648, 152064, 1e-6, 1e6, "bf16")
 
 WORKLOADS = {
     # tiny fp32 decoder: 2 prompts x 4 samples, 32-token prompts, 32 generated tokens
-    "tiny": Workload("tiny", TINY, 2, 4, (32, 32), 32, 0.0, 32, seed=20250919 + 0),
+    "tiny": Workload("tiny", TINY, 2, 4, (32, 32), 32, 0.0, 32, seed=20250919 + 0, init="normal"),
     # Qwen2.5-1.5B shape: 64 prompts x 8, prompts U[128,512], lognormal(600) capped at 1024
     "qwen1.5b": Workload("qwen1.5b", QWEN_1_5B, 64, 8, (128, 512), 600, 0.5, 1024, seed=20250919 + 1),
     # Llama-2-7B embodied shape: 256 envs, 256 patch rows + 32 text tokens, 7 action tokens per env step

@@ -136,6 +136,7 @@ struct rl_decode_ctx {
     std::vector<Pending> pending;
     std::vector<hipEvent_t> ev_pool;
     rl_kernel_stats stats[RL_K_COUNT]{};
+    rl_attn_plan_stats plan{};
     std::string err;
 
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
@@ -262,6 +263,9 @@ struct Fwd {
     int n_tiles = 0;
     const int32_t* split_blocks = nullptr;   // first item of every split block
     int n_split_blocks = 0;
+    // decode attention plan (build_items): work items, those over a shared
+    // prompt chunk, pair items, workgroups staging a shared chunk in LDS
+    int plan_items = 0, plan_shared = 0, plan_pairs = 0, plan_lds = 0;
     double attn_kv_positions = 0;           // algorithmic KV positions read per kv-head
     double attn_score_positions = 0;        // sum over rows of keys attended
     const int32_t* final_sel = nullptr;     // rows fed to the LM head (nullptr: all)
@@ -757,11 +761,21 @@ rl_status build_items(rl_decode_ctx* c, Meta* m, const std::vector<Block>& block
         }
     }
     for (size_t i = 0; i < split_first.size(); ++i) split[i] = newpos[split_first[i]];
+    f->plan_items = f->plan_shared = f->plan_pairs = f->plan_lds = 0;
+    for (size_t x = 0; x < order.size(); ++x) {
+        if (order[x] < 0) continue;
+        f->plan_items += 1;
+        f->plan_shared += key[order[x]] >= 0;
+        f->plan_pairs += its[order[x]].qrow_b >= 0;
+    }
     if (any_shared) {   // workgroups whose four items read one shared chunk stage it through LDS
         for (size_t x = 0; x + 3 < order.size(); x += 4) {
             bool same = order[x] >= 0 && key[order[x]] >= 0;
             for (int t = 1; t < 4 && same; ++t) same = order[x + t] >= 0 && key[order[x + t]] == key[order[x]];
-            if (same) items[x].pad = 1;
+            if (same) {
+                items[x].pad = 1;
+                f->plan_lds += 1;
+            }
         }
     }
     f->items = dItems;
@@ -1350,6 +1364,11 @@ rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, co
     st = run_forward(c, f);
     if (st != RL_OK) return st;
     for (int i = 0; i < n; ++i) c->len[slots[i]] += 1;
+    c->plan.steps += 1;
+    c->plan.items += f.plan_items;
+    c->plan.shared_items += f.plan_shared;
+    c->plan.pair_items += f.plan_pairs;
+    c->plan.lds_workgroups += f.plan_lds;
     return RL_OK;
 }
 
@@ -1595,6 +1614,13 @@ rl_status rl_decode_kernel_stats(rl_decode_ctx* ctx, int32_t kclass, rl_kernel_s
     return RL_OK;
 }
 
+rl_status rl_decode_attn_plan_stats(const rl_decode_ctx* ctx, rl_attn_plan_stats* out) {
+    if (!ctx_ok(ctx)) return RL_ERR_STATE;
+    if (!out) return RL_ERR_INVALID_ARG;
+    *out = ctx->plan;
+    return RL_OK;
+}
+
 rl_status rl_decode_reset_stats(rl_decode_ctx* ctx) {
     if (!ctx_ok(ctx)) return RL_ERR_STATE;
     DeviceGuard g(ctx->device);
@@ -1606,7 +1632,19 @@ rl_status rl_decode_reset_stats(rl_decode_ctx* ctx) {
         ctx->stats[i].alg_bytes = 0;
         ctx->stats[i].alg_flops = 0;
     }
+    ctx->plan = rl_attn_plan_stats{};
     return RL_OK;
+}
+
+rl_status rl_probe_gumbel_bound(uint32_t lo, uint64_t count, int32_t n_blocks, uint32_t* viol, float* min_margin,
+                                void* stream) {
+    if (!viol || !min_margin || n_blocks < 1 || n_blocks > 65536) return RL_ERR_INVALID_ARG;
+    if (count == 0 || count > (1ull << 32) || lo + (count - 1) > 0xFFFFFFFFull) return RL_ERR_INVALID_ARG;
+    if (!aligned(viol, 4) || !aligned(min_margin, 4)) return RL_ERR_INVALID_ARG;
+    return launch_gumbel_bound_probe(lo, count, n_blocks, viol, min_margin, static_cast<hipStream_t>(stream)) ==
+                   hipSuccess
+               ? RL_OK
+               : RL_ERR_HIP;
 }
 
 rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream) {

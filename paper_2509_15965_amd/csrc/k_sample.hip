@@ -186,6 +186,48 @@ __global__ void __launch_bounds__(64) sample_merge_kernel(const SamplePart* __re
     sample_finish(b, a, logits + static_cast<size_t>(row) * ld, V, forced ? forced[o] : -1, T, o, out_tok, out_logp);
 }
 
+// Check of the noise bounds the sampler relies on, over the words
+// [lo, lo + count): for x < kGumbelLowWords, gumbel_upper_low(x) >= g(x) and
+// kGumbelLowMax >= g(x); above, kGumbelMax >= g(x).  Each workgroup writes its
+// count of violations and its smallest margin gumbel_upper_low(x) - g(x).
+__global__ void __launch_bounds__(256) gumbel_bound_probe_kernel(uint32_t lo, uint64_t count,
+                                                                 uint32_t* __restrict__ viol,
+                                                                 float* __restrict__ min_margin) {
+    __shared__ uint32_t sv[4];
+    __shared__ float sm[4];
+    uint32_t bad = 0;
+    float mm = INFINITY;
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count; i += stride) {
+        const uint32_t x = lo + static_cast<uint32_t>(i);
+        const float g = gumbel_of_word(x);
+        if (x < kGumbelLowWords) {
+            const float b = gumbel_upper_low(x);
+            bad += !(b >= g);
+            bad += !(kGumbelLowMax >= g);
+            mm = fminf(mm, b - g);
+        } else {
+            bad += !(kGumbelMax >= g);
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        bad += __shfl_xor(bad, off, 64);
+        mm = fminf(mm, __shfl_xor(mm, off, 64));
+    }
+    if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = bad; sm[threadIdx.x >> 6] = mm; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        viol[blockIdx.x] = sv[0] + sv[1] + sv[2] + sv[3];
+        min_margin[blockIdx.x] = fminf(fminf(sm[0], sm[1]), fminf(sm[2], sm[3]));
+    }
+}
+
+hipError_t launch_gumbel_bound_probe(uint32_t lo, uint64_t count, int n_blocks, uint32_t* viol,
+                                     float* min_margin, hipStream_t s) {
+    hipLaunchKernelGGL(gumbel_bound_probe_kernel, dim3(n_blocks), dim3(256), 0, s, lo, count, viol, min_margin);
+    return hipGetLastError();
+}
+
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
                          uint64_t seed, float T, SamplePart* parts,

@@ -182,4 +182,9 @@ hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, co
 
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
 
+// Sampler noise-bound check over words [lo, lo + count): per workgroup, the
+// number of violated bounds and the smallest margin of the fp32 bound.
+hipError_t launch_gumbel_bound_probe(uint32_t lo, uint64_t count, int n_blocks, uint32_t* viol,
+                                     float* min_margin, hipStream_t s);
+
 }  // namespace rl

@@ -2,9 +2,18 @@
 and the benchmark.
 
 This module draws random numbers and lays them out; it holds none of the
-decoder's arithmetic.  Weights: every linear and embedding matrix is drawn
-i.i.d. N(0, 0.02) in fp32 and rounded once to the model dtype (torch's
-round-to-nearest-even for bf16); RMSNorm gains are 1.0.  Prompts are uniform
+decoder's arithmetic.  Weights are drawn in fp32 and rounded once to the
+model dtype (torch's round-to-nearest-even for bf16); RMSNorm gains are 1.0.
+Two initialisations:
+  "normal"  every linear and embedding matrix i.i.d. N(0, 0.02);
+  "fanin"   unit-variance (fan-in) init: every matrix N(0, 1/fan_in), with
+            the residual-branch output projections (w_o, w_down) further
+            divided by sqrt(2 L) and embedding rows N(0, 1) (the scale of
+            caller-provided N(0, 1) embedding rows).  The residual stream then
+            starts at the scale of its inputs and each layer adds a bounded
+            fraction to it, so one storage ulp changed anywhere is not
+            amplified across the depth.
+Prompts are uniform
 token ids; prompt lengths are uniform integers in the workload's range;
 response lengths are lognormal around the workload's median, clamped to
 [1, cap] (the long tail of Sec. 2.2, Fig. 2).
@@ -41,11 +50,26 @@ def weight_shapes(m: ModelShape) -> Dict[str, tuple]:
     }
 
 
-def make_weights(m: ModelShape, seed: int, device="cpu", resid_scaled: bool = False) -> Dict[str, torch.Tensor]:
+INITS = ("normal", "fanin")
+
+
+def init_std(m: ModelShape, name: str, init: str) -> float:
+    """Standard deviation of weight matrix `name` under initialisation `init`."""
+    if init not in INITS:
+        raise ValueError(f"unknown init {init!r}")
+    if init == "normal":
+        return INIT_STD
+    if name == "embed":
+        return 1.0
+    fan_in = {"w_o": m.n_q_heads * m.head_dim, "w_down": m.ffn}.get(name, m.hidden)
+    if name in ("w_o", "w_down"):
+        return 1.0 / math.sqrt(fan_in * 2.0 * m.n_layers)
+    return 1.0 / math.sqrt(fan_in)
+
+
+def make_weights(m: ModelShape, seed: int, device="cpu", init: str = "normal") -> Dict[str, torch.Tensor]:
     """Random-init decoder weights on `device`, drawn one layer slice at a time
-    (bounded temporary memory) from a single seeded generator.  With
-    resid_scaled, the two residual-branch output projections (w_o, w_down)
-    use std 0.02 / sqrt(2 * n_layers) instead of 0.02."""
+    (bounded temporary memory) from a single seeded generator."""
     dt = torch_dtype(m)
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
@@ -55,9 +79,7 @@ def make_weights(m: ModelShape, seed: int, device="cpu", resid_scaled: bool = Fa
         if name.endswith("norm"):
             t.fill_(1.0)
         elif len(shp) == 3:
-            std = INIT_STD
-            if resid_scaled and name in ("w_o", "w_down"):
-                std = INIT_STD / math.sqrt(2.0 * m.n_layers)
+            std = init_std(m, name, init)
             for l in range(shp[0]):
                 r = torch.randn(shp[1:], generator=gen, device=device, dtype=torch.float32)
                 t[l].copy_(r.mul_(std))
@@ -68,7 +90,7 @@ def make_weights(m: ModelShape, seed: int, device="cpu", resid_scaled: bool = Fa
             for r0 in range(0, rows, step):
                 r1 = min(rows, r0 + step)
                 r = torch.randn((r1 - r0, shp[1]), generator=gen, device=device, dtype=torch.float32)
-                t[r0:r1].copy_(r.mul_(INIT_STD))
+                t[r0:r1].copy_(r.mul_(init_std(m, name, init)))
                 del r
         out[name] = t
     return out

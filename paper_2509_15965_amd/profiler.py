@@ -167,7 +167,7 @@ def main():
         dev = torch.device("cuda:0")
         torch.cuda.set_device(dev)
         plan = rollout_plan(wl)
-        weights = make_weights(shape, wl.seed, device=dev)
+        weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
         n_params = sum(v.numel() for v in weights.values())
         wbytes = sum(v.numel() * v.element_size() for v in weights.values())
         seed, T = 20250919, wl.temperature

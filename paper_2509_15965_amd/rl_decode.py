@@ -33,7 +33,8 @@ EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create"
            "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
            "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
            "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
-           "rl_decode_reset_stats", "rl_probe_copy", "rl_status_string", "rl_decode_last_error")
+           "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_gumbel_bound",
+           "rl_status_string", "rl_decode_last_error")
 
 
 class ModelConfig(C.Structure):
@@ -56,6 +57,11 @@ class SampleParams(C.Structure):
 class KernelStats(C.Structure):
     _fields_ = [("launches", C.c_int64), ("total_ms", C.c_double), ("alg_bytes", C.c_double),
                 ("alg_flops", C.c_double), ("name", C.c_char * 48)]
+
+
+class AttnPlanStats(C.Structure):
+    _fields_ = [("steps", C.c_int64), ("items", C.c_int64), ("shared_items", C.c_int64),
+                ("pair_items", C.c_int64), ("lds_workgroups", C.c_int64)]
 
 
 _lib = None
@@ -107,8 +113,12 @@ def lib():
     L.rl_decode_kernel_stats.argtypes = [vp, i32, C.POINTER(KernelStats)]
     L.rl_decode_reset_stats.restype = C.c_int
     L.rl_decode_reset_stats.argtypes = [vp]
+    L.rl_decode_attn_plan_stats.restype = C.c_int
+    L.rl_decode_attn_plan_stats.argtypes = [vp, C.POINTER(AttnPlanStats)]
     L.rl_probe_copy.restype = C.c_int
     L.rl_probe_copy.argtypes = [vp, vp, sz, vp]
+    L.rl_probe_gumbel_bound.restype = C.c_int
+    L.rl_probe_gumbel_bound.argtypes = [C.c_uint32, C.c_uint64, i32, vp, vp, vp]
     L.rl_status_string.restype = C.c_char_p
     L.rl_status_string.argtypes = [C.c_int]
     L.rl_decode_last_error.restype = C.c_char_p
@@ -287,6 +297,11 @@ class Engine:
                          "alg_flops": s.alg_flops}
         return out
 
+    def attn_plan_stats(self) -> Dict[str, int]:
+        s = AttnPlanStats()
+        self._check(lib().rl_decode_attn_plan_stats(self.h, C.byref(s)), "rl_decode_attn_plan_stats")
+        return {name: int(getattr(s, name)) for name, _ in AttnPlanStats._fields_}
+
     def reset_stats(self):
         self._check(lib().rl_decode_reset_stats(self.h), "rl_decode_reset_stats")
 
@@ -308,3 +323,17 @@ def probe_copy(dst: torch.Tensor, src: torch.Tensor, nbytes: int, stream=None):
     st = lib().rl_probe_copy(dst.data_ptr(), src.data_ptr(), nbytes, stream.cuda_stream)
     if st != RL_OK:
         raise RLError(st, "rl_probe_copy")
+
+
+def probe_gumbel_bound(lo: int, count: int, n_blocks: int = 4096, device="cuda"):
+    """Run the sampler's noise-bound check over words [lo, lo + count);
+    returns (violations, smallest margin of the fp32 bound)."""
+    viol = torch.empty(n_blocks, dtype=torch.int32, device=device)
+    mm = torch.empty(n_blocks, dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream(torch.device(device))
+    st = lib().rl_probe_gumbel_bound(int(lo), int(count), n_blocks, viol.data_ptr(), mm.data_ptr(),
+                                     stream.cuda_stream)
+    if st != RL_OK:
+        raise RLError(st, "rl_probe_gumbel_bound")
+    torch.cuda.synchronize(device)
+    return int(viol.to(torch.int64).sum().item()), float(mm.min().item())

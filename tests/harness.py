@@ -24,9 +24,9 @@ def oracle_mode(shape: ModelShape) -> int:
     return oracle.MODE_BF16 if shape.dtype == "bf16" else oracle.MODE_FP32
 
 
-def build_models(shape: ModelShape, seed: int, device="cuda"):
+def build_models(shape: ModelShape, seed: int, device="cuda", init: str = "normal"):
     """Same seeded weights for both sides: device tensors and an oracle model."""
-    w_dev = make_weights(shape, seed, device=device)
+    w_dev = make_weights(shape, seed, device=device, init=init)
     w_host = weights_to_host(w_dev)
     om = oracle.OracleModel(shape.as_dict(), w_host, oracle_mode(shape))
     return w_dev, w_host, om

@@ -13,6 +13,13 @@ host, so every check samples what it can compute one by one:
     responses against the oracle, and one whole GRPO group of the rollout
     workload (the launch configuration its benchmark times) against
     prefill + teacher-forced decoding of the same sequences.
+Every check asserts the stated bars (logits 3e-2 relative per row, log-probs
+2e-2 absolute).  The workloads use the fan-in initialisation
+(inputs.make_weights), under which the decoder does not amplify one storage
+ulp across its depth; each check also measures the oracle's own sensitivity
+to one bf16 ulp flipped in one input element and asserts that it is below
+half the bar (the function is well enough conditioned for the bar to mean
+something).
 """
 import gc
 
@@ -181,9 +188,13 @@ def _record(name, what, errs, lerr, sens=None, lsens=None):
             f.write(json.dumps(rec) + "\n")
 
 
-def _assert_ok(errs, lerr, what):
+def _assert_ok(errs, lerr, what, sens=None, lsens=None):
+    """The stated bars; with the oracle's one-ulp self-sensitivity given,
+    also that it sits below half of each bar."""
     assert max(errs) < LOGIT_REL_TOL, (what, errs)
     assert max(lerr) < LOGP_ABS_TOL, (what, lerr)
+    if sens is not None:
+        assert sens < 0.5 * LOGIT_REL_TOL and lsens < 0.5 * LOGP_ABS_TOL, (what, "ill-conditioned", sens, lsens)
 
 
 @pytest.mark.timeout(1500)
@@ -192,7 +203,7 @@ def test_real_shape_parity(name):
     wl = WORKLOADS[name]
     shape = wl.model
     oracle.set_threads(max(1, min(16, len(__import__("os").sched_getaffinity(0)))))
-    w_dev, w_host, om = build_models(shape, wl.seed)
+    w_dev, w_host, om = build_models(shape, wl.seed, init=wl.init)
     rng = np.random.default_rng(wl.seed)
     if wl.patch_rows:
         # embodied prompt: caller-provided patch rows then text tokens (short)
@@ -205,18 +216,12 @@ def test_real_shape_parity(name):
         res = _short_prompt_check(shape, w_dev, w_host, om, prompts, group=2, n_steps=3)
     errs, lerr, sens, lsens = res
     _record(name, "short_prompts", errs, lerr, sens, lsens)
-    # Short model-generated contexts at this depth are ill-conditioned: one
-    # bf16 ulp at the input moves the oracle's own logits and log-probs by
-    # (sens, lsens).  The bar is the stated tolerance or twice that
-    # self-sensitivity, whichever is larger.
-    assert max(errs) < max(LOGIT_REL_TOL, 2 * sens), (name, errs, sens)
-    assert max(lerr) < max(LOGP_ABS_TOL, 2 * lsens), (name, lerr, lsens)
+    _assert_ok(errs, lerr, (name, "short prompts"), sens, lsens)
     _free()
     cap = wl.max_ctx
     errs, lerr, sens, lsens = _long_context_check(shape, w_dev, w_host, om, [cap - 2, cap // 3 + 1])
     _record(name, "long_context", errs, lerr, sens, lsens)
-    assert max(errs) < max(LOGIT_REL_TOL, 2 * sens), (name, errs, sens)
-    assert max(lerr) < max(LOGP_ABS_TOL, 2 * lsens), (name, lerr, lsens)
+    _assert_ok(errs, lerr, (name, "long context"), sens, lsens)
     _free()
 
 
@@ -228,7 +233,7 @@ def test_benchmark_batch_sampled_rows():
     wl = WORKLOADS["qwen7b"]
     shape = wl.model
     oracle.set_threads(max(1, min(16, len(__import__("os").sched_getaffinity(0)))))
-    w_dev, w_host, om = build_models(shape, wl.seed)
+    w_dev, w_host, om = build_models(shape, wl.seed, init=wl.init)
     n = wl.n_seqs
     rng = np.random.default_rng(123)
     lengths = rng.integers(wl.prompt_len[0], wl.prompt_len[1] + 1, size=n).astype(np.int32)
@@ -288,8 +293,7 @@ def test_benchmark_batch_sampled_rows():
         sens.append(row_rel_err(zp, z))
         lsens.append(abs(lpp - lo))
     _record("qwen7b", "benchmark_batch_rows_0_255_511", errs, lerr, max(sens), max(lsens))
-    assert max(errs) < max(LOGIT_REL_TOL, 2 * max(sens)), ("benchmark batch", errs, sens)
-    assert max(lerr) < max(LOGP_ABS_TOL, 2 * max(lsens)), ("benchmark batch", lerr, lsens)
+    _assert_ok(errs, lerr, "benchmark batch", max(sens), max(lsens))
     eng.close()
     del seqs
     _free()
@@ -308,7 +312,7 @@ def test_score_7b_short_sequences_match_oracle():
     wl = WORKLOADS["qwen7b"]
     shape = wl.model
     oracle.set_threads(max(1, min(16, len(__import__("os").sched_getaffinity(0)))))
-    w_dev, w_host, om = build_models(shape, wl.seed)
+    w_dev, w_host, om = build_models(shape, wl.seed, init=wl.init)
     rng = np.random.default_rng(17)
     prompts = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in (5, 9)]
     resp = [rng.integers(0, shape.vocab, size=4).astype(np.int32) for _ in range(4)]
@@ -329,7 +333,7 @@ def test_score_7b_short_sequences_match_oracle():
     lsens = float(np.abs(pert - ref[:4]).max())
     _record("qwen7b", "score_short_sequences", [0.0], lerr, 0.0, lsens)
     assert np.isfinite(got).all()
-    assert lerr.max() < max(LOGP_ABS_TOL, 2 * lsens), (lerr, lsens)
+    _assert_ok([0.0], [float(lerr.max())], "score short sequences", 0.0, lsens)
     del om
     _free()
 
@@ -340,11 +344,9 @@ def test_score_benchmark_group_matches_teacher_forced_decode():
     (prompt + 16 lognormal responses, one call, as the score benchmark runs
     it) against prefill + teacher-forced decode steps of the same 16
     sequences.  Both are bf16 paths checked against the oracle elsewhere.
-    The depth-28 random-init decoder is ill-conditioned: the same scoring
-    call with one bf16 ulp flipped in the prompt's first input row moves the
-    log-probabilities by (sens_max, sens_mean).  Bar: the maximum difference
-    below max(2 x tolerance, 2 x sens_max), the mean below
-    max(tolerance / 10, 2 x sens_mean)."""
+    Bar: every one of the ~27k log-probabilities within the stated 2e-2, the
+    mean difference below 2e-3; the same scoring call with one bf16 ulp
+    flipped in the prompt's first input row is recorded beside them."""
     from paper_2509_15965_amd.inputs import make_weights, rollout_plan
     wl = WORKLOADS["qwen7b"]
     shape = wl.model
@@ -354,7 +356,7 @@ def test_score_benchmark_group_matches_teacher_forced_decode():
     rl = plan["response_lens"][:G].astype(np.int64)
     rng = np.random.default_rng(wl.seed + 7)
     rt = rng.integers(0, shape.vocab, size=int(rl.sum())).astype(np.int32)
-    w_dev = make_weights(shape, wl.seed, device=DEV)
+    w_dev = make_weights(shape, wl.seed, device=DEV, init=wl.init)
     max_ctx = P + int(rl.max())
     eng = Engine(shape, w_dev, max_seqs=G, max_ctx=max_ctx, max_prefill_tokens=P + int(rl.sum()))
     roffs = np.concatenate([[0], np.cumsum(rl)]).astype(np.int32)
@@ -403,6 +405,6 @@ def test_score_benchmark_group_matches_teacher_forced_decode():
     d = np.abs(got - ref)
     _record("qwen7b", "score_group_vs_teacher_forced_decode: diff max, diff mean, ulp-flip max, ulp-flip mean",
             [0.0], [float(d.max()), float(d.mean()), float(sens.max()), float(sens.mean())])
-    assert d.max() < max(2 * LOGP_ABS_TOL, 2 * sens.max()), (d.max(), d.mean(), sens.max(), sens.mean())
-    assert d.mean() < max(0.1 * LOGP_ABS_TOL, 2 * sens.mean()), (d.max(), d.mean(), sens.max(), sens.mean())
+    assert d.max() < LOGP_ABS_TOL, (d.max(), d.mean(), sens.max(), sens.mean())
+    assert d.mean() < 0.1 * LOGP_ABS_TOL, (d.max(), d.mean(), sens.max(), sens.mean())
     _free()

@@ -154,3 +154,59 @@ def test_shared_prompt_counts_each_prompt_once():
     shared_pos = sum(p // 32 * 32 + 4 * (p + 1 - p // 32 * 32) for p in plens)
     assert out[0] == (L * (full * per_pos + q_bytes), L)
     assert out[1] == (L * (shared_pos * per_pos + q_bytes), L)
+
+
+G7 = ModelShape(2, 512, 14, 2, 128, 1024, 1032, 1e-6, 1e4, "bf16")
+
+
+def test_lds_staged_shared_chunks_group16_gqa7():
+    """The decode attention path of the 7B-shape rollout: 7 q-heads per
+    kv-head (two sequences per pair item) and GRPO groups of 16, so each
+    shared prompt chunk is read by 8 pair items, i.e. two workgroups of four
+    items over one chunk that stage each K/V step through LDS once.  One
+    650-token prompt, group 16, prefill and 4 teacher-forced decode steps,
+    every row against the oracle at the stated bars; the plan counters show
+    the LDS-staged workgroups were launched."""
+    rng = np.random.default_rng(56)
+    P, G, steps = 650, 16, 4
+    prompt = rng.integers(0, G7.vocab, size=P).astype(np.int32)
+    w_dev, _, om = build_models(G7, 57)
+    eng = Engine(G7, w_dev, max_seqs=G, max_ctx=P + steps + 2, max_prefill_tokens=P)
+    orc = OracleRollout(om, P + steps + 2)
+    slots = list(range(G))
+    ot = torch.empty(G, dtype=torch.int32, device=DEV)
+    ol = torch.empty(G, dtype=torch.float32, device=DEV)
+    lp = torch.empty((1, G7.vocab), dtype=torch.float32, device=DEV)
+    f0 = uniform_tokens(G, G7.vocab, 3000)
+    eng.prefill(slots, slots, [0, P], _i32(prompt), ot, ol, group=G, forced=_i32(f0), out_logits=lp)
+    torch.cuda.synchronize()
+    z0 = orc.prefill(0, prompt)
+    for k in range(1, G):
+        orc.seqs[k] = orc.seqs[0].clone()
+    assert row_rel_err(lp.cpu().numpy()[0], z0) < LOGIT_REL_TOL
+    lo = np.array([oracle.logprob(z0.astype(np.float32), 1.0, int(f0[i])) for i in range(G)])
+    assert np.abs(ol.cpu().numpy() - lo).max() < LOGP_ABS_TOL
+    eng.reset_stats()
+    lg = torch.empty((G, G7.vocab), dtype=torch.float32, device=DEV)
+    worst = (0.0, 0.0)
+    for st in range(1, steps + 1):
+        tin = uniform_tokens(G, G7.vocab, 3000 + st)
+        tf = uniform_tokens(G, G7.vocab, 4000 + st)
+        eng.step(slots, slots, _i32(tin), ot, ol, forced=_i32(tf), out_logits=lg)
+        torch.cuda.synchronize()
+        zg, lpg = lg.cpu().numpy(), ol.cpu().numpy()
+        for i in slots:
+            z = orc.step(i, tin[i])
+            e = row_rel_err(zg[i], z)
+            le = abs(lpg[i] - oracle.logprob(z.astype(np.float32), 1.0, int(tf[i])))
+            worst = (max(worst[0], e), max(worst[1], le))
+            assert e < LOGIT_REL_TOL, (st, i, e)
+            assert le < LOGP_ABS_TOL, (st, i, le)
+    plan = eng.attn_plan_stats()
+    eng.close()
+    print("worst logits rel / log-prob abs:", worst, "plan:", plan, flush=True)
+    assert plan["steps"] == steps
+    # three shared chunks (positions 0-255, 256-511, 512-639), each read by
+    # 16 sequences = 8 pair items = two LDS-staged workgroups
+    assert plan["pair_items"] == steps * 3 * 8
+    assert plan["lds_workgroups"] == steps * 3 * 2
