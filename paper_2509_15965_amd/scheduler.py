@@ -1,4 +1,4 @@
-"""Worker scheduling policy (RLinf Sec. 3.4 "Scheduling Policy", Alg. 1).
+"""Worker scheduling policy (RLinf Sec. 3.4, Alg. 1).
 
 Given a workflow graph, an execution-time estimate for every component and
 a device count, find the placement that minimises the time of one
@@ -8,14 +8,14 @@ iteration:
   - a (sub)graph is split along every s-t cut into an upstream part G_s and
     a downstream part G_t (no edge from G_t back to G_s), and for each cut
     - temporal: G_s and G_t share all N devices, G_t starts after G_s, and
-      switching between them costs the offload of G_s's device state plus
-      the reload of G_t's (Sec. 3.4: "plus any resource offloading and
-      reloading overhead");
+      the switch between them costs moving G_s's device state out and G_t's
+      in (Sec. 3.4);
     - spatial: G_s gets N_s devices and G_t the other N_t, and they run as a
-      pipeline over micro-batches of m items (Sec. 3.4:
-      T_critical + (M/m - 1) * T_bottleneck);
-  - the recursion ends at single nodes, whose time is the estimate E;
-  - results are memoised per (subgraph, devices, batch).
+      pipeline over micro-batches of m items, one micro-batch's time through
+      both stages plus (M/m - 1) times the slower stage (Sec. 3.4);
+  - a single node's time is its estimate E;
+  - the best time of every (subgraph, devices, batch) is cached, so each is
+    solved once however many cuts reach it.
 
 Readings (the paper leaves these open):
   - a pipeline's micro-batch times are the subgraphs' own estimates at batch
@@ -178,14 +178,21 @@ def pipelining_time(t_s: float, t_t: float, M: int, m: int) -> float:
 
 
 class Scheduler:
-    """FindSchedule over a workflow; switch_bw = host link bytes/s per
-    device for the temporal mode's offload + reload."""
+    """Schedule search over a workflow; switch_bw = host link bytes/s per
+    device for the temporal mode's offload + reload.
+
+    best(nodes, N, M) is the minimum over the candidates of every s-t cut of
+    `nodes`: the temporal candidate, and the pipeline candidates of every
+    (device split, micro-batch), whose stage times come from a table of the
+    two sides' best times at each device count.  Results are cached per
+    (nodes, N, M)."""
 
     def __init__(self, wf: Workflow, switch_bw: float = INF, min_micro: int = 1):
         self.wf = collapse_cycles(wf)
         self.switch_bw = switch_bw
         self.min_micro = min_micro
         self.memo: Dict[Tuple[FrozenSet[str], int, int], Tuple[float, Optional[Schedule]]] = {}
+        self._cuts: Dict[FrozenSet[str], List[Tuple[FrozenSet[str], FrozenSet[str]]]] = {}
 
     def switch_cost(self, S: FrozenSet[str], T: FrozenSet[str]) -> float:
         if self.switch_bw == INF:
@@ -199,39 +206,52 @@ class Scheduler:
             return INF
         return c.time(N, M)
 
-    def find(self, nodes: FrozenSet[str], N: int, M: int) -> Tuple[float, Optional[Schedule]]:
+    def cuts(self, nodes: FrozenSet[str]):
+        if nodes not in self._cuts:
+            self._cuts[nodes] = st_cuts(nodes, self.wf.edges)
+        return self._cuts[nodes]
+
+    # -- candidates ------------------------------------------------------------
+    def _temporal(self, S, T, N, M):
+        ts, ss = self.best(S, N, M)
+        tt, st = self.best(T, N, M)
+        return ts + tt + self.switch_cost(S, T), Schedule("temporal", N, M, parts=(ss, st))
+
+    def _pipelines(self, S, T, N, M):
+        splits = device_splits(N)
+        for m in micro_batches(M, self.min_micro):
+            up = {n: self.best(S, n, m) for n in splits}
+            down = {n: self.best(T, n, m) for n in {N - k for k in splits}}
+            for Ns in splits:
+                (a, sa), (b, sb) = up[Ns], down[N - Ns]
+                if a < INF and b < INF:
+                    yield pipelining_time(a, b, M, m), Schedule("pipeline", N, M, parts=(sa, sb), micro_batch=m)
+
+    def _candidates(self, nodes, N, M):
+        for S, T in self.cuts(nodes):
+            yield self._temporal(S, T, N, M)
+            yield from self._pipelines(S, T, N, M)
+
+    def best(self, nodes: FrozenSet[str], N: int, M: int) -> Tuple[float, Optional[Schedule]]:
         key = (nodes, N, M)
-        if key in self.memo:
-            return self.memo[key]
+        hit = self.memo.get(key)
+        if hit is not None:
+            return hit
         if len(nodes) == 1:
             (u,) = tuple(nodes)
             res = (self.node_time(u, N, M), Schedule("node", N, M, node=u))
-            self.memo[key] = res
-            return res
-        best, sched = INF, None
-        for S, T in st_cuts(nodes, self.wf.edges):
-            ts, ss = self.find(S, N, M)
-            tt, st = self.find(T, N, M)
-            t = ts + tt + self.switch_cost(S, T)
-            if t < best:
-                best, sched = t, Schedule("temporal", N, M, parts=(ss, st))
-            for Ns in device_splits(N):
-                Nt = N - Ns
-                for m in micro_batches(M, self.min_micro):
-                    a, sa = self.find(S, Ns, m)
-                    if a == INF:
-                        continue
-                    b, sb = self.find(T, Nt, m)
-                    if b == INF:
-                        continue
-                    t = pipelining_time(a, b, M, m)
-                    if t < best:
-                        best, sched = t, Schedule("pipeline", N, M, parts=(sa, sb), micro_batch=m)
-        self.memo[key] = (best, sched)
-        return best, sched
+        else:
+            res = (INF, None)
+            for cand in self._candidates(nodes, N, M):
+                if cand[0] < res[0]:
+                    res = cand
+        self.memo[key] = res
+        return res
+
+    find = best
 
     def schedule(self, N: int, M: int) -> Tuple[float, Optional[Schedule]]:
-        return self.find(frozenset(self.wf.components), N, M)
+        return self.best(frozenset(self.wf.components), N, M)
 
 
 def brute_force(wf: Workflow, N: int, M: int, switch_bw: float = INF, min_micro: int = 1) -> float:
