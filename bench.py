@@ -62,12 +62,13 @@ def parse():
     ap.add_argument("--workload", default="qwen7b")
     ap.add_argument("--slots", type=int, default=256, help="--stage continuous: KV slots (sequences in flight)")
     ap.add_argument("--emit-every", type=int, default=64, help="--stage continuous: responses per emitted chunk")
-    ap.add_argument("--stage", choices=("rollout", "score", "switch", "continuous"), default="rollout",
+    ap.add_argument("--stage", choices=("rollout", "score", "switch", "continuous", "embodied"), default="rollout",
                     help="rollout: the decode hot path (default); score: the inference stage "
                          "(log-probabilities of given responses, one GRPO group per call); switch: "
                          "context-switch cost (weights and live K/V to pinned host memory and back); "
                          "continuous: the rollout's 512 sequences through fewer slots, continuous batching "
-                         "with chunked emission against static batches of the same size")
+                         "with chunked emission against static batches of the same size; embodied: the "
+                         "Llama-2-7B-shaped policy over 256 environments, env steps of prefill + 6 decode steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -510,6 +511,117 @@ def cpu_baseline_rollout(shape, weights, seconds: float):
             "single_thread_value": round(n1 / el1, 4), "cpu_model": cpu_model()}
 
 
+def describe_shape(m):
+    return (f"{m.n_layers} layers, hidden {m.hidden}, {m.n_q_heads} q / {m.n_kv_heads} kv heads of {m.head_dim}, "
+            f"ffn {m.ffn}, vocab {m.vocab}, {m.dtype}")
+
+
+def embodied_main(args):
+    """The embodied workload (Llama-2-7B-shaped policy, 256 parallel
+    environments), one env step at a time: every env's observation is a
+    fresh prefill of 256 caller-provided patch rows (seeded N(0, 1) per env
+    and step) plus 32 text tokens, then 6 decode steps for the remaining
+    action tokens (7 per env step, the first sampled by the prefill); the K/V
+    of the previous step is dropped.  K env steps are timed after W warm-up
+    env steps."""
+    import numpy as np
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights, patch_rows
+    from paper_2509_15965_amd.rl_decode import Engine
+
+    wl = WORKLOADS["llama7b-embodied"]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    E, R, TXT, ACT = wl.n_prompts, wl.patch_rows, wl.prompt_len[0], wl.response_cap
+    plen = R + TXT
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
+    eng = Engine(shape, weights, max_seqs=E, max_ctx=plen + ACT, max_prefill_tokens=E * plen, device=dev)
+    stream = eng.stream
+    slots = np.arange(E, dtype=np.int32)
+    offs = (np.arange(E + 1) * plen).astype(np.int32)
+    rng = np.random.default_rng(wl.seed)
+    text = torch.as_tensor(rng.integers(0, shape.vocab, size=(E, TXT)).astype(np.int32), device=dev)
+    # prompt ids: -(e*R + r) - 1 selects patch row r of env e, then the text tokens
+    rows_id = -(torch.arange(E * R, device=dev, dtype=torch.int32).view(E, R) + 1)
+    tokens = torch.cat([rows_id, text], dim=1).reshape(-1).contiguous()
+    toks = torch.empty((ACT, E), dtype=torch.int32, device=dev)
+    logps = torch.empty((ACT, E), dtype=torch.float32, device=dev)
+    n_env_steps = args.steps if args.steps else 4
+    warm = min(args.warmup, 1)
+    seed, T = 20250919, wl.temperature
+    kv_tok = shape.kv_bytes_per_token()
+
+    def observe(k):
+        return patch_rows(E * R, shape.hidden, wl.seed * 1000 + k, device=dev)
+
+    def env_step(k, emb, timing=None):
+        uids = (np.arange(E, dtype=np.uint64) * np.uint64(wl.env_steps) + np.uint64(k))
+        eng.release(slots)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        eng.prefill(slots, uids, offs, tokens, toks[0], logps[0], group=1, embeds=emb, seed=seed, temperature=T)
+        ev[1].record(stream)
+        for j in range(1, ACT):
+            eng.step(slots, uids, toks[j - 1], toks[j], logps[j], seed=seed, temperature=T)
+        ev[2].record(stream)
+        if timing is not None:
+            timing.append(ev)
+
+    for k in range(warm):
+        env_step(10_000 + k, observe(10_000 + k))
+    # the observations (the environments' output) exist before the timed region
+    obs = [observe(k) for k in range(n_env_steps)]
+    torch.cuda.synchronize()
+    timing = []
+    t0 = time.perf_counter()
+    for k in range(n_env_steps):
+        env_step(k, obs[k], timing)
+        print(f"[bench] env step {k + 1}/{n_env_steps} enqueued", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    pre_ms = sum(e[0].elapsed_time(e[1]) for e in timing)
+    dec_ms = sum(e[1].elapsed_time(e[2]) for e in timing)
+    # decode-step algorithmic bytes: parameters + every env's K/V context and new row + embedding row
+    dec_bytes = sum(shape.decode_params() * shape.elem_bytes + E * ((plen + j + 1) * kv_tok + kv_tok +
+                                                                    shape.hidden * shape.elem_bytes + 12)
+                    for j in range(ACT - 1)) * n_env_steps
+    L, H, F, V = shape.n_layers, shape.hidden, shape.ffn, shape.vocab
+    qkv = (shape.n_q_heads + 2 * shape.n_kv_heads) * shape.head_dim
+    pre_flops = (2.0 * E * plen * (L * (H * qkv + shape.n_q_heads * shape.head_dim * H + 3 * H * F)) +
+                 2.0 * E * H * V + 4.0 * L * shape.n_q_heads * shape.head_dim * E * plen * (plen + 1) / 2) * n_env_steps
+    finite = bool(torch.isfinite(logps).all())
+    out = {
+        "metric": "embodied rollout env-steps/sec (1 GPU), Llama-2-7B-shaped policy, 256 envs",
+        "value": round(E * n_env_steps / wall, 2),
+        "unit": "env steps/s",
+        "n_gpus": 1,
+        "steps": n_env_steps,
+        "warmup": warm,
+        "ms_per_step": round(wall * 1e3 / n_env_steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": f"synthetic (seeded random-init weights, {wl.init} init; N(0,1) patch rows, uniform text tokens)",
+        "config": {"workload": f"{wl.name}: {describe_shape(shape)}; {E} envs, each env step a fresh prefill of "
+                               f"{R} patch rows + {TXT} text tokens then {ACT - 1} decode steps ({ACT} action "
+                               f"tokens), K/V dropped between env steps"},
+        "action_tokens_per_s": round(E * ACT * n_env_steps / wall, 1),
+        "prefill_ms_per_env_step": round(pre_ms / n_env_steps, 3),
+        "decode_ms_per_env_step": round(dec_ms / n_env_steps, 3),
+        "prefill_TFLOPs": round(pre_flops / (pre_ms * 1e9), 1),
+        "prefill_mfma_frac": round(pre_flops / (pre_ms * 1e9) / BF16_PEAK_TFLOPS, 4),
+        "decode_step_alg_GBps": round(dec_bytes / (dec_ms * 1e6), 1),
+        "decode_step_hbm_frac": round(dec_bytes / (dec_ms * 1e6) / HBM_PEAK_GBS, 4),
+        "all_finite": finite,
+    }
+    eng.close()
+    print(json.dumps(out), flush=True)
+
+
 def sample_steps(max_steps: int, k: int):
     """k decode steps spread evenly over the rollout (all steps when k <= 0
     or k >= max_steps)."""
@@ -536,6 +648,9 @@ def main():
         return
     if args.stage == "continuous":
         continuous_main(args)
+        return
+    if args.stage == "embodied":
+        embodied_main(args)
         return
     import numpy as np
     import torch
@@ -661,7 +776,8 @@ def main():
     roll_gbs_u = float(unique.sum()) / rollout_gpu / 1e9
     prompt_tokens = int(plens.sum())
     out = {
-        "metric": "rollout tokens/sec (1 GPU) at 7B shape; decode-step HBM GB/s vs peak",
+        "metric": "rollout tokens/sec (1 GPU) at 7B shape; decode-step HBM GB/s vs peak" if wl.name == "qwen7b"
+                  else f"rollout tokens/sec (1 GPU), {wl.name} workload; decode-step HBM GB/s vs peak",
         "value": round(gen / wall_s, 1),
         "unit": "generated tokens/s",
         "n_gpus": 1,
@@ -673,11 +789,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": f"synthetic (seeded random-init weights, {wl.init} init, and uniform prompt tokens)",
-        "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped decoder (28 layers, hidden 3584, 28 q / 4 kv heads, "
-                               f"ffn 18944, vocab 152064); {P} prompts x {G} samples, prompts U[{wl.prompt_len[0]},"
-                               f"{wl.prompt_len[1]}], lognormal responses (median {wl.response_median}, sigma "
-                               f"{wl.response_sigma}, cap {wl.response_cap}); the timed steps are spread evenly "
-                               f"over the whole rollout",
+        "config": {"workload": f"{wl.name}: {describe_shape(shape)}; {P} prompts x {G} samples, prompts "
+                               f"U[{wl.prompt_len[0]},{wl.prompt_len[1]}], lognormal responses (median "
+                               f"{wl.response_median}, sigma {wl.response_sigma}, cap {wl.response_cap}); the timed "
+                               f"steps are spread evenly over the whole rollout",
                    "n_seqs": n_seq, "prompt_tokens": prompt_tokens, "decode_steps_in_rollout": max_steps,
                    "timed_steps": sampled if len(sampled) <= 64 else f"all {len(sampled)}",
                    "generated_tokens_timed": gen},

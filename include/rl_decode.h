@@ -391,8 +391,9 @@ typedef enum rl_kernel_class {
     RL_K_SPLITK_REDUCE, RL_K_SAMPLE, RL_K_COUNT
 } rl_kernel_class;
 
-/* Accumulated per-class figures since the last reset, collected while
- * RL_OPT_PROFILE is on.  alg_bytes / alg_flops are the algorithmic HBM bytes
+/* Accumulated per-class figures since the last reset, collected for the
+ * launches made while RL_OPT_PROFILE selects the class (launches made with
+ * the class deselected are neither counted nor timed).  alg_bytes / alg_flops are the algorithmic HBM bytes
  * and FLOPs of the launches (what the operation must move or compute, not
  * what the kernel happens to move).  Synchronises the stream. */
 typedef struct rl_kernel_stats {

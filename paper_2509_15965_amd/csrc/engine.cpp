@@ -186,14 +186,18 @@ hipError_t harvest(rl_decode_ctx* c) {
     return hipSuccess;
 }
 
+// Launches of a class are counted (with their algorithmic bytes and FLOPs)
+// and timed only while RL_OPT_PROFILE selects the class.
 struct Prof {
-    rl_decode_ctx* c; int kc; hipEvent_t a = nullptr;
+    rl_decode_ctx* c; int kc; hipEvent_t a = nullptr; bool on = false;
     Prof(rl_decode_ctx* c_, int kc_) : c(c_), kc(kc_) {
-        if ((c->profile >> kc) & 1u) {
+        on = ((c->profile >> kc) & 1u) != 0;
+        if (on) {
             if ((a = get_event(c))) (void)hipEventRecord(a, c->stream);
         }
     }
     void done(double bytes, double flops) {
+        if (!on) return;
         c->stats[kc].launches += 1;
         c->stats[kc].alg_bytes += bytes;
         c->stats[kc].alg_flops += flops;

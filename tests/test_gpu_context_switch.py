@@ -146,3 +146,50 @@ def test_switch_argument_errors():
         eng.kv_onload([3], [58], small[:100])                                            # too small
     assert eng.kv_offload_bytes([99]) == 0
     eng.close()
+
+
+@pytest.mark.parametrize("shape", [GQA, WORKLOADS["tiny"].model], ids=["bf16", "fp32"])
+def test_switched_continuation_matches_oracle(shape):
+    """After offload, new device buffers (rebind) and onload into renumbered
+    slots, the continuation's logits and log-probabilities against the
+    oracle run of the same sequences, at the stated bars (bf16) or 1e-4
+    (fp32)."""
+    import oracle
+    from harness import (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL, LOGIT_REL_TOL, LOGP_ABS_TOL, OracleRollout,
+                         row_rel_err)
+    w_dev, _, om = build_models(shape, 65)
+    prompts = _case(shape)
+    old, new = list(range(6)), [11, 7, 9, 6, 10, 8]
+    group = 3
+    eng = _engine(shape, w_dev)
+    _prefill(eng, old, prompts, group)
+    orc = OracleRollout(om, 128)
+    for p, pr in enumerate(prompts):
+        orc.prefill(old[p * group], pr)
+        for k in range(1, group):
+            orc.seqs[old[p * group + k]] = orc.seqs[old[p * group]].clone()
+    for k in range(3):
+        _step(eng, old, k, shape.vocab)
+        tin = uniform_tokens(len(old), shape.vocab, 70 + k)
+        for i, s in enumerate(old):
+            orc.step(s, tin[i])
+    lengths = [eng.slot_length(s) for s in old]
+    host = torch.empty(eng.kv_offload_bytes(old), dtype=torch.uint8, pin_memory=True)
+    eng.kv_offload(old, host)
+    torch.cuda.synchronize()
+    eng.release(old)
+    w2 = {k: v.clone() for k, v in w_dev.items()}
+    kv2 = torch.full_like(eng.kv, 0x7F)
+    ws2 = torch.full_like(eng.ws, 0x3C)
+    eng.kv.zero_()
+    eng.rebind(w2, kv2, ws2)
+    eng.kv_onload(new, lengths, host)
+    tol = (LOGIT_REL_TOL, LOGP_ABS_TOL) if shape.dtype == "bf16" else (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL)
+    for k in range(3, 6):
+        lg, ot, ol = _step(eng, new, k, shape.vocab)
+        tin = uniform_tokens(len(new), shape.vocab, 70 + k)
+        for i, s in enumerate(old):
+            z = orc.step(s, tin[i])
+            assert row_rel_err(lg[i], z) < tol[0], (k, i)
+            assert abs(ol[i] - oracle.logprob(z.astype(np.float32), 1.0, int(ot[i]))) < tol[1], (k, i)
+    eng.close()

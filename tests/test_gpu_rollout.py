@@ -82,3 +82,44 @@ def test_continuous_batching_bf16_responses_are_complete():
         assert len(r.tokens) == resp[q] and r.prompt == q // G
         assert np.all((r.tokens >= 0) & (r.tokens < GQA.vocab))
         assert np.isfinite(r.logps).all() and np.all(r.logps <= 1e-6)
+
+
+def test_continuous_batching_fp32_matches_oracle():
+    """Continuous batching through 5 slots against the oracle, sequence by
+    sequence: the oracle prefills the prompt and then follows the GPU's
+    token stream, and at every position the GPU's token must be the oracle's
+    sample (a near tie excused only if the GPU took the runner-up) and its
+    log-probability the oracle's within 1e-4."""
+    import oracle
+    from harness import F32_LOGP_ABS_TOL, check_token
+    shape = WORKLOADS["tiny"].model
+    w_dev, _, om = build_models(shape, 85)
+    P, G, seed, T = 4, 3, 9, 1.0
+    prompts, resp, uids = _workload(shape, P, G, 86)
+    resp = np.minimum(resp, 14)
+    max_ctx = max(len(p) for p in prompts) + int(resp.max())
+    eng = Engine(shape, w_dev, max_seqs=5, max_ctx=max_ctx, max_prefill_tokens=sum(len(p) for p in prompts))
+    chunks = []
+    ro = ContinuousRollout(eng, prompts, G, resp, uids, seed=seed, temperature=T, n_slots=5, emit_every=4,
+                           on_emit=chunks.append)
+    ro.run()
+    eng.close()
+    got = _by_uid([r for c in chunks for r in c])
+    assert sorted(got) == sorted(int(u) for u in uids)
+    excused, checked = [], 0
+    for q, u in enumerate(uids):
+        r = got[int(u)]
+        assert len(r.tokens) == resp[q]
+        s = om.new_seq(max_ctx)
+        for t in prompts[q // G]:
+            z = s.forward(int(t))
+        for j, tok in enumerate(r.tokens):
+            pos = s.length
+            assert check_token(int(tok), z, T, seed, int(u), pos, excused), (int(u), j)
+            lp = oracle.logprob(z.astype(np.float32), T, int(tok))
+            assert abs(float(r.logps[j]) - lp) < F32_LOGP_ABS_TOL, (int(u), j)
+            checked += 1
+            if j + 1 < len(r.tokens):
+                z = s.forward(int(tok))
+    print(f"{checked} tokens checked, {len(excused)} near ties excused", flush=True)
+    assert checked == int(resp.sum())
