@@ -267,6 +267,31 @@ rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits,
                            const int32_t* forced, const rl_sample_params* sp,
                            int32_t* out_tok, float* out_logp);
 
+/* Allocation-free variant of rl_sample_logits, for callers that cannot
+ * allocate device memory or own a workspace: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Needs no context,
+ * calls no allocating routine, and gives the same tokens and
+ * log-probabilities as rl_sample_logits for the same inputs.
+ *  n          rows, 0 <= n <= 2^20 (0 is a no-op).
+ *  vocab      entries per row, a multiple of 4, <= 2^24.
+ *  logits     device float [n][ld], 16-byte aligned; ld >= vocab, ld % 4 == 0.
+ *  seq_uids   device uint64 [n]; pos_new device int32 [n] (>= 0): the noise
+ *             key of each row, as in rl_decode_step.
+ *  forced     device int32 [n] or NULL.  sp host (as rl_decode_step).
+ *  out_tok, out_logp  device [n].
+ *  stream     hipStream_t of the current device.
+ * The per-chunk partial results go to a fixed device array of the library
+ * (4096 entries of 16 bytes, 64 KiB; every n fits), one per device, held
+ * until the process ends.  Every call on a device shares that array: calls
+ * that overlap on one device (two streams, or two threads) race and give
+ * wrong results; calls on one stream are ordered and safe.
+ * RL_ERR_INVALID_ARG for bad sizes or pointers, RL_ERR_CAPACITY if a launch
+ * would need more partials than the array holds, RL_ERR_HIP if the launch
+ * or the array's lookup fails. */
+rl_status rl_sample_logits_noalloc(int32_t n, int32_t vocab, const float* logits, int32_t ld,
+                                   const uint64_t* seq_uids, const int32_t* pos_new, const int32_t* forced,
+                                   const rl_sample_params* sp, int32_t* out_tok, float* out_logp, void* stream);
+
 /* ---------------------------------------------------------------------
  * Slot bookkeeping (host only; nothing is enqueued).
  * ------------------------------------------------------------------- */

@@ -24,6 +24,7 @@ constexpr int kPartItems = 8192;            // split-KV partial slots per call
 constexpr int kAttnWaveTarget = 1024;       // split-KV: keep about one wave per SIMD, each as long as possible
 constexpr int kSharedDecodeChunk = 256;     // split-KV keys per item in decode steps that read shared prompts
 constexpr int kPrefillChunk = 1024;         // default keys per prefill work item
+constexpr int kNoAllocMaxRows = 1 << 20;    // rows of one rl_sample_logits_noalloc call
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -1411,6 +1412,24 @@ rl_status rl_sample_logits(rl_decode_ctx* ctx, int32_t n, const float* logits, c
     if (e != hipSuccess) return hip_fail(c, e, "sample launch");
     pr.done(n * (c->cfg.vocab * 4.0 + 8.0), 0.0);
     return RL_OK;
+}
+
+rl_status rl_sample_logits_noalloc(int32_t n, int32_t vocab, const float* logits, int32_t ld,
+                                   const uint64_t* seq_uids, const int32_t* pos_new, const int32_t* forced,
+                                   const rl_sample_params* sp, int32_t* out_tok, float* out_logp, void* stream) {
+    if (n < 0 || n > kNoAllocMaxRows) return RL_ERR_INVALID_ARG;
+    if (vocab < 1 || vocab > (1 << 24) || vocab % 4 != 0 || ld < vocab || ld % 4 != 0) return RL_ERR_INVALID_ARG;
+    if (!sp || sp->reserved != 0 || !(sp->temperature >= 0.0f) || !std::isfinite(sp->temperature))
+        return RL_ERR_INVALID_ARG;
+    if (n == 0) return RL_OK;
+    if (!logits || !seq_uids || !pos_new || !out_tok || !out_logp) return RL_ERR_INVALID_ARG;
+    if (!aligned(logits, 16)) return RL_ERR_INVALID_ARG;
+    if (sample_parts_needed(n, vocab) > static_cast<size_t>(kStaticSampleParts)) return RL_ERR_CAPACITY;
+    SamplePart* parts = nullptr;
+    if (static_sample_parts(&parts) != hipSuccess) return RL_ERR_HIP;
+    const hipError_t e = launch_sample(logits, ld, n, vocab, nullptr, seq_uids, pos_new, forced, sp->seed,
+                                       sp->temperature, parts, out_tok, out_logp, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? RL_OK : RL_ERR_HIP;
 }
 
 namespace {

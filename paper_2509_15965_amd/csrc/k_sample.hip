@@ -13,6 +13,9 @@
 #include "rl_device.h"
 #include "rl_internal.h"
 
+#include <mutex>
+#include <vector>
+
 namespace rl {
 
 __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
@@ -228,16 +231,31 @@ hipError_t launch_gumbel_bound_probe(uint32_t lo, uint64_t count, int n_blocks, 
     return hipGetLastError();
 }
 
+// Vocabulary split of a sampling launch: about 2048 workgroups in all, chunks
+// of whole 1024-entry blocks, at most kSampleMaxChunks per row.
+static void sample_split(int n, int V, int* nchunks_out, int* chunk_out) {
+    int nchunks = (2048 + n - 1) / n;
+    nchunks = nchunks < 1 ? 1 : nchunks > kSampleMaxChunks ? kSampleMaxChunks : nchunks;
+    int chunk = (V + nchunks - 1) / nchunks;
+    chunk = (chunk + 1023) / 1024 * 1024;
+    *nchunks_out = (V + chunk - 1) / chunk;
+    *chunk_out = chunk;
+}
+
+size_t sample_parts_needed(int n, int V) {
+    if (n <= 0) return 0;
+    int nchunks, chunk;
+    sample_split(n, V, &nchunks, &chunk);
+    return nchunks > 1 ? static_cast<size_t>(n) * nchunks : 0;
+}
+
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
                          uint64_t seed, float T, SamplePart* parts,
                          int32_t* out_tok, float* out_logp, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    int nchunks = (2048 + n - 1) / n;
-    nchunks = nchunks < 1 ? 1 : nchunks > kSampleMaxChunks ? kSampleMaxChunks : nchunks;
-    int chunk = (V + nchunks - 1) / nchunks;
-    chunk = (chunk + 1023) / 1024 * 1024;
-    nchunks = (V + chunk - 1) / chunk;
+    int nchunks, chunk;
+    sample_split(n, V, &nchunks, &chunk);
     hipLaunchKernelGGL(sample_kernel, dim3(n, nchunks), dim3(256), 0, s, logits, ld, V, logit_row, uid,
                        pos_new, forced, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
                        T, chunk, parts, out_tok, out_logp);
@@ -294,6 +312,32 @@ hipError_t launch_logprob(const float* logits, int ld, int n_rows, int V, const 
     hipLaunchKernelGGL(logprob_kernel, dim3(n_rows), dim3(256), 0, s, logits, ld, V, row_items, item_idx,
                        targets, T, out);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free sampling: the chunk partials live in a file-scope device
+// array instead of a caller's workspace.  Each device the library runs on
+// holds its own copy until the process ends; host code reaches it only
+// through the address hipGetSymbolAddress returns on that device.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) SamplePart scratch[kStaticSampleParts];
+
+hipError_t static_sample_parts(SamplePart** out) {
+    static std::mutex mu;
+    static std::vector<SamplePart*> addr;   // per device ordinal
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    if (static_cast<size_t>(dev) >= addr.size()) addr.resize(static_cast<size_t>(dev) + 1, nullptr);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<SamplePart*>(p);
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace rl

@@ -166,6 +166,16 @@ hipError_t launch_logprob(const float* logits, int ld, int n_rows, int V, const 
                           const int32_t* item_idx, const int32_t* targets, float T, float* out,
                           hipStream_t s);
 
+// SampleParts a launch over n rows of V logits writes (0: a single chunk per
+// row, no partials).
+size_t sample_parts_needed(int n, int V);
+
+// The sampler's allocation-free partial buffer: kStaticSampleParts entries
+// in device memory of the current device (n * ceil(2048 / n) < 4096 for every
+// n, so every launch fits).
+constexpr int kStaticSampleParts = 4096;
+hipError_t static_sample_parts(SamplePart** out);
+
 hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_t* logit_row,
                          const uint64_t* uid, const int32_t* pos_new, const int32_t* forced,
                          uint64_t seed, float T, SamplePart* parts,

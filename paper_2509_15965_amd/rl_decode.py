@@ -34,7 +34,7 @@ EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create"
            "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
            "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
            "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_gumbel_bound",
-           "rl_status_string", "rl_decode_last_error")
+           "rl_sample_logits_noalloc", "rl_status_string", "rl_decode_last_error")
 
 
 class ModelConfig(C.Structure):
@@ -117,6 +117,8 @@ def lib():
     L.rl_decode_attn_plan_stats.argtypes = [vp, C.POINTER(AttnPlanStats)]
     L.rl_probe_copy.restype = C.c_int
     L.rl_probe_copy.argtypes = [vp, vp, sz, vp]
+    L.rl_sample_logits_noalloc.restype = C.c_int
+    L.rl_sample_logits_noalloc.argtypes = [i32, i32, vp, i32, vp, vp, vp, C.POINTER(SampleParams), vp, vp, vp]
     L.rl_probe_gumbel_bound.restype = C.c_int
     L.rl_probe_gumbel_bound.argtypes = [C.c_uint32, C.c_uint64, i32, vp, vp, vp]
     L.rl_status_string.restype = C.c_char_p
@@ -337,3 +339,18 @@ def probe_gumbel_bound(lo: int, count: int, n_blocks: int = 4096, device="cuda")
         raise RLError(st, "rl_probe_gumbel_bound")
     torch.cuda.synchronize(device)
     return int(viol.to(torch.int64).sum().item()), float(mm.min().item())
+
+
+def sample_logits_noalloc(logits: torch.Tensor, uids: torch.Tensor, pos_new: torch.Tensor, out_tok: torch.Tensor,
+                          out_logp: torch.Tensor, *, forced: Optional[torch.Tensor] = None, seed: int = 0,
+                          temperature: float = 1.0, stream=None):
+    """rl_sample_logits_noalloc: logits [n][ld] fp32, uids uint64 (int64
+    tensor) and pos_new int32 on the device."""
+    n, ld = int(logits.shape[0]), int(logits.stride(0))
+    stream = stream if stream is not None else torch.cuda.current_stream(logits.device)
+    sp = SampleParams(seed, temperature, 0)
+    st = lib().rl_sample_logits_noalloc(n, int(logits.shape[1]), logits.data_ptr(), ld, uids.data_ptr(),
+                                        pos_new.data_ptr(), _p(forced), C.byref(sp), out_tok.data_ptr(),
+                                        out_logp.data_ptr(), stream.cuda_stream)
+    if st != RL_OK:
+        raise RLError(st, "rl_sample_logits_noalloc")
