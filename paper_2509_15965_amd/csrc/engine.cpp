@@ -577,6 +577,12 @@ int choose_chunk(const std::vector<Block>& blocks, int Hkv, int64_t forced, int 
             // 7.4% less attention time than the long-item rule (512: 6.8% less,
             // 128: 1% less).
             C = kSharedDecodeChunk;
+            // few rows: shorter items, so that enough waves stream the keys
+            while (C > 64) {
+                count(C, &items, &multi, &most);
+                if (items * Hkv >= 2 * kAttnWaveTarget) break;
+                C /= 2;
+            }
         } else {
             C = 64;
             while (C < (1 << 16)) {

@@ -159,19 +159,25 @@ def test_shared_prompt_counts_each_prompt_once():
 G7 = ModelShape(2, 512, 14, 2, 128, 1024, 1032, 1e-6, 1e4, "bf16")
 
 
-def test_lds_staged_shared_chunks_group16_gqa7():
+@pytest.mark.parametrize("chunk,n_chunks", [(256, 3), (0, 10)], ids=["256-key", "auto"])
+def test_lds_staged_shared_chunks_group16_gqa7(chunk, n_chunks):
     """The decode attention path of the 7B-shape rollout: 7 q-heads per
     kv-head (two sequences per pair item) and GRPO groups of 16, so each
     shared prompt chunk is read by 8 pair items, i.e. two workgroups of four
     items over one chunk that stage each K/V step through LDS once.  One
     650-token prompt, group 16, prefill and 4 teacher-forced decode steps,
     every row against the oracle at the stated bars; the plan counters show
-    the LDS-staged workgroups were launched."""
+    the LDS-staged workgroups were launched.  With 256-key items (what the
+    rollout's steps at 512 rows use) the 640 shared positions make 3 chunks;
+    with the automatic choice this small step takes 64-key items (few rows:
+    shorter items), 10 chunks."""
     rng = np.random.default_rng(56)
     P, G, steps = 650, 16, 4
     prompt = rng.integers(0, G7.vocab, size=P).astype(np.int32)
     w_dev, _, om = build_models(G7, 57)
     eng = Engine(G7, w_dev, max_seqs=G, max_ctx=P + steps + 2, max_prefill_tokens=P)
+    if chunk:
+        eng.set_option(RL_OPT_ATTN_CHUNK, chunk)
     orc = OracleRollout(om, P + steps + 2)
     slots = list(range(G))
     ot = torch.empty(G, dtype=torch.int32, device=DEV)
@@ -206,7 +212,7 @@ def test_lds_staged_shared_chunks_group16_gqa7():
     eng.close()
     print("worst logits rel / log-prob abs:", worst, "plan:", plan, flush=True)
     assert plan["steps"] == steps
-    # three shared chunks (positions 0-255, 256-511, 512-639), each read by
-    # 16 sequences = 8 pair items = two LDS-staged workgroups
-    assert plan["pair_items"] == steps * 3 * 8
-    assert plan["lds_workgroups"] == steps * 3 * 2
+    # every shared chunk of the 640 shared positions is read by 16 sequences
+    # = 8 pair items = two LDS-staged workgroups
+    assert plan["pair_items"] == steps * n_chunks * 8
+    assert plan["lds_workgroups"] == steps * n_chunks * 2
