@@ -67,13 +67,21 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
 }
 
 // The row's token (the arg-max) and the log-probability of the token, or of
-// `forced` when it is a vocabulary index.
+// `forced` when it is a vocabulary index.  A NaN score never wins a
+// comparison, so a row whose every score is NaN ranks no entry and keeps
+// the initial index: its token is -1 and its log-probability NaN (z is never
+// read at an index outside [0, V)).
 __device__ __forceinline__ void sample_finish(Best b, Lse a, const float* z, int V, int forced, float T, int o,
                                               int32_t* out_tok, float* out_logp) {
     const float lse = a.m + logf(a.s);
-    const int r = (forced >= 0 && forced < V) ? forced : b.v;
+    const bool ranked = b.v >= 0 && b.v < V;
+    const int r = (forced >= 0 && forced < V) ? forced : ranked ? b.v : -1;
+    out_tok[o] = ranked ? b.v : -1;
+    if (r < 0) {
+        out_logp[o] = __builtin_nanf("");
+        return;
+    }
     const float zr = T == 0.0f ? z[r] : z[r] / T;
-    out_tok[o] = b.v;
     out_logp[o] = zr - lse;
 }
 
