@@ -62,19 +62,44 @@ def parse():
     ap.add_argument("--workload", default="qwen7b")
     ap.add_argument("--slots", type=int, default=256, help="--stage continuous: KV slots (sequences in flight)")
     ap.add_argument("--emit-every", type=int, default=64, help="--stage continuous: responses per emitted chunk")
-    ap.add_argument("--stage", choices=("rollout", "score", "switch", "continuous", "embodied"), default="rollout",
+    ap.add_argument("--rows", default="1,8,16,32,64,128,256,512",
+                    help="--stage curve: batch sizes (comma-separated)")
+    ap.add_argument("--ctx", type=int, default=2048, help="--stage curve: context of every row")
+    ap.add_argument("--stage", choices=("rollout", "score", "switch", "continuous", "embodied", "curve"),
+                    default="rollout",
                     help="rollout: the decode hot path (default); score: the inference stage "
                          "(log-probabilities of given responses, one GRPO group per call); switch: "
                          "context-switch cost (weights and live K/V to pinned host memory and back); "
                          "continuous: the rollout's 512 sequences through fewer slots, continuous batching "
                          "with chunked emission against static batches of the same size; embodied: the "
-                         "Llama-2-7B-shaped policy over 256 environments, env steps of prefill + 6 decode steps")
+                         "Llama-2-7B-shaped policy over 256 environments, env steps of prefill + 6 decode steps; "
+                         "curve: decode steps at fixed batch sizes (--rows) and context (--ctx), per-class times")
+    ap.add_argument("--no-tune", action="store_true",
+                    help="keep the cost-model GEMM plans (skip the measured plans taken before warm-up)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run the library's plain copy kernel over this many MiB, 4 times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters against a known size)")
     return ap.parse_args()
+
+
+# Batch sizes at which the decode GEMM plans are measured before warm-up; a
+# step of n rows uses the plan of the smallest listed size >= n.
+TUNE_SIZES = (1, 2, 4, 8, 12, 16, 20, 24, 32, 40, 48, 64, 80, 96, 112, 128, 160, 192, 224, 256, 288, 320, 384,
+              448, 512)
+
+
+def tune_gemms(eng, max_rows: int, skip: bool):
+    """Measure the GEMM plans up to max_rows rows (untimed set-up, like the
+    warm-up); returns what was done for the JSON line."""
+    if skip:
+        return {"measured": False}
+    sizes = [n for n in TUNE_SIZES if n < max_rows] + [max_rows]
+    t0 = time.perf_counter()
+    eng.tune_gemms(sizes)
+    return {"measured": True, "sizes": len(sizes), "largest": max_rows,
+            "seconds": round(time.perf_counter() - t0, 2)}
 
 
 def copy_probe(mib: int):
@@ -368,6 +393,7 @@ def continuous_main(args):
     eng = Engine(shape, weights, max_seqs=S, max_ctx=int(plens.max() + resp.max()),
                  max_prefill_tokens=int(max(plens[i:i + per].sum() for i in range(0, P, per))), device=dev)
     seed, T = 20250919, wl.temperature
+    tuning = tune_gemms(eng, S, args.no_tune)
     # warm-up: a short static run
     w = StaticRollout(eng, plan["prompts"][:per], G, np.minimum(resp[:S], 16), uids[:S], seed, T)
     w.run()
@@ -420,6 +446,7 @@ def continuous_main(args):
         "speedup_vs_static": round(t_static / t_cont, 3),
         "first_chunk_s": round(marks[0][0], 3) if marks else None,
         "chunk_times_s": [round(m[0], 2) for m in marks],
+        "gemm_plans": tuning,
     }
     print(json.dumps(out), flush=True)
 
@@ -540,6 +567,7 @@ def embodied_main(args):
     weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     eng = Engine(shape, weights, max_seqs=E, max_ctx=plen + ACT, max_prefill_tokens=E * plen, device=dev)
     stream = eng.stream
+    tuning = tune_gemms(eng, E, args.no_tune)
     slots = np.arange(E, dtype=np.int32)
     offs = (np.arange(E + 1) * plen).astype(np.int32)
     rng = np.random.default_rng(wl.seed)
@@ -617,8 +645,103 @@ def embodied_main(args):
         "decode_step_alg_GBps": round(dec_bytes / (dec_ms * 1e6), 1),
         "decode_step_hbm_frac": round(dec_bytes / (dec_ms * 1e6) / HBM_PEAK_GBS, 4),
         "all_finite": finite,
+        "gemm_plans": tuning,
     }
     eng.close()
+    print(json.dumps(out), flush=True)
+
+
+def curve_main(args):
+    """Decode-step time against batch size: for every n in --rows, n rows of
+    --ctx positions each (own K/V, no shared prompt; seeded N(0, 1) cache),
+    W warm-up steps, then K timed steps (one event pair around all K), then
+    the same K steps again with every kernel class timed by HIP events.
+    Algorithmic bytes per step: the decode-read parameters plus every row's
+    K/V context, new K/V row, embedding row and 12 bytes of token /
+    log-probability; algorithmic flops: 2 per parameter and row plus the
+    attention's 4 * q-heads * head_dim per row and key."""
+    import torch
+
+    from paper_2509_15965_amd.configs import WORKLOADS
+    from paper_2509_15965_amd.inputs import make_weights
+    from paper_2509_15965_amd.rl_decode import KERNEL_CLASSES, RL_OPT_PROFILE, Engine
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rows = [int(x) for x in args.rows.split(",")]
+    K = args.steps if args.steps else 10
+    W = min(args.warmup, 3)
+    ctx = args.ctx
+    weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
+    eng = Engine(shape, weights, max_seqs=max(rows), max_ctx=ctx + W + 2 * K + 2, max_prefill_tokens=8,
+                 device=dev)
+    stream = eng.stream
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed)
+    kc, vc = eng.kv_views()
+    kc.normal_(generator=gen)
+    vc.normal_(generator=gen)
+    tuning = tune_gemms(eng, max(rows), args.no_tune)
+    es, kv_tok = shape.elem_bytes, shape.kv_bytes_per_token()
+    all_mask = (1 << len(KERNEL_CLASSES)) - 1
+    curve = []
+    for n in rows:
+        slots = list(range(n))
+        tok = torch.randint(0, shape.vocab, (n,), dtype=torch.int32, device=dev, generator=gen)
+        ot = torch.empty(n, dtype=torch.int32, device=dev)
+        ol = torch.empty(n, dtype=torch.float32, device=dev)
+        eng.set_lengths(slots, [ctx] * n)
+        for _ in range(W):
+            eng.step(slots, slots, tok, ot, ol)
+        eng.set_lengths(slots, [ctx] * n)
+        torch.cuda.synchronize()
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record(stream)
+        for _ in range(K):
+            eng.step(slots, slots, tok, ot, ol)
+        eb.record(stream)
+        torch.cuda.synchronize()
+        ms = ea.elapsed_time(eb) / K
+        eng.set_lengths(slots, [ctx] * n)
+        eng.reset_stats()
+        eng.set_option(RL_OPT_PROFILE, all_mask)
+        for _ in range(K):
+            eng.step(slots, slots, tok, ot, ol)
+        eng.set_option(RL_OPT_PROFILE, 0)
+        torch.cuda.synchronize()
+        st = eng.kernel_stats()
+        # mean context over the K timed steps: ctx + (K - 1) / 2 keys before the new one
+        mean_ctx = ctx + (K - 1) / 2.0
+        step_bytes = shape.decode_params() * es + n * ((mean_ctx + 1) * kv_tok + kv_tok + shape.hidden * es + 12)
+        classes = {}
+        for c in KERNEL_CLASSES:
+            d = st[c]
+            if d["launches"] == 0:
+                continue
+            e = {"ms_per_step": round(d["total_ms"] / K, 4)}
+            if c.startswith("gemm") and d["total_ms"] > 0:
+                tf = d["alg_flops"] / (d["total_ms"] * 1e9)
+                e.update({"TFLOPs": round(tf, 1), "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                          "GBps": round(d["alg_bytes"] / (d["total_ms"] * 1e6), 1)})
+            elif d["total_ms"] > 0:
+                e["GBps"] = round(d["alg_bytes"] / (d["total_ms"] * 1e6), 1)
+            classes[c] = e
+        gbs = step_bytes / (ms * 1e6)
+        curve.append({"rows": n, "ctx": ctx, "ms_per_step": round(ms, 4),
+                      "tokens_per_s": round(n / (ms * 1e-3), 1), "alg_GBps": round(gbs, 1),
+                      "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                      "profiled_ms_per_step": round(sum(st[c]["total_ms"] for c in KERNEL_CLASSES) / K, 4),
+                      "classes": classes})
+        print(f"[bench] rows {n}: {ms:.3f} ms per step", file=sys.stderr, flush=True)
+    eng.close()
+    out = {"metric": "decode-step time by batch size (1 GPU)", "unit": "ms/step", "n_gpus": 1, "steps": K,
+           "warmup": W, "higher_is_better": False, "dtype": "bf16",
+           "data": f"synthetic (seeded random-init weights, {wl.init} init; N(0,1) K/V cache)",
+           "config": {"workload": f"{wl.name}: {describe_shape(shape)}; every row {ctx} positions of its own "
+                                  f"K/V (no shared prompt)"},
+           "gemm_plans": tuning, "curve": curve}
     print(json.dumps(out), flush=True)
 
 
@@ -651,6 +774,9 @@ def main():
         return
     if args.stage == "embodied":
         embodied_main(args)
+        return
+    if args.stage == "curve":
+        curve_main(args)
         return
     import numpy as np
     import torch
@@ -685,7 +811,9 @@ def main():
     is_sampled[sampled] = True
     nominal, unique = rollout_step_bytes(shape, plens, resp, G, max_steps)
 
-    # ---- warm-up (untimed) ----
+    # ---- measured GEMM plans and warm-up (untimed) ----
+    tuning = tune_gemms(eng, n_seq, args.no_tune)
+    print(f"[bench] GEMM plans: {tuning}", file=sys.stderr, flush=True)
     ro.prefill()
     for t in range(min(args.warmup, max_steps)):
         ro.step(t)
@@ -813,6 +941,7 @@ def main():
                                                       (rollout_wall + prefill_s), 1)},
         "roofline": roof,
         "timed_classes": classes,
+        "gemm_plans": tuning,
     }
     eng.close()
     del eng, ro

@@ -108,7 +108,9 @@ typedef struct rl_weights {
 /* Sampling: seed keys the generator; temperature T >= 0 divides the logits
  * both for sampling and for the reported log-probability.  T == 0 selects
  * the arg-max token (lowest index on ties) and reports its T = 1
- * log-probability. */
+ * log-probability.  A NaN logit never wins: a row with NaN entries samples
+ * among its other entries and reports a NaN log-probability; a row of NaN
+ * logits gets token -1 (an input row of zeros if fed back) and NaN. */
 typedef struct rl_sample_params {
     uint64_t seed;
     float    temperature;
@@ -415,6 +417,38 @@ typedef enum rl_kernel_class {
     RL_K_ATTN_COMBINE, RL_K_GEMM_O, RL_K_GEMM_GATE_UP, RL_K_GEMM_DOWN, RL_K_GEMM_LM_HEAD,
     RL_K_SPLITK_REDUCE, RL_K_SAMPLE, RL_K_COUNT
 } rl_kernel_class;
+
+/* Measured GEMM plans.  The decode batch of a rollout shrinks from the whole
+ * batch to a few long responses (Sec. 2.2, the long tail), so the bf16
+ * projections run at every row count from max_seqs down to 1.  For each
+ * batch size in `sizes` (host array of n_sizes strictly increasing values in
+ * [1, max_seqs]) and each of the q|k|v, o, gate-up, down and LM-head
+ * projections, every plan of the cost model's search space (tile kernel,
+ * split-K count, two-segment launch) is timed on the context's stream with
+ * HIP events, each together with the kernel that consumes its output as a
+ * decode step issues it; the fastest few and the cost model's plan are then
+ * timed inside whole decode steps of that many rows, one projection at a
+ * time, and the fastest step's plan is kept.  A GEMM of M rows then uses the
+ * plan measured for the smallest listed size >= M; larger M keep the cost
+ * model, and RL_OPT_GEMM_PLAN still overrides.  n_sizes = 0 clears the
+ * table.  The context must hold no live sequence (every slot length 0:
+ * before the first prefill, or after releasing every slot; RL_ERR_INVALID_ARG
+ * otherwise): the measuring steps decode slots 0 .. largest size - 1 at a
+ * short context, overwrite their K/V and the workspace, and leave every
+ * length at 0.  Synchronises the stream.  Every plan gives results within
+ * the parity tolerances; the bits depend on the plan (fp32 summation
+ * order), so the table is part of a run's configuration.  bf16 models only
+ * (RL_ERR_UNSUPPORTED for fp32 when n_sizes > 0).  Takes about 0.3 s per
+ * size at the 7B shape. */
+rl_status rl_decode_tune_gemms(rl_decode_ctx* ctx, int32_t n_sizes, const int32_t* sizes);
+
+/* The plan a projection of class kclass (one of the five GEMM classes) at
+ * `rows` rows (1 .. max(max_seqs, max_prefill_tokens)) uses now, as an
+ * RL_OPT_GEMM_PLAN code in *plan_code, and its measured microseconds per
+ * layer (unit time with its consumer) in *tuned_us (may be NULL), or -1 when
+ * the plan comes from the cost model or the override.  bf16 models only. */
+rl_status rl_decode_gemm_plan(rl_decode_ctx* ctx, int32_t kclass, int32_t rows, int64_t* plan_code,
+                              float* tuned_us);
 
 /* Accumulated per-class figures since the last reset, collected for the
  * launches made while RL_OPT_PROFILE selects the class (launches made with

@@ -138,6 +138,9 @@ struct rl_decode_ctx {
     std::vector<hipEvent_t> ev_pool;
     rl_kernel_stats stats[RL_K_COUNT]{};
     rl_attn_plan_stats plan{};
+    // measured GEMM plans (rl_decode_tune_gemms), sorted by (class, rows)
+    struct TunedPlan { int kc, M, Nw, K, epi; GemmPlan p; float us; };
+    std::vector<TunedPlan> tuned;
     std::string err;
 
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
@@ -300,9 +303,43 @@ struct Fwd {
 // with `defer` set (q|k|v and residual projections) *splits reports the slice
 // count and the caller reduces.  A residual GEMM with one split adds into x
 // directly (bf16); the fp32 model always goes through the partial buffer.
+// The measured plan of the smallest tuned batch size >= M for this class and
+// GEMM shape (false: none tuned).
+bool tuned_plan(const rl_decode_ctx* c, int kc, int M, int Nw, int K, int epi, GemmPlan* p, float* us) {
+    for (const auto& t : c->tuned) {
+        if (t.kc != kc || t.Nw != Nw || t.K != K || t.epi != epi || t.M < M) continue;
+        *p = t.p;
+        if (us) *us = t.us;
+        return true;   // sorted by rows: the first match is the smallest
+    }
+    return false;
+}
+
+// Plan of a bf16 GEMM: the RL_OPT_GEMM_PLAN override when it can serve this
+// GEMM, else the measured plan, else the cost model.
+GemmPlan choose_plan(const rl_decode_ctx* c, int kc, int M, int Nw, int K, int epi) {
+    GemmPlan p;
+    const int F = c->cfg.ffn;
+    if (c->opt_gemm != 0 && plan_gemm_forced(M, Nw, K, epi, F, c->opt_gemm, &p)) return p;
+    if (tuned_plan(c, kc, M, Nw, K, epi, &p, nullptr)) return p;
+    return plan_gemm_bf16(M, Nw, K, epi, F);
+}
+
+rl_status run_gemm_plan(rl_decode_ctx* c, int kc, const GemmPlan* plan, const void* A, int lda, const void* W,
+                        int M, int Nw, int K, int epi, float* out_f32, int ldo, float* resid, int ldr, void* act,
+                        int ld_act, bool defer, int* splits);
+
 rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void* W, int M, int Nw,
                    int K, int epi, float* out_f32, int ldo, float* resid, int ldr, void* act,
                    int ld_act, bool defer, int* splits) {
+    return run_gemm_plan(c, kc, nullptr, A, lda, W, M, Nw, K, epi, out_f32, ldo, resid, ldr, act, ld_act, defer,
+                         splits);
+}
+
+// run_gemm with a given plan (nullptr: choose_plan's)
+rl_status run_gemm_plan(rl_decode_ctx* c, int kc, const GemmPlan* plan, const void* A, int lda, const void* W,
+                        int M, int Nw, int K, int epi, float* out_f32, int ldo, float* resid, int ldr, void* act,
+                        int ld_act, bool defer, int* splits) {
     const rl_model_config& cf = c->cfg;
     GemmArgs a{};
     a.A = A; a.lda = lda; a.W = W; a.ldw = K; a.M = M; a.Nw = Nw; a.K = K; a.epi = epi;
@@ -317,9 +354,7 @@ rl_status run_gemm(rl_decode_ctx* c, int kc, const void* A, int lda, const void*
     hipError_t e;
     *splits = 0;
     if (c->bf16()) {
-        GemmPlan p;
-        if (c->opt_gemm == 0 || !plan_gemm_forced(M, Nw, K, epi, cf.ffn, c->opt_gemm, &p))
-            p = plan_gemm_bf16(M, Nw, K, epi, cf.ffn);
+        const GemmPlan p = plan ? *plan : choose_plan(c, kc, M, Nw, K, epi);
         {
             Prof pr(c, kc);
             e = launch_gemm_bf16(a, p, c->stream);
@@ -534,6 +569,231 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         if (e != hipSuccess) return hip_fail(c, e, "sample launch");
         pr.done(f.n_out * (cf.vocab * 4.0 + 8.0), 0.0);
     }
+    return RL_OK;
+}
+
+// ---- GEMM plan measurement ------------------------------------------------
+// One timed unit of a decode GEMM class at M rows on layer l: the GEMM with
+// plan p, then the kernel that consumes its output as a decode step issues it
+// (q|k|v: RoPE summing the split-K slices, with no K/V destination; o and
+// down: residual sum + RMSNorm; gate-up and LM head: their split-K
+// reduction).  Operands are the workspace's activation buffers; `zeros` holds
+// M zero positions.
+rl_status tune_unit(rl_decode_ctx* c, int kc, const GemmPlan& p, int M, int l, const int32_t* zeros) {
+    const rl_model_config& cf = c->cfg;
+    const Layout& L = c->lay;
+    const int H = cf.hidden, Hq = cf.n_q_heads, Hkv = cf.n_kv_heads, D = cf.head_dim, F = cf.ffn;
+    const int HqD = Hq * D;
+    const size_t esz = static_cast<size_t>(L.es);
+    auto lw = [&](const void* base, size_t per_layer) {
+        return static_cast<const uint8_t*>(base) + static_cast<size_t>(l) * per_layer * esz;
+    };
+    float* x = c->wsp<float>(L.off_x);
+    void* h = c->ws + L.off_h;
+    float* qkv = c->wsp<float>(L.off_qkv);
+    const float eps = static_cast<float>(cf.rms_eps);
+    int splits = 0;
+    rl_status st;
+    switch (kc) {
+        case RL_K_GEMM_QKV: {
+            st = run_gemm_plan(c, kc, &p, h, H, lw(c->w.w_qkv, static_cast<size_t>(L.nqkv) * H), M, L.nqkv, H,
+                               EPI_F32, qkv, L.nqkv, nullptr, 0, nullptr, 0, true, &splits);
+            if (st != RL_OK) return st;
+            const float* src = splits > 1 ? c->wsp<float>(L.off_part) : qkv;
+            const hipError_t e = launch_rope_append(DT_BF16, src, splits > 1 ? splits : 1, M, zeros, zeros, 0, nullptr,
+                                                    c->wsp<float>(L.off_rope), L.cap * (D / 2), Hq, Hkv, D,
+                                                    cf.max_seqs, L.cap, l, c->ws + L.off_q, c->kslab(), c->vslab(),
+                                                    c->stream);
+            return e == hipSuccess ? RL_OK : hip_fail(c, e, "rope launch");
+        }
+        case RL_K_GEMM_O:
+            st = run_gemm_plan(c, kc, &p, c->ws + L.off_attn, HqD, lw(c->w.w_o, static_cast<size_t>(H) * HqD), M, H,
+                               HqD, EPI_RESID, nullptr, 0, x, H, nullptr, 0, true, &splits);
+            if (st != RL_OK) return st;
+            return resid_then_norm(c, DT_BF16, splits, x, M, H, lw(c->w.mlp_norm, H), eps, h);
+        case RL_K_GEMM_GATE_UP:
+            return run_gemm_plan(c, kc, &p, h, H, lw(c->w.w_gate_up, static_cast<size_t>(2) * F * H), M, 2 * F, H,
+                                 EPI_SWIGLU, nullptr, 0, nullptr, 0, c->ws + L.off_mlp, F, false, &splits);
+        case RL_K_GEMM_DOWN:
+            st = run_gemm_plan(c, kc, &p, c->ws + L.off_mlp, F, lw(c->w.w_down, static_cast<size_t>(H) * F), M, H, F,
+                               EPI_RESID, nullptr, 0, x, H, nullptr, 0, true, &splits);
+            if (st != RL_OK) return st;
+            return resid_then_norm(c, DT_BF16, splits, x, M, H, lw(c->w.attn_norm, H), eps, h);
+        default:
+            return run_gemm_plan(c, kc, &p, h, H, c->w.lm_head, M, cf.vocab, H, EPI_F32, c->wsp<float>(L.off_logits),
+                                 cf.vocab, nullptr, 0, nullptr, 0, false, &splits);
+    }
+}
+
+struct TuneTimer {
+    rl_decode_ctx* c;
+    const int32_t* zeros;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    // mean microseconds per unit over `layers`, after one untimed unit on `warm`
+    rl_status run(int kc, const GemmPlan& p, int M, const std::vector<int>& layers, int warm, float* us) {
+        rl_status st = tune_unit(c, kc, p, M, warm, zeros);
+        if (st != RL_OK) return st;
+        hipError_t e = hipEventRecord(e0, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "event record");
+        for (int l : layers) {
+            st = tune_unit(c, kc, p, M, l, zeros);
+            if (st != RL_OK) return st;
+        }
+        if ((e = hipEventRecord(e1, c->stream)) != hipSuccess) return hip_fail(c, e, "event record");
+        if ((e = hipEventSynchronize(e1)) != hipSuccess) return hip_fail(c, e, "event synchronize");
+        float ms = 0.0f;
+        if ((e = hipEventElapsedTime(&ms, e0, e1)) != hipSuccess) return hip_fail(c, e, "event time");
+        *us = ms * 1000.0f / static_cast<float>(layers.size());
+        return RL_OK;
+    }
+};
+
+constexpr int kTuneFinalists = 2;   // isolated-unit winners measured again inside decode steps
+constexpr int kTuneCtx = 64;        // context of every row of a measuring step
+constexpr int kTuneSteps = 2;       // timed measuring steps per finalist (after one untimed)
+
+// Device time of a decode step of rows 0 .. M-1 at context ctx0 (mean over
+// kTuneSteps steps after one untimed step).
+struct TuneStepper {
+    rl_decode_ctx* c;
+    int32_t* tok = nullptr;   // device: zero input tokens, then output tokens and log-probs
+    std::vector<int32_t> slots;
+    std::vector<uint64_t> uids;
+    int ctx0 = 0;
+    rl_status time(int M, hipEvent_t e0, hipEvent_t e1, float* ms) {
+        const rl_sample_params sp{0, 1.0f, 0};
+        for (int i = 0; i < M; ++i) c->len[i] = ctx0;
+        int32_t* out_tok = tok + c->cfg.max_seqs;
+        float* out_lp = reinterpret_cast<float*>(tok + 2 * c->cfg.max_seqs);
+        rl_status st = rl_decode_step(c, M, slots.data(), uids.data(), tok, nullptr, &sp, out_tok, out_lp, nullptr);
+        if (st != RL_OK) return st;
+        hipError_t e = hipEventRecord(e0, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "event record");
+        for (int k = 0; k < kTuneSteps; ++k) {
+            st = rl_decode_step(c, M, slots.data(), uids.data(), tok, nullptr, &sp, out_tok, out_lp, nullptr);
+            if (st != RL_OK) return st;
+        }
+        if ((e = hipEventRecord(e1, c->stream)) != hipSuccess) return hip_fail(c, e, "event record");
+        if ((e = hipEventSynchronize(e1)) != hipSuccess) return hip_fail(c, e, "event synchronize");
+        if ((e = hipEventElapsedTime(ms, e0, e1)) != hipSuccess) return hip_fail(c, e, "event time");
+        *ms /= kTuneSteps;
+        return RL_OK;
+    }
+};
+
+// For every batch size M (ascending) and decode GEMM class: every candidate
+// plan is timed as an isolated unit over a few layers (consecutive
+// candidates on disjoint layers, so that a layer's weights are not still
+// cached from the previous candidate); then, one class at a time with the
+// other classes at their current choice, the fastest few and the cost
+// model's plan are each timed inside whole decode steps of M rows, which
+// also price what a plan costs its neighbours, and the fastest step wins.
+// The context holds no live sequence; the measuring steps use slots
+// 0 .. M-1 at a short context and leave every length at 0.
+rl_status tune_gemms(rl_decode_ctx* c, const std::vector<int>& sizes) {
+    const rl_model_config& cf = c->cfg;
+    const Layout& L = c->lay;
+    const int H = cf.hidden, F = cf.ffn, HqD = cf.n_q_heads * cf.head_dim, NL = cf.n_layers;
+    struct Shape { int kc, Nw, K, epi; };
+    const Shape shapes[5] = {{RL_K_GEMM_QKV, L.nqkv, H, EPI_F32}, {RL_K_GEMM_O, H, HqD, EPI_RESID},
+                             {RL_K_GEMM_GATE_UP, 2 * F, H, EPI_SWIGLU}, {RL_K_GEMM_DOWN, H, F, EPI_RESID},
+                             {RL_K_GEMM_LM_HEAD, cf.vocab, H, EPI_F32}};
+    const int order[5] = {2, 3, 0, 1, 4};   // step-level choice: largest share of the step first
+    // finite operands: zero activations, positions, destinations and K/V
+    // (no sequence is live, so the pool holds nothing to keep)
+    hipError_t e = hipMemsetAsync(c->ws + L.off_x, 0, L.off_part - L.off_x, c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->ws + L.off_tok, 0, static_cast<size_t>(L.R) * 4, c->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->kv, 0, L.kv_bytes, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "workspace clear");
+    TuneTimer tm{c, c->wsp<int32_t>(L.off_tok)};
+    TuneStepper stp{c};
+    stp.ctx0 = std::max(0, std::min(kTuneCtx, cf.max_ctx - (kTuneSteps + 2)));
+    const int max_m = sizes.back();
+    for (int i = 0; i < max_m; ++i) {
+        stp.slots.push_back(i);
+        stp.uids.push_back(static_cast<uint64_t>(i));
+    }
+    if ((e = hipMalloc(&stp.tok, static_cast<size_t>(3) * cf.max_seqs * 4)) != hipSuccess)
+        return hip_fail(c, e, "tuning buffers");
+    e = hipMemsetAsync(stp.tok, 0, static_cast<size_t>(3) * cf.max_seqs * 4, c->stream);
+    if (e == hipSuccess) e = hipEventCreate(&tm.e0);
+    if (e == hipSuccess) e = hipEventCreate(&tm.e1);
+    const uint32_t profile = c->profile;
+    const rl_attn_plan_stats plan_stats = c->plan;
+    c->profile = 0;
+    rl_status st = e == hipSuccess ? RL_OK : hip_fail(c, e, "tuning set-up");
+    std::vector<int> all(NL);
+    for (int l = 0; l < NL; ++l) all[l] = l;
+    std::vector<GemmPlan> cand[5];
+    std::vector<float> unit_us[5];
+    for (size_t si = 0; si < sizes.size() && st == RL_OK; ++si) {
+        const int M = sizes[si];
+        std::vector<int> fin[5];
+        for (int k = 0; k < 5 && st == RL_OK; ++k) {
+            const Shape& sh = shapes[k];
+            const bool head = sh.kc == RL_K_GEMM_LM_HEAD;
+            GemmPlan buf[kMaxGemmCandidates];
+            const int n = plan_gemm_candidates(M, sh.Nw, sh.K, sh.epi, F, buf, kMaxGemmCandidates);
+            cand[k].assign(buf, buf + n);
+            unit_us[k].assign(n, 0.0f);
+            std::vector<std::pair<float, int>> first;
+            for (int i = 0; i < n && st == RL_OK; ++i) {
+                std::vector<int> lay;
+                int warm = 0;
+                if (head) {
+                    lay = {0};
+                } else if (NL < 5) {
+                    lay = all;
+                } else {
+                    warm = (5 * i) % NL;
+                    for (int q = 1; q <= 4; ++q) lay.push_back((warm + q) % NL);
+                }
+                st = tm.run(sh.kc, cand[k][i], M, lay, warm, &unit_us[k][i]);
+                first.emplace_back(unit_us[k][i], i);
+            }
+            std::sort(first.begin(), first.end());
+            fin[k].push_back(0);   // the cost model's plan
+            for (int j = 0; j < static_cast<int>(first.size()) && static_cast<int>(fin[k].size()) <= kTuneFinalists; ++j)
+                if (first[j].second != 0) fin[k].push_back(first[j].second);
+        }
+        if (st != RL_OK) break;
+        // this size's entries, at the cost model's plans; sizes ascend, so a
+        // lookup at M finds these before any larger size's
+        const size_t base = c->tuned.size();
+        for (int k = 0; k < 5; ++k)
+            c->tuned.push_back({shapes[k].kc, M, shapes[k].Nw, shapes[k].K, shapes[k].epi, cand[k][0], unit_us[k][0]});
+        for (int oi = 0; oi < 5 && st == RL_OK; ++oi) {
+            const int k = order[oi];
+            if (fin[k].size() < 2) continue;
+            int best = -1;
+            float best_ms = 0.0f;
+            for (int i : fin[k]) {
+                c->tuned[base + k].p = cand[k][i];
+                float ms = 0.0f;
+                st = stp.time(M, tm.e0, tm.e1, &ms);
+                if (st != RL_OK) break;
+                if (best < 0 || ms < best_ms) { best = i; best_ms = ms; }
+            }
+            if (st != RL_OK) break;
+            c->tuned[base + k].p = cand[k][best];
+            c->tuned[base + k].us = unit_us[k][best];
+        }
+    }
+    for (int i = 0; i < max_m; ++i) c->len[i] = 0;
+    c->profile = profile;
+    c->plan = plan_stats;
+    if (tm.e0) (void)hipEventDestroy(tm.e0);
+    if (tm.e1) (void)hipEventDestroy(tm.e1);
+    (void)hipStreamSynchronize(c->stream);
+    (void)hipFree(stp.tok);
+    if (st != RL_OK) {
+        c->tuned.clear();
+        return st;
+    }
+    std::stable_sort(c->tuned.begin(), c->tuned.end(),
+                     [](const rl_decode_ctx::TunedPlan& a, const rl_decode_ctx::TunedPlan& b) {
+                         return a.kc != b.kc ? a.kc < b.kc : a.M < b.M;
+                     });
     return RL_OK;
 }
 
@@ -1631,6 +1891,52 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
         default:
             return fail(ctx, RL_ERR_INVALID_ARG, "unknown option");
     }
+}
+
+rl_status rl_decode_tune_gemms(rl_decode_ctx* ctx, int32_t n_sizes, const int32_t* sizes) {
+    if (!ctx_ok(ctx)) return RL_ERR_INVALID_ARG;
+    if (n_sizes < 0 || n_sizes > 4096 || (n_sizes > 0 && !sizes))
+        return fail(ctx, RL_ERR_INVALID_ARG, "n_sizes must be in [0, 4096] with a size array");
+    std::vector<int> v(sizes, sizes + n_sizes);
+    for (int i = 0; i < n_sizes; ++i) {
+        if (v[i] < 1 || v[i] > ctx->cfg.max_seqs)
+            return fail(ctx, RL_ERR_INVALID_ARG, "batch sizes must be in [1, max_seqs]");
+        if (i > 0 && v[i] <= v[i - 1]) return fail(ctx, RL_ERR_INVALID_ARG, "batch sizes must be increasing");
+    }
+    if (n_sizes > 0 && !ctx->bf16()) return fail(ctx, RL_ERR_UNSUPPORTED, "GEMM plans are tuned for bf16 models only");
+    for (int32_t l : ctx->len)
+        if (l != 0) return fail(ctx, RL_ERR_INVALID_ARG, "GEMM plans are measured with no live sequence (every length 0)");
+    ctx->tuned.clear();
+    if (n_sizes == 0) return RL_OK;
+    DeviceGuard g(ctx->device);
+    return tune_gemms(ctx, v);
+}
+
+rl_status rl_decode_gemm_plan(rl_decode_ctx* ctx, int32_t kclass, int32_t rows, int64_t* plan_code,
+                              float* tuned_us) {
+    if (!ctx_ok(ctx)) return RL_ERR_INVALID_ARG;
+    if (kclass != RL_K_GEMM_QKV && kclass != RL_K_GEMM_O && kclass != RL_K_GEMM_GATE_UP &&
+        kclass != RL_K_GEMM_DOWN && kclass != RL_K_GEMM_LM_HEAD)
+        return fail(ctx, RL_ERR_INVALID_ARG, "kclass must be a GEMM class");
+    if (rows < 1 || rows > std::max(ctx->cfg.max_seqs, ctx->cfg.max_prefill_tokens))
+        return fail(ctx, RL_ERR_INVALID_ARG, "rows out of range");
+    if (!plan_code) return fail(ctx, RL_ERR_INVALID_ARG, "plan_code is NULL");
+    if (!ctx->bf16()) return fail(ctx, RL_ERR_UNSUPPORTED, "GEMM plans exist for bf16 models only");
+    const rl_model_config& cf = ctx->cfg;
+    const int H = cf.hidden, F = cf.ffn, HqD = cf.n_q_heads * cf.head_dim;
+    int Nw = cf.vocab, K = H, epi = EPI_F32;
+    if (kclass == RL_K_GEMM_QKV) Nw = ctx->lay.nqkv;
+    if (kclass == RL_K_GEMM_O) { Nw = H; K = HqD; epi = EPI_RESID; }
+    if (kclass == RL_K_GEMM_GATE_UP) { Nw = 2 * F; epi = EPI_SWIGLU; }
+    if (kclass == RL_K_GEMM_DOWN) { Nw = H; K = F; epi = EPI_RESID; }
+    GemmPlan p;
+    float us = -1.0f;
+    if (!(ctx->opt_gemm != 0 && plan_gemm_forced(rows, Nw, K, epi, F, ctx->opt_gemm, &p)) &&
+        !tuned_plan(ctx, kclass, rows, Nw, K, epi, &p, &us))
+        p = plan_gemm_bf16(rows, Nw, K, epi, F);
+    *plan_code = gemm_plan_code_of(p);
+    if (tuned_us) *tuned_us = us;
+    return RL_OK;
 }
 
 rl_status rl_decode_kernel_stats(rl_decode_ctx* ctx, int32_t kclass, rl_kernel_stats* out) {

@@ -182,6 +182,90 @@ GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F) {
     return best_p;
 }
 
+// Every plan of the cost model's search space for this GEMM, its own choice
+// first: the direct-load kernel (M <= 64) at split counts 1..16, the
+// GEMV-shaped kernel (M <= 32), and from 16 rows each batched tile kernel at
+// every split count the cost model prices (powers of two, slices of at least
+// 256 k, partials within budget) and the two-segment launches of whole
+// 256 x 256 rounds plus a smaller tile kernel (below 16 rows the tiles are
+// mostly empty rows and were never faster than the GEMV or direct kernels).
+// K % 64 != 0 has no alternatives.  Returns the count written (at most cap).
+constexpr int kMinTileCandidateRows = 16;
+int plan_gemm_candidates(int M, int Nw, int K, int epi, int F, GemmPlan* out, int cap) {
+    int n = 0;
+    auto same = [](const GemmPlan& a, const GemmPlan& b) {
+        return a.variant == b.variant && a.splits == b.splits && a.ksplit == b.ksplit && a.n_split == b.n_split &&
+               a.variant2 == b.variant2 && a.grid_x == b.grid_x && a.grid_y == b.grid_y;
+    };
+    auto add = [&](const GemmPlan& p) {
+        for (int i = 0; i < n; ++i)
+            if (same(out[i], p)) return;
+        if (n < cap) out[n++] = p;
+    };
+    add(plan_gemm_bf16(M, Nw, K, epi, F));
+    if (K % 64 != 0) return n;
+    const int n_out = epi == EPI_SWIGLU ? F : Nw;
+    if (M <= 64) {
+        for (int s = 1; s <= 16; s *= 2) {
+            GemmPlan p = plan_direct(M, Nw, K, epi, F);
+            const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+            if (static_cast<size_t>(ceil_div(K, ks)) * M * Nw > kPartCapFloats) break;
+            p.ksplit = ks;
+            p.splits = ceil_div(K, ks);
+            add(p);
+        }
+    }
+    if (M <= 32) {
+        GemmPlan p{};
+        p.variant = kGemvVariant; p.splits = 1; p.ksplit = K;
+        add(p);
+    }
+    if (M < kMinTileCandidateRows) return n;
+    for (const TileKernel& t : kLineTiles) {
+        for (int s = 1; s <= kMaxSplits; s *= 2) {
+            const int ks = ceil_div(ceil_div(K, s), 64) * 64;
+            if (s > 1 && (ceil_div(K, ks) != s || ks < 256 || static_cast<size_t>(s) * M * Nw > kPartCapFloats))
+                break;
+            GemmPlan p{};
+            p.variant = t.variant; p.splits = s; p.ksplit = ks;
+            add(p);
+        }
+    }
+    const TileKernel& big = kLineTiles[0];
+    const long big_tiles = tiles_of(big, M, n_out, epi);
+    const int m_tiles = ceil_div(M, big.BM);
+    const int bno = epi == EPI_SWIGLU ? big.BN / 2 : big.BN;
+    const long full_cols = (big_tiles / kCUs) * kCUs / m_tiles;
+    if (full_cols > 0 && full_cols * bno < n_out) {
+        for (int v = 1; v < 4; ++v) {
+            GemmPlan p{};
+            p.variant = big.variant; p.splits = 1; p.ksplit = K;
+            p.n_split = static_cast<int>(full_cols * bno); p.variant2 = kLineTiles[v].variant;
+            add(p);
+        }
+    }
+    return n;
+}
+
+// The RL_OPT_GEMM_PLAN code of a plan (0 when it has none).
+int64_t gemm_plan_code_of(const GemmPlan& p) {
+    auto code = [](int v) -> int64_t {
+        switch (v) {
+            case kLineVariant256x256: return RL_GEMM_T256;
+            case kLineVariant128x256: return RL_GEMM_T128X256;
+            case kLineVariant128x128: return RL_GEMM_T128;
+            case kLineVariant128x128Deep: return RL_GEMM_T128_DEEP;
+            case kGemvVariant: return RL_GEMM_GEMV;
+            default: return v >= 0 && v < kNumGemmShapes ? RL_GEMM_DIRECT : 0;
+        }
+    };
+    const int64_t k1 = code(p.variant);
+    if (k1 == 0) return 0;
+    const int64_t s = p.splits > 1 ? p.splits : 0;
+    const int64_t k2 = p.n_split > 0 ? code(p.variant2) : 0;
+    return k1 | (s << 8) | (k2 << 16);
+}
+
 bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPlan* out) {
     const int k1 = static_cast<int>(code & 0xff), s = static_cast<int>((code >> 8) & 0xff);
     const int k2 = static_cast<int>((code >> 16) & 0xff);

@@ -82,6 +82,11 @@ constexpr int kMaxSplits = 32;
 constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget
 
 GemmPlan plan_gemm_bf16(int M, int Nw, int K, int epi, int F);
+// the cost model's search space, its choice first; returns the count (<= cap)
+int plan_gemm_candidates(int M, int Nw, int K, int epi, int F, GemmPlan* out, int cap);
+// RL_OPT_GEMM_PLAN code of a plan (0: none)
+int64_t gemm_plan_code_of(const GemmPlan& p);
+constexpr int kMaxGemmCandidates = 48;
 // RL_OPT_GEMM_PLAN override; false when it cannot serve this GEMM
 bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPlan* p);
 

@@ -34,7 +34,8 @@ EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create"
            "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
            "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
            "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_gumbel_bound",
-           "rl_sample_logits_noalloc", "rl_status_string", "rl_decode_last_error")
+           "rl_sample_logits_noalloc", "rl_decode_tune_gemms", "rl_decode_gemm_plan", "rl_status_string",
+           "rl_decode_last_error")
 
 
 class ModelConfig(C.Structure):
@@ -109,6 +110,10 @@ def lib():
     L.rl_decode_rebind.argtypes = [vp, C.POINTER(Weights), vp, sz, vp, sz]
     L.rl_decode_set_option.restype = C.c_int
     L.rl_decode_set_option.argtypes = [vp, i32, C.c_int64]
+    L.rl_decode_tune_gemms.restype = C.c_int
+    L.rl_decode_tune_gemms.argtypes = [vp, i32, vp]
+    L.rl_decode_gemm_plan.restype = C.c_int
+    L.rl_decode_gemm_plan.argtypes = [vp, i32, i32, C.POINTER(C.c_int64), C.POINTER(C.c_float)]
     L.rl_decode_kernel_stats.restype = C.c_int
     L.rl_decode_kernel_stats.argtypes = [vp, i32, C.POINTER(KernelStats)]
     L.rl_decode_reset_stats.restype = C.c_int
@@ -289,6 +294,19 @@ class Engine:
 
     def set_option(self, option: int, value: int):
         self._check(lib().rl_decode_set_option(self.h, option, value), "rl_decode_set_option")
+
+    def tune_gemms(self, sizes: Sequence[int]):
+        """Measure the GEMM plans at these batch sizes (increasing); [] clears."""
+        s = _host_i32(sizes)
+        self._check(lib().rl_decode_tune_gemms(self.h, len(s), s.ctypes.data if len(s) else None),
+                    "rl_decode_tune_gemms")
+
+    def gemm_plan(self, kclass: str, rows: int):
+        """(RL_OPT_GEMM_PLAN code, measured us per layer or -1) of a GEMM class at `rows` rows."""
+        code, us = C.c_int64(0), C.c_float(0.0)
+        self._check(lib().rl_decode_gemm_plan(self.h, KERNEL_CLASSES.index(kclass), rows, C.byref(code),
+                                              C.byref(us)), "rl_decode_gemm_plan")
+        return int(code.value), float(us.value)
 
     def kernel_stats(self) -> Dict[str, dict]:
         out = {}

@@ -14,7 +14,7 @@ from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 from paper_2509_15965_amd.inputs import rollout_plan, uniform_tokens
 from paper_2509_15965_amd.rl_decode import (RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T128, RL_GEMM_T128_DEEP,
                                            RL_GEMM_T128X256, RL_GEMM_T256, RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN,
-                                           Engine, gemm_plan_code)
+                                           Engine, RLError, gemm_plan_code)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +33,7 @@ def _free_memory():
 
 
 def teacher_forced_run(shape, seed, prompts, group, n_steps, T=1.0, sample_seed=5, max_ctx=None,
-                       embed_rows=None, gemm_plan=0):
+                       embed_rows=None, gemm_plan=0, tune_sizes=None):
     """Prefill `prompts` (group slots each), then n_steps decode steps that feed
     seeded forced tokens.  Returns per-step (gpu logits, oracle logits, gpu
     logp, oracle logp, gpu tokens, oracle sampled tokens)."""
@@ -44,6 +44,8 @@ def teacher_forced_run(shape, seed, prompts, group, n_steps, T=1.0, sample_seed=
     eng = Engine(shape, w_dev, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=sum(plens))
     if gemm_plan:
         eng.set_option(RL_OPT_GEMM_PLAN, gemm_plan)
+    if tune_sizes:
+        eng.tune_gemms(tune_sizes)
     slots = list(range(n_seq))
     uids = [1000 + i for i in range(n_seq)]
     offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
@@ -118,6 +120,44 @@ def test_sampler_matches_oracle_on_given_logits():
                 assert gt[i] == ot, (T, i)
                 assert abs(gl[i] - ol) < 1e-5, (T, i, gl[i], ol)
     assert out_tok.cpu().numpy()[5] in (7, 100)
+    eng.close()
+
+
+@pytest.mark.parametrize("n", [6, 2048], ids=["merged-chunks", "single-chunk"])
+def test_sampler_nan_rows_never_index_outside_the_row(n):
+    """A NaN score never wins a comparison.  A row of NaN logits ranks no
+    entry: token -1 and a NaN log-probability (no logit outside the row is
+    read).  A row with some NaN entries samples among its other entries (the
+    oracle's sample with the NaN entries at -inf) and has a NaN
+    log-probability (its log-sum-exp is NaN).  The other rows are unchanged.
+    Both the merge kernel (few rows, several vocabulary chunks per row) and
+    the single-chunk path (2048 rows) are covered."""
+    shape = WORKLOADS["tiny"].model
+    w_dev, _, _ = build_models(shape, 5)
+    V = shape.vocab
+    eng = Engine(shape, w_dev, max_seqs=n, max_ctx=16, max_prefill_tokens=16)
+    rng = np.random.default_rng(2)
+    z = rng.normal(0, 2.0, size=(n, V)).astype(np.float32)
+    z[0, :] = np.nan
+    z[1, ::3] = np.nan
+    zt = torch.from_numpy(z).to(DEV)
+    z_inf = np.where(np.isnan(z[1]), -np.inf, z[1]).astype(np.float32)
+    uids = [int(u) for u in rng.integers(0, 2 ** 63, size=n, dtype=np.int64)]
+    pos = [int(p) for p in rng.integers(0, 5000, size=n)]
+    forced = rng.integers(0, V, size=n).astype(np.int32)
+    out_tok = torch.empty(n, dtype=torch.int32, device=DEV)
+    out_lp = torch.empty(n, dtype=torch.float32, device=DEV)
+    for T in (1.0, 0.0):
+        for use_forced in (False, True):
+            eng.sample_logits(zt, uids, pos, out_tok, out_lp, seed=91, temperature=T,
+                              forced=_i32(forced) if use_forced else None)
+            torch.cuda.synchronize()
+            gt, gl = out_tok.cpu().numpy(), out_lp.cpu().numpy()
+            assert gt[0] == -1 and np.isnan(gl[0]), (T, use_forced)
+            assert gt[1] == oracle.sample(z_inf, T, 91, uids[1], pos[1])[0] and np.isnan(gl[1]), (T, use_forced)
+            for i in range(2, min(n, 40)):
+                ot, ol = oracle.sample(z[i], T, 91, uids[i], pos[i], forced=int(forced[i]) if use_forced else -1)
+                assert gt[i] == ot and abs(gl[i] - ol) < 1e-5, (T, use_forced, i)
     eng.close()
 
 
@@ -375,6 +415,40 @@ def test_every_gemm_kernel_matches_oracle(name, code):
     for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
         assert row_rel_err(zg, zo) < LOGIT_REL_TOL, (name, k)
         assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, (name, k)
+
+
+def test_measured_gemm_plans_match_oracle():
+    """Plans chosen by measurement (rl_decode_tune_gemms) at 1, 8 and 24 rows:
+    decode at 24 rows uses the plans measured there and matches the oracle;
+    the plan query reports them with their time, and the cost model (time
+    -1) beyond the largest measured size."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e6, "bf16")
+    rng = np.random.default_rng(78)
+    prompts = [rng.integers(0, shape.vocab, size=6).astype(np.int32) for _ in range(24)]
+    res = teacher_forced_run(shape, 92, prompts, group=1, n_steps=2, T=1.0, tune_sizes=[1, 8, 24])
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+    w_dev, _, _ = build_models(shape, 93)
+    eng = Engine(shape, w_dev, max_seqs=24, max_ctx=16, max_prefill_tokens=144)
+    eng.tune_gemms([1, 8, 24])
+    for kc in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head"):
+        for rows in (1, 5, 8, 20, 24):
+            code, us = eng.gemm_plan(kc, rows)
+            assert code != 0 and us > 0, (kc, rows)
+        code, us = eng.gemm_plan(kc, 100)
+        assert code != 0 and us == -1.0, kc
+    assert all(eng.slot_length(i) == 0 for i in range(24))
+    eng.tune_gemms([])
+    assert eng.gemm_plan("gemm_o", 8)[1] == -1.0
+    for bad in ([0], [8, 8], [25], [4, 2]):
+        with pytest.raises(RLError):
+            eng.tune_gemms(bad)
+    eng.set_lengths([3], [5])                # a live sequence: refused, table untouched
+    with pytest.raises(RLError):
+        eng.tune_gemms([8])
+    assert eng.slot_length(3) == 5 and eng.gemm_plan("gemm_o", 8)[1] == -1.0
+    eng.close()
 
 
 @pytest.mark.parametrize("n_prompts", [64, 20])
