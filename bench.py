@@ -42,14 +42,16 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
 # HBM traffic of the attention kernel per algorithmic byte, from two
-# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over this whole rollout,
-# each counter scaled by what it reads for the library's plain copy kernel of
-# known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0): 504.9 MB fetched + 22.7 MB
-# written per launch against 483.5 MB algorithmic (unique K/V: each group's
-# shared prompt once).  Valid for the attention kernel and work-item layout as
-# of that measurement (256-key items in steps that read shared prompts); set
-# to None when either changes until the counters are taken again.
-ATTN_TRAFFIC_PER_ALG_BYTE = 1.0913
+# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of this benchmark's
+# default command, over the 2 x 4095 x 28 attention launches of its two
+# rollout passes, each counter scaled by what it reads for the library's
+# plain copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0):
+# 505.4 MB fetched + 24.1 MB written per launch against 483.5 MB algorithmic
+# (unique K/V: each group's shared prompt once).  Valid for the attention
+# kernel and work-item layout as of that measurement (shared-prompt items of
+# 256 keys, shorter in steps with few rows); set to None when either changes
+# until the counters are taken again.
+ATTN_TRAFFIC_PER_ALG_BYTE = 1.0951
 
 
 def parse():

@@ -366,7 +366,11 @@ typedef enum rl_option {
                                 items fit the workspace                        */
     RL_OPT_PROFILE = 2,      /* bit mask over rl_kernel_class: launches of the
                                 selected classes are timed with HIP events on
-                                the context's stream; 0 = off (default),
+                                the context's stream (the bf16 decode
+                                attention by events stamped at the kernel's
+                                own start and end; the other classes by an
+                                event pair around the launch, which also spans
+                                the dispatch gap); 0 = off (default),
                                 -1 = every class                              */
     RL_OPT_GEMM_PLAN = 3,    /* bf16 GEMM kernel override (testing every tile
                                 kernel on small models): 0 = the cost-model

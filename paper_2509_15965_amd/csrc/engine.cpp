@@ -192,23 +192,37 @@ hipError_t harvest(rl_decode_ctx* c) {
 
 // Launches of a class are counted (with their algorithmic bytes and FLOPs)
 // and timed only while RL_OPT_PROFILE selects the class.
+// Times one launch of a kernel class when RL_OPT_PROFILE selects it: an
+// event pair recorded around the launch (which also spans the dispatch gap
+// before the kernel starts), or, for a launch that takes them (attached),
+// events stamped by the dispatch itself at the kernel's start and end.
 struct Prof {
-    rl_decode_ctx* c; int kc; hipEvent_t a = nullptr; bool on = false;
-    Prof(rl_decode_ctx* c_, int kc_) : c(c_), kc(kc_) {
+    rl_decode_ctx* c; int kc; hipEvent_t a = nullptr, b = nullptr; bool on = false, attached = false;
+    Prof(rl_decode_ctx* c_, int kc_, bool attach = false) : c(c_), kc(kc_), attached(attach) {
         on = ((c->profile >> kc) & 1u) != 0;
-        if (on) {
-            if ((a = get_event(c))) (void)hipEventRecord(a, c->stream);
+        if (!on) return;
+        a = get_event(c);
+        if (attached) {
+            b = get_event(c);
+        } else if (a) {
+            (void)hipEventRecord(a, c->stream);
         }
     }
+    // events for a launch that stamps them itself (null when not profiled)
+    hipEvent_t start() const { return attached && a && b ? a : nullptr; }
+    hipEvent_t stop() const { return attached && a && b ? b : nullptr; }
     void done(double bytes, double flops) {
         if (!on) return;
         c->stats[kc].launches += 1;
         c->stats[kc].alg_bytes += bytes;
         c->stats[kc].alg_flops += flops;
-        if (!a) return;
-        hipEvent_t b = get_event(c);
-        if (!b) { c->ev_pool.push_back(a); return; }
-        (void)hipEventRecord(b, c->stream);
+        if (!attached && a) b = get_event(c);
+        if (!a || !b) {
+            if (a) c->ev_pool.push_back(a);
+            if (b) c->ev_pool.push_back(b);
+            return;
+        }
+        if (!attached) (void)hipEventRecord(b, c->stream);
         c->pending.push_back({kc, a, b});
         if (c->pending.size() >= 4096) (void)harvest(c);
     }
@@ -492,13 +506,13 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
             pr.done(n * (qs * L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
         }
         {
-            Prof pr(c, RL_K_ATTENTION);
+            Prof pr(c, RL_K_ATTENTION, c->bf16() && !f.tiles);
             if (c->bf16() && f.tiles)
                 e = launch_attention_prefill(f.tiles, f.n_tiles, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv, D,
                                              L.cap, l, attn, c->stream);
             else if (c->bf16())
                 e = launch_attention_bf16(f.items, f.n_items, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv,
-                                          D, L.cap, l, attn, apart, c->stream);
+                                          D, L.cap, l, attn, apart, c->stream, pr.start(), pr.stop());
             else
                 e = launch_attention_f32(n, f.row_slot, f.row_pos, static_cast<const float*>(q),
                                          reinterpret_cast<const float*>(c->kslab()),

@@ -22,6 +22,8 @@
 // invalidate the whole L2 and slow every co-running wave.)
 //
 // fp32 path: one workgroup per (row, q-head), plain VALU (tiny model only).
+#include <hip/hip_ext.h>
+
 #include "rl_device.h"
 #include "rl_internal.h"
 
@@ -271,14 +273,20 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
 hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
                                  const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
                                  int D, int cap, int layer, void* out, float* part,
-                                 hipStream_t s) {
+                                 hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (n_items <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     dim3 grid((n_items + 3) / 4, Hkv), block(256);
     auto go = [&](auto kern) {
-        hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
-                           cap, layer, scale_log2, static_cast<uint16_t*>(out), part);
+        if (ev_start || ev_stop)
+            hipExtLaunchKernelGGL(kern, grid, block, 0, s, ev_start, ev_stop, 0, items, n_items,
+                                  static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
+                                  static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer, scale_log2,
+                                  static_cast<uint16_t*>(out), part);
+        else
+            hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
+                               static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq,
+                               Hkv, cap, layer, scale_log2, static_cast<uint16_t*>(out), part);
     };
     if (D == 128) go(attn_bf16_kernel<128>); else go(attn_bf16_kernel<64>);
     return hipGetLastError();

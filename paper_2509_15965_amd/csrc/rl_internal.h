@@ -122,10 +122,12 @@ hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, 
                               int max_seqs, int cap, int layer,
                               void* q_out, void* kc, void* vc, hipStream_t s);
 
+// ev_start / ev_stop (may be null): events stamped with the kernel's own
+// start and end (attached to the dispatch, not recorded around it)
 hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
                                  const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
                                  int D, int cap, int layer, void* out, float* part,
-                                 hipStream_t s);
+                                 hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // Most items one split block may have (bounds the combine's LDS).
 constexpr int kMaxCombine = 64;
