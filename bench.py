@@ -100,8 +100,11 @@ def tune_gemms(eng, max_rows: int, skip: bool):
     sizes = [n for n in TUNE_SIZES if n < max_rows] + [max_rows]
     t0 = time.perf_counter()
     eng.tune_gemms(sizes)
-    return {"measured": True, "sizes": len(sizes), "largest": max_rows,
-            "seconds": round(time.perf_counter() - t0, 2)}
+    el = time.perf_counter() - t0
+    # the measured table is part of the run's configuration (the plan decides the fp32 summation order)
+    table = {c: [eng.gemm_plan("gemm_" + c, n)[0] for n in sizes] for c in ("qkv", "o", "gate_up", "down", "lm_head")}
+    return {"measured": True, "sizes": sizes, "seconds": round(el, 2),
+            "plan_codes": table}
 
 
 def copy_probe(mib: int):
