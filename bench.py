@@ -107,6 +107,49 @@ def tune_gemms(eng, max_rows: int, skip: bool):
             "plan_codes": table}
 
 
+def measured_peaks():
+    """HBM and matrix-core peaks measured on this GPU with the library's probes
+    (a read-only stream and a copy of 2 GiB; 1024 workgroups x 4 waves x 4000
+    rounds of 8 MFMA 32x32x16 bf16), best of 5 launches each, HIP events."""
+    import torch
+
+    from paper_2509_15965_amd.rl_decode import probe_copy, probe_mfma, probe_read
+    dev = torch.device("cuda:0")
+    nbytes = 2 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    words = torch.empty(8192, dtype=torch.int32, device=dev)
+    acc = torch.empty(4 * 1024, dtype=torch.float32, device=dev)
+
+    def best(fn):
+        fn()
+        ms = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        return min(ms)
+
+    t_read = best(lambda: probe_read(src, nbytes, words))
+    t_copy = best(lambda: probe_copy(dst, src, nbytes))
+    iters = 4000
+    # one and four waves per SIMD (256 and 1024 workgroups of four waves)
+    mfma = {nb: nb * 4 * iters * 8 * 32768.0 / (best(lambda nb=nb: probe_mfma(nb, iters, acc)) * 1e9)
+            for nb in (256, 1024)}
+    out = {"hbm_read_GBps": round(nbytes / (t_read * 1e6), 1),
+           "hbm_copy_GBps": round(2 * nbytes / (t_copy * 1e6), 1),
+           "mfma_bf16_TFLOPs": round(max(mfma.values()), 1),
+           "mfma_bf16_TFLOPs_by_waves_per_simd": {"1": round(mfma[256], 1), "4": round(mfma[1024], 1)},
+           "probe": "read-only stream and copy of 2 GiB (copy counts read + write bytes); 256 or 1024 "
+                    f"workgroups x 4 waves x {iters} x 8 MFMA 32x32x16 bf16; best of 5"}
+    del src, dst, words, acc
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_probe(mib: int):
     import torch
 
@@ -297,6 +340,8 @@ def switch_main(args):
     shape = wl.model
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    peaks = measured_peaks()
+    print(f"[bench] measured peaks: {peaks}", file=sys.stderr, flush=True)
     plan = rollout_plan(wl)
     P, G = wl.n_prompts, wl.group
     n = P * G
@@ -387,6 +432,8 @@ def continuous_main(args):
     shape = wl.model
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    peaks = measured_peaks()
+    print(f"[bench] measured peaks: {peaks}", file=sys.stderr, flush=True)
     plan = rollout_plan(wl)
     P, G = wl.n_prompts, wl.group
     S = args.slots
@@ -795,6 +842,8 @@ def main():
     shape = wl.model
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    peaks = measured_peaks()
+    print(f"[bench] measured peaks: {peaks}", file=sys.stderr, flush=True)
     plan = rollout_plan(wl)
     P, G = wl.n_prompts, wl.group
     n_seq = P * G
@@ -888,6 +937,8 @@ def main():
 
     dom, roof = roofline_of(stats, prof_classes)
     roof.pop("alg_flops_per_launch")
+    roof["frac_of_measured_peak"] = round(roof["achieved"] / (peaks["hbm_read_GBps"] if roof["bound"] == "hbm"
+                                                              else peaks["mfma_bf16_TFLOPs"]), 4)
     d = stats[dom]
     if dom == "attention" and ATTN_TRAFFIC_PER_ALG_BYTE is not None:
         roof["traffic"] = round(ATTN_TRAFFIC_PER_ALG_BYTE * d["alg_bytes"] / max(1, d["launches"]))
@@ -945,6 +996,7 @@ def main():
                     "paper_style_tokens_per_s": round((prompt_tokens + gen_all + n_seq) /
                                                       (rollout_wall + prefill_s), 1)},
         "roofline": roof,
+        "measured_peaks": peaks,
         "timed_classes": classes,
         "gemm_plans": tuning,
     }

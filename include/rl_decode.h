@@ -494,6 +494,20 @@ rl_status rl_decode_reset_stats(rl_decode_ctx* ctx);
  * `stream`.  Used to calibrate hardware byte counters against a known size. */
 rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream);
 
+/* Measured peaks beside the published ones.  rl_probe_read: a read-only
+ * stream of `bytes` bytes at src (a multiple of 16; 16-byte aligned) by
+ * n_blocks (1..65536) workgroups, four 16-byte loads in flight per thread;
+ * out (device, n_blocks uint32) receives each workgroup's XOR of the words
+ * it read (so the reads cannot be elided; the XOR of all entries is the XOR
+ * of every 32-bit word of the buffer).  rl_probe_mfma: n_blocks (1..65536)
+ * workgroups of four waves, each wave iters (1..2^20) rounds of eight
+ * independent 32x32x16 bf16 MFMAs (32768 FLOPs each) on operands of 1.0 and
+ * no memory traffic; out (device, 4 * n_blocks floats) receives 128 * iters
+ * per wave.  Both asynchronous on `stream`; RL_ERR_INVALID_ARG for bad
+ * sizes or pointers.  Test probes, not part of the decode path. */
+rl_status rl_probe_read(const void* src, size_t bytes, int32_t n_blocks, uint32_t* out, void* stream);
+rl_status rl_probe_mfma(int32_t n_blocks, int32_t iters, float* out, void* stream);
+
 /* Check of the two upper bounds of the Gumbel noise g(x) = fl32(-log(-log u)),
  * u = (x + 1/2) 2^-32, that the sampler uses to skip the exact fp64 noise of
  * entries that cannot win (the sample stays the exhaustive arg-max only if

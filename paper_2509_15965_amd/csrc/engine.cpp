@@ -2002,4 +2002,17 @@ rl_status rl_probe_copy(void* dst, const void* src, size_t bytes, void* stream) 
     return e == hipSuccess ? RL_OK : RL_ERR_HIP;
 }
 
+rl_status rl_probe_read(const void* src, size_t bytes, int32_t n_blocks, uint32_t* out, void* stream) {
+    if (!src || !out || bytes % 16 || !aligned(src, 16) || n_blocks < 1 || n_blocks > 65536)
+        return RL_ERR_INVALID_ARG;
+    hipError_t e = launch_read16(src, bytes / 16, out, n_blocks, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? RL_OK : RL_ERR_HIP;
+}
+
+rl_status rl_probe_mfma(int32_t n_blocks, int32_t iters, float* out, void* stream) {
+    if (!out || n_blocks < 1 || n_blocks > 65536 || iters < 1 || iters > (1 << 20)) return RL_ERR_INVALID_ARG;
+    hipError_t e = launch_mfma_probe(n_blocks, iters, out, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? RL_OK : RL_ERR_HIP;
+}
+
 }  // extern "C"

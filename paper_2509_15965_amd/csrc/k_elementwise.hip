@@ -442,6 +442,34 @@ __global__ void __launch_bounds__(256) copy16_kernel(u32x4* __restrict__ dst,
         dst[i] = src[i];
 }
 
+// Read-only stream: every thread XORs the 16-byte words it reads (four
+// independent loads in flight per iteration) and each workgroup writes one
+// word, so the kernel moves n16 * 16 bytes in and 4 bytes per workgroup out.
+__global__ void __launch_bounds__(256) read16_kernel(const u32x4* __restrict__ src, size_t n16,
+                                                     uint32_t* __restrict__ out) {
+    __shared__ uint32_t red[4];
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        acc ^= a ^ b ^ c ^ d;
+    }
+    for (; i < n16; i += stride) acc ^= src[i];
+    uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+    for (int o = 32; o > 0; o >>= 1) x ^= static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), o, 64));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) out[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+hipError_t launch_read16(const void* src, size_t n16, uint32_t* out, int n_blocks, hipStream_t s) {
+    if (n_blocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(read16_kernel, dim3(static_cast<unsigned>(n_blocks)), dim3(256), 0, s,
+                       static_cast<const u32x4*>(src), n16, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s) {
     if (n16 == 0) return hipSuccess;
     size_t blocks = (n16 + 255) / 256;

@@ -693,6 +693,36 @@ hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const flo
 }
 
 // ---------------------------------------------------------------------------
+// Matrix-core rate probe: every wave runs `iters` rounds of eight independent
+// 32x32x16 bf16 MFMAs (all operands 1.0, so each accumulator element gains
+// 16 per MFMA), then lane 0 writes its first accumulator element summed over
+// the eight chains (= 128 * iters).  No memory traffic in the loop.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) mfma_probe_kernel(int iters, float* __restrict__ out) {
+    const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 pairs
+    const bf16x8 a = as_bf16x8(ones);
+    f32x16 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = mfma32x32x16(a, a, acc[j]);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += acc[j][0];
+    if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = s;
+}
+
+hipError_t launch_mfma_probe(int n_blocks, int iters, float* out, hipStream_t s) {
+    if (n_blocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(mfma_probe_kernel, dim3(static_cast<unsigned>(n_blocks)), dim3(256), 0, s, iters, out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // fp32 VALU kernel: out_f32[m][n] = sum_k A[m][k] W[n][k]
 // 32 x 64 output tile, 2 x 4 per thread, k tiles of 32 through LDS.
 // ---------------------------------------------------------------------------

@@ -198,6 +198,10 @@ hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, co
                           hipStream_t s);
 
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
+// read-only stream of n16 16-byte words by n_blocks workgroups; out[b] = XOR of workgroup b's words
+hipError_t launch_read16(const void* src, size_t n16, uint32_t* out, int n_blocks, hipStream_t s);
+// n_blocks workgroups of four waves, each wave iters x 8 MFMA 32x32x16 bf16; out [n_blocks * 4]
+hipError_t launch_mfma_probe(int n_blocks, int iters, float* out, hipStream_t s);
 
 // Sampler noise-bound check over words [lo, lo + count): per workgroup, the
 // number of violated bounds and the smallest margin of the fp32 bound.

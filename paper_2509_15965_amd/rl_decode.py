@@ -33,7 +33,8 @@ EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create"
            "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
            "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
            "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
-           "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_gumbel_bound",
+           "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_read", "rl_probe_mfma",
+           "rl_probe_gumbel_bound",
            "rl_sample_logits_noalloc", "rl_decode_tune_gemms", "rl_decode_gemm_plan", "rl_status_string",
            "rl_decode_last_error")
 
@@ -122,6 +123,10 @@ def lib():
     L.rl_decode_attn_plan_stats.argtypes = [vp, C.POINTER(AttnPlanStats)]
     L.rl_probe_copy.restype = C.c_int
     L.rl_probe_copy.argtypes = [vp, vp, sz, vp]
+    L.rl_probe_read.restype = C.c_int
+    L.rl_probe_read.argtypes = [vp, sz, i32, vp, vp]
+    L.rl_probe_mfma.restype = C.c_int
+    L.rl_probe_mfma.argtypes = [i32, i32, vp, vp]
     L.rl_sample_logits_noalloc.restype = C.c_int
     L.rl_sample_logits_noalloc.argtypes = [i32, i32, vp, i32, vp, vp, vp, C.POINTER(SampleParams), vp, vp, vp]
     L.rl_probe_gumbel_bound.restype = C.c_int
@@ -343,6 +348,24 @@ def probe_copy(dst: torch.Tensor, src: torch.Tensor, nbytes: int, stream=None):
     st = lib().rl_probe_copy(dst.data_ptr(), src.data_ptr(), nbytes, stream.cuda_stream)
     if st != RL_OK:
         raise RLError(st, "rl_probe_copy")
+
+
+def probe_read(src: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None):
+    """Read-only stream of nbytes of src by out.numel() workgroups (out: int32, one word each)."""
+    stream = stream if stream is not None else torch.cuda.current_stream(src.device)
+    st = lib().rl_probe_read(src.data_ptr(), nbytes, out.numel(), out.data_ptr(), stream.cuda_stream)
+    if st != RL_OK:
+        raise RLError(st, "rl_probe_read")
+
+
+def probe_mfma(n_blocks: int, iters: int, out: torch.Tensor, stream=None):
+    """n_blocks x 4 waves x iters x 8 MFMA 32x32x16 bf16 (out: float32 [4 * n_blocks])."""
+    if out.numel() < 4 * n_blocks or out.dtype != torch.float32:
+        raise ValueError("out must hold 4 * n_blocks float32")
+    stream = stream if stream is not None else torch.cuda.current_stream(out.device)
+    st = lib().rl_probe_mfma(n_blocks, iters, out.data_ptr(), stream.cuda_stream)
+    if st != RL_OK:
+        raise RLError(st, "rl_probe_mfma")
 
 
 def probe_gumbel_bound(lo: int, count: int, n_blocks: int = 4096, device="cuda"):
