@@ -174,8 +174,9 @@ def _long_context_check(shape, w_dev, w_host, om, lengths, n_steps=2):
 
 
 def _record(name, what, errs, lerr, sens=None, lsens=None):
-    """Append the measured errors to gpurun_out/parity_fullshape.jsonl when that
-    directory exists (a record of the margins, not an input to any check)."""
+    """Print the measured errors, and append them to the file named by
+    RL_PARITY_LOG when that is set (a record of the margins, not an input to
+    any check)."""
     import json
     import os
     rec = {"workload": name, "check": what, "logit_rel_err": [float(e) for e in errs],
@@ -183,8 +184,9 @@ def _record(name, what, errs, lerr, sens=None, lsens=None):
     if sens is not None:
         rec["oracle_self_sensitivity"] = {"logit_rel": float(sens), "logp_abs": float(lsens)}
     print(json.dumps(rec), flush=True)
-    if os.path.isdir("gpurun_out"):
-        with open(os.path.join("gpurun_out", "parity_fullshape.jsonl"), "a") as f:
+    path = os.environ.get("RL_PARITY_LOG")
+    if path:
+        with open(path, "a") as f:
             f.write(json.dumps(rec) + "\n")
 
 
