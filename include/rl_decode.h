@@ -76,6 +76,8 @@ typedef struct rl_model_config {
     int32_t max_seqs;
     int32_t max_ctx;
     int32_t max_prefill_tokens;
+    int32_t kv_page_size;         /* 0: contiguous slots; else positions per K/V page (a power of two in [32, 65536]) */
+    int32_t kv_pages;             /* pages in the pool (0: max_seqs * ceil(max_ctx / kv_page_size)); 0 without pages */
     int32_t reserved;             /* must be 0 */
 } rl_model_config;
 
@@ -129,6 +131,17 @@ typedef struct rl_decode_ctx rl_decode_ctx;
  *   V slab at byte offset rl_decode_kv_bytes(cfg) / 2, in 8-position blocks:
  *     V[l][s][h][t][i]  at element  ((((l*S + s)*Hkv + h)*(cap/8) + t/8)*d + i)*8 + t%8
  * Position t of a slot holds the token at position t of that sequence.
+ *
+ * Paged pool (kv_page_size = P > 0, NP = kv_pages or max_seqs * ceil(max_ctx / P)):
+ *     K[l][s][h][t][i]  at element  (((l*NP + pg)*Hkv + h)*P + t%P)*d + i
+ *     V[l][s][h][t][i]  at element  ((((l*NP + pg)*Hkv + h)*(P/8) + (t%P)/8)*d + i)*8 + t%8
+ * with pg the page that holds positions [P*(t/P), P*(t/P + 1)) of slot s.  A
+ * slot is given pages as its length grows (prefill, decode steps, scoring,
+ * set lengths, onload) and gives them back when released or shortened, so a
+ * pool of fewer pages than max_seqs * max_ctx positions serves sequences of
+ * uneven lengths; a call that would need more pages than are free fails with
+ * RL_ERR_CAPACITY and changes nothing.  The page table travels with each
+ * call's metadata (4 * max_seqs * ceil(max_ctx / P) bytes).
  * Returns 0 when cfg is invalid or unsupported.
  * ------------------------------------------------------------------- */
 size_t rl_decode_kv_bytes(const rl_model_config* cfg);

@@ -31,6 +31,7 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 struct Layout {
     int es = 0, cap = 0, R = 0, nqkv = 0, items_cap = 0;
+    int page = 0, pages = 0, maxp = 1;   // K/V pages: positions each, pool size, table row length
     size_t kv_bytes = 0, ws_bytes = 0;
     size_t off_x = 0, off_h = 0, off_qkv = 0, off_q = 0, off_attn = 0, off_mlp = 0;
     size_t off_part = 0, off_apart = 0, off_logits = 0, off_rope = 0, off_meta = 0;
@@ -43,6 +44,11 @@ bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
     auto bad = [&](rl_status s, const char* m) { *code = s; *why = m; return false; };
     if (!c) return bad(RL_ERR_INVALID_ARG, "config is NULL");
     if (c->reserved != 0) return bad(RL_ERR_INVALID_ARG, "config.reserved must be 0");
+    if (c->kv_page_size != 0 &&
+        (c->kv_page_size < 32 || c->kv_page_size > 65536 || (c->kv_page_size & (c->kv_page_size - 1)) != 0))
+        return bad(RL_ERR_INVALID_ARG, "kv_page_size must be 0 or a power of two in [32, 65536]");
+    if (c->kv_pages < 0 || (c->kv_page_size == 0 && c->kv_pages != 0) || c->kv_pages > (1 << 26))
+        return bad(RL_ERR_INVALID_ARG, "kv_pages must be >= 0, and 0 without pages");
     if (c->n_layers < 1 || c->n_layers > 4096) return bad(RL_ERR_INVALID_ARG, "n_layers out of range");
     if (c->hidden < 8 || c->hidden > (1 << 16)) return bad(RL_ERR_INVALID_ARG, "hidden out of range");
     if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads > 1024) return bad(RL_ERR_INVALID_ARG, "head counts out of range");
@@ -78,7 +84,16 @@ Layout make_layout(const rl_model_config& c) {
     L.items_cap = std::max(kPartItems, L.R + c.max_seqs);
     const size_t es = L.es, R = L.R, H = c.hidden, F = c.ffn, V = c.vocab;
     const size_t HqD = static_cast<size_t>(c.n_q_heads) * c.head_dim;
-    L.kv_bytes = 2ull * c.n_layers * c.max_seqs * c.n_kv_heads * static_cast<size_t>(L.cap) * c.head_dim * es;
+    if (c.kv_page_size > 0) {
+        L.page = c.kv_page_size;
+        L.maxp = static_cast<int>((static_cast<size_t>(c.max_ctx) + L.page - 1) / L.page);
+        L.pages = c.kv_pages > 0 ? c.kv_pages : c.max_seqs * L.maxp;
+    } else {
+        L.page = L.cap;
+        L.maxp = 1;
+        L.pages = c.max_seqs;
+    }
+    L.kv_bytes = 2ull * c.n_layers * L.pages * c.n_kv_heads * static_cast<size_t>(L.page) * c.head_dim * es;
     L.part_floats = kPartCapFloats;
     if (c.dtype == RL_DTYPE_FP32) L.part_floats = std::max(L.part_floats, R * std::max(H, 2 * F));
     L.apart_floats = static_cast<size_t>(kPartItems) * c.n_kv_heads * 16 * (c.head_dim + 2);
@@ -87,6 +102,8 @@ Layout make_layout(const rl_model_config& c) {
     // attention work items
     L.meta_bytes = 4 * (7 * R + 4 * static_cast<size_t>(c.max_seqs)) + 8 * static_cast<size_t>(c.max_seqs) +
                    sizeof(AttnItem) * static_cast<size_t>(L.items_cap) + 4096;
+    // a paged pool's table travels with every call's metadata
+    if (c.kv_page_size > 0) L.meta_bytes += 4 * static_cast<size_t>(c.max_seqs) * L.maxp + 16;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
     L.off_x = take(R * H * 4);
@@ -143,9 +160,18 @@ struct rl_decode_ctx {
     std::vector<TunedPlan> tuned;
     std::string err;
 
+    // K/V pages (kv_page_size > 0): per slot its pages in position order
+    // (ptab[s * maxp + j], -1 = none; npages[s] of them), and the free pages
+    std::vector<int32_t> ptab, npages, free_pages;
+
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
     uint8_t* kslab() const { return kv; }
     uint8_t* vslab() const { return kv + lay.kv_bytes / 2; }
+    bool paged() const { return cfg.kv_page_size > 0; }
+    // addressing of the contiguous pool, or of a paged one through a device copy of the table
+    KvPages kvp(const int32_t* dev_table) const {
+        return KvPages{paged() ? dev_table : nullptr, lay.maxp, lay.page, lay.pages};
+    }
     SamplePart* sample_parts() const { return reinterpret_cast<SamplePart*>(ws + lay.off_spart); }
     bool bf16() const { return cfg.dtype == RL_DTYPE_BF16; }
 };
@@ -242,6 +268,69 @@ struct Meta {
     }
 };
 
+// ---- K/V pages --------------------------------------------------------------
+int pages_for(const rl_decode_ctx* c, int len) { return (len + c->lay.page - 1) / c->lay.page; }
+
+// Distinct slots with their final lengths (a later entry for a slot wins).
+std::vector<std::pair<int, int>> final_lengths(int n, const int32_t* slots, const int32_t* lens) {
+    std::vector<std::pair<int, int>> v;
+    for (int i = 0; i < n; ++i) {
+        bool found = false;
+        for (auto& e : v)
+            if (e.first == slots[i]) { e.second = lens[i]; found = true; }
+        if (!found) v.emplace_back(slots[i], lens[i]);
+    }
+    return v;
+}
+
+// Whether the slots can hold these lengths with the free pages (pages a slot
+// gives back count).  Always true for a contiguous pool.
+bool pages_fit(const rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want) {
+    if (!c->paged()) return true;
+    int64_t need = 0, back = 0;
+    for (const auto& e : want) {
+        const int d = pages_for(c, e.second) - c->npages[e.first];
+        if (d > 0) need += d; else back -= d;
+    }
+    return need <= static_cast<int64_t>(c->free_pages.size()) + back;
+}
+
+// Give every slot exactly the pages its length needs (pages_fit held).
+void set_pages(rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want) {
+    if (!c->paged()) return;
+    const size_t mp = static_cast<size_t>(c->lay.maxp);
+    for (const auto& e : want) {   // shrink first: the pages given back serve the others
+        const int s = e.first, keep = pages_for(c, e.second);
+        while (c->npages[s] > keep) {
+            int32_t& pg = c->ptab[s * mp + --c->npages[s]];
+            c->free_pages.push_back(pg);
+            pg = -1;
+        }
+    }
+    for (const auto& e : want) {
+        const int s = e.first, need = pages_for(c, e.second);
+        while (c->npages[s] < need) {
+            c->ptab[s * mp + c->npages[s]++] = c->free_pages.back();
+            c->free_pages.pop_back();
+        }
+    }
+}
+
+// A paged pool's table region in this call's metadata (taken with the other
+// arrays, filled once the call's pages are set).
+struct PageStage { int32_t* host = nullptr; int32_t* dev = nullptr; };
+
+PageStage take_pages(rl_decode_ctx* c, Meta* m) {
+    PageStage ps;
+    if (c->paged()) ps.host = m->take<int32_t>(c->ptab.size(), &ps.dev);
+    return ps;
+}
+
+KvPages fill_pages(rl_decode_ctx* c, const PageStage& ps) {
+    if (c->paged() && ps.host) std::memcpy(ps.host, c->ptab.data(), c->ptab.size() * sizeof(int32_t));
+    return c->kvp(ps.dev);
+}
+
 rl_status begin_meta(rl_decode_ctx* c, Meta* m, int* stage) {
     int s = c->stage_next;
     if (c->stage_used[s]) {
@@ -269,6 +358,7 @@ rl_status upload_meta(rl_decode_ctx* c, Meta* m, int stage) {
 
 // ---- forward pass description ----------------------------------------------
 struct Fwd {
+    KvPages kvp{nullptr, 1, 0, 0};          // K/V addressing of this call
     int rows = 0;
     const int32_t* tok = nullptr;
     const void* embeds = nullptr;
@@ -501,23 +591,23 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
             const float* src = splits > 1 ? c->wsp<float>(L.off_part) : qkv;
             Prof pr(c, RL_K_ROPE_APPEND);
             e = launch_rope_append(dt, src, qs, n, f.row_pos, f.row_dst, f.n_dst, f.dst_slots, cs, cs_stride, Hq,
-                                   Hkv, D, cf.max_seqs, L.cap, l, q, c->kslab(), c->vslab(), c->stream);
+                                   Hkv, D, f.kvp, l, q, c->kslab(), c->vslab(), c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "rope/append launch");
             pr.done(n * (qs * L.nqkv * 4.0 + HqD * es + f.n_dst * 2.0 * Hkv * D * es), 0.0);
         }
         {
             Prof pr(c, RL_K_ATTENTION, c->bf16() && !f.tiles);
             if (c->bf16() && f.tiles)
-                e = launch_attention_prefill(f.tiles, f.n_tiles, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv, D,
-                                             L.cap, l, attn, c->stream);
+                e = launch_attention_prefill(f.tiles, f.n_tiles, q, c->kslab(), c->vslab(), f.kvp, Hq, Hkv, D,
+                                             l, attn, c->stream);
             else if (c->bf16())
-                e = launch_attention_bf16(f.items, f.n_items, q, c->kslab(), c->vslab(), cf.max_seqs, Hq, Hkv,
-                                          D, L.cap, l, attn, apart, c->stream, pr.start(), pr.stop());
+                e = launch_attention_bf16(f.items, f.n_items, q, c->kslab(), c->vslab(), f.kvp, Hq, Hkv,
+                                          D, l, attn, apart, c->stream, pr.start(), pr.stop());
             else
                 e = launch_attention_f32(n, f.row_slot, f.row_pos, static_cast<const float*>(q),
                                          reinterpret_cast<const float*>(c->kslab()),
-                                         reinterpret_cast<const float*>(c->vslab()), cf.max_seqs, Hq, Hkv, D,
-                                         L.cap, l, static_cast<float*>(attn), c->stream);
+                                         reinterpret_cast<const float*>(c->vslab()), f.kvp, Hq, Hkv, D,
+                                         l, static_cast<float*>(attn), c->stream);
             if (e != hipSuccess) return hip_fail(c, e, "attention launch");
             pr.done(f.attn_kv_positions * Hkv * 2.0 * D * es + 2.0 * n * HqD * es,
                     4.0 * Hq * D * f.attn_score_positions);
@@ -614,9 +704,10 @@ rl_status tune_unit(rl_decode_ctx* c, int kc, const GemmPlan& p, int M, int l, c
                                EPI_F32, qkv, L.nqkv, nullptr, 0, nullptr, 0, true, &splits);
             if (st != RL_OK) return st;
             const float* src = splits > 1 ? c->wsp<float>(L.off_part) : qkv;
+            // no K/V destination (n_dst = 0), so the pool is not addressed
             const hipError_t e = launch_rope_append(DT_BF16, src, splits > 1 ? splits : 1, M, zeros, zeros, 0, nullptr,
                                                     c->wsp<float>(L.off_rope), L.cap * (D / 2), Hq, Hkv, D,
-                                                    cf.max_seqs, L.cap, l, c->ws + L.off_q, c->kslab(), c->vslab(),
+                                                    c->kvp(nullptr), l, c->ws + L.off_q, c->kslab(), c->vslab(),
                                                     c->stream);
             return e == hipSuccess ? RL_OK : hip_fail(c, e, "rope launch");
         }
@@ -793,7 +884,12 @@ rl_status tune_gemms(rl_decode_ctx* c, const std::vector<int>& sizes) {
             c->tuned[base + k].us = unit_us[k][best];
         }
     }
-    for (int i = 0; i < max_m; ++i) c->len[i] = 0;
+    std::vector<std::pair<int, int>> none;
+    for (int i = 0; i < max_m; ++i) {
+        c->len[i] = 0;
+        none.emplace_back(i, 0);
+    }
+    set_pages(c, none);
     c->profile = profile;
     c->plan = plan_stats;
     if (tm.e0) (void)hipEventDestroy(tm.e0);
@@ -1250,6 +1346,12 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
     c->len.assign(static_cast<size_t>(cfg->max_seqs), 0);
     c->share_src.assign(static_cast<size_t>(cfg->max_seqs), -1);
     c->share_len.assign(static_cast<size_t>(cfg->max_seqs), 0);
+    if (c->paged()) {
+        c->ptab.assign(static_cast<size_t>(cfg->max_seqs) * L.maxp, -1);
+        c->npages.assign(static_cast<size_t>(cfg->max_seqs), 0);
+        c->free_pages.resize(static_cast<size_t>(L.pages));
+        for (int i = 0; i < L.pages; ++i) c->free_pages[i] = L.pages - 1 - i;   // handed out from page 0 up
+    }
     auto cleanup = [&](rl_status s) {
         for (int i = 0; i < kStages; ++i) {
             if (c->staging[i]) (void)hipHostFree(c->staging[i]);
@@ -1319,12 +1421,17 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     }
     if (total > cf.max_prefill_tokens) return fail(c, RL_ERR_CAPACITY, "prompts exceed max_prefill_tokens");
     const int R = static_cast<int>(total);
+    std::vector<int32_t> new_len(static_cast<size_t>(n_out));
+    for (int o = 0; o < n_out; ++o) new_len[o] = prompt_offsets[o / group + 1] - prompt_offsets[o / group];
+    const auto want = final_lengths(n_out, slots, new_len.data());
+    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
 
     Meta m{};
     int stage = 0;
     st = begin_meta(c, &m, &stage);
     if (st != RL_OK) return st;
+    const PageStage ps = take_pages(c, &m);
     int32_t *d_row_pos, *d_row_dst, *d_row_slot, *d_dst, *d_lrow, *d_posn, *d_last;
     uint64_t* d_uid;
     int32_t* row_pos = m.take<int32_t>(R, &d_row_pos);
@@ -1396,6 +1503,8 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     f.T = sp->temperature;
     f.out_tok = out_tok;
     f.out_logp = out_logp;
+    set_pages(c, want);
+    f.kvp = fill_pages(c, ps);
     st = upload_meta(c, &m, stage);
     if (st != RL_OK) return st;
     st = run_forward(c, f);
@@ -1455,12 +1564,20 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
         return fail(c, RL_ERR_CAPACITY, "prompt + response tokens exceed max_prefill_tokens");
     const int R1 = static_cast<int>(r1), R = static_cast<int>(r1 + r2);
     const int n_sel = n_prompts + static_cast<int>(r2) - n_seq;   // LM-head rows
+    // each slot holds its group's prompt and its own response while scoring
+    std::vector<int32_t> new_len(static_cast<size_t>(n_seq));
+    for (int sq = 0; sq < n_seq; ++sq)
+        new_len[sq] = prompt_offsets[sq / group + 1] - prompt_offsets[sq / group] + resp_offsets[sq + 1] -
+                      resp_offsets[sq];
+    const auto want = final_lengths(n_seq, slots, new_len.data());
+    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
 
     Meta m{};
     int stage = 0;
     st = begin_meta(c, &m, &stage);
     if (st != RL_OK) return st;
+    const PageStage ps = take_pages(c, &m);
     int32_t *d_row_pos, *d_row_dst, *d_row_slot, *d_dst, *d_sel, *d_items, *d_idx;
     int32_t* row_pos = m.take<int32_t>(R, &d_row_pos);
     int32_t* row_dst = m.take<int32_t>(R, &d_row_dst);
@@ -1556,6 +1673,8 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     f.score_items = d_items;
     f.score_idx = d_idx;
     f.score_targets = resp_tokens;
+    set_pages(c, want);
+    f.kvp = fill_pages(c, ps);
     st = upload_meta(c, &m, stage);
     if (st != RL_OK) return st;
     int32_t* tok = c->wsp<int32_t>(c->lay.off_tok);
@@ -1567,6 +1686,9 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     unshare(c, n_seq, slots);
     st = run_forward(c, f);
     for (int i = 0; i < n_seq; ++i) c->len[slots[i]] = 0;   // the slots were scratch
+    std::vector<std::pair<int, int>> none;
+    for (const auto& e : want) none.emplace_back(e.first, 0);
+    set_pages(c, none);   // a later call's K/V writes are ordered after this call's kernels
     return st;
 }
 
@@ -1589,12 +1711,18 @@ rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, co
     if (st != RL_OK) return st;
     for (int i = 0; i < n; ++i)
         if (c->len[slots[i]] >= cf.max_ctx) return fail(c, RL_ERR_CAPACITY, "slot is full (length == max_ctx)");
+    std::vector<std::pair<int, int>> want;
+    if (c->paged()) {
+        for (int i = 0; i < n; ++i) want.emplace_back(slots[i], c->len[slots[i]] + 1);
+        if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
+    }
     DeviceGuard g(c->device);
 
     Meta m{};
     int stage = 0;
     st = begin_meta(c, &m, &stage);
     if (st != RL_OK) return st;
+    const PageStage ps = take_pages(c, &m);
     int32_t *d_pos, *d_dst, *d_slot, *d_posn;
     uint64_t* d_uid;
     int32_t* pos = m.take<int32_t>(n, &d_pos);
@@ -1644,6 +1772,8 @@ rl_status rl_decode_step(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, co
     f.T = sp->temperature;
     f.out_tok = out_tok;
     f.out_logp = out_logp;
+    set_pages(c, want);
+    f.kvp = fill_pages(c, ps);
     st = upload_meta(c, &m, stage);
     if (st != RL_OK) return st;
     st = run_forward(c, f);
@@ -1736,6 +1866,7 @@ rl_status kv_transfer(rl_decode_ctx* c, int dir, int n, const int32_t* slots, co
         int stage = 0;
         rl_status st = begin_meta(c, &m, &stage);
         if (st != RL_OK) return st;
+        const PageStage ps = take_pages(c, &m);
         int32_t *d_slots, *d_lens;
         int64_t* d_base;
         int32_t* hs = m.take<int32_t>(i1 - i0, &d_slots);
@@ -1749,13 +1880,14 @@ rl_status kv_transfer(rl_decode_ctx* c, int dir, int n, const int32_t* slots, co
             hb[i - i0] = static_cast<int64_t>(b);
             b += kv_slot_packed_bytes(c, lens[i]);
         }
+        const KvPages kp = fill_pages(c, ps);
         st = upload_meta(c, &m, stage);
         if (st != RL_OK) return st;
         uint8_t* stg = c->ws + L.off_stage;
         hipError_t e = hipSuccess;
         if (dir == 1) e = hipMemcpyAsync(stg, host + host_off, bytes, hipMemcpyHostToDevice, c->stream);
         if (e == hipSuccess)
-            e = launch_kv_pack(dir, d_slots, d_lens, d_base, i1 - i0, cf.n_layers, cf.max_seqs, cf.n_kv_heads, L.cap,
+            e = launch_kv_pack(dir, d_slots, d_lens, d_base, i1 - i0, cf.n_layers, kp, cf.n_kv_heads,
                                cf.head_dim * L.es, c->kslab(), c->vslab(), stg, c->stream);
         if (e == hipSuccess && dir == 0) e = hipMemcpyAsync(host + host_off, stg, bytes, hipMemcpyDeviceToHost, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, dir == 0 ? "KV offload" : "KV onload");
@@ -1817,7 +1949,10 @@ rl_status rl_kv_onload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, cons
         total += b;
     }
     if (total > host_bytes) return fail(c, RL_ERR_CAPACITY, "host buffer smaller than the packed K/V of these lengths");
+    const auto want = final_lengths(n, slots, lengths);
+    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
+    set_pages(c, want);
     st = kv_transfer(c, 1, n, slots, lengths, static_cast<uint8_t*>(const_cast<void*>(host_src)));
     if (st != RL_OK) return st;
     for (int i = 0; i < n; ++i) c->len[slots[i]] = lengths[i];
@@ -1849,7 +1984,12 @@ rl_status rl_release_slots(rl_decode_ctx* ctx, int32_t n, const int32_t* slots) 
     if (n < 0 || (n > 0 && !slots)) return fail(ctx, RL_ERR_INVALID_ARG, "bad slot list");
     for (int i = 0; i < n; ++i)
         if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return fail(ctx, RL_ERR_INVALID_ARG, "slot out of range");
-    for (int i = 0; i < n; ++i) ctx->len[slots[i]] = 0;
+    std::vector<std::pair<int, int>> none;
+    for (int i = 0; i < n; ++i) {
+        ctx->len[slots[i]] = 0;
+        none.emplace_back(slots[i], 0);
+    }
+    set_pages(ctx, none);
     unshare(ctx, n, slots);
     return RL_OK;
 }
@@ -1861,6 +2001,9 @@ rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slot
         if (slots[i] < 0 || slots[i] >= ctx->cfg.max_seqs) return fail(ctx, RL_ERR_INVALID_ARG, "slot out of range");
         if (lengths[i] < 0 || lengths[i] > ctx->cfg.max_ctx) return fail(ctx, RL_ERR_INVALID_ARG, "length out of range");
     }
+    const auto want = final_lengths(n, slots, lengths);
+    if (!pages_fit(ctx, want)) return fail(ctx, RL_ERR_CAPACITY, "not enough free K/V pages");
+    set_pages(ctx, want);
     for (int i = 0; i < n; ++i) ctx->len[slots[i]] = lengths[i];
     unshare(ctx, n, slots);
     return RL_OK;

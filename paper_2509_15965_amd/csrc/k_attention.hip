@@ -155,10 +155,12 @@ __device__ __forceinline__ void step_frags(const uint8_t* kl, const uint8_t* vl,
 // vmcnt(0) with expcnt and lgkmcnt left alone (gfx9 encoding)
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
-template <int D>
+// PAGED: the item's key range may cross pages, so each 32-position step
+// looks its page up; otherwise the slot's block is fixed for the item.
+template <int D, bool PAGED>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __restrict__ items,
         int n_items, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-        const uint16_t* __restrict__ vc, int S, int Hq, int Hkv, int cap, int layer,
+        const uint16_t* __restrict__ vc, KvPages kp, int Hq, int Hkv, int layer,
         float scale_log2, uint16_t* __restrict__ out, float* __restrict__ part) {
     constexpr int KG = D / 32;   // 32-wide k groups of a head
     constexpr int DT = D / 16;   // 16-wide d tiles of the output
@@ -192,9 +194,21 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
         for (int j = 0; j < KG; ++j) qf[j] = cvalid ? ld16(qp + 32 * j) : zero;
     }
 
-    const size_t base = ((static_cast<size_t>(layer) * S + it.slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
-    const uint16_t* kb = kc + base;
-    const uint16_t* vb = vc + base;
+    // K / V block of the step at position t0 (element pointers) and t0's
+    // position inside it
+    const size_t base = PAGED ? 0 : kv_block(kp, layer, Hkv, it.slot, kvh, D);
+    auto block_of = [&](int t0, const uint16_t** kbp, const uint16_t** vbp) {
+        if (!PAGED) {
+            *kbp = kc + base;
+            *vbp = vc + base;
+            return t0;
+        }
+        int lt;
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, it.slot, t0, &lt), kvh, D);
+        *kbp = kc + b;
+        *vbp = vc + b;
+        return lt;
+    };
 
     float m = -INFINITY, l = 0.0f;
     f32x4 o[DT];
@@ -208,25 +222,31 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
     // waves resident on the chip keep HBM busy without a per-wave prefetch)
     u32x4 k0[KG], k1[KG], vf[DT];
     auto load_step = [&](int t0, u32x4 (&a0)[KG], u32x4 (&a1)[KG], u32x4 (&vv)[DT]) {
-        const uint16_t* kp0 = kb + static_cast<size_t>(t0 + krow) * D + 8 * kq;
+        const uint16_t *kb, *vb;
+        const int lt = block_of(t0, &kb, &vb);
+        const uint16_t* kp0 = kb + static_cast<size_t>(lt + krow) * D + 8 * kq;
         const uint16_t* kp1 = kp0 + 4 * D;
 #pragma unroll
         for (int j = 0; j < KG; ++j) {
             a0[j] = ld16(kp0 + 32 * j);
             a1[j] = ld16(kp1 + 32 * j);
         }
-        const uint16_t* vp = vb + (static_cast<size_t>((t0 + 8 * kq) >> 3) * D + col) * 8;
+        const uint16_t* vp = vb + (static_cast<size_t>((lt + 8 * kq) >> 3) * D + col) * 8;
 #pragma unroll
         for (int i = 0; i < DT; ++i) vv[i] = ld16(vp + 16 * 8 * i);
     };
+    auto dma_step = [&](int t0, int buf) {
+        const uint16_t *kb, *vb;
+        const int lt = block_of(t0, &kb, &vb);
+        step_dma<D, 4>(kb, vb, lt, wave, lane, lds[buf][0], lds[buf][1]);
+    };
     if (wg_lds) {
         const int nsteps = (hi - it.kv_lo + 31) / 32;
-        if (nsteps > 0) step_dma<D, 4>(kb, vb, it.kv_lo, wave, lane, lds[0][0], lds[0][1]);
+        if (nsteps > 0) dma_step(it.kv_lo, 0);
         for (int s = 0; s < nsteps; ++s) {
             wait_vm0();        // this wave's DMAs (and q loads) landed
             __syncthreads();   // every wave's part of step s is in LDS; step s-1 retired
-            if (s + 1 < nsteps)
-                step_dma<D, 4>(kb, vb, it.kv_lo + 32 * (s + 1), wave, lane, lds[(s + 1) & 1][0], lds[(s + 1) & 1][1]);
+            if (s + 1 < nsteps) dma_step(it.kv_lo + 32 * (s + 1), (s + 1) & 1);
             step_frags<D>(lds[s & 1][0], lds[s & 1][1], krow, kq, col, k0, k1, vf);
             attn_step<D>(k0, k1, vf, qf, it.kv_lo + 32 * s, hi, limit, kq, scale_log2, m, l, o);
         }
@@ -271,8 +291,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
 }
 
 hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
-                                 const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
-                                 int D, int cap, int layer, void* out, float* part,
+                                 const void* kc, const void* vc, const KvPages& kp, int Hq, int Hkv,
+                                 int D, int layer, void* out, float* part,
                                  hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (n_items <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
@@ -281,14 +301,18 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
         if (ev_start || ev_stop)
             hipExtLaunchKernelGGL(kern, grid, block, 0, s, ev_start, ev_stop, 0, items, n_items,
                                   static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kc),
-                                  static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv, cap, layer, scale_log2,
+                                  static_cast<const uint16_t*>(vc), kp, Hq, Hkv, layer, scale_log2,
                                   static_cast<uint16_t*>(out), part);
         else
             hipLaunchKernelGGL(kern, grid, block, 0, s, items, n_items, static_cast<const uint16_t*>(q),
-                               static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq,
-                               Hkv, cap, layer, scale_log2, static_cast<uint16_t*>(out), part);
+                               static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), kp, Hq,
+                               Hkv, layer, scale_log2, static_cast<uint16_t*>(out), part);
     };
-    if (D == 128) go(attn_bf16_kernel<128>); else go(attn_bf16_kernel<64>);
+    if (kp.table) {
+        if (D == 128) go(attn_bf16_kernel<128, true>); else go(attn_bf16_kernel<64, true>);
+    } else {
+        if (D == 128) go(attn_bf16_kernel<128, false>); else go(attn_bf16_kernel<64, false>);
+    }
     return hipGetLastError();
 }
 
@@ -306,8 +330,8 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
 
 template <int D>
 __global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const PrefillTile* __restrict__ tiles,
-        const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int S,
-        int Hq, int Hkv, int cap, int layer, float scale_log2, uint16_t* __restrict__ out) {
+        const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+        KvPages kp, int Hq, int Hkv, int layer, float scale_log2, uint16_t* __restrict__ out) {
     constexpr int KG = D / 32, DT = D / 16;
     constexpr int STEPB = 32 * D * 2;               // bytes of K (and of V) per 32-position step
     static_assert(STEPB % 1024 == 0, "whole 1 KB DMA instructions per step");
@@ -330,9 +354,12 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const 
     const int wave_last = tl.pos0 + tok0 + nq - 1;  // last key any column of this wave sees
     const int nsteps = (hi + 31) / 32;
 
-    const size_t base = ((static_cast<size_t>(layer) * S + tl.slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
-    const uint16_t* kb = kc + base;
-    const uint16_t* vb = vc + base;
+    // the K/V of the step at position t0: its page's blocks and t0 inside the page
+    auto dma_step = [&](int t0, int buf) {
+        int lt;
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, tl.slot, t0, &lt), kvh, D);
+        step_dma<D, kPrefillWaves>(kc + b, vc + b, lt, wave, lane, lds[buf][0], lds[buf][1]);
+    };
 
     const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 qf[KG];
@@ -347,12 +374,11 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const 
     for (int i = 0; i < DT; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int krow = 8 * (col >> 2) + (col & 3);
 
-    if (nsteps > 0) step_dma<D, kPrefillWaves>(kb, vb, 0, wave, lane, lds[0][0], lds[0][1]);
+    if (nsteps > 0) dma_step(0, 0);
     for (int s = 0; s < nsteps; ++s) {
         wait_vm0();        // this wave's DMAs (and q loads) landed
         __syncthreads();   // every wave's part of step s is in LDS; step s-1 retired
-        if (s + 1 < nsteps)
-            step_dma<D, kPrefillWaves>(kb, vb, 32 * (s + 1), wave, lane, lds[(s + 1) & 1][0], lds[(s + 1) & 1][1]);
+        if (s + 1 < nsteps) dma_step(32 * (s + 1), (s + 1) & 1);
         const int t0 = 32 * s;
         if (nq == 0 || t0 > wave_last) continue;       // wave-uniform: nothing of this step is visible
         u32x4 k0[KG], k1[KG], vf[DT];
@@ -375,19 +401,19 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const 
 }
 
 hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const void* q, const void* kc,
-                                    const void* vc, int max_seqs, int Hq, int Hkv, int D, int cap, int layer,
+                                    const void* vc, const KvPages& kp, int Hq, int Hkv, int D, int layer,
                                     void* out, hipStream_t s) {
     if (n_tiles <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     dim3 grid(n_tiles, Hkv), block(64 * kPrefillWaves);
     if (D == 128)
         hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, block, 0, s, tiles, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
-                           cap, layer, scale_log2, static_cast<uint16_t*>(out));
+                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), kp, Hq, Hkv,
+                           layer, scale_log2, static_cast<uint16_t*>(out));
     else
         hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, block, 0, s, tiles, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), max_seqs, Hq, Hkv,
-                           cap, layer, scale_log2, static_cast<uint16_t*>(out));
+                           static_cast<const uint16_t*>(kc), static_cast<const uint16_t*>(vc), kp, Hq, Hkv,
+                           layer, scale_log2, static_cast<uint16_t*>(out));
     return hipGetLastError();
 }
 
@@ -462,8 +488,8 @@ hipError_t launch_attn_combine(const int32_t* blocks, int n_blocks, const AttnIt
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict__ row_slot,
         const int32_t* __restrict__ row_pos, const float* __restrict__ q,
-        const float* __restrict__ kc, const float* __restrict__ vc, int S, int Hq, int Hkv, int D,
-        int cap, int layer, float* __restrict__ out) {
+        const float* __restrict__ kc, const float* __restrict__ vc, KvPages kp, int Hq, int Hkv, int D,
+        int layer, float* __restrict__ out) {
     __shared__ float qs[128];
     __shared__ float ps[64];
     const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
@@ -472,9 +498,17 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict_
     const float* qr = q + (static_cast<size_t>(r) * Hq + h) * D;
     for (int i = lane; i < D; i += 64) qs[i] = qr[i];
     __syncthreads();
-    const size_t base = ((static_cast<size_t>(layer) * S + slot) * Hkv + kvh) * static_cast<size_t>(cap) * D;
-    const float* kb = kc + base;
-    const float* vb = vc + base;
+    // K row and V block start of position t (its page's block, t inside it)
+    auto krow_of = [&](int t) {
+        int lt;
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh, D);
+        return kc + b + static_cast<size_t>(lt) * D;
+    };
+    auto vblk_of = [&](int t) {
+        int lt;
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh, D);
+        return vc + b + static_cast<size_t>(lt >> 3) * D * 8 + (lt & 7);
+    };
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     float m = -INFINITY, l = 0.0f;
     float acc0 = 0.0f, acc1 = 0.0f;   // d = lane, lane + 64
@@ -482,7 +516,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict_
         const int t = t0 + lane;
         float s = -INFINITY;
         if (t <= pos) {
-            const float* kr = kb + static_cast<size_t>(t) * D;
+            const float* kr = krow_of(t);
             float d = 0.0f;
             for (int i = 0; i < D; ++i) d = fmaf(qs[i], kr[i], d);
             s = d * scale;
@@ -499,8 +533,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict_
         acc1 *= alpha;
         const int nt = min(64, pos + 1 - t0);
         for (int tt = 0; tt < nt; ++tt) {
-            const int tp = t0 + tt;
-            const float* vblk = vb + static_cast<size_t>(tp >> 3) * D * 8 + (tp & 7);
+            const float* vblk = vblk_of(t0 + tt);
             if (lane < D) acc0 = fmaf(ps[tt], vblk[static_cast<size_t>(lane) * 8], acc0);
             if (lane + 64 < D) acc1 = fmaf(ps[tt], vblk[static_cast<size_t>(lane + 64) * 8], acc1);
         }
@@ -512,12 +545,12 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict_
 }
 
 hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
-                                const float* q, const float* kc, const float* vc, int max_seqs,
-                                int Hq, int Hkv, int D, int cap, int layer, float* out,
+                                const float* q, const float* kc, const float* vc, const KvPages& kp,
+                                int Hq, int Hkv, int D, int layer, float* out,
                                 hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
     hipLaunchKernelGGL(attn_f32_kernel, dim3(n_rows, Hq), dim3(64), 0, s, row_slot, row_pos, q, kc,
-                       vc, max_seqs, Hq, Hkv, D, cap, layer, out);
+                       vc, kp, Hq, Hkv, D, layer, out);
     return hipGetLastError();
 }
 

@@ -332,7 +332,7 @@ template <typename T>
 __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restrict__ qkv, int splits,
         size_t slice, int n_rows, const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_dst,
         int n_dst, const int32_t* __restrict__ dst_slots, const float* __restrict__ cs, int cs_stride, int Hq,
-        int Hkv, int D, int S, int cap, int layer, T* __restrict__ q_out, T* __restrict__ kc,
+        int Hkv, int D, KvPages kp, int layer, T* __restrict__ q_out, T* __restrict__ kc,
         T* __restrict__ vc) {
     const int half = D / 2;
     const int nh = Hq + 2 * Hkv;
@@ -363,8 +363,9 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
         const int nd = d0 < 0 ? 1 : n_dst;
         for (int g = 0; g < nd; ++g) {
             const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
-            T* kr = kc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq)) * static_cast<size_t>(cap) * D +
-                    static_cast<size_t>(pos) * D;
+            int lp;
+            const int pid = kv_page(kp, slot, pos, &lp);
+            T* kr = kc + kv_block(kp, layer, Hkv, pid, h - Hq, D) + static_cast<size_t>(lp) * D;
             Elem<T>::store(kr, i, x0);
             Elem<T>::store(kr, i + half, x1);
         }
@@ -374,16 +375,18 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
     const int nd = d0 < 0 ? 1 : n_dst;
     for (int g = 0; g < nd; ++g) {
         const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
-        T* vb = vc + ((static_cast<size_t>(layer) * S + slot) * Hkv + (h - Hq - Hkv)) * static_cast<size_t>(cap) * D;
-        Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i) * 8 + (pos & 7), a);
-        Elem<T>::store(vb, (static_cast<size_t>(pos >> 3) * D + i + half) * 8 + (pos & 7), b);
+        int lp;
+        const int pid = kv_page(kp, slot, pos, &lp);
+        T* vb = vc + kv_block(kp, layer, Hkv, pid, h - Hq - Hkv, D);
+        Elem<T>::store(vb, (static_cast<size_t>(lp >> 3) * D + i) * 8 + (lp & 7), a);
+        Elem<T>::store(vb, (static_cast<size_t>(lp >> 3) * D + i + half) * 8 + (lp & 7), b);
     }
 }
 
 hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, const int32_t* row_pos,
                               const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
                               const float* cs, int cs_stride, int Hq, int Hkv, int D,
-                              int max_seqs, int cap, int layer,
+                              const KvPages& kp, int layer,
                               void* q_out, void* kc, void* vc, hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
     const size_t threads = static_cast<size_t>(n_rows) * (Hq + 2 * Hkv) * (D / 2);
@@ -392,11 +395,11 @@ hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, 
     const int sp = splits < 1 ? 1 : splits;
     if (dt == DT_BF16)
         hipLaunchKernelGGL(rope_append_kernel<uint16_t>, grid, block, 0, s, qkv, sp, slice, n_rows, row_pos, row_dst,
-                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, max_seqs, cap, layer,
+                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, kp, layer,
                            static_cast<uint16_t*>(q_out), static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc));
     else
         hipLaunchKernelGGL(rope_append_kernel<float>, grid, block, 0, s, qkv, sp, slice, n_rows, row_pos, row_dst,
-                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, max_seqs, cap, layer,
+                           n_dst, dst_slots, cs, cs_stride, Hq, Hkv, D, kp, layer,
                            static_cast<float*>(q_out), static_cast<float*>(kc), static_cast<float*>(vc));
     return hipGetLastError();
 }
@@ -407,28 +410,38 @@ hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, 
 // in the pool and are copied as they are, 16 bytes per lane.  Packed layout
 // of slot i at byte base[i]: for l, h: K rows then V blocks.
 __global__ void __launch_bounds__(256) kv_pack_kernel(int dir, const int32_t* __restrict__ slots,
-        const int32_t* __restrict__ lens, const int64_t* __restrict__ base, int S, int Hkv, int cap,
+        const int32_t* __restrict__ lens, const int64_t* __restrict__ base, KvPages kp, int Hkv,
         int rowbytes, uint8_t* __restrict__ kslab, uint8_t* __restrict__ vslab, uint8_t* __restrict__ stage) {
     const int i = blockIdx.x, lh = blockIdx.y, kv = blockIdx.z;
     const int l = lh / Hkv, h = lh - l * Hkv;
     const int len = lens[i], len8 = (len + 7) / 8 * 8;
-    const size_t pool_off = ((static_cast<size_t>(l) * S + slots[i]) * Hkv + h) * static_cast<size_t>(cap) * rowbytes;
+    const int rows = kv ? len8 : len;   // K rows, or V positions in whole 8-position blocks
     const size_t st_off = static_cast<size_t>(base[i]) +
                           (static_cast<size_t>(lh) * (len + len8) + (kv ? len : 0)) * rowbytes;
-    u32x4* pool = reinterpret_cast<u32x4*>((kv ? vslab : kslab) + pool_off);
     u32x4* st = reinterpret_cast<u32x4*>(stage + st_off);
-    const size_t n16 = static_cast<size_t>(kv ? len8 : len) * rowbytes / 16;
-    for (size_t j = threadIdx.x; j < n16; j += blockDim.x) {
-        if (dir == 0) st[j] = pool[j];
-        else pool[j] = st[j];
+    const size_t per_row = static_cast<size_t>(rowbytes) / 16;
+    // page by page (one page: every position of a contiguous slot); the rows
+    // of a page are contiguous in both layouts (V: its 8-position blocks)
+    for (int p0 = 0; p0 < rows; p0 += kp.page) {
+        int lp;
+        const int pid = kv_page(kp, slots[i], p0, &lp);
+        const size_t pool_off = (kv_block(kp, l, Hkv, pid, h, 1) + lp) * rowbytes;
+        u32x4* pool = reinterpret_cast<u32x4*>((kv ? vslab : kslab) + pool_off);
+        const int n_rows = min(kp.page, rows - p0);
+        const size_t n16 = static_cast<size_t>(n_rows) * per_row;
+        u32x4* sp = st + static_cast<size_t>(p0) * per_row;
+        for (size_t j = threadIdx.x; j < n16; j += blockDim.x) {
+            if (dir == 0) sp[j] = pool[j];
+            else pool[j] = sp[j];
+        }
     }
 }
 
 hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
-                          int S, int Hkv, int cap, int rowbytes, void* kslab, void* vslab, void* stage,
+                          const KvPages& kp, int Hkv, int rowbytes, void* kslab, void* vslab, void* stage,
                           hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(kv_pack_kernel, dim3(n, L * Hkv, 2), dim3(256), 0, s, dir, slots, lens, base, S, Hkv, cap,
+    hipLaunchKernelGGL(kv_pack_kernel, dim3(n, L * Hkv, 2), dim3(256), 0, s, dir, slots, lens, base, kp, Hkv,
                        rowbytes, static_cast<uint8_t*>(kslab), static_cast<uint8_t*>(vslab),
                        static_cast<uint8_t*>(stage));
     return hipGetLastError();

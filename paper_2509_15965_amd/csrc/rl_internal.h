@@ -11,6 +11,38 @@ namespace rl {
 // Element encodings of the model dtype.
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
+// Where the K/V of (slot, position) lives.  The K slab is [L][pages][Hkv][page][d]
+// and the V slab [L][pages][Hkv][page/8][d][8].  table == nullptr: slot s is
+// page s and holds all `page` (= the slot capacity) positions.  Otherwise
+// position p of slot s is in page table[s * maxp + p / page] at p % page
+// (page a multiple of 32, so a 32-position step never straddles pages).
+struct KvPages {
+    const int32_t* table;
+    int maxp;
+    int page;
+    int pages;
+};
+
+// Page of (slot, pos) and the position inside it; an id outside the pool is
+// clamped into it (the host never stores one; this only keeps every address
+// inside the slab).
+__device__ __forceinline__ int kv_page(const KvPages& kp, int slot, int pos, int* local) {
+    if (!kp.table) {
+        *local = pos;
+        return slot;
+    }
+    const int j = pos / kp.page;
+    int pid = kp.table[static_cast<size_t>(slot) * kp.maxp + j];
+    pid = pid < 0 ? 0 : pid >= kp.pages ? kp.pages - 1 : pid;
+    *local = pos - j * kp.page;
+    return pid;
+}
+
+// Element offset of the K (or V) block of (layer, page, kv-head): page * d elements.
+__device__ __forceinline__ size_t kv_block(const KvPages& kp, int layer, int Hkv, int pid, int head, int D) {
+    return ((static_cast<size_t>(layer) * kp.pages + pid) * Hkv + head) * static_cast<size_t>(kp.page) * D;
+}
+
 // GEMM epilogues: Y = X . W^T followed by
 enum Epi {
     EPI_F32 = 0,      // store fp32 Y
@@ -119,14 +151,14 @@ hipError_t launch_splitk_reduce(int dt, const GemmArgs& a, int splits, const flo
 hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, const int32_t* row_pos,
                               const int32_t* row_dst, int n_dst, const int32_t* dst_slots,
                               const float* cs, int cs_stride, int Hq, int Hkv, int D,
-                              int max_seqs, int cap, int layer,
+                              const KvPages& kp, int layer,
                               void* q_out, void* kc, void* vc, hipStream_t s);
 
 // ev_start / ev_stop (may be null): events stamped with the kernel's own
 // start and end (attached to the dispatch, not recorded around it)
 hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void* q,
-                                 const void* kc, const void* vc, int max_seqs, int Hq, int Hkv,
-                                 int D, int cap, int layer, void* out, float* part,
+                                 const void* kc, const void* vc, const KvPages& kp, int Hq, int Hkv,
+                                 int D, int layer, void* out, float* part,
                                  hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // Most items one split block may have (bounds the combine's LDS).
@@ -151,13 +183,13 @@ constexpr int kPrefillWaves = 8;
 // loaded once into LDS and used by every wave (wave w takes the tile's tokens
 // [w * 16/G, (w+1) * 16/G)); outputs are final (no split partials).
 hipError_t launch_attention_prefill(const PrefillTile* tiles, int n_tiles, const void* q, const void* kc,
-                                    const void* vc, int max_seqs, int Hq, int Hkv, int D, int cap, int layer,
+                                    const void* vc, const KvPages& kp, int Hq, int Hkv, int D, int layer,
                                     void* out, hipStream_t s);
 
 // fp32 model dtype: one workgroup per (row, q-head), keys 0..row_pos[r].
 hipError_t launch_attention_f32(int n_rows, const int32_t* row_slot, const int32_t* row_pos,
-                                const float* q, const float* kc, const float* vc, int max_seqs,
-                                int Hq, int Hkv, int D, int cap, int layer, float* out,
+                                const float* q, const float* kc, const float* vc, const KvPages& kp,
+                                int Hq, int Hkv, int D, int layer, float* out,
                                 hipStream_t s);
 
 // Per-chunk partial of the sampler (merged in chunk order by a second kernel).
@@ -192,9 +224,10 @@ hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_
 // (dir 0: pool -> stage, dir 1: stage -> pool).  Slot i (lens[i] positions)
 // starts at byte base[i] of the stage: for layer l, kv-head h (index
 // l*Hkv + h): lens[i] K rows of rowbytes, then ceil8(lens[i]) / 8 V blocks of
-// 8 * rowbytes (the pool's own layouts).  rowbytes = head_dim * element size.
+// 8 * rowbytes (the pool's own layouts, page after page).  rowbytes =
+// head_dim * element size.
 hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
-                          int S, int Hkv, int cap, int rowbytes, void* kslab, void* vslab, void* stage,
+                          const KvPages& kp, int Hkv, int rowbytes, void* kslab, void* vslab, void* stage,
                           hipStream_t s);
 
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);

@@ -44,7 +44,8 @@ class ModelConfig(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn", C.c_int32),
                 ("vocab", C.c_int32), ("dtype", C.c_int32), ("rms_eps", C.c_double),
                 ("rope_theta", C.c_double), ("max_seqs", C.c_int32), ("max_ctx", C.c_int32),
-                ("max_prefill_tokens", C.c_int32), ("reserved", C.c_int32)]
+                ("max_prefill_tokens", C.c_int32), ("kv_page_size", C.c_int32), ("kv_pages", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class Weights(C.Structure):
@@ -145,13 +146,15 @@ class RLError(RuntimeError):
         self.status = status
 
 
-def make_config(shape: ModelShape, max_seqs: int, max_ctx: int, max_prefill_tokens: int) -> ModelConfig:
+def make_config(shape: ModelShape, max_seqs: int, max_ctx: int, max_prefill_tokens: int,
+                kv_page_size: int = 0, kv_pages: int = 0) -> ModelConfig:
     c = ModelConfig()
     c.n_layers, c.hidden, c.n_q_heads = shape.n_layers, shape.hidden, shape.n_q_heads
     c.n_kv_heads, c.head_dim, c.ffn, c.vocab = shape.n_kv_heads, shape.head_dim, shape.ffn, shape.vocab
     c.dtype = RL_DTYPE_BF16 if shape.dtype == "bf16" else RL_DTYPE_FP32
     c.rms_eps, c.rope_theta = float(shape.rms_eps), float(shape.rope_theta)
-    c.max_seqs, c.max_ctx, c.max_prefill_tokens, c.reserved = max_seqs, max_ctx, max_prefill_tokens, 0
+    c.max_seqs, c.max_ctx, c.max_prefill_tokens = max_seqs, max_ctx, max_prefill_tokens
+    c.kv_page_size, c.kv_pages, c.reserved = kv_page_size, kv_pages, 0
     return c
 
 
@@ -180,10 +183,11 @@ class Engine:
     allocated here with torch, and the current torch stream."""
 
     def __init__(self, shape: ModelShape, weights: Dict[str, torch.Tensor], max_seqs: int,
-                 max_ctx: int, max_prefill_tokens: int, device="cuda", stream=None):
+                 max_ctx: int, max_prefill_tokens: int, device="cuda", stream=None,
+                 kv_page_size: int = 0, kv_pages: int = 0):
         L = lib()
         self.shape = shape
-        self.cfg = make_config(shape, max_seqs, max_ctx, max_prefill_tokens)
+        self.cfg = make_config(shape, max_seqs, max_ctx, max_prefill_tokens, kv_page_size, kv_pages)
         self.kv_nbytes = kv_bytes(self.cfg)
         self.ws_nbytes = workspace_bytes(self.cfg)
         if self.kv_nbytes == 0 or self.ws_nbytes == 0:
@@ -332,8 +336,10 @@ class Engine:
 
     # -- KV pool views (layout of include/rl_decode.h) --------------------
     def kv_views(self):
-        """(K, V) torch views of the pool: K [L][S][Hkv][cap][d],
+        """(K, V) torch views of a contiguous pool: K [L][S][Hkv][cap][d],
         V [L][S][Hkv][cap/8][d][8] (8-position blocks), model dtype."""
+        if self.cfg.kv_page_size:
+            raise ValueError("a paged pool has no per-slot views")
         s = self.shape
         cap = (self.cfg.max_ctx + 31) // 32 * 32
         dt = torch.float32 if s.dtype == "fp32" else torch.bfloat16
