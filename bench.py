@@ -78,6 +78,9 @@ def parse():
                          "curve: decode steps at fixed batch sizes (--rows) and context (--ctx), per-class times")
     ap.add_argument("--no-tune", action="store_true",
                     help="keep the cost-model GEMM plans (skip the measured plans taken before warm-up)")
+    ap.add_argument("--kv-page-size", type=int, default=0,
+                    help="rollout stage: paged K/V pool with pages of this many positions (0: one contiguous "
+                         "block per slot); the pool holds exactly the pages the rollout's sequences reach")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -851,8 +854,14 @@ def main():
     resp = plan["response_lens"]
     weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     max_ctx = int(plens.max() + resp.max())
+    page = args.kv_page_size
+    # a finished sequence keeps its pages until the next prefill, so the pool
+    # needs the pages of every sequence's final length
+    final_len = np.repeat(plens, G) + resp
+    kv_pages = int(((final_len + page - 1) // page).sum()) if page else 0
     eng = Engine(shape, weights, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=int(plens.sum()),
-                 device=dev)
+                 device=dev, kv_page_size=page, kv_pages=kv_pages)
+    kv_pool = {"page": page or None, "pages": kv_pages or n_seq, "bytes": eng.kv_nbytes}
     stream = eng.stream
 
     # the rollout driver orders slots by response length (longest first), so
@@ -999,6 +1008,7 @@ def main():
         "measured_peaks": peaks,
         "timed_classes": classes,
         "gemm_plans": tuning,
+        "kv_pool": kv_pool,
     }
     eng.close()
     del eng, ro

@@ -76,7 +76,7 @@ typedef struct rl_model_config {
     int32_t max_seqs;
     int32_t max_ctx;
     int32_t max_prefill_tokens;
-    int32_t kv_page_size;         /* 0: contiguous slots; else positions per K/V page (a power of two in [32, 65536]) */
+    int32_t kv_page_size;         /* 0: contiguous slots; else positions per K/V page (a multiple of 32 in [32, 65536]) */
     int32_t kv_pages;             /* pages in the pool (0: max_seqs * ceil(max_ctx / kv_page_size)); 0 without pages */
     int32_t reserved;             /* must be 0 */
 } rl_model_config;
@@ -133,9 +133,12 @@ typedef struct rl_decode_ctx rl_decode_ctx;
  * Position t of a slot holds the token at position t of that sequence.
  *
  * Paged pool (kv_page_size = P > 0, NP = kv_pages or max_seqs * ceil(max_ctx / P)):
- *     K[l][s][h][t][i]  at element  (((l*NP + pg)*Hkv + h)*P + t%P)*d + i
- *     V[l][s][h][t][i]  at element  ((((l*NP + pg)*Hkv + h)*(P/8) + (t%P)/8)*d + i)*8 + t%8
- * with pg the page that holds positions [P*(t/P), P*(t/P + 1)) of slot s.  A
+ *     K[l][s][h][t][i]  at element  ((l*NP + pg)*Hkv + h)*B + (t%P)*d + i
+ *     V[l][s][h][t][i]  at element  ((l*NP + pg)*Hkv + h)*B + (((t%P)/8)*d + i)*8 + t%8
+ * with pg the page that holds positions [P*(t/P), P*(t/P + 1)) of slot s and
+ * B * E = P*d*E bytes rounded up to an odd multiple of 256 (so that blocks
+ * are never a power of two apart; K and V slabs are 2*L*NP*Hkv*B*E bytes
+ * together).  A
  * slot is given pages as its length grows (prefill, decode steps, scoring,
  * set lengths, onload) and gives them back when released or shortened, so a
  * pool of fewer pages than max_seqs * max_ctx positions serves sequences of

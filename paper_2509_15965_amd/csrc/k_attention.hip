@@ -195,18 +195,33 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(const AttnItem* __res
     }
 
     // K / V block of the step at position t0 (element pointers) and t0's
-    // position inside it
-    const size_t base = PAGED ? 0 : kv_block(kp, layer, Hkv, it.slot, kvh, D);
+    // position inside it.  A paged item reads the table entry of its first
+    // page here, right after the q loads, and each later entry one page
+    // ahead (steps ascend 32 positions at a time, so they enter pages in
+    // order).
+    size_t base = 0;
+    int base_page = 0, next_pid = 0;
+    if (!PAGED) {
+        base = kv_block(kp, layer, Hkv, it.slot, kvh);
+    } else {
+        base_page = it.kv_lo / kp.page;
+        if (base_page < kp.maxp) base = kv_block(kp, layer, Hkv, kv_clamp(kp, kv_table(kp, it.slot, base_page)), kvh);
+        if (base_page + 1 < kp.maxp) next_pid = kv_table(kp, it.slot, base_page + 1);
+    }
     auto block_of = [&](int t0, const uint16_t** kbp, const uint16_t** vbp) {
-        if (!PAGED) {
-            *kbp = kc + base;
-            *vbp = vc + base;
-            return t0;
+        int lt = t0;
+        if (PAGED) {
+            const int j = t0 / kp.page;
+            if (j != base_page) {
+                const int pid = j == base_page + 1 ? next_pid : kv_table(kp, it.slot, j);
+                base = kv_block(kp, layer, Hkv, kv_clamp(kp, pid), kvh);
+                base_page = j;
+                next_pid = j + 1 < kp.maxp ? kv_table(kp, it.slot, j + 1) : 0;
+            }
+            lt = t0 - j * kp.page;
         }
-        int lt;
-        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, it.slot, t0, &lt), kvh, D);
-        *kbp = kc + b;
-        *vbp = vc + b;
+        *kbp = kc + base;
+        *vbp = vc + base;
         return lt;
     };
 
@@ -357,7 +372,7 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) attn_prefill_kernel(const 
     // the K/V of the step at position t0: its page's blocks and t0 inside the page
     auto dma_step = [&](int t0, int buf) {
         int lt;
-        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, tl.slot, t0, &lt), kvh, D);
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, tl.slot, t0, &lt), kvh);
         step_dma<D, kPrefillWaves>(kc + b, vc + b, lt, wave, lane, lds[buf][0], lds[buf][1]);
     };
 
@@ -501,12 +516,12 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const int32_t* __restrict_
     // K row and V block start of position t (its page's block, t inside it)
     auto krow_of = [&](int t) {
         int lt;
-        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh, D);
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh);
         return kc + b + static_cast<size_t>(lt) * D;
     };
     auto vblk_of = [&](int t) {
         int lt;
-        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh, D);
+        const size_t b = kv_block(kp, layer, Hkv, kv_page(kp, slot, t, &lt), kvh);
         return vc + b + static_cast<size_t>(lt >> 3) * D * 8 + (lt & 7);
     };
     const float scale = 1.0f / sqrtf(static_cast<float>(D));

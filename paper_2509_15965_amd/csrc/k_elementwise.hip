@@ -365,7 +365,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
             const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
             int lp;
             const int pid = kv_page(kp, slot, pos, &lp);
-            T* kr = kc + kv_block(kp, layer, Hkv, pid, h - Hq, D) + static_cast<size_t>(lp) * D;
+            T* kr = kc + kv_block(kp, layer, Hkv, pid, h - Hq) + static_cast<size_t>(lp) * D;
             Elem<T>::store(kr, i, x0);
             Elem<T>::store(kr, i + half, x1);
         }
@@ -377,7 +377,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const float* __restric
         const int slot = d0 < 0 ? -(d0 + 1) : dst_slots[d0 + g];
         int lp;
         const int pid = kv_page(kp, slot, pos, &lp);
-        T* vb = vc + kv_block(kp, layer, Hkv, pid, h - Hq - Hkv, D);
+        T* vb = vc + kv_block(kp, layer, Hkv, pid, h - Hq - Hkv);
         Elem<T>::store(vb, (static_cast<size_t>(lp >> 3) * D + i) * 8 + (lp & 7), a);
         Elem<T>::store(vb, (static_cast<size_t>(lp >> 3) * D + i + half) * 8 + (lp & 7), b);
     }
@@ -411,7 +411,7 @@ hipError_t launch_rope_append(int dt, const float* qkv, int splits, int n_rows, 
 // of slot i at byte base[i]: for l, h: K rows then V blocks.
 __global__ void __launch_bounds__(256) kv_pack_kernel(int dir, const int32_t* __restrict__ slots,
         const int32_t* __restrict__ lens, const int64_t* __restrict__ base, KvPages kp, int Hkv,
-        int rowbytes, uint8_t* __restrict__ kslab, uint8_t* __restrict__ vslab, uint8_t* __restrict__ stage) {
+        int rowbytes, int es, uint8_t* __restrict__ kslab, uint8_t* __restrict__ vslab, uint8_t* __restrict__ stage) {
     const int i = blockIdx.x, lh = blockIdx.y, kv = blockIdx.z;
     const int l = lh / Hkv, h = lh - l * Hkv;
     const int len = lens[i], len8 = (len + 7) / 8 * 8;
@@ -425,7 +425,7 @@ __global__ void __launch_bounds__(256) kv_pack_kernel(int dir, const int32_t* __
     for (int p0 = 0; p0 < rows; p0 += kp.page) {
         int lp;
         const int pid = kv_page(kp, slots[i], p0, &lp);
-        const size_t pool_off = (kv_block(kp, l, Hkv, pid, h, 1) + lp) * rowbytes;
+        const size_t pool_off = kv_block(kp, l, Hkv, pid, h) * es + static_cast<size_t>(lp) * rowbytes;
         u32x4* pool = reinterpret_cast<u32x4*>((kv ? vslab : kslab) + pool_off);
         const int n_rows = min(kp.page, rows - p0);
         const size_t n16 = static_cast<size_t>(n_rows) * per_row;
@@ -438,11 +438,11 @@ __global__ void __launch_bounds__(256) kv_pack_kernel(int dir, const int32_t* __
 }
 
 hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
-                          const KvPages& kp, int Hkv, int rowbytes, void* kslab, void* vslab, void* stage,
-                          hipStream_t s) {
+                          const KvPages& kp, int Hkv, int rowbytes, int es, void* kslab, void* vslab,
+                          void* stage, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(kv_pack_kernel, dim3(n, L * Hkv, 2), dim3(256), 0, s, dir, slots, lens, base, kp, Hkv,
-                       rowbytes, static_cast<uint8_t*>(kslab), static_cast<uint8_t*>(vslab),
+                       rowbytes, es, static_cast<uint8_t*>(kslab), static_cast<uint8_t*>(vslab),
                        static_cast<uint8_t*>(stage));
     return hipGetLastError();
 }

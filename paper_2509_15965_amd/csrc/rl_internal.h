@@ -11,36 +11,44 @@ namespace rl {
 // Element encodings of the model dtype.
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
-// Where the K/V of (slot, position) lives.  The K slab is [L][pages][Hkv][page][d]
-// and the V slab [L][pages][Hkv][page/8][d][8].  table == nullptr: slot s is
-// page s and holds all `page` (= the slot capacity) positions.  Otherwise
-// position p of slot s is in page table[s * maxp + p / page] at p % page
-// (page a multiple of 32, so a 32-position step never straddles pages).
+// Where the K/V of (slot, position) lives.  The K slab is blocks of
+// [page][d] and the V slab blocks of [page/8][d][8], one per (layer, page,
+// kv-head) in that order, `stride` elements apart (>= page * d).
+// table == nullptr: slot s is page s and holds all `page` (= the slot
+// capacity) positions.  Otherwise position p of slot s is in page
+// table[s * maxp + p / page] at p % page (page a multiple of 32, so a
+// 32-position step never straddles pages).
 struct KvPages {
     const int32_t* table;
     int maxp;
     int page;
     int pages;
+    size_t stride;
 };
 
 // Page of (slot, pos) and the position inside it; an id outside the pool is
 // clamped into it (the host never stores one; this only keeps every address
 // inside the slab).
+__device__ __forceinline__ int kv_clamp(const KvPages& kp, int pid) {
+    return pid < 0 ? 0 : pid >= kp.pages ? kp.pages - 1 : pid;
+}
+// Table entry j (< maxp) of a slot, as stored.
+__device__ __forceinline__ int kv_table(const KvPages& kp, int slot, int j) {
+    return kp.table[static_cast<size_t>(slot) * kp.maxp + j];
+}
 __device__ __forceinline__ int kv_page(const KvPages& kp, int slot, int pos, int* local) {
     if (!kp.table) {
         *local = pos;
         return slot;
     }
     const int j = pos / kp.page;
-    int pid = kp.table[static_cast<size_t>(slot) * kp.maxp + j];
-    pid = pid < 0 ? 0 : pid >= kp.pages ? kp.pages - 1 : pid;
     *local = pos - j * kp.page;
-    return pid;
+    return kv_clamp(kp, kv_table(kp, slot, j));
 }
 
-// Element offset of the K (or V) block of (layer, page, kv-head): page * d elements.
-__device__ __forceinline__ size_t kv_block(const KvPages& kp, int layer, int Hkv, int pid, int head, int D) {
-    return ((static_cast<size_t>(layer) * kp.pages + pid) * Hkv + head) * static_cast<size_t>(kp.page) * D;
+// Element offset of the K (or V) block of (layer, page, kv-head).
+__device__ __forceinline__ size_t kv_block(const KvPages& kp, int layer, int Hkv, int pid, int head) {
+    return ((static_cast<size_t>(layer) * kp.pages + pid) * Hkv + head) * kp.stride;
 }
 
 // GEMM epilogues: Y = X . W^T followed by
@@ -225,10 +233,10 @@ hipError_t launch_sample(const float* logits, int ld, int n, int V, const int32_
 // starts at byte base[i] of the stage: for layer l, kv-head h (index
 // l*Hkv + h): lens[i] K rows of rowbytes, then ceil8(lens[i]) / 8 V blocks of
 // 8 * rowbytes (the pool's own layouts, page after page).  rowbytes =
-// head_dim * element size.
+// head_dim * es, es = element size.
 hipError_t launch_kv_pack(int dir, const int32_t* slots, const int32_t* lens, const int64_t* base, int n, int L,
-                          const KvPages& kp, int Hkv, int rowbytes, void* kslab, void* vslab, void* stage,
-                          hipStream_t s);
+                          const KvPages& kp, int Hkv, int rowbytes, int es, void* kslab, void* vslab,
+                          void* stage, hipStream_t s);
 
 hipError_t launch_copy16(void* dst, const void* src, size_t n16, hipStream_t s);
 // read-only stream of n16 16-byte words by n_blocks workgroups; out[b] = XOR of workgroup b's words

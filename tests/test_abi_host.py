@@ -46,11 +46,14 @@ def test_paged_kv_bytes_follow_documented_layout():
     for name in WORKLOADS:
         m = WORKLOADS[name].model
         es = 4 if m.dtype == "fp32" else 2
+        # a (layer, page, kv-head) block: 32 rows rounded up to an odd number of 256 bytes
+        n = -(-32 * m.head_dim * es // 256)
+        block = (n + 1 - n % 2) * 256
         # 3 slots of 50 positions in pages of 32: 2 pages each by default, or a pool of 4 pages
         c = R.make_config(m, 3, 50, 64, kv_page_size=32)
-        assert R.kv_bytes(c) == 2 * m.n_layers * 6 * m.n_kv_heads * 32 * m.head_dim * es
+        assert R.kv_bytes(c) == 2 * m.n_layers * 6 * m.n_kv_heads * block
         c = R.make_config(m, 3, 50, 64, kv_page_size=32, kv_pages=4)
-        assert R.kv_bytes(c) == 2 * m.n_layers * 4 * m.n_kv_heads * 32 * m.head_dim * es
+        assert R.kv_bytes(c) == 2 * m.n_layers * 4 * m.n_kv_heads * block
         # the page table travels with every call's metadata: the workspace grows with it
         assert R.workspace_bytes(c) >= R.workspace_bytes(cfg_for(name, 3, 50, 64))
 
@@ -72,7 +75,7 @@ def test_workspace_grows_with_capacity():
     ("rope_theta", 1.0, R.RL_ERR_INVALID_ARG),
     ("reserved", 1, R.RL_ERR_INVALID_ARG),
     ("max_seqs", 0, R.RL_ERR_INVALID_ARG),
-    ("kv_page_size", 48, R.RL_ERR_INVALID_ARG),      # not a power of two
+    ("kv_page_size", 48, R.RL_ERR_INVALID_ARG),      # not a multiple of 32
     ("kv_page_size", 16, R.RL_ERR_INVALID_ARG),      # below 32
     ("kv_pages", 5, R.RL_ERR_INVALID_ARG),           # pages without a page size
     ("kv_pages", -1, R.RL_ERR_INVALID_ARG),

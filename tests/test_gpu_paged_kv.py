@@ -75,7 +75,7 @@ def _assert_same(a, b):
             assert np.array_equal(u, v), k
 
 
-@pytest.mark.parametrize("page,group", [(32, 1), (32, 4), (64, 4), (128, 1)])
+@pytest.mark.parametrize("page,group", [(32, 1), (32, 4), (64, 4), (96, 4), (128, 1)])
 def test_paged_decode_equals_contiguous(page, group):
     """Prompts of 37-90 tokens, 40 decode steps (every sequence crosses at
     least one page boundary while decoding), shared prompts with group 4."""
