@@ -393,8 +393,11 @@ typedef enum rl_option {
                                 planner (default); else
                                   bits 0-7:   rl_gemm_kernel of all columns
                                               (or of the first half, below),
-                                  bits 8-15:  split-K count (0 or 1 = none,
-                                              else a power of two <= 32),
+                                  bits 8-15:  split-K count s (0 or 1 = none,
+                                              else <= 32; the K slices are
+                                              whole 64-wide blocks, so the
+                                              count used is K over
+                                              ceil(K/s) rounded up to 64),
                                   bits 16-23: rl_gemm_kernel of the second
                                               half of the output columns
                                               (0 = one segment; no split-K).

@@ -2047,7 +2047,7 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
             const int64_t k1 = value & 0xff, sp = (value >> 8) & 0xff, k2 = (value >> 16) & 0xff;
             const bool ok = value == 0 ||
                             (value >= 0 && (value >> 24) == 0 && k1 >= RL_GEMM_DIRECT && k1 <= RL_GEMM_T128_DEEP &&
-                             (sp == 0 || (sp <= 32 && (sp & (sp - 1)) == 0)) &&
+                             sp <= kMaxSplits &&
                              (k2 == 0 || (k2 >= RL_GEMM_T128X256 && k2 <= RL_GEMM_T128_DEEP)));
             if (!ok) return fail(ctx, RL_ERR_INVALID_ARG, "invalid GEMM plan override");
             ctx->opt_gemm = value;

@@ -283,7 +283,7 @@ bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPl
         const int bn = v == kLineVariant128x128 || v == kLineVariant128x128Deep ? 128 : 256;
         return epi == EPI_SWIGLU ? bn / 2 : bn;
     };
-    if (s != 0 && (s & (s - 1)) != 0) return false;
+    if (s > kMaxSplits) return false;
     GemmPlan p{};
     if (k1 == RL_GEMM_DIRECT) {
         if (M > 64 || k2 != 0) return false;

@@ -362,7 +362,7 @@ def test_step_rejects_bad_arguments_without_side_effects():
                                                RL_OPT_SHARED_PREFIX)
     for opt, bad in [(RL_OPT_ATTN_CHUNK, 16), (RL_OPT_ATTN_CHUNK, 33), (RL_OPT_ATTN_CHUNK, 65568),
                      (RL_OPT_ATTN_CHUNK, -32), (RL_OPT_SHARED_PREFIX, 2), (RL_OPT_PREFILL_ATTENTION, -1),
-                     (RL_OPT_GEMM_PLAN, 7), (RL_OPT_GEMM_PLAN, 5 | (3 << 8)), (RL_OPT_GEMM_PLAN, 5 | (2 << 16)),
+                     (RL_OPT_GEMM_PLAN, 7), (RL_OPT_GEMM_PLAN, 5 | (33 << 8)), (RL_OPT_GEMM_PLAN, 5 | (2 << 16)),
                      (99, 0)]:
         with pytest.raises(RLError) as e:
             eng.set_option(opt, bad)
@@ -393,6 +393,8 @@ _FORCED_PLANS = [
     ("direct_s4", gemm_plan_code(RL_GEMM_DIRECT, 4)),
     ("t256", gemm_plan_code(RL_GEMM_T256)),
     ("t256_s4", gemm_plan_code(RL_GEMM_T256, 4)),
+    ("t256_s3", gemm_plan_code(RL_GEMM_T256, 3)),
+    ("t128x256_s6", gemm_plan_code(RL_GEMM_T128X256, 6)),
     ("t128x256_s2", gemm_plan_code(RL_GEMM_T128X256, 2)),
     ("t128", gemm_plan_code(RL_GEMM_T128)),
     ("t128deep_s8", gemm_plan_code(RL_GEMM_T128_DEEP, 8)),
