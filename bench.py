@@ -80,7 +80,8 @@ def parse():
                     help="keep the cost-model GEMM plans (skip the measured plans taken before warm-up)")
     ap.add_argument("--kv-page-size", type=int, default=0,
                     help="rollout stage: paged K/V pool with pages of this many positions (0: one contiguous "
-                         "block per slot); the pool holds exactly the pages the rollout's sequences reach")
+                         "block per slot); the pool holds exactly the pages the rollout's sequences reach, "
+                         "each group's full prompt pages once")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -856,9 +857,11 @@ def main():
     max_ctx = int(plens.max() + resp.max())
     page = args.kv_page_size
     # a finished sequence keeps its pages until the next prefill, so the pool
-    # needs the pages of every sequence's final length
+    # needs the pages of every sequence's final length; a group holds the
+    # pages its prompt fills once
     final_len = np.repeat(plens, G) + resp
-    kv_pages = int(((final_len + page - 1) // page).sum()) if page else 0
+    shared = np.repeat(plens // page, G) if page else 0
+    kv_pages = int((plens // page).sum() + ((final_len + page - 1) // page - shared).sum()) if page else 0
     eng = Engine(shape, weights, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=int(plens.sum()),
                  device=dev, kv_page_size=page, kv_pages=kv_pages)
     kv_pool = {"page": page or None, "pages": kv_pages or n_seq, "bytes": eng.kv_nbytes}

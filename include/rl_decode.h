@@ -143,8 +143,14 @@ typedef struct rl_decode_ctx rl_decode_ctx;
  * set lengths, onload) and gives them back when released or shortened, so a
  * pool of fewer pages than max_seqs * max_ctx positions serves sequences of
  * uneven lengths; a call that would need more pages than are free fails with
- * RL_ERR_CAPACITY and changes nothing.  The page table travels with each
- * call's metadata (4 * max_seqs * ceil(max_ctx / P) bytes).
+ * RL_ERR_CAPACITY and changes nothing.  The slots of a GRPO group (prefill
+ * or scoring with group > 1) share the pages their prompt fills completely:
+ * those K/V rows are written once and held by every slot of the group until
+ * the last one lets them go; the rest of the prompt and each response are
+ * in pages of the slot's own.  A slot whose length is set to end inside a
+ * shared page first gets its own copy of that page (rl_set_slot_lengths).
+ * The page table travels with each call's metadata
+ * (4 * max_seqs * ceil(max_ctx / P) bytes).
  * Returns 0 when cfg is invalid or unsupported.
  * ------------------------------------------------------------------- */
 size_t rl_decode_kv_bytes(const rl_model_config* cfg);
@@ -318,12 +324,20 @@ rl_status rl_sample_logits_noalloc(int32_t n, int32_t vocab, const float* logits
 rl_status rl_release_slots(rl_decode_ctx* ctx, int32_t n, const int32_t* slots);
 
 /* Declare lengths of slots whose K/V the caller wrote into the pool itself
- * (layout above).  lengths[i] in [0, max_ctx]. */
+ * (layout above), or cut sequences short.  lengths[i] in [0, max_ctx].  On a
+ * paged pool a length that ends inside a page shared with other slots
+ * enqueues a copy of that page on the context's stream. */
 rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slots,
                               const int32_t* lengths);
 
 /* Length of a slot, or -1 for an invalid context or slot. */
 int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot);
+
+/* Free pages of a paged K/V pool (admission control: a prompt group of
+ * length p and group g needs floor(p/P) shared pages plus, per slot, the
+ * pages of the rest of its length); -1 for a contiguous pool or an invalid
+ * context. */
+int64_t rl_kv_free_pages(const rl_decode_ctx* ctx);
 
 /* ---------------------------------------------------------------------
  * Context switching (Sec. 3: in temporal mode a worker's GPU state is

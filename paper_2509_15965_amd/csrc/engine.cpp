@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 using namespace rl;
@@ -177,8 +178,10 @@ struct rl_decode_ctx {
     std::string err;
 
     // K/V pages (kv_page_size > 0): per slot its pages in position order
-    // (ptab[s * maxp + j], -1 = none; npages[s] of them), and the free pages
-    std::vector<int32_t> ptab, npages, free_pages;
+    // (ptab[s * maxp + j], -1 = none; npages[s] of them), the free pages,
+    // and per page the number of slots holding it (0 = free; the slots of a
+    // GRPO group share the pages their prompt fills)
+    std::vector<int32_t> ptab, npages, free_pages, pref;
 
     template <typename T> T* wsp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
     uint8_t* kslab() const { return kv; }
@@ -299,40 +302,144 @@ std::vector<std::pair<int, int>> final_lengths(int n, const int32_t* slots, cons
     return v;
 }
 
-// Whether the slots can hold these lengths with the free pages (pages a slot
-// gives back count).  Always true for a contiguous pool.
-bool pages_fit(const rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want) {
-    if (!c->paged()) return true;
-    int64_t need = 0, back = 0;
-    for (const auto& e : want) {
-        const int d = pages_for(c, e.second) - c->npages[e.first];
-        if (d > 0) need += d; else back -= d;
-    }
-    return need <= static_cast<int64_t>(c->free_pages.size()) + back;
+// Pages freed by dropping, for each (slot, k), the slot's pages from index k
+// on: those whose every holder is dropped.
+int64_t pages_freed(const rl_decode_ctx* c, const std::vector<std::pair<int, int>>& drop) {
+    const size_t mp = static_cast<size_t>(c->lay.maxp);
+    std::unordered_map<int32_t, int> refs;
+    for (const auto& d : drop)
+        for (int j = d.second; j < c->npages[d.first]; ++j) ++refs[c->ptab[d.first * mp + j]];
+    int64_t n = 0;
+    for (const auto& e : refs) n += c->pref[e.first] == e.second;
+    return n;
 }
 
-// Give every slot exactly the pages its length needs (pages_fit held).
-void set_pages(rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want) {
-    if (!c->paged()) return;
+// Slot s keeps its first `keep` pages; a page nobody holds any more is free.
+void drop_pages(rl_decode_ctx* c, int s, int keep, bool* freed) {
     const size_t mp = static_cast<size_t>(c->lay.maxp);
-    bool freed = false;
-    for (const auto& e : want) {   // shrink first: the pages given back serve the others
-        const int s = e.first, keep = pages_for(c, e.second);
-        while (c->npages[s] > keep) {
-            int32_t& pg = c->ptab[s * mp + --c->npages[s]];
+    while (c->npages[s] > keep) {
+        int32_t& pg = c->ptab[s * mp + --c->npages[s]];
+        if (--c->pref[pg] == 0) {
             c->free_pages.push_back(pg);
-            pg = -1;
-            freed = true;
+            *freed = true;
         }
+        pg = -1;
     }
-    // lowest page first: a slab that has been filled and emptied again hands
-    // out neighbouring pages to the positions of one sequence, as a fresh one does
-    if (freed) std::sort(c->free_pages.begin(), c->free_pages.end(), std::greater<int32_t>());
+}
+
+// lowest page first: a slab that has been filled and emptied again hands out
+// neighbouring pages to the positions of one sequence, as a fresh one does
+void sort_free(rl_decode_ctx* c) {
+    std::sort(c->free_pages.begin(), c->free_pages.end(), std::greater<int32_t>());
+}
+
+int32_t take_page(rl_decode_ctx* c, int holders) {
+    const int32_t pg = c->free_pages.back();
+    c->free_pages.pop_back();
+    c->pref[pg] = holders;
+    return pg;
+}
+
+// Whether the slots can hold these lengths with the free pages (pages given
+// back count).  fresh: the slots' pages are replaced from position 0 (their
+// K/V is rewritten); otherwise each keeps the pages up to its new length.
+// Always true for a contiguous pool.
+bool pages_fit(const rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want, bool fresh = false,
+               int64_t extra = 0) {
+    if (!c->paged()) return true;
+    int64_t need = extra;
+    std::vector<std::pair<int, int>> drop;
+    for (const auto& e : want) {
+        const int keep = fresh ? 0 : std::min(pages_for(c, e.second), c->npages[e.first]);
+        drop.emplace_back(e.first, keep);
+        need += pages_for(c, e.second) - keep;
+    }
+    return need <= static_cast<int64_t>(c->free_pages.size()) + pages_freed(c, drop);
+}
+
+// Give every slot exactly the pages its length needs (pages_fit held); new
+// pages are the slot's own.
+void set_pages(rl_decode_ctx* c, const std::vector<std::pair<int, int>>& want, bool fresh = false) {
+    if (!c->paged()) return;
+    bool freed = false;
+    for (const auto& e : want) drop_pages(c, e.first, fresh ? 0 : pages_for(c, e.second), &freed);
+    if (freed) sort_free(c);
+    const size_t mp = static_cast<size_t>(c->lay.maxp);
     for (const auto& e : want) {
         const int s = e.first, need = pages_for(c, e.second);
-        while (c->npages[s] < need) {
-            c->ptab[s * mp + c->npages[s]++] = c->free_pages.back();
-            c->free_pages.pop_back();
+        while (c->npages[s] < need) c->ptab[s * mp + c->npages[s]++] = take_page(c, 1);
+    }
+}
+
+// Index of the page holding position len of slot s when len ends inside a
+// page that other slots also hold, else -1.
+int shared_tail_page(const rl_decode_ctx* c, int s, int len) {
+    if (!c->paged() || len % c->lay.page == 0) return -1;
+    const int j = len / c->lay.page;
+    if (j >= c->npages[s]) return -1;
+    return c->pref[c->ptab[s * static_cast<size_t>(c->lay.maxp) + j]] > 1 ? j : -1;
+}
+
+// Copy page `from` into page `to`: every layer's and kv-head's K and V block.
+hipError_t copy_page(rl_decode_ctx* c, int32_t from, int32_t to) {
+    const Layout& L = c->lay;
+    const size_t pitch = L.block * L.es;
+    const size_t rows = static_cast<size_t>(L.page) * c->cfg.head_dim * L.es;
+    const size_t Hkv = static_cast<size_t>(c->cfg.n_kv_heads);
+    for (int v = 0; v < 2; ++v) {
+        uint8_t* slab = v ? c->vslab() : c->kslab();
+        for (int l = 0; l < c->cfg.n_layers; ++l) {
+            const uint8_t* src = slab + (static_cast<size_t>(l) * L.pages + from) * Hkv * pitch;
+            uint8_t* dst = slab + (static_cast<size_t>(l) * L.pages + to) * Hkv * pitch;
+            const hipError_t e = hipMemcpy2DAsync(dst, pitch, src, pitch, rows, Hkv, hipMemcpyDeviceToDevice,
+                                                  c->stream);
+            if (e != hipSuccess) return e;
+        }
+    }
+    return hipSuccess;
+}
+
+// Pages of a group's prompt that the group shares: the ones it fills (0 for
+// a contiguous pool).  Prefill and scoring write those K/V rows once.
+int shared_prompt_pages(const rl_decode_ctx* c, int plen) { return c->paged() ? plen / c->lay.page : 0; }
+
+// Pages for a call that writes each slot's K/V from position 0: slot
+// slots[g * group + k] holds prompt g (plen[g] positions, its full pages
+// shared by the group) and then its own positions up to lens[g * group + k].
+bool group_pages_fit(const rl_decode_ctx* c, int n_prompts, int group, const int32_t* slots,
+                     const std::vector<int>& plen, const std::vector<int32_t>& lens) {
+    if (!c->paged()) return true;
+    int64_t need = 0;
+    std::vector<std::pair<int, int>> drop;
+    for (int g = 0; g < n_prompts; ++g) {
+        const int sh = shared_prompt_pages(c, plen[g]);
+        need += sh;
+        for (int k = 0; k < group; ++k) {
+            const int i = g * group + k;
+            drop.emplace_back(slots[i], 0);
+            need += pages_for(c, lens[i]) - sh;
+        }
+    }
+    return need <= static_cast<int64_t>(c->free_pages.size()) + pages_freed(c, drop);
+}
+
+void set_group_pages(rl_decode_ctx* c, int n_prompts, int group, const int32_t* slots,
+                     const std::vector<int>& plen, const std::vector<int32_t>& lens) {
+    if (!c->paged()) return;
+    bool freed = false;
+    for (int i = 0; i < n_prompts * group; ++i) drop_pages(c, slots[i], 0, &freed);
+    if (freed) sort_free(c);
+    const size_t mp = static_cast<size_t>(c->lay.maxp);
+    for (int g = 0; g < n_prompts; ++g) {
+        const int sh = shared_prompt_pages(c, plen[g]);
+        for (int j = 0; j < sh; ++j) {
+            const int32_t pg = take_page(c, group);
+            for (int k = 0; k < group; ++k) c->ptab[slots[g * group + k] * mp + j] = pg;
+        }
+        for (int k = 0; k < group; ++k) {
+            const int i = g * group + k, s = slots[i];
+            c->npages[s] = sh;
+            while (c->npages[s] < pages_for(c, lens[i])) c->ptab[s * mp + c->npages[s]++] = take_page(c, 1);
         }
     }
 }
@@ -1372,6 +1479,7 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
         c->npages.assign(static_cast<size_t>(cfg->max_seqs), 0);
         c->free_pages.resize(static_cast<size_t>(L.pages));
         for (int i = 0; i < L.pages; ++i) c->free_pages[i] = L.pages - 1 - i;   // handed out from page 0 up
+        c->pref.assign(static_cast<size_t>(L.pages), 0);
     }
     auto cleanup = [&](rl_status s) {
         for (int i = 0; i < kStages; ++i) {
@@ -1442,10 +1550,12 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     }
     if (total > cf.max_prefill_tokens) return fail(c, RL_ERR_CAPACITY, "prompts exceed max_prefill_tokens");
     const int R = static_cast<int>(total);
+    std::vector<int> plens(static_cast<size_t>(n_prompts));
+    for (int p = 0; p < n_prompts; ++p) plens[p] = prompt_offsets[p + 1] - prompt_offsets[p];
     std::vector<int32_t> new_len(static_cast<size_t>(n_out));
-    for (int o = 0; o < n_out; ++o) new_len[o] = prompt_offsets[o / group + 1] - prompt_offsets[o / group];
-    const auto want = final_lengths(n_out, slots, new_len.data());
-    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
+    for (int o = 0; o < n_out; ++o) new_len[o] = plens[o / group];
+    if (!group_pages_fit(c, n_prompts, group, slots, plens, new_len))
+        return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
 
     Meta m{};
@@ -1470,9 +1580,11 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     double kvpos = 0;
     for (int p = 0; p < n_prompts; ++p) {
         const int b = prompt_offsets[p], len = prompt_offsets[p + 1] - b;
+        // rows in the group's shared pages are written once, through its first slot
+        const int shared_rows = shared_prompt_pages(c, len) * c->lay.page;
         for (int t = 0; t < len; ++t) {
             row_pos[b + t] = t;
-            row_dst[b + t] = p * group;
+            row_dst[b + t] = t < shared_rows ? -(slots[p * group] + 1) : p * group;
             row_slot[b + t] = slots[p * group];
         }
         last[p] = b + len - 1;
@@ -1524,7 +1636,7 @@ rl_status rl_prefill(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const
     f.T = sp->temperature;
     f.out_tok = out_tok;
     f.out_logp = out_logp;
-    set_pages(c, want);
+    set_group_pages(c, n_prompts, group, slots, plens, new_len);
     f.kvp = fill_pages(c, ps);
     st = upload_meta(c, &m, stage);
     if (st != RL_OK) return st;
@@ -1586,12 +1698,12 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     const int R1 = static_cast<int>(r1), R = static_cast<int>(r1 + r2);
     const int n_sel = n_prompts + static_cast<int>(r2) - n_seq;   // LM-head rows
     // each slot holds its group's prompt and its own response while scoring
+    std::vector<int> plens(static_cast<size_t>(n_prompts));
+    for (int p = 0; p < n_prompts; ++p) plens[p] = prompt_offsets[p + 1] - prompt_offsets[p];
     std::vector<int32_t> new_len(static_cast<size_t>(n_seq));
-    for (int sq = 0; sq < n_seq; ++sq)
-        new_len[sq] = prompt_offsets[sq / group + 1] - prompt_offsets[sq / group] + resp_offsets[sq + 1] -
-                      resp_offsets[sq];
-    const auto want = final_lengths(n_seq, slots, new_len.data());
-    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
+    for (int sq = 0; sq < n_seq; ++sq) new_len[sq] = plens[sq / group] + resp_offsets[sq + 1] - resp_offsets[sq];
+    if (!group_pages_fit(c, n_prompts, group, slots, plens, new_len))
+        return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
 
     Meta m{};
@@ -1620,9 +1732,10 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     int ns = 0, ni = 0;
     for (int p = 0; p < n_prompts; ++p) {
         const int b = prompt_offsets[p], len = prompt_offsets[p + 1] - b;
+        const int shared_rows = shared_prompt_pages(c, len) * c->lay.page;
         for (int t = 0; t < len; ++t) {
             row_pos[b + t] = t;
-            row_dst[b + t] = p * group;
+            row_dst[b + t] = t < shared_rows ? -(slots[p * group] + 1) : p * group;
             row_slot[b + t] = slots[p * group];
         }
         for (int k = 0; k < group; ++k) dst[p * group + k] = slots[p * group + k];
@@ -1694,7 +1807,7 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     f.score_items = d_items;
     f.score_idx = d_idx;
     f.score_targets = resp_tokens;
-    set_pages(c, want);
+    set_group_pages(c, n_prompts, group, slots, plens, new_len);
     f.kvp = fill_pages(c, ps);
     st = upload_meta(c, &m, stage);
     if (st != RL_OK) return st;
@@ -1706,9 +1819,11 @@ rl_status rl_score(rl_decode_ctx* ctx, int32_t n_prompts, int32_t group, const i
     if (e != hipSuccess) return hip_fail(c, e, "token copy");
     unshare(c, n_seq, slots);
     st = run_forward(c, f);
-    for (int i = 0; i < n_seq; ++i) c->len[slots[i]] = 0;   // the slots were scratch
     std::vector<std::pair<int, int>> none;
-    for (const auto& e : want) none.emplace_back(e.first, 0);
+    for (int i = 0; i < n_seq; ++i) {   // the slots were scratch
+        c->len[slots[i]] = 0;
+        none.emplace_back(slots[i], 0);
+    }
     set_pages(c, none);   // a later call's K/V writes are ordered after this call's kernels
     return st;
 }
@@ -1970,10 +2085,11 @@ rl_status rl_kv_onload(rl_decode_ctx* ctx, int32_t n, const int32_t* slots, cons
         total += b;
     }
     if (total > host_bytes) return fail(c, RL_ERR_CAPACITY, "host buffer smaller than the packed K/V of these lengths");
+    // the slots' K/V is rewritten from position 0: new pages of their own
     const auto want = final_lengths(n, slots, lengths);
-    if (!pages_fit(c, want)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
+    if (!pages_fit(c, want, true)) return fail(c, RL_ERR_CAPACITY, "not enough free K/V pages");
     DeviceGuard g(c->device);
-    set_pages(c, want);
+    set_pages(c, want, true);
     st = kv_transfer(c, 1, n, slots, lengths, static_cast<uint8_t*>(const_cast<void*>(host_src)));
     if (st != RL_OK) return st;
     for (int i = 0; i < n; ++i) c->len[slots[i]] = lengths[i];
@@ -2023,11 +2139,33 @@ rl_status rl_set_slot_lengths(rl_decode_ctx* ctx, int32_t n, const int32_t* slot
         if (lengths[i] < 0 || lengths[i] > ctx->cfg.max_ctx) return fail(ctx, RL_ERR_INVALID_ARG, "length out of range");
     }
     const auto want = final_lengths(n, slots, lengths);
-    if (!pages_fit(ctx, want)) return fail(ctx, RL_ERR_CAPACITY, "not enough free K/V pages");
+    // A length that ends inside a page the slot shares with others (its
+    // group's prompt) takes a copy of that page: the slot's next K/V row goes
+    // there.  (Counted before the call's pages are given back: conservative.)
+    int64_t copies = 0;
+    for (const auto& e : want) copies += shared_tail_page(ctx, e.first, e.second) >= 0;
+    if (!pages_fit(ctx, want, false, copies)) return fail(ctx, RL_ERR_CAPACITY, "not enough free K/V pages");
     set_pages(ctx, want);
+    const size_t mp = static_cast<size_t>(ctx->lay.maxp);
+    for (const auto& e : want) {
+        const int j = shared_tail_page(ctx, e.first, e.second);
+        if (j < 0) continue;
+        int32_t& pg = ctx->ptab[e.first * mp + j];
+        const int32_t own = take_page(ctx, 1);
+        DeviceGuard g(ctx->device);
+        const hipError_t err = copy_page(ctx, pg, own);
+        --ctx->pref[pg];
+        pg = own;
+        if (err != hipSuccess) return hip_fail(ctx, err, "K/V page copy");
+    }
     for (int i = 0; i < n; ++i) ctx->len[slots[i]] = lengths[i];
     unshare(ctx, n, slots);
     return RL_OK;
+}
+
+int64_t rl_kv_free_pages(const rl_decode_ctx* ctx) {
+    if (!ctx_ok(ctx) || !ctx->paged()) return -1;
+    return static_cast<int64_t>(ctx->free_pages.size());
 }
 
 int32_t rl_slot_length(const rl_decode_ctx* ctx, int32_t slot) {

@@ -31,7 +31,7 @@ KERNEL_CLASSES = ("embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "a
 
 EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create", "rl_decode_destroy",
            "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
-           "rl_set_slot_lengths", "rl_slot_length", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
+           "rl_set_slot_lengths", "rl_slot_length", "rl_kv_free_pages", "rl_kv_offload_bytes", "rl_kv_offload", "rl_kv_onload",
            "rl_decode_rebind", "rl_decode_set_option", "rl_decode_kernel_stats",
            "rl_decode_reset_stats", "rl_decode_attn_plan_stats", "rl_probe_copy", "rl_probe_read", "rl_probe_mfma",
            "rl_probe_gumbel_bound",
@@ -102,6 +102,8 @@ def lib():
     L.rl_set_slot_lengths.argtypes = [vp, i32, vp, vp]
     L.rl_slot_length.restype = i32
     L.rl_slot_length.argtypes = [vp, i32]
+    L.rl_kv_free_pages.restype = C.c_int64
+    L.rl_kv_free_pages.argtypes = [vp]
     L.rl_kv_offload_bytes.restype = sz
     L.rl_kv_offload_bytes.argtypes = [vp, i32, vp]
     L.rl_kv_offload.restype = C.c_int
@@ -276,6 +278,10 @@ class Engine:
 
     def slot_length(self, slot: int) -> int:
         return int(lib().rl_slot_length(self.h, slot))
+
+    def kv_free_pages(self) -> int:
+        """Free pages of a paged K/V pool (-1 for a contiguous pool)."""
+        return int(lib().rl_kv_free_pages(self.h))
 
     def kv_offload_bytes(self, slots: Sequence[int]) -> int:
         s = _host_i32(slots)

@@ -226,3 +226,62 @@ def test_paged_pool_exhaustion_is_refused_without_side_effects():
     assert eng.slot_length(0) == 97
     torch.cuda.synchronize()
     eng.close()
+
+
+def test_group_prompt_pages_are_shared_and_counted():
+    """A group's full prompt pages are held once for all its slots; each slot's
+    partial last prompt page is its own.  Releasing slots gives back exactly the
+    pages no other slot holds."""
+    w_dev, _, _ = build_models(GQA, 77)
+    rng = np.random.default_rng(78)
+    prompts = [rng.integers(0, GQA.vocab, size=n).astype(np.int32) for n in (70, 100)]
+    eng = Engine(GQA, w_dev, max_seqs=8, max_ctx=128, max_prefill_tokens=170, kv_page_size=32, kv_pages=40)
+    assert eng.kv_free_pages() == 40
+    ot = torch.zeros(8, dtype=torch.int32, device=DEV)
+    ol = torch.empty(8, dtype=torch.float32, device=DEV)
+    eng.prefill(list(range(8)), list(range(8)), [0, 70, 170], _i32(np.concatenate(prompts)), ot, ol, group=4)
+    # prompt 0: 2 shared + 4 own (positions 64..69); prompt 1: 3 shared + 4 own (96..99)
+    assert eng.kv_free_pages() == 40 - 6 - 7
+    eng.release([0, 1, 2])
+    assert eng.kv_free_pages() == 40 - 13 + 3
+    eng.release([3])
+    assert eng.kv_free_pages() == 40 - 7
+    eng.release([4, 5, 6, 7])
+    assert eng.kv_free_pages() == 40
+    assert Engine(GQA, w_dev, max_seqs=2, max_ctx=64, max_prefill_tokens=8).kv_free_pages() == -1
+    eng.close()
+
+
+def _truncated_group_run(page, cut_slot, cut_len, steps=6):
+    w_dev, _, _ = build_models(GQA, 79)
+    rng = np.random.default_rng(80)
+    prompt = rng.integers(0, GQA.vocab, size=100).astype(np.int32)
+    eng = Engine(GQA, w_dev, max_seqs=4, max_ctx=128, max_prefill_tokens=100, kv_page_size=page)
+    slots = [0, 1, 2, 3]
+    ot = torch.zeros(4, dtype=torch.int32, device=DEV)
+    ol = torch.empty(4, dtype=torch.float32, device=DEV)
+    z = torch.empty((4, GQA.vocab), dtype=torch.float32, device=DEV)
+    eng.prefill(slots, slots, [0, 100], _i32(prompt), ot, ol, group=4)
+    free0 = eng.kv_free_pages()
+    eng.set_lengths([cut_slot], [cut_len])
+    free1 = eng.kv_free_pages()
+    frng = np.random.default_rng(81)
+    outs = []
+    for _ in range(steps):
+        tin = _i32(frng.integers(0, GQA.vocab, size=4))
+        eng.step(slots, slots, tin, ot, ol, out_logits=z)
+        outs.append(z.cpu().numpy())
+    eng.close()
+    return outs, free0, free1
+
+
+def test_cutting_into_a_shared_page_copies_it():
+    """A slot cut back into its group's shared prompt page writes its next rows
+    into a copy of that page: every slot of the group decodes as on the
+    contiguous pool (the others' prompt rows are untouched)."""
+    ref, _, _ = _truncated_group_run(0, 1, 50)
+    got, free0, free1 = _truncated_group_run(32, 1, 50)
+    _assert_same(got, ref)
+    # slot 1 let go of shared page 2 (still held by three) and of its own page 3,
+    # and took one page for the copy of page 1
+    assert free1 == free0
