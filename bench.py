@@ -51,7 +51,7 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 # kernel and work-item layout as of that measurement (shared-prompt items of
 # 256 keys, shorter in steps with few rows); set to None when either changes
 # until the counters are taken again.
-ATTN_TRAFFIC_PER_ALG_BYTE = 1.0951
+ATTN_TRAFFIC_PER_ALG_BYTE = 1.0950
 
 
 def parse():
