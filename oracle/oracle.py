@@ -26,6 +26,8 @@ class _Model(C.Structure):
         ("embed", C.c_void_p), ("attn_norm", C.c_void_p), ("w_qkv", C.c_void_p),
         ("w_o", C.c_void_p), ("mlp_norm", C.c_void_p), ("w_gate_up", C.c_void_p),
         ("w_down", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
+        ("E", C.c_int32), ("topk", C.c_int32), ("Fe", C.c_int32),
+        ("w_router", C.c_void_p), ("w_exp_gate_up", C.c_void_p), ("w_exp_down", C.c_void_p),
     ]
 
 
@@ -62,6 +64,7 @@ def load():
     lib.orc_rope_cos_sin.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_double, _dp, _dp]
     lib.orc_rope.argtypes = [_dp, C.c_int32, C.c_int32, C.c_double]
     lib.orc_attend.argtypes = [_dp, _dp, _dp, C.c_int64, C.c_int32, C.c_int32, _dp]
+    lib.orc_route.argtypes = [_dp, C.c_int32, C.c_int32, C.POINTER(C.c_int32), _dp]
     lib.orc_seq_create.restype = C.c_void_p
     lib.orc_seq_create.argtypes = [C.POINTER(_Model), C.c_int32]
     lib.orc_seq_destroy.argtypes = [C.c_void_p]
@@ -186,6 +189,15 @@ def rope(v, pos: int, theta: float):
     return v
 
 
+def route(r, k: int):
+    """Top-k routing of one row of router logits: (experts, weights)."""
+    r = np.ascontiguousarray(r, dtype=np.float64)
+    sel = np.empty(k, dtype=np.int32)
+    w = np.empty(k, dtype=np.float64)
+    load().orc_route(_d(r), len(r), int(k), sel.ctypes.data_as(C.POINTER(C.c_int32)), _d(w))
+    return sel, w
+
+
 def attend(q, K, V):
     q = np.ascontiguousarray(q, dtype=np.float64)
     K = np.ascontiguousarray(K, dtype=np.float64)
@@ -202,10 +214,13 @@ class OracleModel:
     weights: dict with embed [V,H], attn_norm [L,H], w_qkv [L,(Hq+2Hkv)D,H],
     w_o [L,H,Hq*D], mlp_norm [L,H], w_gate_up [L,2F,H], w_down [L,H,F],
     final_norm [H], lm_head [V,H]; all float32 or all uint16 (bf16 bits).
+    A mixture-of-experts model (cfg n_experts E > 0, top_k, expert_ffn Fe)
+    has w_router [L,E,H], w_exp_gate_up [L,E,2Fe,H] and w_exp_down
+    [L,E,H,Fe] instead of w_gate_up and w_down.
     """
 
     NAMES = ("embed", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up",
-             "w_down", "final_norm", "lm_head")
+             "w_down", "final_norm", "lm_head", "w_router", "w_exp_gate_up", "w_exp_down")
 
     def __init__(self, cfg, weights, mode: int):
         self.lib = load()
@@ -213,6 +228,8 @@ class OracleModel:
         self._keep = {}
         wdts = set()
         for n in self.NAMES:
+            if n not in weights:
+                continue
             wdt, arr = _w(weights[n])
             wdts.add(wdt)
             self._keep[n] = arr
@@ -223,8 +240,13 @@ class OracleModel:
         m.D, m.F, m.V = cfg["head_dim"], cfg["ffn"], cfg["vocab"]
         m.eps, m.theta = float(cfg["rms_eps"]), float(cfg["rope_theta"])
         m.mode, m.wdt = int(mode), wdts.pop()
+        m.E, m.topk, m.Fe = int(cfg.get("n_experts", 0)), int(cfg.get("top_k", 0)), int(cfg.get("expert_ffn", 0))
+        need = self.NAMES[:5] + self.NAMES[7:9] + (self.NAMES[9:] if m.E > 0 else self.NAMES[5:7])
+        for n in need:
+            if n not in self._keep:
+                raise ValueError(f"missing weight {n}")
         for n in self.NAMES:
-            setattr(m, n, self._keep[n].ctypes.data)
+            setattr(m, n, self._keep[n].ctypes.data if n in self._keep else None)
         self.m = m
         self.wdt = m.wdt
         self.mode = mode

@@ -17,7 +17,12 @@
  *   trains (Qwen2.5 in Sec. 5.1.1, OpenVLA on a Llama-2 backbone in
  *   Sec. 5.1.2) are pre-norm decoders with RMSNorm, rotate-half RoPE,
  *   grouped-query attention, SwiGLU MLP and an untied LM head; that is the
- *   function written out below, with no biases.
+ *   function written out below, with no biases.  The mixture-of-experts
+ *   policy it also names (Qwen3-30B-A3B, Sec. 5.1.1) replaces each layer's
+ *   MLP by E SwiGLU experts of which each token uses its top k: a router
+ *   row r = h . W_r^T (stored fp32), the k largest entries of r (equal
+ *   values: the lower expert first), weights w = softmax of those k entries,
+ *   MLP output = sum_j w_j * expert_{e_j}(h) in selection order.
  *
  * Precision model (the same function the GPU path must compute):
  *   - every dot product, norm statistic, softmax and log-sum-exp is
@@ -334,7 +339,30 @@ typedef struct {
     const void* w_down;     /* [L][H][F]             */
     const void* final_norm; /* [H]                   */
     const void* lm_head;    /* [V][H]                */
+    /* mixture of experts (E > 0: replaces w_gate_up / w_down) */
+    int32_t E, topk, Fe;
+    const void* w_router;       /* [L][E][H]            */
+    const void* w_exp_gate_up;  /* [L][E][2Fe][H], gate rows first */
+    const void* w_exp_down;     /* [L][E][H][Fe]        */
 } orc_model;
+
+/* Top-k routing of one row: the k largest r[e] (equal values: lower e
+ * first) in decreasing order, and their softmax weights. */
+void orc_route(const double* r, int32_t E, int32_t k, int32_t* sel, double* w)
+{
+    for (int32_t j = 0; j < k; ++j) {
+        int32_t best = -1;
+        for (int32_t e = 0; e < E; ++e) {
+            int taken = 0;
+            for (int32_t i = 0; i < j; ++i) taken |= sel[i] == e;
+            if (!taken && (best < 0 || r[e] > r[best])) best = e;
+        }
+        sel[j] = best;
+    }
+    double m = r[sel[0]], sum = 0.0;
+    for (int32_t j = 0; j < k; ++j) { w[j] = exp(r[sel[j]] - m); sum += w[j]; }
+    for (int32_t j = 0; j < k; ++j) w[j] /= sum;
+}
 
 typedef struct {
     int32_t max_ctx;
@@ -429,10 +457,17 @@ int orc_forward_token(const orc_model* m, orc_seq* s, int32_t tok, const void* e
     double* h    = (double*)malloc(sizeof(double) * (size_t)H);
     double* qkv  = (double*)malloc(sizeof(double) * (size_t)NQKV);
     double* att  = (double*)malloc(sizeof(double) * (size_t)Hq * (size_t)D);
-    double* y    = (double*)malloc(sizeof(double) * (size_t)(H > 2 * F ? H : 2 * F));
-    double* mm   = (double*)malloc(sizeof(double) * (size_t)F);
-    if (!x || !h || !qkv || !att || !y || !mm) {
+    const int32_t E = m->E, Fe = m->Fe, FF = E > 0 ? Fe : F;
+    double* y    = (double*)malloc(sizeof(double) * (size_t)(H > 2 * FF ? H : 2 * FF));
+    double* mm   = (double*)malloc(sizeof(double) * (size_t)FF);
+    double* r    = (double*)malloc(sizeof(double) * (size_t)(E > 0 ? E : 1));
+    double* acc  = (double*)malloc(sizeof(double) * (size_t)H);
+    double* y2   = (double*)malloc(sizeof(double) * (size_t)H);
+    int32_t* sel = (int32_t*)malloc(sizeof(int32_t) * (size_t)(m->topk > 0 ? m->topk : 1));
+    double* wsel = (double*)malloc(sizeof(double) * (size_t)(m->topk > 0 ? m->topk : 1));
+    if (!x || !h || !qkv || !att || !y || !mm || !r || !acc || !y2 || !sel || !wsel) {
         free(x); free(h); free(qkv); free(att); free(y); free(mm);
+        free(r); free(acc); free(y2); free(sel); free(wsel);
         return -2;
     }
 
@@ -479,14 +514,34 @@ int orc_forward_token(const orc_model* m, orc_seq* s, int32_t tok, const void* e
         for (int32_t i = 0; i < H; ++i) x[i] = resid_round(mode, x[i] + y[i]);
         /* 2g. SwiGLU MLP */
         orc_rmsnorm(x, wdt, m->mlp_norm, (size_t)l * (size_t)H, H, m->eps, mode, h);
-        orc_matvec(wdt, m->w_gate_up, (size_t)l * 2u * (size_t)F * (size_t)H, 2 * F, H, h, y);
-        for (int32_t i = 0; i < F; ++i) {
-            double a = y[i], b = y[F + i];
-            double silu = a / (1.0 + exp(-a));
-            mm[i] = store_round(mode, silu * b);
+        if (E == 0) {
+            orc_matvec(wdt, m->w_gate_up, (size_t)l * 2u * (size_t)F * (size_t)H, 2 * F, H, h, y);
+            for (int32_t i = 0; i < F; ++i) {
+                double a = y[i], b = y[F + i];
+                double silu = a / (1.0 + exp(-a));
+                mm[i] = store_round(mode, silu * b);
+            }
+            orc_matvec(wdt, m->w_down, (size_t)l * (size_t)H * (size_t)F, H, F, mm, y);
+            for (int32_t i = 0; i < H; ++i) x[i] = resid_round(mode, x[i] + y[i]);
+        } else {
+            /* 2g'. mixture of experts: route, then the selected SwiGLU experts */
+            orc_matvec(wdt, m->w_router, (size_t)l * (size_t)E * (size_t)H, E, H, h, r);
+            for (int32_t e = 0; e < E; ++e) r[e] = resid_round(mode, r[e]);
+            orc_route(r, E, m->topk, sel, wsel);
+            for (int32_t i = 0; i < H; ++i) acc[i] = 0.0;
+            for (int32_t j = 0; j < m->topk; ++j) {
+                const size_t ex = (size_t)l * (size_t)E + (size_t)sel[j];
+                orc_matvec(wdt, m->w_exp_gate_up, ex * 2u * (size_t)Fe * (size_t)H, 2 * Fe, H, h, y);
+                for (int32_t i = 0; i < Fe; ++i) {
+                    double a = y[i], b = y[Fe + i];
+                    double silu = a / (1.0 + exp(-a));
+                    mm[i] = store_round(mode, silu * b);
+                }
+                orc_matvec(wdt, m->w_exp_down, ex * (size_t)H * (size_t)Fe, H, Fe, mm, y2);
+                for (int32_t i = 0; i < H; ++i) acc[i] += wsel[j] * y2[i];
+            }
+            for (int32_t i = 0; i < H; ++i) x[i] = resid_round(mode, x[i] + acc[i]);
         }
-        orc_matvec(wdt, m->w_down, (size_t)l * (size_t)H * (size_t)F, H, F, mm, y);
-        for (int32_t i = 0; i < H; ++i) x[i] = resid_round(mode, x[i] + y[i]);
     }
 
     /* 3. final norm and LM head (fp32 logits) */
@@ -496,6 +551,7 @@ int orc_forward_token(const orc_model* m, orc_seq* s, int32_t tok, const void* e
 
     s->len = pos + 1;
     free(x); free(h); free(qkv); free(att); free(y); free(mm);
+    free(r); free(acc); free(y2); free(sel); free(wsel);
     return 0;
 }
 

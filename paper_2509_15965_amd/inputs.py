@@ -26,8 +26,6 @@ import torch
 
 from .configs import ModelShape, Workload
 
-WEIGHT_NAMES = ("embed", "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up",
-                "w_down", "final_norm", "lm_head")
 INIT_STD = 0.02
 
 
@@ -36,18 +34,24 @@ def torch_dtype(shape: ModelShape):
 
 
 def weight_shapes(m: ModelShape) -> Dict[str, tuple]:
+    """Shapes of the model's weight tensors; a mixture of experts has a router
+    and stacked experts (gate rows first in each expert's gate|up) in place of
+    w_gate_up and w_down."""
     L, H, F, V = m.n_layers, m.hidden, m.ffn, m.vocab
-    return {
+    out = {
         "embed": (V, H),
         "attn_norm": (L, H),
         "w_qkv": (L, m.qkv_rows, H),
         "w_o": (L, H, m.n_q_heads * m.head_dim),
         "mlp_norm": (L, H),
-        "w_gate_up": (L, 2 * F, H),
-        "w_down": (L, H, F),
-        "final_norm": (H,),
-        "lm_head": (V, H),
     }
+    if m.moe:
+        E, Fe = m.n_experts, m.expert_ffn
+        out.update({"w_router": (L, E, H), "w_exp_gate_up": (L, E, 2 * Fe, H), "w_exp_down": (L, E, H, Fe)})
+    else:
+        out.update({"w_gate_up": (L, 2 * F, H), "w_down": (L, H, F)})
+    out.update({"final_norm": (H,), "lm_head": (V, H)})
+    return out
 
 
 INITS = ("normal", "fanin")
@@ -61,8 +65,8 @@ def init_std(m: ModelShape, name: str, init: str) -> float:
         return INIT_STD
     if name == "embed":
         return 1.0
-    fan_in = {"w_o": m.n_q_heads * m.head_dim, "w_down": m.ffn}.get(name, m.hidden)
-    if name in ("w_o", "w_down"):
+    fan_in = {"w_o": m.n_q_heads * m.head_dim, "w_down": m.ffn, "w_exp_down": m.expert_ffn}.get(name, m.hidden)
+    if name in ("w_o", "w_down", "w_exp_down"):
         return 1.0 / math.sqrt(fan_in * 2.0 * m.n_layers)
     return 1.0 / math.sqrt(fan_in)
 
@@ -78,6 +82,13 @@ def make_weights(m: ModelShape, seed: int, device="cpu", init: str = "normal") -
         t = torch.empty(shp, dtype=dt, device=device)
         if name.endswith("norm"):
             t.fill_(1.0)
+        elif len(shp) == 4:   # stacked experts: one (layer, expert) slice at a time
+            std = init_std(m, name, init)
+            for l in range(shp[0]):
+                for e in range(shp[1]):
+                    r = torch.randn(shp[2:], generator=gen, device=device, dtype=torch.float32)
+                    t[l, e].copy_(r.mul_(std))
+                    del r
         elif len(shp) == 3:
             std = init_std(m, name, init)
             for l in range(shp[0]):

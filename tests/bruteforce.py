@@ -71,6 +71,27 @@ def _rotate(X, c, s):
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
 
+def _moe(cfg, W, l, Hn, st, res):
+    """Mixture-of-experts MLP output [n, H]: router logits stored like the
+    residual, the k largest per row (a stable sort, so equal logits keep the
+    lower expert first), softmax over those k, then the weighted sum of the
+    selected SwiGLU experts."""
+    k, Fe = cfg["top_k"], cfg["expert_ffn"]
+    R = res(Hn @ W["w_router"][l].T)                              # [n, E]
+    idx = np.argsort(-R, axis=1, kind="stable")[:, :k]
+    sel = np.take_along_axis(R, idx, axis=1)
+    wts = np.exp(sel - sel[:, :1])
+    wts = wts / wts.sum(axis=1, keepdims=True)
+    out = np.zeros((Hn.shape[0], Hn.shape[1]))
+    for e in np.unique(idx):
+        rows, slot = np.nonzero(idx == e)
+        GU = Hn[rows] @ W["w_exp_gate_up"][l, e].T
+        a, b = GU[:, :Fe], GU[:, Fe:]
+        M = st(a / (1.0 + np.exp(-a)) * b)
+        out[rows] += wts[rows, slot][:, None] * (M @ W["w_exp_down"][l, e].T)
+    return out
+
+
 def forward_all(cfg, weights, tokens, mode="fp64"):
     """Logits [n, V] at every position of `tokens` (list of ids >= 0)."""
     st, res = _storage(mode)
@@ -100,6 +121,9 @@ def forward_all(cfg, weights, tokens, mode="fp64"):
         O = st(np.einsum("hpt,thd->phd", P, Vv).reshape(n, Hq * D))
         X = res(X + O @ W["w_o"][l].T)
         Hn = st(_rms(X, W["mlp_norm"][l], eps))
+        if cfg.get("n_experts", 0) > 0:
+            X = res(X + _moe(cfg, W, l, Hn, st, res))
+            continue
         GU = Hn @ W["w_gate_up"][l].T
         a, b = GU[:, :F], GU[:, F:]
         M = st(a / (1.0 + np.exp(-a)) * b)
