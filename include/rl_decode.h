@@ -78,6 +78,18 @@ typedef struct rl_model_config {
     int32_t max_prefill_tokens;
     int32_t kv_page_size;         /* 0: contiguous slots; else positions per K/V page (a multiple of 32 in [32, 65536]) */
     int32_t kv_pages;             /* pages in the pool (0: max_seqs * ceil(max_ctx / kv_page_size)); 0 without pages */
+    /* Mixture of experts (Sec. 5.1.1's Qwen3-30B-A3B policy): n_experts > 0
+     * replaces each layer's MLP by n_experts SwiGLU experts of width
+     * expert_ffn of which each token uses its top_k (bf16 only; n_experts
+     * <= 1024, top_k <= min(n_experts, 16), expert_ffn a multiple of 16,
+     * hidden a multiple of 16 and <= 4096; ffn is then not used).  A token's
+     * router row r = h . W_r^T (fp32); its experts are the top_k largest
+     * entries (equal values: the lower expert first) and their weights the
+     * softmax of those entries; the MLP output is the weighted sum of the
+     * chosen experts' outputs. */
+    int32_t n_experts;
+    int32_t top_k;
+    int32_t expert_ffn;
     int32_t reserved;             /* must be 0 */
 } rl_model_config;
 
@@ -93,6 +105,11 @@ typedef struct rl_model_config {
  *   w_down     [L][H][F]
  *   final_norm [H]
  *   lm_head    [vocab][H]
+ * and for a mixture of experts (E = n_experts, Fe = expert_ffn), in place of
+ * w_gate_up and w_down (which may then be NULL):
+ *   w_router       [L][E][H]
+ *   w_exp_gate_up  [L][E][2*Fe][H]     per expert: gate rows, then up rows
+ *   w_exp_down     [L][E][H][Fe]
  * q-head j attends with kv-head j / (Hq / Hkv).  Every row must be 16-byte
  * aligned (guaranteed by the multiple-of-8 shape rules for bf16 and fp32). */
 typedef struct rl_weights {
@@ -105,6 +122,9 @@ typedef struct rl_weights {
     const void* w_down;
     const void* final_norm;
     const void* lm_head;
+    const void* w_router;
+    const void* w_exp_gate_up;
+    const void* w_exp_down;
 } rl_weights;
 
 /* Sampling: seed keys the generator; temperature T >= 0 divides the logits
@@ -452,7 +472,10 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
 typedef enum rl_kernel_class {
     RL_K_EMBED = 0, RL_K_RMSNORM, RL_K_GEMM_QKV, RL_K_ROPE_APPEND, RL_K_ATTENTION,
     RL_K_ATTN_COMBINE, RL_K_GEMM_O, RL_K_GEMM_GATE_UP, RL_K_GEMM_DOWN, RL_K_GEMM_LM_HEAD,
-    RL_K_SPLITK_REDUCE, RL_K_SAMPLE, RL_K_COUNT
+    RL_K_SPLITK_REDUCE, RL_K_SAMPLE,
+    RL_K_MOE_ROUTE,          /* router projection, top-k and grouping by expert */
+    RL_K_MOE_EXPERTS,        /* the grouped expert projections */
+    RL_K_COUNT
 } rl_kernel_class;
 
 /* Measured GEMM plans.  The decode batch of a rollout shrinks from the whole

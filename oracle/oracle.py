@@ -70,6 +70,8 @@ def load():
     lib.orc_seq_destroy.argtypes = [C.c_void_p]
     lib.orc_seq_clone.restype = C.c_void_p
     lib.orc_seq_clone.argtypes = [C.POINTER(_Model), C.c_void_p]
+    lib.orc_seq_route_margin.restype = C.c_double
+    lib.orc_seq_route_margin.argtypes = [C.c_void_p]
     lib.orc_seq_len.restype = C.c_int32
     lib.orc_seq_len.argtypes = [C.c_void_p]
     lib.orc_seq_set_len.argtypes = [C.c_void_p, C.c_int32]
@@ -281,6 +283,12 @@ class OracleSeq:
     @property
     def length(self) -> int:
         return int(self.lib.orc_seq_len(self.h))
+
+    @property
+    def route_margin(self) -> float:
+        """Smallest gap between a chosen router logit and the largest one left
+        out, over every token routed so far (inf for a dense model)."""
+        return float(self.lib.orc_seq_route_margin(self.h))
 
     def set_length(self, n: int) -> None:
         self.lib.orc_seq_set_len(self.h, int(n))

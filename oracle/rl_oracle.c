@@ -369,6 +369,9 @@ typedef struct {
     int32_t len;         /* tokens already in the cache */
     double* K;           /* [L][max_ctx][Hkv][D] */
     double* Vc;          /* [L][max_ctx][Hkv][D] */
+    double route_margin; /* smallest gap between a chosen router logit and the
+                            largest one left out, over every routing so far
+                            (a check that a test's routing has no near ties) */
 } orc_seq;
 
 orc_seq* orc_seq_create(const orc_model* m, int32_t max_ctx)
@@ -377,6 +380,7 @@ orc_seq* orc_seq_create(const orc_model* m, int32_t max_ctx)
     size_t n = (size_t)m->L * (size_t)max_ctx * (size_t)m->Hkv * (size_t)m->D;
     s->max_ctx = max_ctx;
     s->len = 0;
+    s->route_margin = INFINITY;
     s->K = (double*)calloc(n, sizeof(double));
     s->Vc = (double*)calloc(n, sizeof(double));
     if (!s->K || !s->Vc) { free(s->K); free(s->Vc); free(s); return NULL; }
@@ -398,8 +402,11 @@ orc_seq* orc_seq_clone(const orc_model* m, const orc_seq* src)
     memcpy(d->K, src->K, n * sizeof(double));
     memcpy(d->Vc, src->Vc, n * sizeof(double));
     d->len = src->len;
+    d->route_margin = src->route_margin;
     return d;
 }
+
+double orc_seq_route_margin(const orc_seq* s) { return s->route_margin; }
 
 int32_t orc_seq_len(const orc_seq* s) { return s->len; }
 void orc_seq_set_len(orc_seq* s, int32_t len) { s->len = len; }
@@ -528,6 +535,11 @@ int orc_forward_token(const orc_model* m, orc_seq* s, int32_t tok, const void* e
             orc_matvec(wdt, m->w_router, (size_t)l * (size_t)E * (size_t)H, E, H, h, r);
             for (int32_t e = 0; e < E; ++e) r[e] = resid_round(mode, r[e]);
             orc_route(r, E, m->topk, sel, wsel);
+            for (int32_t e = 0; e < E; ++e) {
+                int chosen = 0;
+                for (int32_t j = 0; j < m->topk; ++j) chosen |= sel[j] == e;
+                if (!chosen && r[sel[m->topk - 1]] - r[e] < s->route_margin) s->route_margin = r[sel[m->topk - 1]] - r[e];
+            }
             for (int32_t i = 0; i < H; ++i) acc[i] = 0.0;
             for (int32_t j = 0; j < m->topk; ++j) {
                 const size_t ex = (size_t)l * (size_t)E + (size_t)sel[j];

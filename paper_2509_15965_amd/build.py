@@ -17,7 +17,8 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "librl_decode.so")
 OBJ_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["engine.cpp", "k_elementwise.hip", "k_gemm.hip", "k_gemm_lds.hip", "k_attention.hip", "k_sample.hip"]
+SOURCES = ["engine.cpp", "k_elementwise.hip", "k_gemm.hip", "k_gemm_lds.hip", "k_attention.hip", "k_sample.hip",
+           "k_moe.hip"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

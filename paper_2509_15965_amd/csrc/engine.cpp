@@ -53,6 +53,11 @@ struct Layout {
     size_t off_spart = 0, off_tok = 0;
     size_t off_stage = 0, stage_bytes = 0;   // KV offload staging: the activation buffers x .. split-K partials
     size_t part_floats = 0, apart_floats = 0, meta_bytes = 0;
+    // mixture of experts: router logits [R][E] fp32, per pair its expert and
+    // weight, the pairs grouped by expert and each expert's range, the
+    // pairs' SwiGLU rows [R*k][Fe] and their weighted outputs [k][R][H] fp32
+    size_t off_router = 0, off_moe_ids = 0, off_moe_w = 0, off_moe_pairs = 0, off_moe_off = 0;
+    size_t off_moe_act = 0, off_moe_out = 0;
 };
 
 bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
@@ -67,7 +72,8 @@ bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
     if (c->n_layers < 1 || c->n_layers > 4096) return bad(RL_ERR_INVALID_ARG, "n_layers out of range");
     if (c->hidden < 8 || c->hidden > (1 << 16)) return bad(RL_ERR_INVALID_ARG, "hidden out of range");
     if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads > 1024) return bad(RL_ERR_INVALID_ARG, "head counts out of range");
-    if (c->ffn < 8 || c->ffn > (1 << 20)) return bad(RL_ERR_INVALID_ARG, "ffn out of range");
+    if ((c->n_experts == 0 && c->ffn < 8) || c->ffn < 0 || c->ffn > (1 << 20))
+        return bad(RL_ERR_INVALID_ARG, "ffn out of range");   // a mixture of experts does not use it
     if (c->vocab < 8 || c->vocab > (1 << 24)) return bad(RL_ERR_INVALID_ARG, "vocab out of range");
     if (c->dtype != RL_DTYPE_FP32 && c->dtype != RL_DTYPE_BF16) return bad(RL_ERR_INVALID_ARG, "unknown dtype");
     if (!(c->rms_eps > 0.0) || !std::isfinite(c->rms_eps)) return bad(RL_ERR_INVALID_ARG, "rms_eps must be > 0");
@@ -86,6 +92,16 @@ bool cfg_check(const rl_model_config* c, rl_status* code, std::string* why) {
         const uint64_t widest = std::max({static_cast<uint64_t>(c->vocab) * H, 2 * F * H, qkv * H, H * F,
                                           H * static_cast<uint64_t>(c->n_q_heads) * c->head_dim});
         if (2 * widest > 0xFFFFFFFFull) return bad(RL_ERR_UNSUPPORTED, "a bf16 weight matrix spans 4 GiB or more");
+    }
+    if (c->n_experts != 0 || c->top_k != 0 || c->expert_ffn != 0) {
+        if (c->n_experts < 1 || c->n_experts > kMoeMaxExperts) return bad(RL_ERR_INVALID_ARG, "n_experts out of range");
+        if (c->top_k < 1 || c->top_k > std::min(c->n_experts, kMoeMaxTopK))
+            return bad(RL_ERR_INVALID_ARG, "top_k must be in [1, min(n_experts, 16)]");
+        if (c->expert_ffn < 16 || c->expert_ffn > (1 << 20) || c->expert_ffn % 16)
+            return bad(RL_ERR_INVALID_ARG, "expert_ffn must be a positive multiple of 16");
+        if (c->dtype != RL_DTYPE_BF16) return bad(RL_ERR_UNSUPPORTED, "mixture of experts needs bf16");
+        if (c->hidden % 16 || c->hidden > 4096)
+            return bad(RL_ERR_UNSUPPORTED, "mixture of experts needs hidden a multiple of 16 and <= 4096");
     }
     return true;
 }
@@ -138,6 +154,16 @@ Layout make_layout(const rl_model_config& c) {
     L.off_meta = take(L.meta_bytes);
     L.off_tok = take(R * 4);   // packed token ids of a scoring pass
     L.off_spart = take(sizeof(SamplePart) * static_cast<size_t>(c.max_seqs) * kSampleMaxChunks);
+    if (c.n_experts > 0) {
+        const size_t E = c.n_experts, P = R * c.top_k, Fe = c.expert_ffn;
+        L.off_router = take(R * E * 4);
+        L.off_moe_ids = take(P * 4);
+        L.off_moe_w = take(P * 4);
+        L.off_moe_pairs = take(P * 4);
+        L.off_moe_off = take((E + 1) * 4);
+        L.off_moe_act = take(P * Fe * es);
+        L.off_moe_out = take(P * H * 4);
+    }
     L.ws_bytes = o;
     return L;
 }
@@ -199,7 +225,7 @@ namespace {
 
 const char* kClassNames[RL_K_COUNT] = {
     "embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "attn_combine", "gemm_o",
-    "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample"};
+    "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample", "moe_route", "moe_experts"};
 
 rl_status fail(rl_decode_ctx* c, rl_status s, const std::string& m) {
     if (c) c->err = m;
@@ -644,13 +670,16 @@ rl_status reduce_splits(rl_decode_ctx* c, int epi, int M, int N, int splits, flo
 // fits one float4 per thread (H <= 4096), else from kResidNormMinRows rows
 // (enough rows to hide the grouped loads); below, the wide reduction and the norm.
 constexpr int kResidNormMinRows = 64;
+// part: the slices to add (default: the split-K partials region); a mixture
+// of experts passes its weighted expert outputs (one plane per choice, H <= 4096).
 rl_status resid_then_norm(rl_decode_ctx* c, int dt, int splits, float* x, int n, int H, const void* g, float eps,
-                          void* h) {
+                          void* h, const float* part = nullptr) {
     const double es = c->lay.es;
     hipError_t e;
     if (splits > 0 && H % 4 == 0 && (H <= 4096 || (n >= kResidNormMinRows && H <= 8192))) {
         Prof pr(c, RL_K_SPLITK_REDUCE);
-        e = launch_resid_norm(dt, c->wsp<float>(c->lay.off_part), splits, x, n, H, g, eps, h, c->stream);
+        e = launch_resid_norm(dt, part ? part : c->wsp<float>(c->lay.off_part), splits, x, n, H, g, eps, h,
+                              c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "residual + rmsnorm launch");
         pr.done(n * H * (4.0 * splits + 8.0 + es) + H * es, 0.0);
         return RL_OK;
@@ -663,6 +692,60 @@ rl_status resid_then_norm(rl_decode_ctx* c, int dt, int splits, float* x, int n,
     e = launch_rmsnorm(dt, x, nullptr, n, H, g, eps, h, c->stream);
     if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
     pr.done(n * H * (4.0 + es) + H * es, 0.0);
+    return RL_OK;
+}
+
+// Mixture-of-experts MLP of layer l over n rows of h: router logits, top-k
+// and grouping, then the experts' gate|up (SwiGLU) and down projections,
+// whose routing-weighted outputs land in k planes of [n][H] fp32.
+rl_status run_moe(rl_decode_ctx* c, int l, int n, const void* h) {
+    const rl_model_config& cf = c->cfg;
+    const Layout& L = c->lay;
+    const int H = cf.hidden, E = cf.n_experts, k = cf.top_k, Fe = cf.expert_ffn;
+    const size_t esz = static_cast<size_t>(L.es);
+    const uint8_t* wr = static_cast<const uint8_t*>(c->w.w_router) + static_cast<size_t>(l) * E * H * esz;
+    float* logits = c->wsp<float>(L.off_router);
+    int splits = 0;
+    rl_status st = run_gemm(c, RL_K_MOE_ROUTE, h, H, wr, n, E, H, EPI_F32, logits, E, nullptr, 0, nullptr, 0, false,
+                            &splits);   // split-K slices, if any, are summed inside (not deferred)
+    if (st != RL_OK) return st;
+    int32_t* ids = c->wsp<int32_t>(L.off_moe_ids);
+    float* pw = c->wsp<float>(L.off_moe_w);
+    int32_t* pairs = c->wsp<int32_t>(L.off_moe_pairs);
+    int32_t* off = c->wsp<int32_t>(L.off_moe_off);
+    hipError_t e;
+    {
+        Prof pr(c, RL_K_MOE_ROUTE);
+        e = launch_moe_route(logits, n, E, k, ids, pw, off, pairs, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "expert routing launch");
+        pr.done(n * (E * 4.0 + k * 12.0), 0.0);
+    }
+    MoeArgs a{};
+    a.E = E; a.k = k; a.n_rows = n; a.npairs = n * k;
+    a.off = off; a.pairs = pairs; a.pw = pw;
+    {
+        Prof pr(c, RL_K_MOE_EXPERTS);
+        MoeArgs g = a;   // gate|up: token rows -> SwiGLU rows of the pairs
+        g.A = static_cast<const uint16_t*>(h); g.lda = H;
+        g.W = static_cast<const uint16_t*>(c->w.w_exp_gate_up) + static_cast<size_t>(l) * E * 2 * Fe * H;
+        g.w_expert = static_cast<size_t>(2) * Fe * H; g.ldw = H; g.K = H; g.Nw = 2 * Fe; g.F = Fe;
+        g.groups = (Fe + 7) / 8;
+        g.act = reinterpret_cast<uint16_t*>(c->ws + L.off_moe_act); g.ld_act = Fe;
+        e = launch_moe_gemv(g, EPI_SWIGLU, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "expert gate|up launch");
+        MoeArgs d = a;   // down: SwiGLU rows -> weighted output planes
+        d.A = g.act; d.lda = Fe;
+        d.W = static_cast<const uint16_t*>(c->w.w_exp_down) + static_cast<size_t>(l) * E * H * Fe;
+        d.w_expert = static_cast<size_t>(H) * Fe; d.ldw = Fe; d.K = Fe; d.Nw = H; d.F = 0;
+        d.groups = (H + 15) / 16;
+        d.plane = c->wsp<float>(L.off_moe_out);
+        e = launch_moe_gemv(d, EPI_RESID, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "expert down launch");
+        // bytes: the experts that can be reached (at most n * k of E) and the pairs' rows
+        const double reach = std::min<double>(E, static_cast<double>(n) * k);
+        pr.done(reach * 3.0 * H * Fe * L.es + n * k * (2.0 * Fe * L.es + H * 4.0) + n * H * L.es,
+                2.0 * n * k * 3.0 * H * Fe);
+    }
     return RL_OK;
 }
 
@@ -702,8 +785,9 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         const uint8_t* wqkv = lw(c->w.w_qkv, l, static_cast<size_t>(L.nqkv) * H);
         const uint8_t* wo = lw(c->w.w_o, l, static_cast<size_t>(H) * HqD);
         const uint8_t* mn = lw(c->w.mlp_norm, l, H);
-        const uint8_t* wgu = lw(c->w.w_gate_up, l, static_cast<size_t>(2) * F * H);
-        const uint8_t* wd = lw(c->w.w_down, l, static_cast<size_t>(H) * F);
+        const bool moe = cf.n_experts > 0;   // no dense MLP weights then
+        const uint8_t* wgu = moe ? nullptr : lw(c->w.w_gate_up, l, static_cast<size_t>(2) * F * H);
+        const uint8_t* wd = moe ? nullptr : lw(c->w.w_down, l, static_cast<size_t>(H) * F);
         const bool last_layer = l + 1 == cf.n_layers;
         // norm applied after this layer's down projection: the next layer's
         // attention norm, or the final norm (all rows; prefill selects rows later)
@@ -751,6 +835,13 @@ rl_status run_forward(rl_decode_ctx* c, const Fwd& f) {
         if (st != RL_OK) return st;
         st = resid_then_norm(c, dt, splits, x, n, H, mn, eps, h);   // MLP norm
         if (st != RL_OK) return st;
+        if (moe) {   // mixture of experts; its k weighted outputs are summed with the residual
+            st = run_moe(c, l, n, h);
+            if (st != RL_OK) return st;
+            st = resid_then_norm(c, dt, cf.top_k, x, n, H, next_norm, eps, h, c->wsp<float>(L.off_moe_out));
+            if (st != RL_OK) return st;
+            continue;
+        }
         st = run_gemm(c, RL_K_GEMM_GATE_UP, h, H, wgu, n, 2 * F, H, EPI_SWIGLU, nullptr, 0, nullptr, 0, mlp, F,
                       false, &splits);
         if (st != RL_OK) return st;
@@ -1438,14 +1529,16 @@ hipError_t init_workspace(rl_decode_ctx* c) {
     return e;
 }
 
-bool weights_ok(const rl_weights* w) {
-    if (!w || !w->embed || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up ||
-        !w->w_down || !w->final_norm || !w->lm_head)
-        return false;
-    const void* wp[9] = {w->embed, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm, w->w_gate_up, w->w_down,
-                         w->final_norm, w->lm_head};
+// Every weight the model reads is given and 16-byte aligned (a mixture of
+// experts reads the router and experts instead of w_gate_up / w_down).
+bool weights_ok(const rl_model_config& c, const rl_weights* w) {
+    if (!w) return false;
+    const bool moe = c.n_experts > 0;
+    const void* wp[10] = {w->embed, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm, w->final_norm, w->lm_head,
+                          moe ? w->w_router : w->w_gate_up, moe ? w->w_exp_gate_up : w->w_down,
+                          moe ? w->w_exp_down : w->w_down};
     for (const void* p : wp)
-        if (!aligned(p, 16)) return false;
+        if (!p || !aligned(p, 16)) return false;
     return true;
 }
 
@@ -1458,7 +1551,7 @@ rl_status rl_decode_create(const rl_model_config* cfg, const rl_weights* w, void
     *out = nullptr;
     rl_status code; std::string why;
     if (!cfg_check(cfg, &code, &why)) return code;
-    if (!weights_ok(w)) return RL_ERR_INVALID_ARG;
+    if (!weights_ok(*cfg, w)) return RL_ERR_INVALID_ARG;
     if (!kv_pool || !workspace || !aligned(kv_pool, 256) || !aligned(workspace, 256)) return RL_ERR_INVALID_ARG;
     Layout L = make_layout(*cfg);
     if (kv_bytes < L.kv_bytes || ws_bytes < L.ws_bytes) return RL_ERR_CAPACITY;
@@ -2101,7 +2194,7 @@ rl_status rl_decode_rebind(rl_decode_ctx* ctx, const rl_weights* w, void* kv_poo
                            void* workspace, size_t ws_bytes) {
     if (!ctx_ok(ctx)) return RL_ERR_STATE;
     rl_decode_ctx* c = ctx;
-    if (!weights_ok(w)) return fail(c, RL_ERR_INVALID_ARG, "weights: NULL or misaligned pointer");
+    if (!weights_ok(c->cfg, w)) return fail(c, RL_ERR_INVALID_ARG, "weights: NULL or misaligned pointer");
     if (!kv_pool || !workspace || !aligned(kv_pool, 256) || !aligned(workspace, 256))
         return fail(c, RL_ERR_INVALID_ARG, "KV pool and workspace must be 256-byte aligned device pointers");
     if (kv_bytes < c->lay.kv_bytes || ws_bytes < c->lay.ws_bytes) return fail(c, RL_ERR_CAPACITY, "buffer too small");
@@ -2213,6 +2306,8 @@ rl_status rl_decode_tune_gemms(rl_decode_ctx* ctx, int32_t n_sizes, const int32_
     if (!ctx_ok(ctx)) return RL_ERR_INVALID_ARG;
     if (n_sizes < 0 || n_sizes > 4096 || (n_sizes > 0 && !sizes))
         return fail(ctx, RL_ERR_INVALID_ARG, "n_sizes must be in [0, 4096] with a size array");
+    if (ctx->cfg.n_experts > 0 && n_sizes > 0)
+        return fail(ctx, RL_ERR_UNSUPPORTED, "measured GEMM plans cover dense models (the experts have their own kernel)");
     std::vector<int> v(sizes, sizes + n_sizes);
     for (int i = 0; i < n_sizes; ++i) {
         if (v[i] < 1 || v[i] > ctx->cfg.max_seqs)

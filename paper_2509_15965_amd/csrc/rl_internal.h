@@ -94,6 +94,21 @@ struct GemmArgs {
     float* partial;               // [splits][M][Nw] when splits > 1
 };
 
+// Mixture of experts: one grouped expert projection (k_moe.hip).
+constexpr int kMoeMaxExperts = 1024;
+constexpr int kMoeMaxTopK = 16;
+struct MoeArgs {
+    const uint16_t* A; int lda;            // gate|up: token rows [n][K]; down: the pairs' SwiGLU rows [n*k][K]
+    const uint16_t* W; size_t w_expert;    // expert e's matrix at W + e * w_expert, rows [Nw][K]
+    int ldw, K, Nw, F;                     // F: SwiGLU width (gate|up only; Nw = 2F)
+    int E, groups, k, n_rows, npairs;      // groups: 16-row weight groups per expert
+    const int32_t* off;                    // [E + 1] ranges of pairs per expert
+    const int32_t* pairs;                  // [n*k] pair index p = row * k + j, grouped by expert
+    const float* pw;                       // [n*k] routing weight of pair p (down only)
+    uint16_t* act; int ld_act;             // gate|up output: SwiGLU row of each pair position
+    float* plane;                          // down output: [k][n_rows][Nw], plane j of row `row`
+};
+
 struct GemmPlan {
     int variant;   // tile kernel (index into the tile-shape table or a k*Variant id)
     int splits;
@@ -168,6 +183,14 @@ hipError_t launch_attention_bf16(const AttnItem* items, int n_items, const void*
                                  const void* kc, const void* vc, const KvPages& kp, int Hq, int Hkv,
                                  int D, int layer, void* out, float* part,
                                  hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
+// Router logits [n][E] -> each row's top k experts and weights ([n][k]),
+// then the n * k pairs grouped by expert (off [E + 1], pairs [n * k]).
+hipError_t launch_moe_route(const float* logits, int n, int E, int k, int32_t* ids, float* w, int32_t* off,
+                            int32_t* pairs, hipStream_t s);
+// One grouped expert projection (epi: EPI_SWIGLU for gate|up, EPI_RESID for
+// down, which writes routing-weighted planes).
+hipError_t launch_moe_gemv(const MoeArgs& a, int epi, hipStream_t s);
 
 // Most items one split block may have (bounds the combine's LDS).
 constexpr int kMaxCombine = 64;

@@ -27,7 +27,8 @@ def gemm_plan_code(kernel: int, splits: int = 0, second: int = 0) -> int:
     """Value of RL_OPT_GEMM_PLAN: tile kernel, split-K count, second-half kernel."""
     return int(kernel) | (int(splits) << 8) | (int(second) << 16)
 KERNEL_CLASSES = ("embed", "rmsnorm", "gemm_qkv", "rope_append", "attention", "attn_combine",
-                  "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample")
+                  "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "splitk_reduce", "sample",
+                  "moe_route", "moe_experts")
 
 EXPORTS = ("rl_decode_kv_bytes", "rl_decode_workspace_bytes", "rl_decode_create", "rl_decode_destroy",
            "rl_prefill", "rl_score", "rl_decode_step", "rl_sample_logits", "rl_release_slots",
@@ -45,12 +46,23 @@ class ModelConfig(C.Structure):
                 ("vocab", C.c_int32), ("dtype", C.c_int32), ("rms_eps", C.c_double),
                 ("rope_theta", C.c_double), ("max_seqs", C.c_int32), ("max_ctx", C.c_int32),
                 ("max_prefill_tokens", C.c_int32), ("kv_page_size", C.c_int32), ("kv_pages", C.c_int32),
+                ("n_experts", C.c_int32), ("top_k", C.c_int32), ("expert_ffn", C.c_int32),
                 ("reserved", C.c_int32)]
 
 
 class Weights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("embed", "attn_norm", "w_qkv", "w_o", "mlp_norm",
-                                          "w_gate_up", "w_down", "final_norm", "lm_head")]
+                                          "w_gate_up", "w_down", "final_norm", "lm_head",
+                                          "w_router", "w_exp_gate_up", "w_exp_down")]
+
+
+def _weights_struct(weights: Dict[str, torch.Tensor]) -> "Weights":
+    """Device pointers of the weight tensors (absent ones NULL: the dense MLP
+    of a mixture of experts, the experts of a dense model)."""
+    w = Weights()
+    for name, _ in Weights._fields_:
+        setattr(w, name, weights[name].data_ptr() if name in weights else None)
+    return w
 
 
 class SampleParams(C.Structure):
@@ -157,6 +169,7 @@ def make_config(shape: ModelShape, max_seqs: int, max_ctx: int, max_prefill_toke
     c.rms_eps, c.rope_theta = float(shape.rms_eps), float(shape.rope_theta)
     c.max_seqs, c.max_ctx, c.max_prefill_tokens = max_seqs, max_ctx, max_prefill_tokens
     c.kv_page_size, c.kv_pages, c.reserved = kv_page_size, kv_pages, 0
+    c.n_experts, c.top_k, c.expert_ffn = shape.n_experts, shape.top_k, shape.expert_ffn
     return c
 
 
@@ -198,9 +211,7 @@ class Engine:
         self.kv = torch.empty(self.kv_nbytes, dtype=torch.uint8, device=self.device)
         self.ws = torch.empty(self.ws_nbytes, dtype=torch.uint8, device=self.device)
         self.weights = weights
-        w = Weights()
-        for name, _ in Weights._fields_:
-            setattr(w, name, weights[name].data_ptr())
+        w = _weights_struct(weights)
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         h = C.c_void_p()
         st = L.rl_decode_create(C.byref(self.cfg), C.byref(w), self.kv.data_ptr(), self.kv_nbytes,
@@ -300,9 +311,7 @@ class Engine:
 
     def rebind(self, weights: Dict[str, torch.Tensor], kv: torch.Tensor, ws: torch.Tensor):
         """Point the context at new device buffers (weights, KV pool, workspace)."""
-        w = Weights()
-        for name, _ in Weights._fields_:
-            setattr(w, name, weights[name].data_ptr())
+        w = _weights_struct(weights)
         self._check(lib().rl_decode_rebind(self.h, C.byref(w), kv.data_ptr(), kv.numel(), ws.data_ptr(),
                                            ws.numel()), "rl_decode_rebind")
         self.weights, self.kv, self.ws = weights, kv, ws

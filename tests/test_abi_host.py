@@ -8,7 +8,7 @@ import re
 import pytest
 
 from paper_2509_15965_amd import rl_decode as R
-from paper_2509_15965_amd.configs import WORKLOADS
+from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "rl_decode.h")
@@ -85,11 +85,51 @@ def test_invalid_configs_rejected_before_any_device_call(field, value, status):
     setattr(c, field, value)
     assert R.kv_bytes(c) == 0
     assert R.workspace_bytes(c) == 0
-    w = R.Weights(*([256] * 9))
+    w = R.Weights(*([256] * 12))
     h = C.c_void_p(123)
     st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
     assert st == status
     assert not h.value
+
+
+@pytest.mark.parametrize("fields,status", [
+    ({"n_experts": 1025, "top_k": 8, "expert_ffn": 768}, R.RL_ERR_INVALID_ARG),     # too many experts
+    ({"n_experts": 8, "top_k": 9, "expert_ffn": 768}, R.RL_ERR_INVALID_ARG),        # top_k > n_experts
+    ({"n_experts": 64, "top_k": 17, "expert_ffn": 768}, R.RL_ERR_INVALID_ARG),      # top_k > 16
+    ({"n_experts": 8, "top_k": 2, "expert_ffn": 40}, R.RL_ERR_INVALID_ARG),         # width not a multiple of 16
+    ({"n_experts": 0, "top_k": 2, "expert_ffn": 0}, R.RL_ERR_INVALID_ARG),          # top_k without experts
+    ({"n_experts": 8, "top_k": 2, "expert_ffn": 64, "dtype": 0}, R.RL_ERR_UNSUPPORTED),   # fp32
+    ({"n_experts": 8, "top_k": 2, "expert_ffn": 64, "hidden": 8192}, R.RL_ERR_UNSUPPORTED),
+])
+def test_invalid_moe_configs_rejected(fields, status):
+    c = cfg_for("qwen7b")
+    for k, v in fields.items():
+        setattr(c, k, v)
+    assert R.kv_bytes(c) == 0
+    w = R.Weights(*([256] * 12))
+    h = C.c_void_p(123)
+    st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
+    assert st == status and not h.value
+
+
+def test_moe_workspace_holds_the_expert_buffers():
+    """The Qwen3-30B-A3B shape: the workspace adds the router logits, pair
+    lists and the k planes of expert outputs ([k][rows][hidden] fp32)."""
+    from paper_2509_15965_amd.configs import QWEN3_MOE
+    c = R.make_config(QWEN3_MOE, 512, 2048, 4096)
+    dense = R.make_config(ModelShape(**{**QWEN3_MOE.as_dict(), "n_experts": 0, "top_k": 0, "expert_ffn": 0}),
+                          512, 2048, 4096)
+    extra = R.workspace_bytes(c) - R.workspace_bytes(dense)
+    rows, k, H, E, Fe = 4096, 8, 2048, 128, 768
+    assert extra >= rows * (E * 4 + k * 12 + k * Fe * 2 + k * H * 4)
+    # the MLP weights of a mixture of experts: NULL dense matrices are accepted
+    w = R.Weights(*([256] * 5 + [0, 0] + [256] * 5))
+    h = C.c_void_p(123)
+    st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1, 256, 1, None, C.byref(h))
+    assert st == R.RL_ERR_CAPACITY and not h.value          # weights pass; the tiny buffers do not
+    w = R.Weights(*([256] * 9 + [0, 256, 256]))              # no router
+    st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
+    assert st == R.RL_ERR_INVALID_ARG and not h.value
 
 
 def test_bf16_weight_matrix_of_4_gib_rejected():
@@ -99,7 +139,7 @@ def test_bf16_weight_matrix_of_4_gib_rejected():
     c.vocab = 600000
     assert R.kv_bytes(c) == 0
     h = C.c_void_p(123)
-    w = R.Weights(*([256] * 9))
+    w = R.Weights(*([256] * 12))
     st = R.lib().rl_decode_create(C.byref(c), C.byref(w), 256, 1 << 40, 256, 1 << 40, None, C.byref(h))
     assert st == R.RL_ERR_UNSUPPORTED
     assert not h.value
@@ -111,7 +151,7 @@ def test_create_validates_pointers_and_sizes_first():
     lib = R.lib()
     c = cfg_for("tiny")
     h = C.c_void_p(1)
-    w = R.Weights(*([256] * 9))
+    w = R.Weights(*([256] * 12))
     assert lib.rl_decode_create(C.byref(c), None, 256, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG
     w_bad = R.Weights(*([256] * 8 + [0]))
     assert lib.rl_decode_create(C.byref(c), C.byref(w_bad), 256, 1 << 40, 256, 1 << 40, None, C.byref(h)) == R.RL_ERR_INVALID_ARG

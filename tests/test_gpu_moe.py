@@ -1,0 +1,135 @@
+"""Mixture-of-experts decode (the Qwen3-30B-A3B policy of Sec. 5.1.1) through
+the C ABI against the oracle, at the stated bars: routing, grouping by
+expert, the grouped expert projections and the weighted sum, in prefill,
+decode and scoring.  Each case first checks that the oracle's routing has no
+near ties (the router logits are fp32 on both sides; a near tie could pick
+different experts on the two sides), then compares.  Needs an MI355X."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import LOGIT_REL_TOL, LOGP_ABS_TOL, OracleRollout, build_models, row_rel_err
+from paper_2509_15965_amd.configs import QWEN3_MOE, ModelShape
+from paper_2509_15965_amd.rl_decode import RL_ERR_UNSUPPORTED, Engine, RLError
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+MIN_ROUTE_MARGIN = 1e-4
+TINY_MOE = ModelShape(2, 256, 4, 2, 64, 0, 512, 1e-6, 1e6, "bf16", n_experts=8, top_k=2, expert_ffn=128)
+# the real expert widths (128 experts of 768, top 8, hidden 2048, 32 / 4 heads) at two layers
+QWEN3_WIDTHS = ModelShape(**{**QWEN3_MOE.as_dict(), "n_layers": 2})
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _i32(a):
+    return torch.as_tensor(np.asarray(a, dtype=np.int32), device=DEV)
+
+
+def _moe_run(shape, seed, plens, n_steps, sample_rows, group=1, page=0):
+    """Prefill (one prompt per `group` sequences) + n_steps teacher-forced
+    decode steps on the GPU; the rows in `sample_rows` are replayed on the
+    oracle.  Returns [(gpu logits, oracle logits, gpu logp, oracle logp)] per
+    call, for the sampled rows, and the smallest oracle routing margin."""
+    w_dev, _, om = build_models(shape, seed, init="fanin")
+    rng = np.random.default_rng(seed + 1)
+    prompts = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in plens]
+    n_seq = len(prompts) * group
+    max_ctx = max(plens) + n_steps + 2
+    eng = Engine(shape, w_dev, max_seqs=n_seq, max_ctx=max_ctx, max_prefill_tokens=int(sum(plens)),
+                 kv_page_size=page)
+    slots = list(range(n_seq))
+    offs = np.concatenate([[0], np.cumsum(plens)]).astype(np.int32)
+    forced = [rng.integers(0, shape.vocab, size=n_seq).astype(np.int32) for _ in range(n_steps + 1)]
+    ot = torch.empty(n_seq, dtype=torch.int32, device=DEV)
+    ol = torch.empty(n_seq, dtype=torch.float32, device=DEV)
+    zp = torch.empty((len(prompts), shape.vocab), dtype=torch.float32, device=DEV)
+    eng.prefill(slots, slots, offs, _i32(np.concatenate(prompts)), ot, ol, group=group, forced=_i32(forced[0]),
+                out_logits=zp)
+    gpu = [(zp.cpu().numpy(), ol.cpu().numpy())]
+    z = torch.empty((n_seq, shape.vocab), dtype=torch.float32, device=DEV)
+    for s in range(1, n_steps + 1):
+        eng.step(slots, slots, _i32(forced[s - 1]), ot, ol, forced=_i32(forced[s]), out_logits=z)
+        gpu.append((z.cpu().numpy(), ol.cpu().numpy()))
+    eng.close()
+    orc = OracleRollout(om, max_ctx)
+    out = []
+    zo = {}
+    for i in sample_rows:
+        zo[i] = orc.prefill(i, prompts[i // group])
+    prow = sorted({i // group for i in sample_rows})
+    zpg = np.stack([gpu[0][0][p] for p in prow])
+    zpo = np.stack([zo[min(i for i in sample_rows if i // group == p)] for p in prow])
+    lpo = np.array([oracle.logprob(zo[i].astype(np.float32), 1.0, int(forced[0][i])) for i in sample_rows])
+    out.append((zpg, zpo, gpu[0][1][sample_rows], lpo))
+    for s in range(1, n_steps + 1):
+        zs = np.stack([orc.step(i, forced[s - 1][i]) for i in sample_rows])
+        lpo = np.array([oracle.logprob(zs[j].astype(np.float32), 1.0, int(forced[s][i]))
+                        for j, i in enumerate(sample_rows)])
+        out.append((gpu[s][0][sample_rows], zs, gpu[s][1][sample_rows], lpo))
+    margin = min(orc.seqs[i].route_margin for i in sample_rows)
+    return out, margin
+
+
+def _assert_bars(out, margin):
+    assert margin > MIN_ROUTE_MARGIN, margin     # the data has no near-tie routing
+    for k, (zg, zo, lg, lo) in enumerate(out):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+
+
+def test_moe_decode_matches_oracle():
+    out, margin = _moe_run(TINY_MOE, 101, [9, 23, 40], 6, [0, 1, 2])
+    _assert_bars(out, margin)
+
+
+def test_moe_group_prefill_on_a_paged_pool_matches_oracle():
+    """A GRPO group of 4 per prompt (shared prompt pages, pages of 32) and
+    then decoding; every sequence checked."""
+    out, margin = _moe_run(TINY_MOE, 103, [37, 70], 4, list(range(8)), group=4, page=32)
+    _assert_bars(out, margin)
+
+
+def test_moe_real_widths_sampled_rows_match_oracle():
+    """128 experts of width 768, top 8, hidden 2048, at 128 rows per step
+    (every expert serves several pairs; some serve many), 8 rows replayed on
+    the oracle."""
+    n = 128
+    rows = [0, 17, 40, 63, 64, 99, 120, 127]
+    out, margin = _moe_run(QWEN3_WIDTHS, 107, [5 + (i % 7) for i in range(n)], 2, rows)
+    _assert_bars(out, margin)
+
+
+def test_moe_score_matches_oracle():
+    from harness import build_models as bm
+    w_dev, _, om = bm(TINY_MOE, 109, init="fanin")
+    rng = np.random.default_rng(110)
+    prompts = [rng.integers(0, TINY_MOE.vocab, size=n).astype(np.int32) for n in (12, 30)]
+    group = 2
+    resp = [rng.integers(0, TINY_MOE.vocab, size=m).astype(np.int32) for m in (5, 9, 3, 7)]
+    eng = Engine(TINY_MOE, w_dev, max_seqs=4, max_ctx=48, max_prefill_tokens=100)
+    poffs = np.concatenate([[0], np.cumsum([len(p) for p in prompts])]).astype(np.int32)
+    roffs = np.concatenate([[0], np.cumsum([len(r) for r in resp])]).astype(np.int32)
+    lp = torch.empty(int(roffs[-1]), dtype=torch.float32, device=DEV)
+    eng.score([0, 1, 2, 3], poffs, _i32(np.concatenate(prompts)), roffs, _i32(np.concatenate(resp)), lp,
+              group=group, temperature=1.0)
+    got = lp.cpu().numpy()
+    eng.close()
+    for i, r in enumerate(resp):
+        ref = oracle.score(om, prompts[i // group], r, 1.0)
+        assert np.max(np.abs(got[roffs[i]:roffs[i + 1]] - ref)) < LOGP_ABS_TOL, i
+
+
+def test_moe_refuses_measured_plans():
+    w_dev, _, _ = build_models(TINY_MOE, 111, init="fanin")
+    eng = Engine(TINY_MOE, w_dev, max_seqs=4, max_ctx=16, max_prefill_tokens=16)
+    with pytest.raises(RLError) as e:
+        eng.tune_gemms([1, 4])
+    assert e.value.status == RL_ERR_UNSUPPORTED
+    eng.close()
