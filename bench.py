@@ -98,8 +98,9 @@ TUNE_SIZES = (1, 2, 4, 8, 12, 16, 20, 24, 32, 40, 48, 64, 80, 96, 112, 128, 160,
 
 def tune_gemms(eng, max_rows: int, skip: bool):
     """Measure the GEMM plans up to max_rows rows (untimed set-up, like the
-    warm-up); returns what was done for the JSON line."""
-    if skip:
+    warm-up); returns what was done for the JSON line.  Mixture-of-experts
+    models keep the cost-model plans (their experts have their own kernel)."""
+    if skip or eng.shape.moe:
         return {"measured": False}
     sizes = [n for n in TUNE_SIZES if n < max_rows] + [max_rows]
     t0 = time.perf_counter()
@@ -532,6 +533,8 @@ def rollout_step_bytes(shape, plens, resp, group, steps):
         n = int(act.sum())
         ctx = seq_plen[act] + t + 1
         per_row = n * (kv_tok + shape.hidden * es + 12)
+        if shape.moe:   # the experts that n rows reach (expected, uniform routing)
+            fixed = shape.decode_params(active_experts=expected_experts(shape, n)) * es
         nominal[t] = fixed + per_row + float(ctx.sum()) * kv_tok
         own = ctx - (shared[act] if group > 1 else 0)
         groups_live = np.unique(grp[act]) if group > 1 else np.array([], dtype=np.int64)
@@ -595,8 +598,16 @@ def cpu_baseline_rollout(shape, weights, seconds: float):
 
 
 def describe_shape(m):
+    mlp = (f"{m.n_experts} experts of width {m.expert_ffn}, top {m.top_k}" if m.moe else f"ffn {m.ffn}")
     return (f"{m.n_layers} layers, hidden {m.hidden}, {m.n_q_heads} q / {m.n_kv_heads} kv heads of {m.head_dim}, "
-            f"ffn {m.ffn}, vocab {m.vocab}, {m.dtype}")
+            f"{mlp}, vocab {m.vocab}, {m.dtype}")
+
+
+def expected_experts(shape, n: int) -> float:
+    """Distinct experts a layer reads for n rows when each row's top-k is a
+    uniform draw without replacement (random-init routers are near uniform)."""
+    E, k = shape.n_experts, shape.top_k
+    return E * (1.0 - (1.0 - k / E) ** n)
 
 
 def embodied_main(args):
@@ -856,6 +867,10 @@ def main():
     weights = make_weights(shape, wl.seed, device=dev, init=wl.init)
     max_ctx = int(plens.max() + resp.max())
     page = args.kv_page_size
+    if shape.moe and page == 0:
+        # the mixture-of-experts workload's contiguous pool (512 slots x 5120
+        # positions x 98 KB) would not fit beside its 61 GB of weights
+        page = 256
     # a finished sequence keeps its pages until the next prefill, so the pool
     # needs the pages of every sequence's final length; a group holds the
     # pages its prompt fills once
@@ -926,6 +941,8 @@ def main():
     # ---- pass 2: the same rollout again, kernel classes timed with HIP
     # events on the library's stream during the sampled steps only ----
     prof_classes = ("attention", "gemm_gate_up", "gemm_down", "gemm_lm_head", "gemm_qkv", "gemm_o")
+    if shape.moe:
+        prof_classes = ("attention", "moe_experts", "moe_route", "gemm_lm_head", "gemm_qkv", "gemm_o")
     mask = 0
     for c in prof_classes:
         mask |= 1 << KERNEL_CLASSES.index(c)
@@ -1016,7 +1033,9 @@ def main():
     eng.close()
     del eng, ro
     torch.cuda.synchronize()
-    if not args.no_cpu_baseline:
+    if shape.moe:
+        out["data"] += "; expert bytes counted for the experts n rows reach under uniform routing"
+    if not args.no_cpu_baseline and not shape.moe:   # (the oracle would need a 61 GB host copy of the experts)
         out["cpu_baseline"] = cpu_baseline_rollout(shape, weights, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

@@ -729,7 +729,7 @@ rl_status run_moe(rl_decode_ctx* c, int l, int n, const void* h) {
         g.A = static_cast<const uint16_t*>(h); g.lda = H;
         g.W = static_cast<const uint16_t*>(c->w.w_exp_gate_up) + static_cast<size_t>(l) * E * 2 * Fe * H;
         g.w_expert = static_cast<size_t>(2) * Fe * H; g.ldw = H; g.K = H; g.Nw = 2 * Fe; g.F = Fe;
-        g.groups = (Fe + 7) / 8;
+        g.groups = (Fe + kMoeRowsPerGroup / 2 - 1) / (kMoeRowsPerGroup / 2);
         g.act = reinterpret_cast<uint16_t*>(c->ws + L.off_moe_act); g.ld_act = Fe;
         e = launch_moe_gemv(g, EPI_SWIGLU, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "expert gate|up launch");
@@ -737,7 +737,7 @@ rl_status run_moe(rl_decode_ctx* c, int l, int n, const void* h) {
         d.A = g.act; d.lda = Fe;
         d.W = static_cast<const uint16_t*>(c->w.w_exp_down) + static_cast<size_t>(l) * E * H * Fe;
         d.w_expert = static_cast<size_t>(H) * Fe; d.ldw = Fe; d.K = Fe; d.Nw = H; d.F = 0;
-        d.groups = (H + 15) / 16;
+        d.groups = (H + kMoeRowsPerGroup - 1) / kMoeRowsPerGroup;
         d.plane = c->wsp<float>(L.off_moe_out);
         e = launch_moe_gemv(d, EPI_RESID, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "expert down launch");

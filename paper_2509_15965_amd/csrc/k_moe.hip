@@ -110,32 +110,37 @@ __global__ void __launch_bounds__(1024) moe_group_kernel(const int32_t* __restri
     }
 }
 
-// Grouped expert projection: workgroup (e, g) owns 16 weight rows of expert e
-// (SwiGLU: 8 gate rows and the matching 8 up rows) and the whole K, and runs
-// every pair of e through them, 16 * MR pairs at a time.  Wave w takes the
-// w-th eighth of K, and the eight partial 16 x 16 tiles are summed through
-// LDS in wave order (the dense GEMV's scheme).
-template <int MR, int EPI>
-__global__ void __launch_bounds__(512) moe_gemv_kernel(MoeArgs a, int kw) {
-    constexpr int U = 4;   // 64-wide k blocks per batch of loads
-    __shared__ f32x4 red[8][MR][64];
+// Grouped expert projection: workgroup (e, g) owns 16 * NT weight rows of
+// expert e (SwiGLU: NT groups of 8 gate rows and the matching 8 up rows) and
+// the whole K, and runs every pair of e through them, 16 * MR pairs at a
+// time, so each pair row it gathers serves NT row groups.  Wave w takes the
+// w-th quarter of K; the four partial tiles are summed through LDS in wave
+// order.
+template <int MR, int NT, int EPI>
+__global__ void __launch_bounds__(256) moe_gemv_kernel(MoeArgs a, int kw) {
+    constexpr int U = 2;   // 64-wide k blocks per batch of loads
+    __shared__ f32x4 red[4][MR * NT][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r16 = lane & 15, kq = lane >> 4;
     const int e = blockIdx.x / a.groups, g = blockIdx.x - e * a.groups;
     const int p0 = min(max(a.off[e], 0), a.npairs), p1 = min(max(a.off[e + 1], p0), a.npairs);
     if (p0 == p1) return;
 
-    int n;
-    bool ok;
-    if (EPI == EPI_SWIGLU) {
-        const int c = g * 8 + (r16 & 7);
-        ok = c < a.F;
-        n = r16 < 8 ? c : a.F + c;
-    } else {
-        n = g * 16 + r16;
-        ok = n < a.Nw;
+    int n[NT];
+    bool ok[NT];
+    const uint16_t* wp[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (EPI == EPI_SWIGLU) {
+            const int c = (g * NT + t) * 8 + (r16 & 7);
+            ok[t] = c < a.F;
+            n[t] = r16 < 8 ? c : a.F + c;
+        } else {
+            n[t] = (g * NT + t) * 16 + r16;
+            ok[t] = n[t] < a.Nw;
+        }
+        wp[t] = a.W + static_cast<size_t>(e) * a.w_expert + static_cast<size_t>(ok[t] ? n[t] : 0) * a.ldw + 8 * kq;
     }
-    const uint16_t* wp = a.W + static_cast<size_t>(e) * a.w_expert + static_cast<size_t>(ok ? n : 0) * a.ldw + 8 * kq;
     const int kb = wave * kw;
     const int ke = min(a.K, kb + kw);
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -151,18 +156,21 @@ __global__ void __launch_bounds__(512) moe_gemv_kernel(MoeArgs a, int kw) {
             const int arow = !aok[i] ? 0 : EPI == EPI_SWIGLU ? a.pairs[pos] / a.k : pos;
             ap[i] = a.A + static_cast<size_t>(arow) * a.lda + 8 * kq;
         }
-        f32x4 acc[MR];
+        f32x4 acc[MR][NT];
 #pragma unroll
-        for (int i = 0; i < MR; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < MR; ++i)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int k0 = kb; k0 < ke; k0 += 64 * U) {
-            u32x4 wf[U][2], af[U][2][MR];
+            u32x4 wf[U][2][NT], af[U][2][MR];
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     const int kk = k0 + 64 * u + 32 * j;
                     const bool kok = kk + 8 * kq < ke;
-                    wf[u][j] = (ok && kok) ? ld16(wp + kk) : zero;
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) wf[u][j][t] = (ok[t] && kok) ? ld16(wp[t] + kk) : zero;
 #pragma unroll
                     for (int i = 0; i < MR; ++i) af[u][j][i] = (aok[i] && kok) ? ld16(ap[i] + kk) : zero;
                 }
@@ -172,28 +180,34 @@ __global__ void __launch_bounds__(512) moe_gemv_kernel(MoeArgs a, int kw) {
                 for (int j = 0; j < 2; ++j)
 #pragma unroll
                     for (int i = 0; i < MR; ++i)
-                        acc[i] = mfma16x16x32(as_bf16x8(af[u][j][i]), as_bf16x8(wf[u][j]), acc[i]);
+#pragma unroll
+                        for (int t = 0; t < NT; ++t)
+                            acc[i][t] = mfma16x16x32(as_bf16x8(af[u][j][i]), as_bf16x8(wf[u][j][t]), acc[i][t]);
         }
 #pragma unroll
-        for (int i = 0; i < MR; ++i) red[wave][i][lane] = acc[i];
-        __syncthreads();
-        if (wave < MR) {
-            // wave i sums pair tile i over the 8 waves in order; lane holds D[4 kq + e4][r16]
-            f32x4 v = red[0][wave][lane];
+        for (int i = 0; i < MR; ++i)
 #pragma unroll
-            for (int w = 1; w < 8; ++w) v += red[w][wave][lane];
+            for (int t = 0; t < NT; ++t) red[wave][i * NT + t][lane] = acc[i][t];
+        __syncthreads();
+        // wave w finishes tiles w, w + 4, ...: the four waves' partials summed in
+        // order; lane holds D[4 kq + e4][r16] of pair tile i, row group t
+        for (int q = wave; q < MR * NT; q += 4) {
+            const int i = q / NT, t = q - i * NT;
+            f32x4 v = red[0][q][lane];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) v += red[w][q][lane];
 #pragma unroll
             for (int e4 = 0; e4 < 4; ++e4) {
-                const int pos = c0 + 16 * wave + 4 * kq + e4;
+                const int pos = c0 + 16 * i + 4 * kq + e4;
                 const float val = v[e4];
                 if (EPI == EPI_SWIGLU) {
                     const float up = __shfl(val, (lane & ~15) | ((r16 + 8) & 15), 64);
-                    if (r16 < 8 && ok && pos < p1)
-                        a.act[static_cast<size_t>(pos) * a.ld_act + n] = f32_to_bf16(swiglu_bf16(val, up));
-                } else if (ok && pos < p1) {
+                    if (r16 < 8 && ok[t] && pos < p1)
+                        a.act[static_cast<size_t>(pos) * a.ld_act + n[t]] = f32_to_bf16(swiglu_bf16(val, up));
+                } else if (ok[t] && pos < p1) {
                     const int p = a.pairs[pos];
                     const int row = p / a.k, j = p - row * a.k;
-                    a.plane[(static_cast<size_t>(j) * a.n_rows + row) * a.Nw + n] = a.pw[p] * val;
+                    a.plane[(static_cast<size_t>(j) * a.n_rows + row) * a.Nw + n[t]] = a.pw[p] * val;
                 }
             }
         }
@@ -214,10 +228,14 @@ hipError_t launch_moe_route(const float* logits, int n, int E, int k, int32_t* i
 
 hipError_t launch_moe_gemv(const MoeArgs& a, int epi, hipStream_t s) {
     if (a.npairs <= 0) return hipSuccess;
-    const int kw = ((a.K + 7) / 8 + 63) / 64 * 64;
-    dim3 grid(a.E * a.groups), block(512);
-    if (epi == EPI_SWIGLU) hipLaunchKernelGGL((moe_gemv_kernel<4, EPI_SWIGLU>), grid, block, 0, s, a, kw);
-    else hipLaunchKernelGGL((moe_gemv_kernel<4, EPI_RESID>), grid, block, 0, s, a, kw);
+    if (a.groups != (epi == EPI_SWIGLU ? (a.F + kMoeRowsPerGroup / 2 - 1) / (kMoeRowsPerGroup / 2)
+                                       : (a.Nw + kMoeRowsPerGroup - 1) / kMoeRowsPerGroup))
+        return hipErrorInvalidValue;
+    const int kw = ((a.K + 3) / 4 + 63) / 64 * 64;
+    dim3 grid(a.E * a.groups), block(256);
+    constexpr int NT = kMoeRowsPerGroup / 16;
+    if (epi == EPI_SWIGLU) hipLaunchKernelGGL((moe_gemv_kernel<4, NT, EPI_SWIGLU>), grid, block, 0, s, a, kw);
+    else hipLaunchKernelGGL((moe_gemv_kernel<4, NT, EPI_RESID>), grid, block, 0, s, a, kw);
     return hipGetLastError();
 }
 

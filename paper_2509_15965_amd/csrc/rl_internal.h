@@ -97,11 +97,12 @@ struct GemmArgs {
 // Mixture of experts: one grouped expert projection (k_moe.hip).
 constexpr int kMoeMaxExperts = 1024;
 constexpr int kMoeMaxTopK = 16;
+constexpr int kMoeRowsPerGroup = 64;   // weight rows of one expert per workgroup (SwiGLU: 32 gate + 32 up)
 struct MoeArgs {
     const uint16_t* A; int lda;            // gate|up: token rows [n][K]; down: the pairs' SwiGLU rows [n*k][K]
     const uint16_t* W; size_t w_expert;    // expert e's matrix at W + e * w_expert, rows [Nw][K]
     int ldw, K, Nw, F;                     // F: SwiGLU width (gate|up only; Nw = 2F)
-    int E, groups, k, n_rows, npairs;      // groups: 16-row weight groups per expert
+    int E, groups, k, n_rows, npairs;      // groups: kMoeRowsPerGroup-row weight groups per expert
     const int32_t* off;                    // [E + 1] ranges of pairs per expert
     const int32_t* pairs;                  // [n*k] pair index p = row * k + j, grouped by expert
     const float* pw;                       // [n*k] routing weight of pair p (down only)
