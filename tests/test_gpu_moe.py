@@ -133,3 +133,30 @@ def test_moe_refuses_measured_plans():
         eng.tune_gemms([1, 4])
     assert e.value.status == RL_ERR_UNSUPPORTED
     eng.close()
+
+
+def test_moe_decode_is_bit_reproducible():
+    """Pairs land in their expert's range in whatever order the LDS atomics
+    give; the outputs must not depend on it: two identical runs at the real
+    widths (128 rows, 1024 pairs over 128 experts) give the same bits."""
+    w_dev, _, _ = build_models(QWEN3_WIDTHS, 113, init="fanin")
+    rng = np.random.default_rng(114)
+    n = 128
+    prompts = rng.integers(0, QWEN3_WIDTHS.vocab, size=n * 6).astype(np.int32)
+    toks = [_i32(rng.integers(0, QWEN3_WIDTHS.vocab, size=n)) for _ in range(3)]
+    outs = []
+    for _ in range(2):
+        eng = Engine(QWEN3_WIDTHS, w_dev, max_seqs=n, max_ctx=16, max_prefill_tokens=n * 6)
+        ot = torch.empty(n, dtype=torch.int32, device=DEV)
+        ol = torch.empty(n, dtype=torch.float32, device=DEV)
+        z = torch.empty((n, QWEN3_WIDTHS.vocab), dtype=torch.float32, device=DEV)
+        eng.prefill(list(range(n)), list(range(n)), np.arange(0, n * 6 + 1, 6), _i32(prompts), ot, ol)
+        run = []
+        for t in toks:
+            eng.step(list(range(n)), list(range(n)), t, ot, ol, out_logits=z)
+            run.append((z.cpu().numpy(), ol.cpu().numpy(), ot.cpu().numpy()))
+        eng.close()
+        outs.append(run)
+    for a, b in zip(*outs):
+        for u, v in zip(a, b):
+            assert np.array_equal(u, v)
