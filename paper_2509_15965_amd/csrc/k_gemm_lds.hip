@@ -434,7 +434,7 @@ __device__ __forceinline__ void wait_vm_atmost(int n) {
 
 template <int BM, int BN, int WM, int NW, int SA, int SW, int EPI, bool SPLIT>
 __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ksplit, int m_tiles, int n_tiles, int n0,
-                                                              int gm) {
+                                                              int gm, int xsplit) {
     constexpr int BK = 64, ROWB = 128;
     constexpr int WN = NW / WM;
     constexpr int TM = BM / WM, TN = BN / WN;
@@ -450,12 +450,24 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
 
     const int w = blockIdx.x;
     const int xcd = w & 7, j = w >> 3;
-    const int ntx = (n_tiles + 7) >> 3;
-    const int grp = j / (gm * ntx);
-    const int rem = j - grp * gm * ntx;
-    const int m_tile = grp * gm + rem % gm;
-    const int n_tile = (rem / gm) * 8 + xcd;
-    if (m_tile >= m_tiles || n_tile >= n_tiles) return;
+    int m_tile, n_tile, split;
+    if (xsplit) {
+        // split-K over the XCDs: XCD x % 8 runs split 8y + x % 8 of every tile
+        // (M tiles fastest), so its K range of the activations stays in its L2
+        // and the M tiles of one weight tile run back to back
+        split = static_cast<int>(blockIdx.y) * 8 + xcd;
+        m_tile = j % m_tiles;
+        n_tile = j / m_tiles;
+        if (split * ksplit >= p.K || n_tile >= n_tiles) return;
+    } else {
+        const int ntx = (n_tiles + 7) >> 3;
+        const int grp = j / (gm * ntx);
+        const int rem = j - grp * gm * ntx;
+        m_tile = grp * gm + rem % gm;
+        n_tile = (rem / gm) * 8 + xcd;
+        split = blockIdx.y;
+        if (m_tile >= m_tiles || n_tile >= n_tiles) return;
+    }
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -478,7 +490,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
         }
     };
 
-    const int kb = blockIdx.y * ksplit;
+    const int kb = split * ksplit;
     const int ke = min(K, kb + ksplit);
     const int nk = (ke - kb) / BK;
 
@@ -648,7 +660,7 @@ __global__ void __launch_bounds__(64 * NW) gemm_dma128_kernel(GemmArgs p, int ks
                 const int m = m0 + wm * TM + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
                 if (CHECKED && m >= M) continue;
                 if (SPLIT) {
-                    float* dst = p.partial + (static_cast<size_t>(blockIdx.y) * M + m) * Nw;
+                    float* dst = p.partial + (static_cast<size_t>(split) * M + m) * Nw;
 #pragma unroll
                     for (int t = 0; t < NT; ++t)
                         if (!CHECKED || nok[t]) dst[nrow[t]] = acc[i][t][e];
@@ -688,18 +700,21 @@ hipError_t launch_dma128(const GemmArgs& a, const GemmPlan& p, int n0, int n1, h
     const int gm = m_tiles < 8 ? m_tiles : 8;
     const int ntx = (n_tiles + 7) / 8;
     const int groups = (m_tiles + gm - 1) / gm;
-    dim3 grid(8 * ntx * groups * gm, p.splits), block(64 * NW);
+    // split-K counts that are multiples of 8: one split per XCD (see the kernel)
+    const int xsplit = p.splits >= 8 && p.splits % 8 == 0;
+    const dim3 grid = xsplit ? dim3(8 * m_tiles * n_tiles, p.splits / 8) : dim3(8 * ntx * groups * gm, p.splits);
+    const dim3 block(64 * NW);
     if (p.splits > 1) {
         if (a.epi == EPI_SWIGLU)
-            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm, xsplit);
         else
-            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+            hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm, xsplit);
     } else if (a.epi == EPI_F32) {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm, 0);
     } else if (a.epi == EPI_RESID) {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm, 0);
     } else {
-        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm);
+        hipLaunchKernelGGL((gemm_dma128_kernel<BM, BN, WM, NW, SA, SW, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, m_tiles, n_tiles, n0, gm, 0);
     }
     return hipGetLastError();
 }

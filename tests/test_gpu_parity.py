@@ -394,6 +394,9 @@ _FORCED_PLANS = [
     ("t256", gemm_plan_code(RL_GEMM_T256)),
     ("t256_s4", gemm_plan_code(RL_GEMM_T256, 4)),
     ("t256_s3", gemm_plan_code(RL_GEMM_T256, 3)),
+    ("t256_s8", gemm_plan_code(RL_GEMM_T256, 8)),          # split-K 8 and 16: one split per XCD
+    ("t128_s16", gemm_plan_code(RL_GEMM_T128, 16)),
+    ("t128x256_s8", gemm_plan_code(RL_GEMM_T128X256, 8)),
     ("t128x256_s6", gemm_plan_code(RL_GEMM_T128X256, 6)),
     ("t128x256_s2", gemm_plan_code(RL_GEMM_T128X256, 2)),
     ("t128", gemm_plan_code(RL_GEMM_T128)),
