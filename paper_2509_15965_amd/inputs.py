@@ -7,7 +7,8 @@ model dtype (torch's round-to-nearest-even for bf16); RMSNorm gains are 1.0.
 Two initialisations:
   "normal"  every linear and embedding matrix i.i.d. N(0, 0.02);
   "fanin"   unit-variance (fan-in) init: every matrix N(0, 1/fan_in), with
-            the residual-branch output projections (w_o, w_down) further
+            the residual-branch output projections (w_o, w_down, and the
+            experts' w_exp_down) further
             divided by sqrt(2 L) and embedding rows N(0, 1) (the scale of
             caller-provided N(0, 1) embedding rows).  The residual stream then
             starts at the scale of its inputs and each layer adds a bounded
