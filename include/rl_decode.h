@@ -436,9 +436,11 @@ typedef enum rl_option {
                                               half of the output columns
                                               (0 = one segment; no split-K).
                                 A GEMM the override cannot serve (GEMV with
-                                M > 32, direct-load with M > 64, a tile kernel
-                                with K not a multiple of 64) keeps the
-                                planner's choice.  Results stay within the
+                                M > 32, direct-load or wide GEMV with M > 64,
+                                a tile kernel or either GEMV with K not a
+                                multiple of 64, a wide GEMV whose split-K
+                                partials would exceed 32 Mi floats) keeps
+                                the planner's choice.  Results stay within the
                                 parity tolerances for every choice; the bits
                                 differ (fp32 summation order).               */
     RL_OPT_SHARED_PREFIX = 4, /* 1 (default): decode attention of the slots of
@@ -464,7 +466,9 @@ typedef enum rl_gemm_kernel {
     RL_GEMM_T256 = 3,        /* 256 x 256 tiles, 8 waves                      */
     RL_GEMM_T128X256 = 4,    /* 128 x 256 tiles, 8 waves                      */
     RL_GEMM_T128 = 5,        /* 128 x 128 tiles, 4 waves, two per CU          */
-    RL_GEMM_T128_DEEP = 6    /* 128 x 128 tiles, 4 waves, 4-stage ring        */
+    RL_GEMM_T128_DEEP = 6,   /* 128 x 128 tiles, 4 waves, 4-stage ring        */
+    RL_GEMM_GEMV_WIDE = 7    /* 64 weight rows x a K slice per workgroup
+                                (M <= 64; split-K allowed)                    */
 } rl_gemm_kernel;
 
 rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value);

@@ -2277,7 +2277,7 @@ rl_status rl_decode_set_option(rl_decode_ctx* ctx, int32_t option, int64_t value
         case RL_OPT_GEMM_PLAN: {
             const int64_t k1 = value & 0xff, sp = (value >> 8) & 0xff, k2 = (value >> 16) & 0xff;
             const bool ok = value == 0 ||
-                            (value >= 0 && (value >> 24) == 0 && k1 >= RL_GEMM_DIRECT && k1 <= RL_GEMM_T128_DEEP &&
+                            (value >= 0 && (value >> 24) == 0 && k1 >= RL_GEMM_DIRECT && k1 <= RL_GEMM_GEMV_WIDE &&
                              sp <= kMaxSplits &&
                              (k2 == 0 || (k2 >= RL_GEMM_T128X256 && k2 <= RL_GEMM_T128_DEEP)));
             if (!ok) return fail(ctx, RL_ERR_INVALID_ARG, "invalid GEMM plan override");

@@ -220,6 +220,17 @@ int plan_gemm_candidates(int M, int Nw, int K, int epi, int F, GemmPlan* out, in
         p.variant = kGemvVariant; p.splits = 1; p.ksplit = K;
         add(p);
     }
+    if (M <= 64) {
+        // the wide GEMV at 1..8 K slices of at least 256 (64 per wave)
+        for (int sp = 1; sp <= 8; sp *= 2) {
+            GemmPlan p{};
+            p.variant = kGemvWideVariant;
+            p.ksplit = ceil_div(ceil_div(K, sp), 64) * 64;
+            p.splits = ceil_div(K, p.ksplit);
+            if (sp > 1 && (p.ksplit < 256 || static_cast<size_t>(p.splits) * M * Nw > kPartCapFloats)) break;
+            add(p);
+        }
+    }
     if (M < kMinTileCandidateRows) return n;
     for (const TileKernel& t : kLineTiles) {
         for (int s = 1; s <= kMaxSplits; s *= 2) {
@@ -256,6 +267,7 @@ int64_t gemm_plan_code_of(const GemmPlan& p) {
             case kLineVariant128x128: return RL_GEMM_T128;
             case kLineVariant128x128Deep: return RL_GEMM_T128_DEEP;
             case kGemvVariant: return RL_GEMM_GEMV;
+            case kGemvWideVariant: return RL_GEMM_GEMV_WIDE;
             default: return v >= 0 && v < kNumGemmShapes ? RL_GEMM_DIRECT : 0;
         }
     };
@@ -303,6 +315,15 @@ bool plan_gemm_forced(int M, int Nw, int K, int epi, int F, int64_t code, GemmPl
     if (k1 == RL_GEMM_GEMV) {
         if (M > 32 || K % 64 != 0 || k2 != 0) return false;
         p.variant = kGemvVariant; p.splits = 1; p.ksplit = K;
+        *out = p;
+        return true;
+    }
+    if (k1 == RL_GEMM_GEMV_WIDE) {
+        if (M > 64 || K % 64 != 0 || k2 != 0) return false;
+        p.variant = kGemvWideVariant;
+        p.ksplit = s > 1 ? ceil_div(ceil_div(K, s), 64) * 64 : K;
+        p.splits = ceil_div(K, p.ksplit);
+        if (p.splits > 1 && static_cast<size_t>(p.splits) * M * Nw > kPartCapFloats) return false;
         *out = p;
         return true;
     }
@@ -484,6 +505,7 @@ static hipError_t launch_shape(const GemmArgs& a, const GemmPlan& p, hipStream_t
 }
 
 hipError_t launch_gemv(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemv_wide(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (a.M <= 0) return hipSuccess;
@@ -492,6 +514,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, const GemmPlan& p, hipStream_t s)
         case 1: return launch_shape<2, 4, 1, 4>(a, p, s);
         case 2: return launch_shape<4, 4, 1, 4>(a, p, s);
         case kGemvVariant: return launch_gemv(a, s);
+        case kGemvWideVariant: return launch_gemv_wide(a, p, s);
         default: return launch_gemm_bf16_lds(a, p, s);
     }
 }
@@ -597,6 +620,141 @@ hipError_t launch_gemv(const GemmArgs& a, hipStream_t s) {
     else if (a.M <= 32) RL_GV(2);
     else return hipErrorInvalidValue;
 #undef RL_GV
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Wide GEMV-shaped kernel for M <= 64: one workgroup (4 waves) owns 64 weight
+// rows (SwiGLU: 32 gate rows and the matching 32 up rows) and one K slice
+// (blockIdx.y; the whole K without split-K); wave w takes the w-th quarter
+// of the slice.  Every activation fragment a wave loads feeds four 16-row
+// weight groups, so a workgroup re-reads the M activation rows once per 64
+// weight rows instead of once per 16.  The four partial tiles are summed
+// through LDS in wave order (deterministic); split-K slices land in the
+// partials buffer [splits][M][Nw] like the other kernels' slices.
+// ---------------------------------------------------------------------------
+template <int MR, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(256) gemv_wide_kernel(GemmArgs p, int ksplit, int kw) {
+    constexpr int NT = 4;   // 16-row weight groups per workgroup
+    constexpr int U = 2;    // 64-wide k blocks per batch of loads
+    __shared__ f32x4 red[4][MR * NT][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const int M = p.M;
+
+    int n[NT];
+    bool ok[NT];
+    const uint16_t* wp[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (EPI == EPI_SWIGLU) {
+            const int c = (blockIdx.x * NT + t) * 8 + (r16 & 7);
+            ok[t] = c < p.F;
+            n[t] = r16 < 8 ? c : p.F + c;
+        } else {
+            n[t] = (blockIdx.x * NT + t) * 16 + r16;
+            ok[t] = n[t] < p.Nw;
+        }
+        wp[t] = static_cast<const uint16_t*>(p.W) + static_cast<size_t>(ok[t] ? n[t] : 0) * p.ldw + 8 * kq;
+    }
+    const uint16_t* ap[MR];
+    bool aok[MR];
+#pragma unroll
+    for (int i = 0; i < MR; ++i) {
+        const int m = 16 * i + r16;
+        aok[i] = m < M;
+        ap[i] = static_cast<const uint16_t*>(p.A) + static_cast<size_t>(aok[i] ? m : 0) * p.lda + 8 * kq;
+    }
+    const int ks0 = blockIdx.y * ksplit;
+    const int ks1 = min(p.K, ks0 + ksplit);
+    const int kb = ks0 + wave * kw;
+    const int ke = min(ks1, kb + kw);
+
+    f32x4 acc[MR][NT];
+#pragma unroll
+    for (int i = 0; i < MR; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int k0 = kb; k0 < ke; k0 += 64 * U) {
+        u32x4 wf[U][2][NT], af[U][2][MR];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int kk = k0 + 64 * u + 32 * j;
+                const bool kok = kk + 8 * kq < ke;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) wf[u][j][t] = (ok[t] && kok) ? ld16(wp[t] + kk) : zero;
+#pragma unroll
+                for (int i = 0; i < MR; ++i) af[u][j][i] = (aok[i] && kok) ? ld16(ap[i] + kk) : zero;
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int i = 0; i < MR; ++i)
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+                        acc[i][t] = mfma16x16x32(as_bf16x8(af[u][j][i]), as_bf16x8(wf[u][j][t]), acc[i][t]);
+    }
+#pragma unroll
+    for (int i = 0; i < MR; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) red[wave][i * NT + t][lane] = acc[i][t];
+    __syncthreads();
+    // wave w finishes tiles w, w + 4, ...; lane holds D[4 kq + e][r16] of
+    // activation tile i, weight group t
+    for (int q = wave; q < MR * NT; q += 4) {
+        const int i = q / NT, t = q - i * NT;
+        f32x4 v = red[0][q][lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) v += red[w][q][lane];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int m = 16 * i + 4 * kq + e;
+            const float val = v[e];
+            if (SPLIT) {
+                if (ok[t] && m < M) p.partial[(static_cast<size_t>(blockIdx.y) * M + m) * p.Nw + n[t]] = val;
+            } else if (EPI == EPI_SWIGLU) {
+                const float up = __shfl(val, (lane & ~15) | ((r16 + 8) & 15), 64);
+                if (r16 < 8 && ok[t] && m < M)
+                    static_cast<uint16_t*>(p.act)[static_cast<size_t>(m) * p.ld_act + n[t]] =
+                        f32_to_bf16(swiglu_bf16(val, up));
+            } else if (ok[t] && m < M) {
+                if (EPI == EPI_F32) p.out_f32[static_cast<size_t>(m) * p.ldo + n[t]] = val;
+                else p.resid[static_cast<size_t>(m) * p.ldr + n[t]] += val;
+            }
+        }
+    }
+}
+
+hipError_t launch_gemv_wide(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    if (a.M > 64 || a.K % 64 != 0 || p.ksplit <= 0 || p.ksplit % 64 != 0 || ceil_div(a.K, p.ksplit) != p.splits ||
+        p.splits > kMaxSplits)
+        return hipErrorInvalidValue;
+    const int groups = a.epi == EPI_SWIGLU ? ceil_div(a.F, 32) : ceil_div(a.Nw, 64);
+    const int kw = ceil_div(ceil_div(p.ksplit, 4), 64) * 64;
+    dim3 grid(groups, p.splits), block(256);
+#define RL_GW(MR)                                                                                              \
+    do {                                                                                                       \
+        if (p.splits > 1) {                                                                                    \
+            if (a.epi == EPI_SWIGLU)                                                                           \
+                hipLaunchKernelGGL((gemv_wide_kernel<MR, EPI_SWIGLU, true>), grid, block, 0, s, a, p.ksplit, kw); \
+            else hipLaunchKernelGGL((gemv_wide_kernel<MR, EPI_F32, true>), grid, block, 0, s, a, p.ksplit, kw);   \
+        } else if (a.epi == EPI_F32) {                                                                         \
+            hipLaunchKernelGGL((gemv_wide_kernel<MR, EPI_F32, false>), grid, block, 0, s, a, p.ksplit, kw);      \
+        } else if (a.epi == EPI_RESID) {                                                                       \
+            hipLaunchKernelGGL((gemv_wide_kernel<MR, EPI_RESID, false>), grid, block, 0, s, a, p.ksplit, kw);    \
+        } else {                                                                                               \
+            hipLaunchKernelGGL((gemv_wide_kernel<MR, EPI_SWIGLU, false>), grid, block, 0, s, a, p.ksplit, kw);   \
+        }                                                                                                      \
+    } while (0)
+    if (a.M <= 16) RL_GW(1);
+    else if (a.M <= 32) RL_GW(2);
+    else RL_GW(4);
+#undef RL_GW
     return hipGetLastError();
 }
 

@@ -133,6 +133,7 @@ constexpr int kLineVariant128x128 = 8;      // direct-to-LDS, 128-byte rows, 128
 constexpr int kLineVariant128x256 = 9;      // direct-to-LDS, 128-byte rows, 128 x 256, 8 waves
 constexpr int kLineVariant128x128Deep = 10; // direct-to-LDS, 128-byte rows, 128 x 128, 4 waves, 4-stage ring
 constexpr int kGemvVariant = 11;            // M <= 32: 16 weight rows x all K per 8-wave workgroup, no split-K
+constexpr int kGemvWideVariant = 12;        // M <= 64: 64 weight rows x a K slice per 4-wave workgroup
 
 constexpr int kMaxSplits = 32;
 constexpr size_t kPartCapFloats = size_t(32) << 20;   // split-K partials budget

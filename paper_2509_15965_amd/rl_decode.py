@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(PKG, "librl_decode.so")
 RL_OK, RL_ERR_INVALID_ARG, RL_ERR_UNSUPPORTED, RL_ERR_CAPACITY, RL_ERR_HIP, RL_ERR_STATE = range(6)
 RL_DTYPE_FP32, RL_DTYPE_BF16 = 0, 1
 RL_OPT_ATTN_CHUNK, RL_OPT_PROFILE, RL_OPT_GEMM_PLAN, RL_OPT_SHARED_PREFIX, RL_OPT_PREFILL_ATTENTION = 1, 2, 3, 4, 5
-RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T256, RL_GEMM_T128X256, RL_GEMM_T128, RL_GEMM_T128_DEEP = 1, 2, 3, 4, 5, 6
+(RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T256, RL_GEMM_T128X256, RL_GEMM_T128, RL_GEMM_T128_DEEP,
+ RL_GEMM_GEMV_WIDE) = 1, 2, 3, 4, 5, 6, 7
 
 
 def gemm_plan_code(kernel: int, splits: int = 0, second: int = 0) -> int:

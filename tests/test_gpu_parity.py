@@ -12,7 +12,8 @@ from harness import (F32_LOGIT_REL_TOL, F32_LOGP_ABS_TOL, LOGIT_REL_TOL, LOGP_AB
                      build_models, check_token, inject_random_kv, row_rel_err)
 from paper_2509_15965_amd.configs import WORKLOADS, ModelShape
 from paper_2509_15965_amd.inputs import rollout_plan, uniform_tokens
-from paper_2509_15965_amd.rl_decode import (RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_T128, RL_GEMM_T128_DEEP,
+from paper_2509_15965_amd.rl_decode import (RL_GEMM_DIRECT, RL_GEMM_GEMV, RL_GEMM_GEMV_WIDE, RL_GEMM_T128,
+                                           RL_GEMM_T128_DEEP,
                                            RL_GEMM_T128X256, RL_GEMM_T256, RL_OPT_ATTN_CHUNK, RL_OPT_GEMM_PLAN,
                                            Engine, RLError, gemm_plan_code)
 
@@ -362,7 +363,7 @@ def test_step_rejects_bad_arguments_without_side_effects():
                                                RL_OPT_SHARED_PREFIX)
     for opt, bad in [(RL_OPT_ATTN_CHUNK, 16), (RL_OPT_ATTN_CHUNK, 33), (RL_OPT_ATTN_CHUNK, 65568),
                      (RL_OPT_ATTN_CHUNK, -32), (RL_OPT_SHARED_PREFIX, 2), (RL_OPT_PREFILL_ATTENTION, -1),
-                     (RL_OPT_GEMM_PLAN, 7), (RL_OPT_GEMM_PLAN, 5 | (33 << 8)), (RL_OPT_GEMM_PLAN, 5 | (2 << 16)),
+                     (RL_OPT_GEMM_PLAN, 8), (RL_OPT_GEMM_PLAN, 5 | (33 << 8)), (RL_OPT_GEMM_PLAN, 5 | (2 << 16)),
                      (99, 0)]:
         with pytest.raises(RLError) as e:
             eng.set_option(opt, bad)
@@ -391,6 +392,9 @@ def test_large_batch_gemm_tiles_match_oracle(n_prompts, plen):
 _FORCED_PLANS = [
     ("gemv", gemm_plan_code(RL_GEMM_GEMV)),
     ("direct_s4", gemm_plan_code(RL_GEMM_DIRECT, 4)),
+    ("gemv_wide", gemm_plan_code(RL_GEMM_GEMV_WIDE)),
+    ("gemv_wide_s3", gemm_plan_code(RL_GEMM_GEMV_WIDE, 3)),
+    ("gemv_wide_s8", gemm_plan_code(RL_GEMM_GEMV_WIDE, 8)),
     ("t256", gemm_plan_code(RL_GEMM_T256)),
     ("t256_s4", gemm_plan_code(RL_GEMM_T256, 4)),
     ("t256_s3", gemm_plan_code(RL_GEMM_T256, 3)),
@@ -420,6 +424,24 @@ def test_every_gemm_kernel_matches_oracle(name, code):
     for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
         assert row_rel_err(zg, zo) < LOGIT_REL_TOL, (name, k)
         assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, (name, k)
+
+
+@pytest.mark.parametrize("rows,splits", [(1, 0), (5, 4), (16, 0), (40, 2), (64, 0), (64, 8)])
+def test_wide_gemv_every_row_tile_count_matches_oracle(rows, splits):
+    """The wide GEMV (64 weight rows per workgroup) at one, two and four
+    16-row activation tiles, ragged and full, with and without split-K (at
+    split 8 the 64- and 128-wide K slices leave some of a workgroup's four
+    waves without k blocks), forced for every projection in decode and in
+    prefills of at most 64 rows; the 1032-entry vocabulary leaves a partial
+    last weight group."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e6, "bf16")
+    rng = np.random.default_rng(300 + rows)
+    prompts = [rng.integers(0, shape.vocab, size=3).astype(np.int32) for _ in range(rows)]
+    res = teacher_forced_run(shape, 301 + rows, prompts, group=1, n_steps=2, T=1.0,
+                             gemm_plan=gemm_plan_code(RL_GEMM_GEMV_WIDE, splits))
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
 
 
 def test_measured_gemm_plans_match_oracle():
