@@ -190,3 +190,55 @@ def test_probe_copy_argument_checks():
     assert lib.rl_probe_copy(None, None, 16, None) == R.RL_ERR_INVALID_ARG
     assert lib.rl_probe_copy(256, 512, 15, None) == R.RL_ERR_INVALID_ARG
     assert lib.rl_probe_copy(258, 512, 16, None) == R.RL_ERR_INVALID_ARG
+
+
+def _compile_and_run(tmp_path, body):
+    """Build a C program that includes the header and prints `body`'s lines."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "abi.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "rl_decode.h"\n'
+                   "int main(void) {\n" + body + "return 0;\n}\n")
+    exe = tmp_path / "abi"
+    subprocess.run([cc, "-std=c11", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    return dict(line.split("=") for line in out.split())
+
+
+_STRUCTS = {"rl_model_config": R.ModelConfig, "rl_weights": R.Weights, "rl_sample_params": R.SampleParams,
+            "rl_kernel_stats": R.KernelStats, "rl_attn_plan_stats": R.AttnPlanStats}
+
+
+def test_binding_structs_match_the_header_layout(tmp_path):
+    """Every ctypes mirror has the C struct's size and each field's offset, as
+    the C compiler lays them out from the header."""
+    body = ""
+    for cname, py in _STRUCTS.items():
+        body += f'printf("{cname}=%zu\\n", sizeof({cname}));\n'
+        for f, _ in py._fields_:
+            body += f'printf("{cname}.{f}=%zu\\n", offsetof({cname}, {f}));\n'
+    got = _compile_and_run(tmp_path, body)
+    for cname, py in _STRUCTS.items():
+        assert int(got[cname]) == C.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert int(got[f"{cname}.{f}"]) == getattr(py, f).offset, (cname, f)
+
+
+def test_binding_constants_match_the_header_enums(tmp_path):
+    """Status codes, dtypes, options, GEMM kernel codes and kernel-class
+    indices of the binding equal the header's enum values."""
+    names = [n for n in dir(R) if re.fullmatch(r"RL_(OK|ERR_[A-Z_]+|DTYPE_[A-Z0-9]+|OPT_[A-Z_]+|GEMM_[A-Z0-9_]+)", n)]
+    assert len(names) >= 20
+    body = "".join(f'printf("{n}=%d\\n", (int){n});\n' for n in names)
+    classes = ["RL_K_" + k.upper() for k in R.KERNEL_CLASSES]
+    body += "".join(f'printf("{k}=%d\\n", (int){k});\n' for k in classes)
+    body += 'printf("RL_K_COUNT=%d\\n", (int)RL_K_COUNT);\n'
+    got = _compile_and_run(tmp_path, body)
+    for n in names:
+        assert int(got[n]) == getattr(R, n), n
+    for i, k in enumerate(classes):
+        assert int(got[k]) == i, k
+    assert int(got["RL_K_COUNT"]) == len(R.KERNEL_CLASSES)
