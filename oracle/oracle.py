@@ -333,7 +333,7 @@ class OracleSeq:
         return k, v
 
 
-def score(model: OracleModel, prompt, response, T: float, embeds=None):
+def score(model: OracleModel, prompt, response, T: float, embeds=None, return_margin: bool = False):
     """Inference-stage log-probabilities of one response (Sec. 2.1, GRPO:
     after generation the log-probabilities of the responses are computed by a
     forward pass over them).
@@ -341,7 +341,9 @@ def score(model: OracleModel, prompt, response, T: float, embeds=None):
     Entry j is log softmax(z_j / T)[response[j]], where z_j are the logits
     after prompt + response[:j].  The sequence is fed one token at a time
     through the oracle's KV-cached forward; prompt ids < 0 select rows of
-    `embeds` (row -id-1).  Returns a float64 array of len(response)."""
+    `embeds` (row -id-1).  Returns a float64 array of len(response), and
+    with return_margin also the sequence's smallest routing margin (inf for
+    a dense model)."""
     response = [int(t) for t in response]
     seq = model.new_seq(len(prompt) + len(response))
     z = None
@@ -353,4 +355,4 @@ def score(model: OracleModel, prompt, response, T: float, embeds=None):
         out[j] = logprob(z.astype(np.float32), T, y)
         if j + 1 < len(response):
             z = seq.forward(y)
-    return out
+    return (out, seq.route_margin) if return_margin else out

@@ -1,9 +1,17 @@
 """Mixture-of-experts decode (the Qwen3-30B-A3B policy of Sec. 5.1.1) through
 the C ABI against the oracle, at the stated bars: routing, grouping by
 expert, the grouped expert projections and the weighted sum, in prefill,
-decode and scoring.  Each case first checks that the oracle's routing has no
-near ties (the router logits are fp32 on both sides; a near tie could pick
-different experts on the two sides), then compares.  Needs an MI355X."""
+decode and scoring.  Routing is an integer decided by floating point: both
+sides rank fp32 router logits, but the router's bf16 input can differ by one
+storage ulp in a few elements between the two sides, which moves a router
+logit by about 5e-4 per element (one ulp, 2^-7 relative, times a fan-in
+weight of std H^-1/2 at H = 256) and a gap between two logits by about 7e-4.
+A sequence whose oracle routing margin (smallest gap between a chosen logit
+and the best one left out, over all its tokens) is below ROUTE_NEAR_TIE,
+about 4 such standard deviations, may legitimately route differently and is
+excused; every other sampled sequence is compared at the stated bars, and a
+case must compare at least its stated number of sequences.  Needs an
+MI355X."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +23,7 @@ from paper_2509_15965_amd.rl_decode import RL_ERR_UNSUPPORTED, Engine, RLError
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-MIN_ROUTE_MARGIN = 1e-4
+ROUTE_NEAR_TIE = 3e-3
 TINY_MOE = ModelShape(2, 256, 4, 2, 64, 0, 512, 1e-6, 1e6, "bf16", n_experts=8, top_k=2, expert_ffn=128)
 # the real expert widths (128 experts of 768, top 8, hidden 2048, 32 / 4 heads) at two layers
 QWEN3_WIDTHS = ModelShape(**{**QWEN3_MOE.as_dict(), "n_layers": 2})
@@ -36,7 +44,8 @@ def _moe_run(shape, seed, plens, n_steps, sample_rows, group=1, page=0):
     """Prefill (one prompt per `group` sequences) + n_steps teacher-forced
     decode steps on the GPU; the rows in `sample_rows` are replayed on the
     oracle.  Returns [(gpu logits, oracle logits, gpu logp, oracle logp)] per
-    call, for the sampled rows, and the smallest oracle routing margin."""
+    call, for the sampled rows, and the oracle's routing margins (per sampled
+    row, and per prompt the smallest of its sampled rows')."""
     w_dev, _, om = build_models(shape, seed, init="fanin")
     rng = np.random.default_rng(seed + 1)
     prompts = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in plens]
@@ -73,37 +82,53 @@ def _moe_run(shape, seed, plens, n_steps, sample_rows, group=1, page=0):
         lpo = np.array([oracle.logprob(zs[j].astype(np.float32), 1.0, int(forced[s][i]))
                         for j, i in enumerate(sample_rows)])
         out.append((gpu[s][0][sample_rows], zs, gpu[s][1][sample_rows], lpo))
-    margin = min(orc.seqs[i].route_margin for i in sample_rows)
-    return out, margin
+    margins = np.array([orc.seqs[i].route_margin for i in sample_rows])
+    pmargins = np.array([min(orc.seqs[i].route_margin for i in sample_rows if i // group == p) for p in prow])
+    return out, (margins, pmargins)
 
 
-def _assert_bars(out, margin):
-    assert margin > MIN_ROUTE_MARGIN, margin     # the data has no near-tie routing
+def _assert_bars(out, margins, min_compared):
+    """The stated bars on every sampled sequence (and prompt) without a
+    near-tie routing decision; at least min_compared sequences compared."""
+    rows, prompts = margins[0] > ROUTE_NEAR_TIE, margins[1] > ROUTE_NEAR_TIE
+    print(f"routing: {rows.sum()} of {rows.size} sequences and {prompts.sum()} of {prompts.size} prompts compared")
+    assert rows.sum() >= min_compared and prompts.any(), margins
     for k, (zg, zo, lg, lo) in enumerate(out):
-        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
-        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+        zmask = prompts if k == 0 else rows        # the prefill's logits are per prompt
+        assert row_rel_err(zg[zmask], zo[zmask]) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg[rows] - lo[rows])) < LOGP_ABS_TOL, k
 
 
 def test_moe_decode_matches_oracle():
-    out, margin = _moe_run(TINY_MOE, 101, [9, 23, 40], 6, [0, 1, 2])
-    _assert_bars(out, margin)
+    out, margins = _moe_run(TINY_MOE, 101, [9, 23, 40, 17, 28], 6, [0, 1, 2, 3, 4])
+    _assert_bars(out, margins, 2)
+
+
+@pytest.mark.parametrize("k", [1, 8])
+def test_moe_degenerate_top_k_matches_oracle(k):
+    """Top-1 routing (each row's MLP is one expert, weight 1) and top-k equal
+    to the number of experts (every expert, softmax over all of them)."""
+    shape = ModelShape(**{**TINY_MOE.as_dict(), "top_k": k})
+    out, margins = _moe_run(shape, 121 + k, [7, 19, 33, 12, 25], 4, [0, 1, 2, 3, 4])
+    _assert_bars(out, margins, 2)
 
 
 def test_moe_group_prefill_on_a_paged_pool_matches_oracle():
     """A GRPO group of 4 per prompt (shared prompt pages, pages of 32) and
     then decoding; every sequence checked."""
-    out, margin = _moe_run(TINY_MOE, 103, [37, 70], 4, list(range(8)), group=4, page=32)
-    _assert_bars(out, margin)
+    out, margins = _moe_run(TINY_MOE, 103, [37, 70], 4, list(range(8)), group=4, page=32)
+    _assert_bars(out, margins, 3)
 
 
 def test_moe_real_widths_sampled_rows_match_oracle():
     """128 experts of width 768, top 8, hidden 2048, at 128 rows per step
-    (every expert serves several pairs; some serve many), 8 rows replayed on
-    the oracle."""
+    (every expert serves several pairs; some serve many), 24 rows replayed
+    on the oracle (the gap between the 8th and 9th of 128 router logits is
+    often small, so more rows are replayed than are compared)."""
     n = 128
-    rows = [0, 17, 40, 63, 64, 99, 120, 127]
-    out, margin = _moe_run(QWEN3_WIDTHS, 107, [5 + (i % 7) for i in range(n)], 2, rows)
-    _assert_bars(out, margin)
+    rows = sorted(list(range(0, 128, 16)) + list(range(5, 128, 16)) + list(range(11, 128, 16)))
+    out, margins = _moe_run(QWEN3_WIDTHS, 107, [5 + (i % 7) for i in range(n)], 2, rows)
+    _assert_bars(out, margins, 3)
 
 
 def test_moe_score_matches_oracle():
@@ -121,9 +146,14 @@ def test_moe_score_matches_oracle():
               group=group, temperature=1.0)
     got = lp.cpu().numpy()
     eng.close()
+    compared = 0
     for i, r in enumerate(resp):
-        ref = oracle.score(om, prompts[i // group], r, 1.0)
-        assert np.max(np.abs(got[roffs[i]:roffs[i + 1]] - ref)) < LOGP_ABS_TOL, i
+        ref, margin = oracle.score(om, prompts[i // group], r, 1.0, return_margin=True)
+        if margin > ROUTE_NEAR_TIE:
+            assert np.max(np.abs(got[roffs[i]:roffs[i + 1]] - ref)) < LOGP_ABS_TOL, i
+            compared += 1
+    print(f"routing: {compared} of {len(resp)} responses compared")
+    assert compared >= 2
 
 
 def test_moe_refuses_measured_plans():

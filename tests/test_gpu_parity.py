@@ -376,6 +376,50 @@ def test_step_rejects_bad_arguments_without_side_effects():
     eng.close()
 
 
+def test_empty_calls_are_no_ops_and_empty_prompts_are_refused():
+    """Zero rows is a no-op for every per-row entry point (nothing enqueued,
+    no length changed); an empty prompt or response, or a prefill of no
+    prompts, is refused; the engine decodes normally afterwards."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e6, "bf16")
+    w_dev, _, _ = build_models(shape, 7)
+    eng = Engine(shape, w_dev, max_seqs=4, max_ctx=16, max_prefill_tokens=16)
+    i0 = torch.empty(0, dtype=torch.int32, device=DEV)
+    f0 = torch.empty(0, dtype=torch.float32, device=DEV)
+    eng.step([], [], i0, i0, f0)
+    eng.sample_logits(torch.empty((0, shape.vocab), dtype=torch.float32, device=DEV), [], [], i0, f0)
+    eng.release([])
+    eng.set_lengths([], [])
+    assert eng.kv_offload_bytes([]) == 0
+    assert all(eng.slot_length(i) == 0 for i in range(4))
+    t = _i32([3, 4, 5])
+    ot = torch.empty(4, dtype=torch.int32, device=DEV)
+    ol = torch.empty(4, dtype=torch.float32, device=DEV)
+    for args in (([], [], [0]), ([0], [1], [0, 0]), ([0, 1], [1, 2], [0, 2, 2])):
+        with pytest.raises(RLError) as e:
+            eng.prefill(*args, t, ot, ol)
+        assert e.value.status == 1, args
+    lp = torch.empty(4, dtype=torch.float32, device=DEV)
+    with pytest.raises(RLError) as e:
+        eng.score([0, 1], [0, 2], t, [0, 2, 2], t, lp, group=2)   # second response empty
+    assert e.value.status == 1
+    assert all(eng.slot_length(i) == 0 for i in range(4))
+    eng.prefill([0], [1], [0, 3], t, ot, ol)
+    eng.step([0], [1], ot[:1], ot[1:2], ol[:1])
+    assert eng.slot_length(0) == 4
+    eng.close()
+
+
+def test_one_token_prompts_match_oracle():
+    """Prompts of a single token (each query attends to one key at prefill),
+    shared by a group of 2, then decoding."""
+    shape = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e6, "bf16")
+    prompts = [np.array([5], dtype=np.int32), np.array([1031], dtype=np.int32), np.array([0, 9], dtype=np.int32)]
+    res = teacher_forced_run(shape, 313, prompts, group=2, n_steps=3, T=1.0)
+    for k, (zg, zo, lg, lo, tg, to) in enumerate(res):
+        assert row_rel_err(zg, zo) < LOGIT_REL_TOL, k
+        assert np.max(np.abs(lg - lo)) < LOGP_ABS_TOL, k
+
+
 @pytest.mark.parametrize("n_prompts,plen", [(100, 3), (140, 4), (9, 70)])
 def test_large_batch_gemm_tiles_match_oracle(n_prompts, plen):
     """Batches above 64 rows take the LDS-tiled GEMM (128- and 256-row tiles,
