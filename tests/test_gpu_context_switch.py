@@ -4,7 +4,8 @@ buffers (rl_decode_rebind), through the C ABI (needs an MI355X).
 
 A rollout that is switched out and back in (pool wiped, or weights, pool
 and workspace replaced by new allocations; slots renumbered) must continue
-bit-identically to one that never left the GPU.
+bit-identically to one that never left the GPU (dense and
+mixture-of-experts models).
 """
 import numpy as np
 import pytest
@@ -19,6 +20,7 @@ pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
 GQA = ModelShape(2, 512, 8, 2, 128, 1024, 1032, 1e-6, 1e4, "bf16")
+MOE = ModelShape(2, 256, 4, 2, 64, 0, 512, 1e-6, 1e6, "bf16", n_experts=8, top_k=2, expert_ffn=128)
 
 
 @pytest.fixture(autouse=True)
@@ -61,7 +63,7 @@ def _case(shape):
     return [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in (37, 58)]
 
 
-@pytest.mark.parametrize("shape", [GQA, WORKLOADS["tiny"].model], ids=["bf16", "fp32"])
+@pytest.mark.parametrize("shape", [GQA, WORKLOADS["tiny"].model, MOE], ids=["bf16", "fp32", "moe"])
 @pytest.mark.parametrize("rebind", [False, True], ids=["wipe-pool", "new-buffers"])
 def test_switch_out_and_back_continues_bit_identically(shape, rebind):
     w_dev, _, _ = build_models(shape, 62)
