@@ -36,14 +36,19 @@ def _scramble(eng, page, max_ctx):
     eng.release([0, 2])
 
 
-def _run(shape, w_dev, prompts, group, n_steps, T, page=0, pages=0, slot0=4, max_ctx=None, seed=11):
-    """Prefill + n_steps teacher-forced decode steps on slots slot0.. ; returns
-    every logits row, log-prob and token, in call order."""
+def _run(shape, w_dev, prompts, group, n_steps, T, page=0, pages=0, slot0=4, max_ctx=None, seed=11, tune=None):
+    """Prefill + n_steps teacher-forced decode steps on slots slot0.. (after
+    measuring GEMM plans at the `tune` batch sizes, if given); returns every
+    logits row, log-prob and token, in call order."""
     n_seq = len(prompts) * group
     plens = [len(p) for p in prompts]
     max_ctx = max_ctx or max(plens) + n_steps + 2
     eng = Engine(shape, w_dev, max_seqs=slot0 + n_seq, max_ctx=max_ctx, max_prefill_tokens=sum(plens),
                  kv_page_size=page, kv_pages=pages)
+    if tune:
+        total = eng.kv_free_pages()
+        eng.tune_gemms(tune)                     # its measuring steps take pages and give them all back
+        assert eng.kv_free_pages() == total
     if page:
         _scramble(eng, page, max_ctx)
     slots = list(range(slot0, slot0 + n_seq))
@@ -108,15 +113,18 @@ def test_paged_fp32_equals_contiguous():
     _assert_same(got, ref)
 
 
-def test_paged_decode_matches_oracle():
-    """A paged pool against the oracle at the stated bars (group 2, pages of 32)."""
+@pytest.mark.parametrize("tune", [None, [1, 4, 8]], ids=["cost-model", "measured-plans"])
+def test_paged_decode_matches_oracle(tune):
+    """A paged pool against the oracle at the stated bars (group 2, pages of
+    32), with the cost model's GEMM plans or plans measured on the paged
+    engine first."""
     from harness import OracleRollout
     import oracle
     w_dev, _, om = build_models(GQA, 67)
     rng = np.random.default_rng(68)
     prompts = [rng.integers(0, GQA.vocab, size=n).astype(np.int32) for n in (30, 41)]
     group, n_steps = 2, 6
-    got = _run(GQA, w_dev, prompts, group, n_steps, 1.0, page=32, seed=69)
+    got = _run(GQA, w_dev, prompts, group, n_steps, 1.0, page=32, seed=69, tune=tune)
     max_ctx = max(len(p) for p in prompts) + n_steps + 2
     orc = OracleRollout(om, max_ctx)
     zo = [orc.prefill(p * group, prompts[p]) for p in range(len(prompts))]
