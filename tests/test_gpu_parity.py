@@ -312,10 +312,13 @@ def test_split_kv_long_context_matches_oracle_and_any_chunk():
 
 
 def test_decode_is_deterministic():
+    """Two identical runs give the same bits; a third run that asks for no
+    logits (the benchmark's calls) samples the same tokens with the same
+    log-probabilities."""
     shape = ModelShape(2, 256, 4, 2, 64, 512, 512, 1e-6, 1e6, "bf16")
     w_dev, _, _ = build_models(shape, 5)
     outs = []
-    for _ in range(2):
+    for r in range(3):
         eng = Engine(shape, w_dev, max_seqs=4, max_ctx=64, max_prefill_tokens=64)
         toks = _i32(uniform_tokens(40, shape.vocab, 1))
         ot = torch.empty(4, dtype=torch.int32, device=DEV)
@@ -324,13 +327,14 @@ def test_decode_is_deterministic():
         eng.prefill([0, 1, 2, 3], [9, 8, 7, 6], [0, 10, 40], toks, ot, ol, group=2, seed=3)
         run = []
         for _ in range(5):
-            eng.step([0, 1, 2, 3], [9, 8, 7, 6], ot.clone(), ot, ol, seed=3, out_logits=lg)
+            eng.step([0, 1, 2, 3], [9, 8, 7, 6], ot.clone(), ot, ol, seed=3, out_logits=lg if r < 2 else None)
             run.append((ot.cpu().numpy().copy(), ol.cpu().numpy().copy(), lg.cpu().numpy().copy()))
         outs.append(run)
         eng.close()
-    for a, b in zip(*outs):
+    for a, b, c in zip(*outs):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
+        assert np.array_equal(a[0], c[0]) and np.array_equal(a[1], c[1])
 
 
 def test_step_rejects_bad_arguments_without_side_effects():
