@@ -104,11 +104,13 @@ def test_moe_decode_matches_oracle():
     _assert_bars(out, margins, 2)
 
 
-@pytest.mark.parametrize("k", [1, 8])
-def test_moe_degenerate_top_k_matches_oracle(k):
-    """Top-1 routing (each row's MLP is one expert, weight 1) and top-k equal
-    to the number of experts (every expert, softmax over all of them)."""
-    shape = ModelShape(**{**TINY_MOE.as_dict(), "top_k": k})
+@pytest.mark.parametrize("E,k,Fe", [(8, 1, 128), (8, 8, 128), (100, 6, 80)])
+def test_moe_degenerate_top_k_matches_oracle(E, k, Fe):
+    """Top-1 routing (each row's MLP is one expert, weight 1), top-k equal to
+    the number of experts (every expert, softmax over all of them), and 100
+    experts (the second 64-expert slot of a lane partly empty) of width 80
+    (the last 32-column gate group of each expert partly empty), top 6."""
+    shape = ModelShape(**{**TINY_MOE.as_dict(), "n_experts": E, "top_k": k, "expert_ffn": Fe})
     out, margins = _moe_run(shape, 121 + k, [7, 19, 33, 12, 25], 4, [0, 1, 2, 3, 4])
     _assert_bars(out, margins, 2)
 
