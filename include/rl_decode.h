@@ -487,8 +487,8 @@ typedef enum rl_kernel_class {
  * projections run at every row count from max_seqs down to 1.  For each
  * batch size in `sizes` (host array of n_sizes strictly increasing values in
  * [1, max_seqs]) and each of the q|k|v, o, gate-up, down and LM-head
- * projections, every plan of the cost model's search space (tile kernel,
- * split-K count, two-segment launch) is timed on the context's stream with
+ * projections, every plan of the cost model's search space (tile kernel or
+ * GEMV form, split-K count, two-segment launch) is timed on the context's stream with
  * HIP events, each together with the kernel that consumes its output as a
  * decode step issues it; the fastest few and the cost model's plan are then
  * timed inside whole decode steps of that many rows, one projection at a
@@ -499,10 +499,13 @@ typedef enum rl_kernel_class {
  * before the first prefill, or after releasing every slot; RL_ERR_INVALID_ARG
  * otherwise): the measuring steps decode slots 0 .. largest size - 1 at a
  * short context, overwrite their K/V and the workspace, and leave every
- * length at 0.  Synchronises the stream.  Every plan gives results within
+ * length at 0 (on a paged pool they take pages and return every one; a pool
+ * too small for them fails with RL_ERR_CAPACITY, the table cleared).
+ * Synchronises the stream.  Every plan gives results within
  * the parity tolerances; the bits depend on the plan (fp32 summation
- * order), so the table is part of a run's configuration.  bf16 models only
- * (RL_ERR_UNSUPPORTED for fp32 when n_sizes > 0).  Takes about 0.3 s per
+ * order), so the table is part of a run's configuration.  Dense bf16 models
+ * only (RL_ERR_UNSUPPORTED for fp32 or a mixture of experts when
+ * n_sizes > 0).  Takes about 0.3 s per
  * size at the 7B shape. */
 rl_status rl_decode_tune_gemms(rl_decode_ctx* ctx, int32_t n_sizes, const int32_t* sizes);
 
